@@ -1,0 +1,575 @@
+"""Pins of the CPU oracle against what the paper and the mathematics fix.
+
+None of these compares the oracle with itself: each check uses a closed form,
+an invariant the paper states, a constant the paper prints (tests/golden/), a
+hand-worked example, or brute force by a different route.  CPU only.
+"""
+import json
+import math
+import os
+
+import numpy as np
+import pytest
+
+GOLD = os.path.join(os.path.dirname(__file__), "golden")
+
+
+def _load(name):
+    with open(os.path.join(GOLD, name)) as f:
+        return json.load(f)
+
+
+def _bits(x):
+    from paper_2607_02584_amd.datagen import f32_to_bf16_bits
+    return f32_to_bf16_bits(np.asarray(x, np.float32))
+
+
+def _rand_bits(rng, shape, scale=1.0):
+    return _bits(rng.standard_normal(shape).astype(np.float32) * np.float32(scale))
+
+
+def _orth_blocks(rng, n=64):
+    """Random O(2) blocks: half rotations, half reflections."""
+    R = np.empty((n, 2, 2))
+    for i in range(n):
+        a = rng.uniform(0, 2 * np.pi)
+        c, s = math.cos(a), math.sin(a)
+        R[i] = [[c, s], [-s, c]] if i % 2 == 0 else [[c, s], [s, -c]]
+    return R
+
+
+# ----------------------------------------------------------------- RoPE ----
+
+def test_default_block_is_paper_h2(ora):
+    """Sec. 4.1 H_2 equation: with R merged at position 0 (M = I) the table is H_2."""
+    g = _load("paper_constants.json")["H2"]
+    H2 = np.array(g["matrix_unscaled"], float) / math.sqrt(2.0)
+    geo = ora.Geometry(2, 3, 4)
+    for p in (0, 21, 63):
+        G = ora.rope_block(geo, 0, p, ora.ROT_INTERLEAVED)
+        np.testing.assert_allclose(G, H2, rtol=0, atol=1e-16)
+
+
+def test_rope_blocks_are_so2_and_merged_blocks_o2(ora):
+    """Sec. 3: every RoPE block is in SO(2); Sec. 4.1.2: M R stays a 2x2 orthogonal block."""
+    geo = ora.Geometry(5, 6, 7)
+    rng = np.random.default_rng(0)
+    for _ in range(50):
+        n, p = int(rng.integers(geo.N)), int(rng.integers(64))
+        M = ora.rope_block(geo, n, p, ora.ROT_NONE)
+        G = ora.rope_block(geo, n, p, ora.ROT_INTERLEAVED)
+        np.testing.assert_allclose(M @ M.T, np.eye(2), atol=1e-15)
+        assert abs(np.linalg.det(M) - 1.0) < 1e-15
+        np.testing.assert_allclose(G @ G.T, np.eye(2), atol=1e-15)
+        assert abs(np.linalg.det(G) + 1.0) < 1e-15  # H_2 is a reflection
+
+
+@pytest.mark.parametrize("split,theta,axis,k,pos,omega", [
+    ((44, 42, 42), 1e4, 0, 11, 3, 1e-2),     # theta^(-2*11/44) = 10^-2 exactly
+    ((44, 42, 42), 1e4, 1, 0, 7, 1.0),       # pair 0 of every axis turns by the position
+    ((44, 42, 42), 1e4, 2, 0, 5, 1.0),
+    ((16, 56, 56), 256.0, 0, 4, 5, 1 / 16),  # 256^(-8/16) = 1/16
+    ((16, 56, 56), 256.0, 1, 14, 7, 1 / 16),  # 256^(-28/56)
+    ((16, 56, 56), 256.0, 2, 7, 9, 256.0 ** (-0.25)),
+])
+def test_rope_angle_closed_forms(ora, split, theta, axis, k, pos, omega):
+    """Sec. 3: the pair k of segment a turns by pos_a * theta^(-2k/D_a) (RoFormer
+    frequencies per axis); checked at points where the power is a closed form.
+    The other two coordinates are set to 1 so a wrong axis assignment shows."""
+    geo = ora.Geometry(10, 10, 10, split=split, theta=theta)
+    coords = [1, 1, 1]
+    coords[axis] = pos
+    t, h, w = coords
+    n = (t * geo.Hg + h) * geo.W + w
+    p = sum(s // 2 for s in split[:axis]) + k
+    M = ora.rope_block(geo, n, p, ora.ROT_NONE)
+    ang = math.atan2(M[0, 1], M[0, 0])
+    target = math.remainder(pos * omega, 2 * math.pi)
+    assert abs(ang - target) < 1e-12
+
+
+def test_rope_relative_position_and_segment_isolation(ora):
+    """Sec. 3: RoPE scores depend on the offset between tokens only, and each
+    segment encodes only its own axis (t, h or w)."""
+    geo = ora.Geometry(6, 7, 8)
+    rng = np.random.default_rng(1)
+    x = _rand_bits(rng, (geo.N, 128))
+    y = ora.rope_rot_f64(geo, x, ora.ROT_NONE)
+    xb = ora.bf16_to_f32(x).astype(np.float64)
+
+    def tok(t, h, w):
+        return (t * geo.Hg + h) * geo.W + w
+
+    # same raw q and k vectors placed at (p, p+delta) for two base points
+    q_raw, k_raw = x[tok(0, 0, 0)], x[tok(1, 2, 3)]
+    for delta in [(1, 2, 3), (2, 0, 5), (0, 3, 1)]:
+        vals = []
+        for base in [(0, 0, 0), (3, 2, 2), (2, 1, 0)]:
+            a = tok(*base)
+            b = tok(*(base[i] + delta[i] for i in range(3)))
+            xx = x.copy()
+            xx[a], xx[b] = q_raw, k_raw
+            yy = ora.rope_rot_f64(geo, xx, ora.ROT_NONE)
+            vals.append(yy[a] @ yy[b])
+        assert max(vals) - min(vals) < 1e-11 * max(1.0, abs(vals[0]))
+    # segment isolation: a vector supported on the t-segment only
+    seg = np.zeros(128, bool)
+    seg[:44] = True
+    xs = xb.copy()
+    xs[:, ~seg] = 0
+    ys = ora.rope_rot_f64(geo, _bits(xs), ora.ROT_NONE)
+    s1 = ys[tok(1, 0, 0)] @ ys[tok(3, 0, 0)]
+    # same raw vectors moved to positions with the same dt but other dh, dw
+    xs2 = xs.copy()
+    xs2[tok(1, 5, 6)] = xs[tok(1, 0, 0)]
+    xs2[tok(3, 1, 2)] = xs[tok(3, 0, 0)]
+    ys2 = ora.rope_rot_f64(geo, _bits(xs2), ora.ROT_NONE)
+    s2 = ys2[tok(1, 5, 6)] @ ys2[tok(3, 1, 2)]
+    assert abs(s1 - s2) < 1e-11 * max(1.0, abs(s1))
+    assert y.shape == (geo.N, 128)
+
+
+@pytest.mark.parametrize("rotation", [0, 1, 2])
+def test_rope_rotation_preserves_pair_norms(ora, rotation):
+    """Sec. 4.1: M and R are orthogonal, so every 2-channel pair keeps its norm
+    (for the half rotation: the pair (i, i + D_j/2) of each segment)."""
+    geo = ora.Geometry(3, 5, 7)
+    rng = np.random.default_rng(2)
+    x = _rand_bits(rng, (geo.N, 128), 3.0)
+    xf = ora.bf16_to_f32(x).astype(np.float64)
+    y64 = ora.rope_rot_f64(geo, x, rotation)
+    y32 = ora.rope_rot_f32(geo, x, rotation).astype(np.float64)
+    if rotation == ora.ROT_HALF:
+        n_in = []
+        o = 0
+        for Da in geo.split:
+            h = Da // 2
+            for i in range(h):
+                n_in.append(xf[:, o + i] ** 2 + xf[:, o + i + h] ** 2)
+            o += Da
+        # RoPE acts on adjacent pairs first; only the total norm is preserved here
+        np.testing.assert_allclose((y64 ** 2).sum(1), (xf ** 2).sum(1), rtol=1e-12)
+        np.testing.assert_allclose((y32 ** 2).sum(1), (xf ** 2).sum(1), rtol=1e-6)
+    else:
+        n_in = xf[:, 0::2] ** 2 + xf[:, 1::2] ** 2
+        np.testing.assert_allclose(y64[:, 0::2] ** 2 + y64[:, 1::2] ** 2, n_in, rtol=1e-12, atol=1e-300)
+        np.testing.assert_allclose(y32[:, 0::2] ** 2 + y32[:, 1::2] ** 2, n_in, rtol=2e-6, atol=1e-30)
+
+
+def test_interleaved_equals_rope_then_r(ora):
+    """Sec. 4.1.2 merged-RoPE equation: RoPE(Q) R = Q (M R)."""
+    geo = ora.Geometry(4, 5, 6)
+    rng = np.random.default_rng(3)
+    x = _rand_bits(rng, (geo.N, 128))
+    for rot in (None, _orth_blocks(rng)):
+        R = _orth_blocks(rng) if rot is None else rot
+        Rn = np.tile(np.array([[1, 1], [1, -1]]) / math.sqrt(2), (64, 1, 1)) if rot is None else R
+        y0 = ora.rope_rot_f64(geo, x, ora.ROT_NONE)
+        ym = ora.rope_rot_f64(geo, x, ora.ROT_INTERLEAVED, rot)
+        pairs = y0.reshape(geo.N, 64, 1, 2)
+        expect = (pairs @ Rn[None]).reshape(geo.N, 128)
+        np.testing.assert_allclose(ym, expect, rtol=0, atol=1e-12)
+
+
+def _dense_pi_r(split, R):
+    """Dense 128x128 Pi R of Sec. 4.1.3 built from its description: in segment j,
+    Pi^j moves channel i and i + D_j/2 to adjacent positions (2i, 2i+1); R^j acts
+    on those positions with its blocks."""
+    D = sum(split)
+    Pi = np.zeros((D, D))
+    Rd = np.zeros((D, D))
+    o = 0
+    for Da in split:
+        h = Da // 2
+        for i in range(h):
+            Pi[o + i, o + 2 * i] = 1
+            Pi[o + i + h, o + 2 * i + 1] = 1
+            blk = R[o // 2 + i]
+            Rd[o + 2 * i:o + 2 * i + 2, o + 2 * i:o + 2 * i + 2] = blk
+        o += Da
+    return Pi @ Rd
+
+
+def test_half_equals_rope_then_pi_r(ora):
+    """Sec. 4.1.3 (Q Pi R equation): half rotation = RoPE, then permutation, then blocks."""
+    for split, theta in (((44, 42, 42), 1e4), ((16, 56, 56), 256.0)):
+        geo = ora.Geometry(3, 4, 5, split=split, theta=theta)
+        rng = np.random.default_rng(4)
+        x = _rand_bits(rng, (geo.N, 128))
+        for rot in (None, _orth_blocks(rng)):
+            Rn = np.tile(np.array([[1, 1], [1, -1]]) / math.sqrt(2), (64, 1, 1)) if rot is None else rot
+            y0 = ora.rope_rot_f64(geo, x, ora.ROT_NONE)
+            yh = ora.rope_rot_f64(geo, x, ora.ROT_HALF, rot)
+            np.testing.assert_allclose(yh, y0 @ _dense_pi_r(split, Rn), rtol=0, atol=1e-12)
+
+
+@pytest.mark.parametrize("rotation", [1, 2])
+def test_orthogonal_rotation_preserves_scores(ora, rotation):
+    """Sec. 4.1.1: (Q R)(K R^{-T})^T = Q K^T, with R^{-T} = R for orthogonal R, so the
+    rotated scores equal the unrotated ones; a non-orthogonal R breaks this."""
+    geo = ora.Geometry(4, 4, 8)
+    rng = np.random.default_rng(5)
+    q = _rand_bits(rng, (geo.N, 128))
+    k = _rand_bits(rng, (geo.N, 128))
+    S0 = ora.rope_rot_f64(geo, q, 0) @ ora.rope_rot_f64(geo, k, 0).T
+    for rot in (None, _orth_blocks(rng)):
+        S = ora.rope_rot_f64(geo, q, rotation, rot) @ ora.rope_rot_f64(geo, k, rotation, rot).T
+        assert np.abs(S - S0).max() <= 1e-12 * np.abs(S0).max()
+    bad = np.tile(np.array([[2.0, 0.0], [0.0, 0.5]]), (64, 1, 1))
+    Sb = ora.rope_rot_f64(geo, q, rotation, bad) @ ora.rope_rot_f64(geo, k, rotation, bad).T
+    assert np.abs(Sb - S0).max() > 1e-2 * np.abs(S0).max()
+
+
+@pytest.mark.parametrize("rotation", [0, 1, 2])
+def test_f32_sequence_tracks_f64(ora, rotation):
+    """The binary32 sequence stays within a few ulp of the fp64 mathematics."""
+    geo = ora.Geometry(7, 9, 11)
+    rng = np.random.default_rng(6)
+    x = _rand_bits(rng, (geo.N, 128), 5.0)
+    y32 = ora.rope_rot_f32(geo, x, rotation).astype(np.float64)
+    y64 = ora.rope_rot_f64(geo, x, rotation)
+    scale = np.abs(ora.bf16_to_f32(x)).max()
+    assert np.abs(y32 - y64).max() <= 4 * 2.0 ** -24 * scale * 2
+
+
+# ------------------------------------------------------------- smoothing ----
+
+def test_mean_fixed_close_to_exact_mean_and_order_free(ora):
+    """Sec. 4 smoothing: mu is the per-channel mean over tokens; the fixed-point
+    definition is within 2^-21 (plus one binary32 rounding) of the exact mean and
+    does not depend on the token order."""
+    rng = np.random.default_rng(7)
+    y = (rng.standard_normal((3001, 128)) * rng.uniform(0.01, 40, 128)).astype(np.float32)
+    mu = ora.mean_fixed(y)
+    exact = np.array([math.fsum(y[:, c].astype(np.float64)) / y.shape[0] for c in range(128)])
+    err = np.abs(mu.astype(np.float64) - exact)
+    assert np.all(err <= 2.0 ** -21 + np.abs(exact) * 2.0 ** -24)
+    perm = rng.permutation(y.shape[0])
+    assert np.array_equal(ora.mean_fixed(y[perm]).view(np.uint32), mu.view(np.uint32))
+    # clamp: values beyond 2^12 count as 2^12 in the mean
+    big = np.zeros((4, 128), np.float32)
+    big[0, 0] = 1e9
+    assert ora.mean_fixed(big)[0] == np.float32(4096.0 / 4)
+
+
+def test_k_smoothing_leaves_softmax_unchanged(ora):
+    """Sec. 4: subtracting a per-channel mean from K adds a per-query constant to
+    every score of that query, which softmax removes (exact in fp64)."""
+    rng = np.random.default_rng(8)
+    q, k, v = (rng.standard_normal((64, 128)) for _ in range(3))
+    mu = k.mean(0)
+    O1 = ora.attn_ref_f64(q, k, v)
+    O2 = ora.attn_ref_f64(q, k - mu, v)
+    np.testing.assert_allclose(O1, O2, atol=1e-12)
+    # V smoothing with add-back: rows of softmax sum to one
+    muv = v.mean(0)
+    O3 = ora.attn_ref_f64(q, k, v - muv) + muv
+    np.testing.assert_allclose(O1, O3, atol=1e-12)
+
+
+def test_v_hadamard_commutes_with_smoothing():
+    """Sec. 4.3 (V Hadamard folded into W_v, W_o): (V - 1 mu^T) H = V H - 1 (mu H)^T, and
+    softmax(S) V H H^T = softmax(S) V (H orthogonal)."""
+    g = _load("paper_constants.json")["H4_from_kronecker"]
+    H4 = np.array(g["matrix_unscaled"], float) / 2.0
+    H2 = np.array([[1, 1], [1, -1]]) / math.sqrt(2)
+    np.testing.assert_allclose(np.kron(H2, H2), H4, atol=1e-15)
+    H = H2
+    for _ in range(6):
+        H = np.kron(H2, H)
+    np.testing.assert_allclose(H @ H.T, np.eye(128), atol=1e-12)
+    rng = np.random.default_rng(9)
+    V = rng.standard_normal((50, 128))
+    mu = V.mean(0)
+    np.testing.assert_allclose((V - mu) @ H, V @ H - mu @ H, atol=1e-12)
+
+
+# ---------------------------------------------------------- quantization ----
+
+def test_quant_handworked(ora):
+    """Sec. 5.1 symmetric INT4 quantization on hand-worked groups (tests/golden)."""
+    for case in _load("quant_handworked.json")["cases"]:
+        z = np.array(case["z"], np.float32)
+        Dpad = np.zeros((1, 128), np.float32)
+        Dpad[0, :len(z)] = z
+        codes, scales = ora.quant_tokens(Dpad, 1)
+        assert scales[0] == np.float32(case["scale"])
+        assert codes[0, :len(z)].tolist() == case["codes"]
+
+
+@pytest.mark.parametrize("g", [1, 16, 128, 300])
+def test_quant_token_properties(ora, g):
+    """Codes lie in [-7, 7]; the abs-max element maps to +-7; the reconstruction
+    error is at most half a step; groups are g consecutive tokens, last one ragged."""
+    rng = np.random.default_rng(10)
+    N = 300
+    z = (rng.standard_normal((N, 128)) * rng.uniform(0.1, 30, (N, 1))).astype(np.float32)
+    codes, scales = ora.quant_tokens(z, g)
+    assert codes.min() >= -7 and codes.max() <= 7
+    assert len(scales) == -(-N // g)
+    for gi in range(len(scales)):
+        blk = z[gi * g:(gi + 1) * g]
+        amax = np.abs(blk).max()
+        assert scales[gi] == np.float32(amax / np.float32(7.0))
+        cb = codes[gi * g:(gi + 1) * g]
+        i = np.unravel_index(np.abs(blk).argmax(), blk.shape)
+        assert abs(int(cb[i])) == 7
+        err = np.abs(blk.astype(np.float64) - scales[gi] * cb.astype(np.float64))
+        assert err.max() <= scales[gi] * 0.5 * (1 + 1e-5)
+
+
+def test_quant_lossless_on_grid(ora):
+    """Inputs already on the INT4 grid (z = s * code) are recovered exactly."""
+    rng = np.random.default_rng(11)
+    codes = rng.integers(-7, 8, (40, 128)).astype(np.int8)
+    codes[:, 0] = 7
+    s = np.float32(0.25)
+    z = (codes.astype(np.float32) * s).astype(np.float32)
+    c2, sc = ora.quant_tokens(z, 1)
+    assert np.array_equal(c2, codes) and np.all(sc == np.float32(1.75 / 7))
+
+
+def test_quant_v_groups_per_channel(ora):
+    """Sec. 5.1 per-group V: one scale per (g tokens, channel)."""
+    rng = np.random.default_rng(12)
+    N, g = 333, 128
+    z = (rng.standard_normal((N, 128)) * rng.uniform(0.1, 10, 128)).astype(np.float32)
+    codes, scales = ora.quant_v(z, g)
+    assert scales.shape == (3, 128)
+    for gi in range(3):
+        blk = z[gi * g:(gi + 1) * g]
+        np.testing.assert_array_equal(scales[gi], (np.abs(blk).max(0) / np.float32(7)).astype(np.float32))
+        assert np.all(np.abs(codes[gi * g:(gi + 1) * g]).max(0) == 7)
+    z0 = np.zeros((10, 128), np.float32)
+    c0, s0 = ora.quant_v(z0, 4)
+    assert not c0.any() and not s0.any()
+
+
+# ---------------------------------------------------------------- scores ----
+
+def _attn(ora, qc, qs, kc, ks, vc, vs, mu=None, **kw):
+    base = dict(q_group=1, k_group=1, v_group=kc.shape[0], kv_block=64)
+    base.update(kw)
+    return ora.attn_int4(qc, qs, kc, ks, vc, vs, mu, dumps=True, **base)
+
+
+def test_s_int_closed_forms(ora):
+    """S = Q~ K~^T on codes: all +7 against all +-7 reaches the bound 128*49 = 6272;
+    one-hot codes give the single product."""
+    N = 40
+    qc = np.full((N, 128), 7, np.int8)
+    kc = np.full((N, 128), 7, np.int8)
+    kc[1::2] = -7
+    one = np.ones(N, np.float32)
+    vc = np.zeros((N, 128), np.int8)
+    _, d = _attn(ora, qc, one, kc, one, vc, np.ones((1, 128), np.float32))
+    assert np.all(d["S"][:, 0::2] == 6272) and np.all(d["S"][:, 1::2] == -6272)
+    qc = np.zeros((N, 128), np.int8)
+    kc = np.zeros((N, 128), np.int8)
+    for n in range(N):
+        qc[n, n % 128] = (n % 13) - 6
+        kc[n, (3 * n) % 128] = (n % 7) - 3
+    _, d = _attn(ora, qc, one, kc, one, vc, np.ones((1, 128), np.float32))
+    for i in range(N):
+        for j in range(N):
+            expect = int(qc[i, i % 128]) * int(kc[j, (3 * j) % 128]) if i % 128 == (3 * j) % 128 else 0
+            assert d["S"][i, j] == expect
+
+
+# ------------------------------------------------------- P quantization ----
+
+def test_pcode_thresholds_and_levels(ora):
+    """Sec. 4.2.1 affine mapping: u = P~ + 8 = round(15 P) changes value at
+    P = (k - 1/2)/15, i.e. x = log2((k - 1/2)/15); P = 1 gives P~ = 7 and P -> 0
+    gives P~ = -8.  16 levels against 8 for the symmetric mapping."""
+    c = _load("paper_constants.json")["p_ranges"]
+    L = ora.lib()
+    for k in range(1, 16):
+        xk = math.log2((k - 0.5) / 15)
+        above = L.ora_pcode(L.ora_exp2_f32(xk + 1e-4), ora.PQ_RANGE15)
+        below = L.ora_pcode(L.ora_exp2_f32(xk - 1e-4), ora.PQ_RANGE15)
+        assert (above, below) == (k, k - 1)
+    assert L.ora_pcode(1.0, ora.PQ_RANGE15) - 8 == c["range_max_code"]
+    assert L.ora_pcode(1e-30, ora.PQ_RANGE15) - 8 == c["range_min_code"]
+    assert L.ora_pcode(1.0, ora.PQ_SYM7) == c["sym_max"]
+    P = np.linspace(1e-6, 1.0, 20001).astype(np.float32)
+    lv15 = {L.ora_pcode(float(p), ora.PQ_RANGE15) for p in P}
+    lv7 = {L.ora_pcode(float(p), ora.PQ_SYM7) for p in P}
+    assert len(lv15) == c["range_levels"] and len(lv7) == c["sym_levels"]
+    # monotone
+    u = [L.ora_pcode(float(p), ora.PQ_RANGE15) for p in P]
+    assert all(a <= b for a, b in zip(u, u[1:]))
+
+
+def _int4_inputs(rng, N, outl=True):
+    qc = rng.integers(-7, 8, (N, 128)).astype(np.int8)
+    kc = rng.integers(-7, 8, (N, 128)).astype(np.int8)
+    vc = rng.integers(-7, 8, (N, 128)).astype(np.int8)
+    qs = rng.uniform(0.05, 0.4, N).astype(np.float32)
+    ks = rng.uniform(0.05, 0.4, N).astype(np.float32)
+    return qc, qs, kc, ks, vc
+
+
+@pytest.mark.parametrize("kv", [32, 64, 128, 500])
+def test_equal_scores_give_mean_of_v(ora, kv):
+    """Sec. 4.2: equal scores give P = 1 everywhere, hence u = 15 (P~ = 7) and O is the
+    mean of the dequantized V plus the smoothing mean, for any block size."""
+    rng = np.random.default_rng(13)
+    N = 500
+    _, _, kc, ks, vc = _int4_inputs(rng, N)
+    qc = np.zeros((N, 128), np.int8)
+    qs = np.ones(N, np.float32)
+    vs = rng.uniform(0.1, 1.0, (4, 128)).astype(np.float32)
+    mu = rng.standard_normal(128).astype(np.float32)
+    O, d = _attn(ora, qc, qs, kc, ks, vc, vs, mu, v_group=128, kv_block=kv)
+    assert np.all(d["u"] == 15)
+    deq = vc.astype(np.float64) * (vs.astype(np.float32) / np.float32(15)).astype(np.float64)[np.arange(N) // 128] * 15
+    expect = deq.mean(0) + mu
+    np.testing.assert_allclose(O, np.broadcast_to(expect, O.shape), rtol=1e-12, atol=1e-12)
+
+
+@pytest.mark.parametrize("kv,vg", [(1, 1), (32, 32), (64, 128), (128, 128), (700, 700)])
+def test_online_softmax_without_p_rounding_is_softmax(ora, kv, vg):
+    """Sec. 4.2 (FlashAttention blockwise scores): with the P rounding switched off
+    the blockwise result equals the one-shot softmax of the dequantized scores, for
+    every block size (brute force, different route)."""
+    rng = np.random.default_rng(14)
+    N = 700
+    qc, qs, kc, ks, vc = _int4_inputs(rng, N)
+    vs = rng.uniform(0.1, 1.0, (-(-N // vg), 128)).astype(np.float32)
+    O, _ = _attn(ora, qc, qs, kc, ks, vc, vs, None, v_group=vg, kv_block=kv, p_quant=ora.PQ_NONE)
+    S = (qc.astype(np.float64) * qs[:, None]) @ (kc.astype(np.float64) * ks[:, None]).T / math.sqrt(128)
+    P = np.exp(S - S.max(1, keepdims=True))
+    V = vc.astype(np.float64) * vs.astype(np.float64)[np.arange(N) // vg]
+    ref = (P @ V) / P.sum(1, keepdims=True)
+    assert np.abs(O - ref).max() <= 1e-5 * np.abs(ref).max()
+
+
+@pytest.mark.parametrize("kv,qg,kg", [(32, 1, 1), (64, 16, 64), (128, 7, 32)])
+def test_online_softmax_prefix_max_restatement(ora, kv, qg, kg):
+    """Sec. 4.2: m_ij = max(m_{i,j-1}, rowmax S_ij) and P_ij = exp(S_ij - m_ij). Written
+    without rescaling: key n of block j enters with weight u_n 2^(m_j - m_last) and
+    P_n 2^(m_j - m_last) in the normaliser.  Checked against the oracle's online form,
+    m checked bit for bit against the prefix maximum, u against round(15 * 2^x).
+    Q and K scale groups differ so that a swapped group index shows."""
+    rng = np.random.default_rng(15)
+    N = 613
+    qc, _, kc, _, vc = _int4_inputs(rng, N)
+    qs = rng.uniform(0.05, 0.4, -(-N // qg)).astype(np.float32)
+    ks = rng.uniform(0.05, 0.4, -(-N // kg)).astype(np.float32)
+    vg = kv
+    vs = rng.uniform(0.1, 1.0, (-(-N // vg), 128)).astype(np.float32)
+    mu = rng.standard_normal(128).astype(np.float32)
+    O, d = _attn(ora, qc, qs, kc, ks, vc, vs, mu, v_group=vg, kv_block=kv, q_group=qg, k_group=kg)
+    S = qc.astype(np.int64) @ kc.astype(np.int64).T
+    assert np.array_equal(S, d["S"].astype(np.int64))
+    Kc = np.float32(1 / math.sqrt(128) * math.log2(math.e))
+    cq = (qs * Kc).astype(np.float32)[np.arange(N) // qg]
+    c = (cq[:, None] * ks[np.arange(N) // kg][None, :]).astype(np.float32)   # binary32 products
+    t = (S.astype(np.float32) * c).astype(np.float32)
+    nb = -(-N // kv)
+    bm = np.stack([t[:, j * kv:(j + 1) * kv].max(1) for j in range(nb)], 1)
+    m = np.maximum.accumulate(bm, axis=1)
+    assert np.array_equal(m.view(np.uint32), d["m"].view(np.uint32))
+    blk = np.arange(N) // kv
+    x = d["x"].astype(np.float64)
+    # x is the binary32 value of S*c - m_j (single rounding)
+    exact = S.astype(np.float64) * c.astype(np.float64) - m[:, blk].astype(np.float64)
+    assert np.all(np.abs(x - exact) <= np.abs(exact) * 2.0 ** -24 + 1e-45)
+    u_exact = np.clip(np.round(15 * np.exp2(x)), 0, 15)
+    tie = np.abs(15 * np.exp2(x) - np.floor(15 * np.exp2(x)) - 0.5) < 1e-6
+    assert np.all((u_exact == d["u"]) | tie)
+    w = np.exp2(m[:, blk].astype(np.float64) - m[:, -1:].astype(np.float64))
+    P = np.exp2(x)
+    dq = (vs / np.float32(15)).astype(np.float32).astype(np.float64)[np.arange(N) // vg]
+    V = vc.astype(np.float64) * dq
+    ref = ((d["u"].astype(np.float64) * w) @ V) / (P * w).sum(1, keepdims=True) + mu
+    assert np.abs(O - ref).max() <= 1e-6 * np.abs(ref).max()
+
+
+def test_dominant_first_key_makes_block_size_irrelevant(ora):
+    """When the first key holds every row's maximum, m never changes, all
+    rescale factors are 1 and the result cannot depend on the block size."""
+    rng = np.random.default_rng(16)
+    N = 777
+    qc, qs, kc, ks, vc = _int4_inputs(rng, N)
+    qc[:, :] = np.abs(qc)
+    kc[0, :] = 7
+    ks[0] = 5.0
+    vs = rng.uniform(0.1, 1.0, (1, 128)).astype(np.float32)
+    outs = [_attn(ora, qc, qs, kc, ks, vc, vs, None, v_group=N, kv_block=kv)[0] for kv in (32, 64, 128, 777)]
+    for o in outs[1:]:
+        np.testing.assert_allclose(o, outs[0], rtol=1e-12, atol=1e-14)
+
+
+def test_sym7_uses_eight_levels(ora):
+    """Sec. 4.2.1 baseline: the symmetric mapping only reaches codes 0..7."""
+    rng = np.random.default_rng(17)
+    N = 512
+    qc, qs, kc, ks, vc = _int4_inputs(rng, N)
+    vs = np.ones((1, 128), np.float32)
+    _, d7 = _attn(ora, qc, qs, kc, ks, vc, vs, None, v_group=N, p_quant=ora.PQ_SYM7)
+    _, d15 = _attn(ora, qc, qs, kc, ks, vc, vs, None, v_group=N)
+    assert d7["u"].max() == 7 and len(np.unique(d7["u"])) == 8
+    assert d15["u"].max() == 15 and len(np.unique(d15["u"])) == 16
+
+
+# --------------------------------------------------------- references ----
+
+def test_ref_f64_is_softmax_bruteforce(ora):
+    """Plain softmax attention on a tiny case, computed by a different route."""
+    rng = np.random.default_rng(18)
+    q, k, v = (rng.standard_normal((9, 128)) for _ in range(3))
+    O = ora.attn_ref_f64(q, k, v)
+    for i in range(9):
+        s = [sum(q[i, c] * k[j, c] for c in range(128)) / math.sqrt(128) for j in range(9)]
+        e = [math.exp(t - max(s)) for t in s]
+        for c in (0, 77, 127):
+            assert abs(O[i, c] - sum(e[j] * v[j, c] for j in range(9)) / sum(e)) < 1e-12
+
+
+def test_bf16_fallback_semantics(ora):
+    """Fallback: equal scores give the plain mean of V exactly (P = 1 is exact in
+    bf16); otherwise the result is softmax attention up to bf16 rounding of P."""
+    rng = np.random.default_rng(19)
+    N = 300
+    from paper_2607_02584_amd.datagen import bf16_bits_to_f32
+    kb = _rand_bits(rng, (N, 128))
+    vb = _rand_bits(rng, (N, 128))
+    qb = np.zeros((N, 128), np.uint16)
+    O = ora.attn_bf16(qb, kb, vb, kv_block=64)
+    np.testing.assert_allclose(O, np.broadcast_to(bf16_bits_to_f32(vb).astype(np.float64).mean(0), O.shape),
+                               rtol=1e-13, atol=1e-13)
+    qb = _rand_bits(rng, (N, 128))
+    for kv in (32, 128):
+        O = ora.attn_bf16(qb, kb, vb, kv_block=kv)
+        ref = ora.attn_ref_f64(bf16_bits_to_f32(qb), bf16_bits_to_f32(kb), bf16_bits_to_f32(vb))
+        assert np.abs(O - ref).max() <= 2e-3 * np.abs(ref).max()
+
+
+def test_int4_pipeline_tracks_fp64_attention(ora):
+    """Whole INT4 oracle pipeline against fp64 attention (cosine).  On diffuse
+    Gaussian scores the Range-optimized P mapping is clearly more accurate than
+    the symmetric one (the paper's Sec. 5.4 analysis for high-entropy P); on the
+    tiny outlier workload every rotation stays well correlated."""
+    from paper_2607_02584_amd import datagen as dg
+
+    def cos(a, b):
+        return float((a * b).sum() / np.linalg.norm(a) / np.linalg.norm(b))
+    geo = ora.Geometry(4, 16, 16)
+    rng = np.random.default_rng(3)
+    q, k, v = (dg.f32_to_bf16_bits(rng.standard_normal((1024, 128)).astype(np.float32)) for _ in range(3))
+    ref = ora.ref_head(geo, q, k, v)
+    for rot in (0, 1, 2):
+        O15, _ = ora.fwd_int4_head(geo, ora.Int4Config(rotation=rot, q_group=1, k_group=1), q, k, v)
+        O7, _ = ora.fwd_int4_head(geo, ora.Int4Config(rotation=rot, q_group=1, k_group=1, p_quant=ora.PQ_SYM7),
+                                  q, k, v)
+        assert cos(O15, ref) > 0.95
+        assert np.linalg.norm(O15 - ref) < 0.85 * np.linalg.norm(O7 - ref)
+    w = dg.WORKLOADS["c1"]
+    q, k, v = dg.make_inputs(w)
+    geo = ora.Geometry(w.T, w.Hg, w.W, w.split, w.theta)
+    ref = ora.ref_head(geo, q[0, 0], k[0, 0], v[0, 0])
+    for rot in (0, 1, 2):
+        O, _ = ora.fwd_int4_head(geo, ora.Int4Config(rotation=rot, q_group=1, k_group=1), q[0, 0], k[0, 0], v[0, 0])
+        assert cos(O, ref) > 0.8

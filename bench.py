@@ -1,0 +1,188 @@
+"""Benchmark of the INT4 RotateAttention forward on one MI355X.
+
+One step = the whole INT4 hot path over one batch: Q/K producer (3D RoPE +
+merged interleaved rotation + K smoothing + per-block INT4 quantization), V
+producer (smoothing + per-group INT4), and the INT4 attention kernel, on the
+32760-token video-DiT layer (B=1, H=12, grid 21x30x52, d=128), inputs resident
+in HBM.  value = effective TOPS = 4*B*H*N^2*d / step time.
+
+Also measured in the same run: the attention kernel alone (HIP events around
+its launch inside every timed step), the BF16 fallback (producer + kernel),
+and the CPU oracle on a bounded sample of the same workload.
+"""
+from __future__ import annotations
+
+import argparse
+import json
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+if ROOT not in sys.path:
+    sys.path.insert(0, ROOT)
+
+INT8_PEAK_TOPS = 5000.0   # MI355X dense int8 matrix-core peak (published)
+BF16_PEAK_TFLOPS = 2500.0
+HBM_PEAK_GBS = 8000.0
+
+
+def parse():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=20)
+    ap.add_argument("--warmup", type=int, default=3)
+    ap.add_argument("--workload", default="c2")
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--cpu-seconds", type=float, default=12.0)
+    ap.add_argument("--skip-fallback", action="store_true")
+    return ap.parse_args()
+
+
+def log(*a):
+    print("[bench]", *a, file=sys.stderr, flush=True)
+
+
+def main():
+    args = parse()
+    if args.gpus != 1:
+        print(json.dumps({"error": "this build runs on one GPU only; --gpus must be 1 (the path shards by head "
+                                   "with no communication, see the design notes)"}))
+        sys.exit(2)
+    import numpy as np
+    import torch
+
+    from paper_2607_02584_amd import datagen as dg
+    from paper_2607_02584_amd import rotate_attn as ra
+
+    assert torch.cuda.is_available(), "bench needs a GPU"
+    dev = torch.device("cuda:0")
+    w = dg.WORKLOADS[args.workload]
+    BH, N = w.B * w.H, w.N
+    log(f"workload {w.name}: {w.desc}; generating inputs")
+    q, k, v = dg.make_inputs(w)
+    qd, kd, vd = (ra.to_device_bits(x, dev) for x in (q, k, v))
+    p = ra.make_params(w.B, w.H, (w.T, w.Hg, w.W), w.split, w.theta, rotation=ra.ROT_INTERLEAVED,
+                       q_group=128, k_group=128, v_group=128, kv_block=128, out_dtype=ra.BF16)
+    bufs = ra.alloc_int4(p, dev)
+    ws = ra.workspace(p, ra.PATH_INT4, dev)
+    o = torch.empty((BH, N, 128), dtype=torch.bfloat16, device=dev)
+    stream = torch.cuda.current_stream()
+
+    def step(ev=None):
+        ra.quantize_qk(p, qd, kd, bufs["q_codes"], bufs["q_scale"], bufs["k_codes"], bufs["k_scale"],
+                       bufs["mu_k"], ws)
+        ra.quantize_v(p, vd, bufs["v_codes"], bufs["v_scale"], bufs["mu_v"], ws)
+        if ev is not None:
+            ev[0].record(stream)
+        ra.attn_int4(p, bufs["q_codes"], bufs["q_scale"], bufs["k_codes"], bufs["k_scale"], bufs["v_codes"],
+                     bufs["v_scale"], bufs["mu_v"], o)
+        if ev is not None:
+            ev[1].record(stream)
+
+    for _ in range(args.warmup):
+        step()
+    torch.cuda.synchronize()
+    log(f"warmup done; timing {args.steps} steps")
+    evs = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)) for _ in range(args.steps)]
+    t0 = torch.cuda.Event(enable_timing=True)
+    t1 = torch.cuda.Event(enable_timing=True)
+    torch.cuda.synchronize()
+    t0.record(stream)
+    for i in range(args.steps):
+        step(evs[i])
+    t1.record(stream)
+    torch.cuda.synchronize()
+    ms_step = t0.elapsed_time(t1) / args.steps
+    attn_ms = float(np.mean([a.elapsed_time(b) for a, b in evs]))
+    ops = w.ops()
+    tops = ops / (ms_step * 1e-3) / 1e12
+    attn_tops = ops / (attn_ms * 1e-3) / 1e12
+    log(f"int4 step {ms_step:.3f} ms ({tops:.1f} TOPS); attention kernel {attn_ms:.3f} ms ({attn_tops:.1f} TOPS)")
+
+    extra = {}
+    if not args.skip_fallback:
+        pf = ra.make_params(w.B, w.H, (w.T, w.Hg, w.W), w.split, w.theta, rotation=ra.ROT_NONE, out_dtype=ra.BF16)
+        wsf = ra.workspace(pf, ra.PATH_FP16, dev)
+        of = torch.empty_like(o)
+        for _ in range(2):
+            ra.fwd_fp16(pf, qd, kd, vd, of, wsf)
+        torch.cuda.synchronize()
+        nrep = max(3, args.steps // 2)
+        e = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)) for _ in range(nrep)]
+        a0 = torch.cuda.Event(enable_timing=True)
+        a1 = torch.cuda.Event(enable_timing=True)
+        a0.record(stream)
+        for i in range(nrep):
+            ra.prepare_fp16(pf, qd, kd, vd, wsf)
+            e[i][0].record(stream)
+            ra.attn_fp16(pf, wsf, of)
+            e[i][1].record(stream)
+        a1.record(stream)
+        torch.cuda.synchronize()
+        f_step = a0.elapsed_time(a1) / nrep
+        f_attn = float(np.mean([x.elapsed_time(y) for x, y in e]))
+        extra = {
+            "bf16_fallback": {"op_ms": round(f_step, 4), "kernel_ms": round(f_attn, 4),
+                              "kernel_tflops": round(ops / (f_attn * 1e-3) / 1e12, 1),
+                              "kernel_frac_of_bf16_peak": round(ops / (f_attn * 1e-3) / 1e12 / BF16_PEAK_TFLOPS, 4)},
+            "speedup_vs_bf16": {"kernel": round(f_attn / attn_ms, 3), "op": round(f_step / ms_step, 3)},
+        }
+        log(f"bf16 fallback op {f_step:.3f} ms, kernel {f_attn:.3f} ms; speedup kernel {f_attn / attn_ms:.2f}x")
+
+    cpu = None
+    if not args.no_cpu_baseline:
+        cpu = cpu_baseline(w, q, k, v, args.cpu_seconds)
+
+    line = {
+        "metric": "effective attention TOPS (4*B*H*N^2*d / time), INT4 RotateAttention forward, 32760-token DiT shape",
+        "value": round(tops, 2),
+        "unit": "TOPS",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": round(ms_step, 4),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "int4",
+        "data": "synthetic",
+        "config": {"workload": f"{w.name}: B={w.B} H={w.H} grid {w.T}x{w.Hg}x{w.W} (N={N}) d=128 split "
+                               f"{'/'.join(map(str, w.split))} theta={w.theta:g}, interleaved rotation, "
+                               f"Q/K/V groups 128, kv_block 128, RANGE15 P, bf16 in/out",
+                   "parallelism": "single GPU"},
+        "roofline": {"bound": "mfma", "kernel": "k_attn_int4", "achieved": round(attn_tops, 2),
+                     "peak": INT8_PEAK_TOPS, "unit": "TOPS", "frac": round(attn_tops / INT8_PEAK_TOPS, 4),
+                     "traffic": None},
+        "cpu_baseline": cpu,
+    }
+    line.update(extra)
+    print(json.dumps(line), flush=True)
+
+
+def cpu_baseline(w, q, k, v, seconds):
+    """The oracle (plain C, every host thread) on a bounded sample: one head,
+    its full producer pass, then query rows in blocks of 256 until about
+    `seconds` of attention work; TOPS counted as 4*rows*N*d / wall time."""
+    import oracle as ora
+    geo = ora.Geometry(w.T, w.Hg, w.W, w.split, w.theta)
+    cfg = ora.Int4Config()
+    t = time.perf_counter()
+    qk = ora.quantize_qk_head(geo, cfg, q[0, 0], k[0, 0])
+    vv = ora.quantize_v_head(cfg, v[0, 0])
+    rows = 0
+    while rows < w.N and time.perf_counter() - t < seconds:
+        nr = min(256, w.N - rows)
+        ora.attn_int4(qk["q_codes"], qk["q_scale"], qk["k_codes"], qk["k_scale"], vv["v_codes"], vv["v_scale"],
+                      vv["mu_v"], q_group=128, k_group=128, v_group=128, kv_block=128, rows=(rows, nr))
+        rows += nr
+    el = time.perf_counter() - t
+    val = 4.0 * rows * w.N * 128 / el / 1e12
+    log(f"cpu oracle: {rows} rows of head 0 in {el:.1f} s on {ora.threads()} threads")
+    return {"value": round(val, 5), "unit": "TOPS", "cores": ora.threads(), "kind": "oracle",
+            "sample": f"head 0 of {w.name}: producer pass over all {w.N} tokens + {rows} query rows against all "
+                      f"{w.N} keys ({el:.1f} s wall)"}
+
+
+if __name__ == "__main__":
+    main()

@@ -1,0 +1,204 @@
+/*
+ * rotate_attn.h -- C ABI of the MI355X (gfx950) INT4 RotateAttention library.
+ *
+ * The library implements the attention hot path of RotateAttention
+ * (Liu et al., "RotateAttention: RoPE-Aware Rotation and Range Rectification
+ * for INT4 Quantized Attention in Video Generation"): 3D RoPE fused with the
+ * RoPE-aware Q/K rotation (Sec. 4.1.2 interleaved/merged, Sec. 4.1.3 half),
+ * smoothing (Sec. 4), INT4 quantization of Q, K and V (Sec. 5.1), the INT4
+ * FlashAttention forward with the Range-optimized P quantization (Sec. 4.2),
+ * and the BF16/FP16 fallback attention used for accuracy-sensitive blocks and
+ * denoising steps (abstract; Sec. 5.1 mixed-precision schedule).
+ *
+ * Conventions shared by every entry point
+ * ---------------------------------------
+ *  - All tensor pointers are DEVICE pointers owned by the caller; the library
+ *    never frees them.  `rot_blocks` in ra_params is a HOST pointer.
+ *  - `stream` is a hipStream_t passed as void* (NULL = default stream).  Every
+ *    call only enqueues work on that stream and returns; results are ready when
+ *    the stream reaches them.  Calls that overlap on one device must use
+ *    distinct workspaces.
+ *  - Inputs q, k, v have layout [B][H][N][D] (token-major rows of D elements),
+ *    dtype ra_params.in_dtype (RA_BF16 or RA_FP16).  Output o has the same
+ *    layout in ra_params.out_dtype (RA_BF16, RA_FP16 or RA_FP32).
+ *  - Only D == 128 is supported (RA_ERR_UNSUPPORTED otherwise).
+ *  - Every entry point validates all arguments before touching the GPU and
+ *    returns RA_OK (0) or a negative RA_ERR_* code; no exception crosses the ABI.
+ *    rotate_attn_last_error() returns a thread-local message for the last
+ *    failure on the calling thread.
+ *  - The library keeps, per device, a small cache of RoPE/rotation tables in
+ *    device memory (allocated on first use of a geometry, never freed before
+ *    process exit).  That first call is therefore synchronous and must not be
+ *    made under HIP graph capture; later calls with the same geometry are not.
+ *  - Results are deterministic: repeated calls give identical bytes.
+ *
+ * Packed INT4 layouts (written by the quantize calls, read by the attention)
+ * ------------------------------------------------------------------------
+ *  Npad = N rounded up to a multiple of 128; tokens n >= N hold zero codes.
+ *  A code is a 4-bit two's-complement nibble in [-7, 7].
+ *
+ *  Q/K codes, per head (Npad * 64 bytes, heads contiguous, head bh at
+ *  bh * Npad * 64): token n = 32*c + r, channel pair j (channels 2j and 2j+1)
+ *  lives in byte ((c*8 + j/8)*32 + r)*8 + (j%8); channel 2j in the low nibble,
+ *  channel 2j+1 in the high nibble.
+ *
+ *  V codes, per head (Npad * 64 bytes): token n = 32*c + kappa, channel ch.
+ *  With a = kappa/16, b = (kappa/8)%2, h = (kappa/4)%2, s = kappa%4, the
+ *  nibble index is np = 8a + 2s + b; the code lives in byte
+ *  ((c*2 + h)*128 + ch)*8 + np/2, low nibble when np is even.
+ *  (This order makes each 32-token chunk an operand of the int8 matrix core.)
+ *
+ *  Scales are binary32.  Q scales: [B*H][Npad/q_group]; K scales:
+ *  [B*H][Npad/k_group]; V scales: [B*H][ceil(N/v_group)][128].  Q/K groups
+ *  that hold no valid token have scale 0.
+ */
+#ifndef ROTATE_ATTN_H
+#define ROTATE_ATTN_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+/* status codes */
+#define RA_OK 0
+#define RA_ERR_INVALID (-1)     /* bad shape, split, grid, group, null pointer */
+#define RA_ERR_UNSUPPORTED (-2) /* valid request this build does not implement */
+#define RA_ERR_WORKSPACE (-3)   /* workspace missing or smaller than required */
+#define RA_ERR_HIP (-4)         /* a HIP runtime call failed (see last_error) */
+
+/* rotation applied to Q and K after 3D RoPE (Sec. 4.1) */
+#define RA_ROT_NONE 0
+#define RA_ROT_INTERLEAVED 1 /* Sec. 4.1.2: blocks on (2i, 2i+1), merged into the RoPE table */
+#define RA_ROT_HALF 2        /* Sec. 4.1.3: pairs (i, i + D_j/2) inside each RoPE segment */
+
+/* quantization of P (Sec. 4.2.1) */
+#define RA_PQ_RANGE15 0 /* affine: fixed scale 15, zero-point -8, 16 levels */
+#define RA_PQ_SYM7 1    /* symmetric baseline: round(7 P), 8 levels */
+
+/* smoothing flags (Sec. 4: biases shared by all tokens) */
+#define RA_SMOOTH_K 1 /* subtract the per-channel mean of rotated K (softmax invariant) */
+#define RA_SMOOTH_V 2 /* subtract the per-channel mean of V, add it back to O */
+
+/* dtypes */
+#define RA_BF16 0
+#define RA_FP16 1
+#define RA_FP32 2
+
+/* which forward a workspace is sized for */
+#define RA_PATH_INT4 0
+#define RA_PATH_FP16 1
+
+typedef struct ra_params {
+  int32_t B, H, N, D;      /* batch, heads, tokens (N == T*Hg*W), head dim (128) */
+  int32_t grid[3];         /* T, Hg, W: token n = (t*Hg + h)*W + w (Sec. 3) */
+  int32_t rope_split[3];   /* D_t, D_h, D_w: each even and > 0, sum == D (Sec. 3) */
+  float rope_theta;        /* RoPE base, e.g. 10000 or 256 */
+  int32_t rotation;        /* RA_ROT_* */
+  const double* rot_blocks;/* host, [D/2][2][2] row-major O(2) blocks; NULL = H_2 (Sec. 4.1) */
+  int32_t p_quant;         /* RA_PQ_* */
+  int32_t smooth;          /* RA_SMOOTH_* bitmask */
+  int32_t q_group;         /* tokens per Q scale: 1 (per-token) .. 128, must divide 128 */
+  int32_t k_group;         /* tokens per K scale: 1, 32, 64 or 128 */
+  int32_t v_group;         /* tokens per V scale (per channel): a multiple of kv_block, or >= N */
+  int32_t kv_block;        /* online-softmax block: 64 or 128 (fixes the P semantics) */
+  float sm_scale;          /* softmax scale; 0 = 1/sqrt(D) */
+  int32_t in_dtype;        /* RA_BF16 | RA_FP16 */
+  int32_t out_dtype;       /* RA_BF16 | RA_FP16 | RA_FP32 */
+} ra_params;
+
+/* Sizes of the caller-visible INT4 buffers for these parameters. */
+typedef struct ra_layout {
+  int64_t n_pad;          /* Npad */
+  int64_t qk_code_bytes;  /* bytes of ONE of q_codes / k_codes (all heads) */
+  int64_t q_scale_count;  /* floats in q_scale */
+  int64_t k_scale_count;  /* floats in k_scale */
+  int64_t v_code_bytes;   /* bytes of v_codes */
+  int64_t v_scale_count;  /* floats in v_scale */
+  int64_t mu_count;       /* floats in mu_k / mu_v: B*H*D */
+} ra_layout;
+
+/* Fills *out; RA_ERR_INVALID / RA_ERR_UNSUPPORTED on bad parameters. */
+int rotate_attn_layout(const ra_params* p, ra_layout* out);
+
+/* Workspace bytes needed by the calls of `path` (RA_PATH_INT4 covers
+ * quantize_qk, quantize_v, attn_int4 and fwd_int4; RA_PATH_FP16 covers
+ * fwd_fp16).  The workspace is device memory, 256-byte aligned, owned by the
+ * caller and reused by every call; its content between calls is irrelevant. */
+int rotate_attn_workspace_size(const ra_params* p, int path, size_t* bytes);
+
+/* Producer for Q and K (Sec. 3, 4, 4.1, 5.1): 3D RoPE and the chosen rotation,
+ * K smoothing (if RA_SMOOTH_K), per-group INT4 quantization, nibble packing.
+ * q, k: inputs [B][H][N][D].  q_codes/k_codes: ra_layout.qk_code_bytes each;
+ * q_scale/k_scale: ra_layout.q_scale_count / k_scale_count floats.
+ * mu_k: nullable, receives the K smoothing mean [B*H][D] (zeros if smoothing
+ * is off).  Q is never smoothed. */
+int rotate_attn_quantize_qk(const ra_params* p, const void* q, const void* k, uint8_t* q_codes,
+                            float* q_scale, uint8_t* k_codes, float* k_scale, float* mu_k,
+                            void* workspace, size_t workspace_bytes, void* stream);
+
+/* Producer for V (Sec. 4.3, 5.1): V is taken as given (a Hadamard rotation of
+ * V is folded into W_v/W_o offline), smoothed (if RA_SMOOTH_V) and quantized
+ * per (v_group tokens, channel).  mu_v: nullable, receives the V mean [B*H][D]
+ * that the attention adds back (zeros if smoothing is off). */
+int rotate_attn_quantize_v(const ra_params* p, const void* v, uint8_t* v_codes, float* v_scale,
+                           float* mu_v, void* workspace, size_t workspace_bytes, void* stream);
+
+/* INT4 attention on already quantized operands (Sec. 4.2): S = Q~ K~^T on the
+ * int8 matrix cores (exact int32), blockwise online softmax with blocks of
+ * kv_block keys in ascending order, P mapped to the unsigned code
+ * u = round(15 P) in [0, 15] (the affine code P~ = u - 8), PV on the codes,
+ * O = (sum of dequantized PV) / l + mu_v, l = sum of the unquantized P.
+ * mu_v: nullable (treated as zeros).  o: [B][H][N][D] in out_dtype. */
+int rotate_attn_attn_int4(const ra_params* p, const uint8_t* q_codes, const float* q_scale,
+                          const uint8_t* k_codes, const float* k_scale, const uint8_t* v_codes,
+                          const float* v_scale, const float* mu_v, void* o, void* stream);
+
+/* Debug variant of rotate_attn_attn_int4: runs the same kernel with a dump
+ * enabled for the query rows [row0, row0 + rows) of head bh:
+ *   s_out [rows][N] int32  exact S = Q~ . K~
+ *   u_out [rows][N] uint8  P codes u in [0, 15]
+ *   m_out [rows][ceil(N/kv_block)] binary32 running maximum after each block
+ * (all device pointers, any may be NULL).  o receives the same output as the
+ * plain call. */
+int rotate_attn_attn_int4_debug(const ra_params* p, const uint8_t* q_codes, const float* q_scale,
+                                const uint8_t* k_codes, const float* k_scale,
+                                const uint8_t* v_codes, const float* v_scale, const float* mu_v,
+                                void* o, int32_t bh, int32_t row0, int32_t rows, int32_t* s_out,
+                                uint8_t* u_out, float* m_out, void* stream);
+
+/* Whole INT4 forward: quantize_qk + quantize_v + attn_int4, codes kept in the
+ * workspace (size RA_PATH_INT4). */
+int rotate_attn_fwd_int4(const ra_params* p, const void* q, const void* k, const void* v, void* o,
+                         void* workspace, size_t workspace_bytes, void* stream);
+
+/* Producer of the fallback: plain 3D RoPE (no rotation, no smoothing) of Q and
+ * K rounded to in_dtype, and V re-laid out for the matrix cores, into the
+ * workspace (size RA_PATH_FP16). */
+int rotate_attn_prepare_fp16(const ra_params* p, const void* q, const void* k, const void* v,
+                             void* workspace, size_t workspace_bytes, void* stream);
+
+/* Fallback attention kernel alone on a workspace filled by prepare_fp16:
+ * 16-bit matrix cores, online softmax with blocks of kv_block keys, P rounded
+ * to in_dtype before PV, l from the unrounded P. */
+int rotate_attn_attn_fp16(const ra_params* p, const void* workspace, size_t workspace_bytes, void* o,
+                          void* stream);
+
+/* Whole fallback forward: prepare_fp16 + attn_fp16. */
+int rotate_attn_fwd_fp16(const ra_params* p, const void* q, const void* k, const void* v, void* o,
+                         void* workspace, size_t workspace_bytes, void* stream);
+
+/* Mixed-precision dispatch (abstract; Sec. 5.1 schedule): fallback != 0 runs
+ * fwd_fp16, otherwise fwd_int4.  The workspace must fit the chosen path. */
+int rotate_attn_fwd(const ra_params* p, int fallback, const void* q, const void* k, const void* v,
+                    void* o, void* workspace, size_t workspace_bytes, void* stream);
+
+const char* rotate_attn_error_string(int status);
+const char* rotate_attn_last_error(void);
+
+#ifdef __cplusplus
+}
+#endif
+#endif /* ROTATE_ATTN_H */

@@ -1,0 +1,333 @@
+// ra_attn_int4.hip -- INT4 FlashAttention forward for gfx950 (CDNA4).
+//
+// Computes, per head and query row i, the blockwise online softmax of the
+// paper's Sec. 4.2 over blocks of KV keys in ascending order:
+//   S_ij   = Q~_i K~_j^T                      (exact int32 on the i8 matrix core)
+//   m_ij   = max(m_i,j-1, rowmax fl(S * c)),  c = fl(fl(s_q * Kc) * s_k)
+//   x      = fma(S, c, -m_ij),  P = 2^x       (Kc folds 1/sqrt(D) and log2 e)
+//   u      = round(15 P) in [0, 15]           (Range-optimized P, Sec. 4.2.1:
+//                                              P~ = u - 8, fixed scale 15)
+//   l      = alpha * l + sum P,  alpha = 2^(m_i,j-1 - m_ij)
+//   O      = alpha * O + sum_g fl(s_v[g]/15) * (u . V~)
+// and writes O / l + mu_v.
+//
+// Matrix-core mapping (v_mfma_i32_32x32x32_i8, one wave = 32 queries):
+//   S^T = K Q^T : A = K tile (32 keys x 32 channels), B = Q^T, so every lane
+//                 holds 16 keys of ONE query: the row max and sum need no
+//                 cross-lane work except one exchange between the wave halves.
+//   O^T = V^T P^T: B = P^T comes straight from the S^T accumulator lanes (the
+//                 P codes of a lane are the B operand of that lane), A = V^T
+//                 read from LDS; the V codes are stored with the key order the
+//                 accumulator layout implies, so no register shuffle is needed.
+// K and V codes arrive packed (two per byte); a workgroup stages one KV block
+// in LDS, expanding each nibble c to the int8 value 16c with two bit
+// operations per four codes (the factor 16 is folded into the scales, which is
+// exact).  Q is expanded once per wave to plain int8 codes.
+#include "ra_internal.h"
+
+namespace ra {
+namespace {
+
+typedef int v4i __attribute__((ext_vector_type(4)));
+typedef int v16i __attribute__((ext_vector_type(16)));
+
+constexpr int kBlockM = 128;  // queries per workgroup (4 waves x 32)
+
+// nibbles at bits 0-3 of each byte, sign-extended to int8 codes
+__device__ __forceinline__ uint32_t sext_lo(uint32_t w) {
+  const uint32_t u = w & 0x0F0F0F0Fu;
+  return u | ((u & 0x08080808u) * 30u);
+}
+// nibbles at bits 4-7 of each byte, sign-extended to int8 codes
+__device__ __forceinline__ uint32_t sext_hi(uint32_t w) {
+  const uint32_t u = (w >> 4) & 0x0F0F0F0Fu;
+  return u | ((u & 0x08080808u) * 30u);
+}
+
+// 8 packed bytes -> 16 int8 values 16*code, order [lo(w0) hi(w0) lo(w1) hi(w1)]
+__device__ __forceinline__ uint4 expand16(uint2 w) {
+  return make_uint4((w.x << 4) & 0xF0F0F0F0u, w.x & 0xF0F0F0F0u, (w.y << 4) & 0xF0F0F0F0u, w.y & 0xF0F0F0F0u);
+}
+
+template <int KV>
+struct Stage {
+  uint4 k[KV / 64];
+  uint4 v[KV / 64];
+};
+
+template <int KV>
+__device__ __forceinline__ void stage_load(const AttnArgs& a, int bh, int jb, Stage<KV>& st) {
+  const int tid = threadIdx.x;
+  const uint8_t* kb = a.kc + static_cast<size_t>(bh) * a.Npad * 64 + static_cast<size_t>(jb) * KV * 64;
+  const uint8_t* vb = a.vc + static_cast<size_t>(bh) * a.Npad * 64 + static_cast<size_t>(jb) * KV * 64;
+#pragma unroll
+  for (int i = 0; i < KV / 64; ++i) {
+    st.k[i] = *reinterpret_cast<const uint4*>(kb + (i * 256 + tid) * 16);
+    st.v[i] = *reinterpret_cast<const uint4*>(vb + (i * 256 + tid) * 16);
+  }
+}
+
+// LDS int8 offset = 2 x packed offset (each 8-byte unit expands to 16 bytes)
+template <int KV>
+__device__ __forceinline__ void stage_store(const Stage<KV>& st, uint8_t* sk, uint8_t* sv) {
+  const int tid = threadIdx.x;
+#pragma unroll
+  for (int i = 0; i < KV / 64; ++i) {
+    const int o = (i * 256 + tid) * 32;
+    *reinterpret_cast<uint4*>(sk + o) = expand16(make_uint2(st.k[i].x, st.k[i].y));
+    *reinterpret_cast<uint4*>(sk + o + 16) = expand16(make_uint2(st.k[i].z, st.k[i].w));
+    *reinterpret_cast<uint4*>(sv + o) = expand16(make_uint2(st.v[i].x, st.v[i].y));
+    *reinterpret_cast<uint4*>(sv + o + 16) = expand16(make_uint2(st.v[i].z, st.v[i].w));
+  }
+}
+
+template <int KV, bool KTOK, bool SYM7, bool DEBUG>
+__global__ __launch_bounds__(256, 1) void k_attn_int4(AttnArgs a) {
+  constexpr int NCH = KV / 32;
+  __shared__ __align__(16) uint8_t sK[2][KV * 128];
+  __shared__ __align__(16) uint8_t sV[2][KV * 128];
+  __shared__ __align__(16) float sDq[2][kD];
+  __shared__ __align__(16) float sKs[2][KTOK ? KV : 1];
+
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int hh = lane >> 5, j = lane & 31;
+  const int bh = blockIdx.y;
+  const int qrow = blockIdx.x * kBlockM + wave * 32 + j;
+  const int N = a.N;
+  const int nblocks = (N + KV - 1) / KV;
+  const int kstride = a.Npad / a.k_group;
+
+  // ---- Q operand: plain int8 codes in the order of the K expansion ----
+  v4i qop[4];
+  {
+    const uint8_t* qp = a.qc + static_cast<size_t>(bh) * a.Npad * 64 + static_cast<size_t>(qrow >> 5) * 2048 +
+                        (qrow & 31) * 8;
+#pragma unroll
+    for (int kc = 0; kc < 4; ++kc) {
+      const uint2 w = *reinterpret_cast<const uint2*>(qp + (2 * kc + hh) * 256);
+      qop[kc] = v4i{static_cast<int>(sext_lo(w.x)), static_cast<int>(sext_hi(w.x)), static_cast<int>(sext_lo(w.y)),
+                    static_cast<int>(sext_hi(w.y))};
+    }
+  }
+  const float cq = __fmul_rn(a.qs[static_cast<size_t>(bh) * (a.Npad / a.q_group) + qrow / a.q_group], a.Kc);
+  const float pscale = SYM7 ? 7.0f : 15.0f;
+
+  auto stage_aux = [&](int jb, int buf) {
+    // V dequantization factors fl(s_v/15) / 16 for the block's group (exact /16)
+    if (tid < kD) {
+      int g = (jb * KV) / a.v_group;
+      if (g >= a.nvgroups) g = a.nvgroups - 1;
+      const float s = a.vs[(static_cast<size_t>(bh) * a.nvgroups + g) * kD + tid];
+      sDq[buf][tid] = __fmul_rn(__fdiv_rn(s, pscale), 0.0625f);
+    }
+    if (KTOK && tid < KV) {
+      sKs[buf][tid] = a.ks[static_cast<size_t>(bh) * kstride + jb * KV + tid];
+    }
+  };
+
+  float of[4][16];
+#pragma unroll
+  for (int mt = 0; mt < 4; ++mt)
+#pragma unroll
+    for (int r = 0; r < 16; ++r) of[mt][r] = 0.f;
+  float m = -INFINITY, l = 0.f;
+
+  Stage<KV> st;
+  stage_load<KV>(a, bh, 0, st);
+  stage_store<KV>(st, sK[0], sV[0]);
+  stage_aux(0, 0);
+  __syncthreads();
+
+  for (int jb = 0; jb < nblocks; ++jb) {
+    const int buf = jb & 1;
+    const bool more = jb + 1 < nblocks;
+    if (more) stage_load<KV>(a, bh, jb + 1, st);
+    const int key0 = jb * KV;
+    const bool last = key0 + KV > N;
+
+    // ---- S^T = K Q^T (int32, 16 x true S) ----
+    v16i s[NCH];
+#pragma unroll
+    for (int ch = 0; ch < NCH; ++ch) {
+      s[ch] = v16i{0, 0, 0, 0, 0, 0, 0, 0, 0, 0, 0, 0, 0, 0, 0, 0};
+#pragma unroll
+      for (int kc = 0; kc < 4; ++kc) {
+        const v4i A = *reinterpret_cast<const v4i*>(&sK[buf][(((ch * 8) + 2 * kc + hh) * 32 + j) * 16]);
+        s[ch] = __builtin_amdgcn_mfma_i32_32x32x32_i8(A, qop[kc], s[ch], 0, 0, 0);
+      }
+    }
+
+    // key of accumulator register r in chunk ch: key0 + ch*32 + 8*(r/4) + 4*hh + r%4
+    // ---- block row maximum ----
+    float c16[NCH];
+    float tmax = -INFINITY;
+    if (!KTOK) {
+#pragma unroll
+      for (int ch = 0; ch < NCH; ++ch) {
+        const int kbase = key0 + ch * 32;
+        c16[ch] = __fmul_rn(__fmul_rn(cq, a.ks[static_cast<size_t>(bh) * kstride + kbase / a.k_group]), 0.0625f);
+        if (kbase < N) {
+          int mx = INT_MIN;
+#pragma unroll
+          for (int r = 0; r < 16; ++r) {
+            const int key = kbase + 8 * (r >> 2) + 4 * hh + (r & 3);
+            const int v = (!last || key < N) ? s[ch][r] : INT_MIN;
+            mx = max(mx, v);
+          }
+          if (mx != INT_MIN) tmax = fmaxf(tmax, __fmul_rn(static_cast<float>(mx), c16[ch]));
+        }
+      }
+    } else {
+#pragma unroll
+      for (int ch = 0; ch < NCH; ++ch) {
+#pragma unroll
+        for (int r = 0; r < 16; ++r) {
+          const int kl = ch * 32 + 8 * (r >> 2) + 4 * hh + (r & 3);
+          const float c = __fmul_rn(__fmul_rn(cq, sKs[buf][kl]), 0.0625f);
+          if (!last || key0 + kl < N) tmax = fmaxf(tmax, __fmul_rn(static_cast<float>(s[ch][r]), c));
+        }
+      }
+    }
+    tmax = fmaxf(tmax, __shfl_xor(tmax, 32));
+    const float mnew = fmaxf(m, tmax);
+    const float alpha = __builtin_amdgcn_exp2f(m - mnew);
+    m = mnew;
+
+    // ---- P, its codes (B operand of O^T = V^T P^T) and the row sum ----
+    uint32_t pk[NCH][4];
+    float lsum = 0.f;
+#pragma unroll
+    for (int ch = 0; ch < NCH; ++ch) {
+#pragma unroll
+      for (int q = 0; q < 4; ++q) {
+        uint32_t word = 0;
+#pragma unroll
+        for (int t = 0; t < 4; ++t) {
+          const int r = 4 * q + t;
+          const int kl = ch * 32 + 8 * (r >> 2) + 4 * hh + (r & 3);
+          const float c = KTOK ? __fmul_rn(__fmul_rn(cq, sKs[buf][kl]), 0.0625f) : c16[ch];
+          const float x = __fmaf_rn(static_cast<float>(s[ch][r]), c, -mnew);
+          float P = __builtin_amdgcn_exp2f(x);
+          if (last && key0 + kl >= N) P = 0.f;
+          lsum += P;
+          word = __builtin_amdgcn_cvt_pk_u8_f32(__fmul_rn(P, pscale), t, word);
+        }
+        pk[ch][q] = word;
+      }
+    }
+    l = __fmaf_rn(l, alpha, lsum);
+
+    if (DEBUG) {
+      if (bh == a.dbg_bh && qrow >= a.dbg_row0 && qrow < a.dbg_row0 + a.dbg_rows) {
+        const size_t rowo = static_cast<size_t>(qrow - a.dbg_row0);
+#pragma unroll
+        for (int ch = 0; ch < NCH; ++ch)
+#pragma unroll
+          for (int r = 0; r < 16; ++r) {
+            const int key = key0 + ch * 32 + 8 * (r >> 2) + 4 * hh + (r & 3);
+            if (key < N) {
+              if (a.dbg_s) a.dbg_s[rowo * N + key] = s[ch][r] >> 4;
+              if (a.dbg_u) a.dbg_u[rowo * N + key] = static_cast<uint8_t>((pk[ch][r >> 2] >> (8 * (r & 3))) & 0xFF);
+            }
+          }
+        if (a.dbg_m && hh == 0) a.dbg_m[rowo * nblocks + jb] = mnew;
+      }
+    }
+
+    // ---- O^T += V^T P^T (int32), one 32-channel tile at a time, then rescale
+    //      and dequantize into the binary32 accumulator ----
+#pragma unroll
+    for (int mt = 0; mt < 4; ++mt) {
+      v16i acc = v16i{0, 0, 0, 0, 0, 0, 0, 0, 0, 0, 0, 0, 0, 0, 0, 0};
+#pragma unroll
+      for (int ch = 0; ch < NCH; ++ch) {
+        const v4i B = v4i{static_cast<int>(pk[ch][0]), static_cast<int>(pk[ch][1]), static_cast<int>(pk[ch][2]),
+                          static_cast<int>(pk[ch][3])};
+        const v4i A = *reinterpret_cast<const v4i*>(&sV[buf][((ch * 2 + hh) * 128 + mt * 32 + j) * 16]);
+        acc = __builtin_amdgcn_mfma_i32_32x32x32_i8(A, B, acc, 0, 0, 0);
+      }
+#pragma unroll
+      for (int rq = 0; rq < 4; ++rq) {
+        const float4 dq = *reinterpret_cast<const float4*>(&sDq[buf][mt * 32 + 8 * rq + 4 * hh]);
+        const float d4[4] = {dq.x, dq.y, dq.z, dq.w};
+#pragma unroll
+        for (int t = 0; t < 4; ++t) {
+          const int r = 4 * rq + t;
+          of[mt][r] = __fmaf_rn(static_cast<float>(acc[r]), d4[t], __fmul_rn(of[mt][r], alpha));
+        }
+      }
+    }
+
+    if (more) {
+      stage_store<KV>(st, sK[buf ^ 1], sV[buf ^ 1]);
+      stage_aux(jb + 1, buf ^ 1);
+    }
+    __syncthreads();
+  }
+
+  // ---- epilogue: O / l + mu_v ----
+  const float ltot = l + __shfl_xor(l, 32);
+  if (qrow < N) {
+    const float inv = 1.0f / ltot;
+    const size_t obase = (static_cast<size_t>(bh) * N + qrow) * kD;
+#pragma unroll
+    for (int mt = 0; mt < 4; ++mt)
+#pragma unroll
+      for (int rq = 0; rq < 4; ++rq) {
+        const int c0 = mt * 32 + 8 * rq + 4 * hh;
+        float v[4];
+#pragma unroll
+        for (int t = 0; t < 4; ++t) {
+          v[t] = of[mt][4 * rq + t] * inv;
+          if (a.mu_v) v[t] += a.mu_v[bh * kD + c0 + t];
+        }
+        if (a.out_dtype == 2) {
+          *reinterpret_cast<float4*>(static_cast<float*>(a.o) + obase + c0) = make_float4(v[0], v[1], v[2], v[3]);
+        } else if (a.out_dtype == 0) {
+          uint16_t b[4];
+#pragma unroll
+          for (int t = 0; t < 4; ++t) b[t] = __bfloat16_as_ushort(__float2bfloat16(v[t]));
+          *reinterpret_cast<uint2*>(static_cast<uint16_t*>(a.o) + obase + c0) =
+              make_uint2(b[0] | (static_cast<uint32_t>(b[1]) << 16), b[2] | (static_cast<uint32_t>(b[3]) << 16));
+        } else {
+          uint16_t b[4];
+#pragma unroll
+          for (int t = 0; t < 4; ++t) b[t] = __half_as_ushort(__float2half(v[t]));
+          *reinterpret_cast<uint2*>(static_cast<uint16_t*>(a.o) + obase + c0) =
+              make_uint2(b[0] | (static_cast<uint32_t>(b[1]) << 16), b[2] | (static_cast<uint32_t>(b[3]) << 16));
+        }
+      }
+  }
+}
+
+template <int KV, bool KTOK, bool SYM7, bool DEBUG>
+hipError_t launch_t(const AttnArgs& a, hipStream_t s) {
+  const dim3 grid(a.Npad / kBlockM, a.BH);
+  hipLaunchKernelGGL((k_attn_int4<KV, KTOK, SYM7, DEBUG>), grid, dim3(256), 0, s, a);
+  return hipGetLastError();
+}
+
+template <int KV, bool KTOK, bool SYM7>
+hipError_t launch_d(const AttnArgs& a, bool debug, hipStream_t s) {
+  return debug ? launch_t<KV, KTOK, SYM7, true>(a, s) : launch_t<KV, KTOK, SYM7, false>(a, s);
+}
+
+template <int KV, bool KTOK>
+hipError_t launch_p(const AttnArgs& a, bool sym7, bool debug, hipStream_t s) {
+  return sym7 ? launch_d<KV, KTOK, true>(a, debug, s) : launch_d<KV, KTOK, false>(a, debug, s);
+}
+
+template <int KV>
+hipError_t launch_k(const AttnArgs& a, bool ktok, bool sym7, bool debug, hipStream_t s) {
+  return ktok ? launch_p<KV, true>(a, sym7, debug, s) : launch_p<KV, false>(a, sym7, debug, s);
+}
+
+}  // namespace
+
+hipError_t launch_attn_int4(const AttnArgs& a, int kv_block, bool k_per_token, bool sym7, bool debug,
+                            hipStream_t s) {
+  if (kv_block == 64) return launch_k<64>(a, k_per_token, sym7, debug, s);
+  return launch_k<128>(a, k_per_token, sym7, debug, s);
+}
+
+}  // namespace ra

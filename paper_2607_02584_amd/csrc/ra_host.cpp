@@ -1,0 +1,546 @@
+// ra_host.cpp -- host side of librotate_attn.so: argument validation, RoPE
+// table construction and caching, workspace partitioning, kernel launches.
+// Every entry point validates before it touches the GPU.
+#include <hip/hip_runtime.h>
+
+#include <cmath>
+#include <cstdio>
+#include <cstring>
+#include <map>
+#include <mutex>
+#include <string>
+#include <vector>
+
+#include "../../include/rotate_attn.h"
+#include "ra_internal.h"
+
+namespace {
+
+thread_local std::string g_err;
+
+int fail(int code, const std::string& msg) {
+  g_err = msg;
+  return code;
+}
+
+#define RA_CHECK_HIP(expr)                                                            \
+  do {                                                                                \
+    hipError_t e_ = (expr);                                                           \
+    if (e_ != hipSuccess) return fail(RA_ERR_HIP, std::string(#expr) + ": " + hipGetErrorString(e_)); \
+  } while (0)
+
+constexpr int kD = 128;
+constexpr size_t kAlign = 256;
+
+size_t align_up(size_t x) { return (x + kAlign - 1) / kAlign * kAlign; }
+
+int64_t npad_of(int N) { return (static_cast<int64_t>(N) + 127) / 128 * 128; }
+
+int validate(const ra_params* p) {
+  if (!p) return fail(RA_ERR_INVALID, "params is NULL");
+  if (p->D != kD) return fail(RA_ERR_UNSUPPORTED, "only D == 128 is supported");
+  if (p->B < 1 || p->H < 1 || p->N < 1) return fail(RA_ERR_INVALID, "B, H, N must be >= 1");
+  if (p->N > (1 << 21)) return fail(RA_ERR_UNSUPPORTED, "N above 2^21 tokens is not supported");
+  if (static_cast<int64_t>(p->B) * p->H > (1 << 20)) return fail(RA_ERR_UNSUPPORTED, "B*H too large");
+  for (int i = 0; i < 3; ++i)
+    if (p->grid[i] < 1) return fail(RA_ERR_INVALID, "grid extents must be >= 1");
+  if (static_cast<int64_t>(p->grid[0]) * p->grid[1] * p->grid[2] != p->N)
+    return fail(RA_ERR_INVALID, "grid T*Hg*W must equal N");
+  int sum = 0;
+  for (int i = 0; i < 3; ++i) {
+    if (p->rope_split[i] < 2 || (p->rope_split[i] & 1)) return fail(RA_ERR_INVALID, "rope_split entries must be even and >= 2");
+    sum += p->rope_split[i];
+  }
+  if (sum != p->D) return fail(RA_ERR_INVALID, "rope_split must sum to D");
+  if (!(p->rope_theta > 0.0f) || !std::isfinite(p->rope_theta)) return fail(RA_ERR_INVALID, "rope_theta must be > 0");
+  if (p->rotation < RA_ROT_NONE || p->rotation > RA_ROT_HALF) return fail(RA_ERR_INVALID, "unknown rotation");
+  if (p->rot_blocks) {
+    for (int i = 0; i < 4 * (kD / 2); ++i)
+      if (!std::isfinite(p->rot_blocks[i])) return fail(RA_ERR_INVALID, "rot_blocks must be finite");
+  }
+  if (p->p_quant != RA_PQ_RANGE15 && p->p_quant != RA_PQ_SYM7) return fail(RA_ERR_INVALID, "unknown p_quant");
+  if (p->smooth < 0 || p->smooth > (RA_SMOOTH_K | RA_SMOOTH_V)) return fail(RA_ERR_INVALID, "unknown smooth flags");
+  if (p->q_group < 1 || p->q_group > 128 || (128 % p->q_group) != 0)
+    return fail(RA_ERR_UNSUPPORTED, "q_group must divide 128");
+  if (p->k_group != 1 && p->k_group != 32 && p->k_group != 64 && p->k_group != 128)
+    return fail(RA_ERR_UNSUPPORTED, "k_group must be 1, 32, 64 or 128");
+  if (p->kv_block != 64 && p->kv_block != 128) return fail(RA_ERR_UNSUPPORTED, "kv_block must be 64 or 128");
+  if (p->v_group < 1) return fail(RA_ERR_INVALID, "v_group must be >= 1");
+  if ((p->v_group % p->kv_block) != 0 && p->v_group < p->N)
+    return fail(RA_ERR_UNSUPPORTED, "v_group must be a multiple of kv_block or >= N");
+  if (!(p->sm_scale >= 0.0f) || !std::isfinite(p->sm_scale)) return fail(RA_ERR_INVALID, "sm_scale must be >= 0");
+  if (p->in_dtype != RA_BF16 && p->in_dtype != RA_FP16) return fail(RA_ERR_INVALID, "in_dtype must be BF16 or FP16");
+  if (p->out_dtype != RA_BF16 && p->out_dtype != RA_FP16 && p->out_dtype != RA_FP32)
+    return fail(RA_ERR_INVALID, "out_dtype must be BF16, FP16 or FP32");
+  return RA_OK;
+}
+
+struct Sizes {
+  int64_t BH, Npad, ntiles, nvgroups;
+  size_t codes, qscale, kscale, vscale, mu, partial, amax;
+};
+
+Sizes sizes_of(const ra_params* p) {
+  Sizes s;
+  s.BH = static_cast<int64_t>(p->B) * p->H;
+  s.Npad = npad_of(p->N);
+  s.ntiles = s.Npad / 128;
+  s.nvgroups = (p->N + p->v_group - 1) / p->v_group;
+  s.codes = static_cast<size_t>(s.BH * s.Npad * 64);
+  s.qscale = static_cast<size_t>(s.BH * (s.Npad / p->q_group));
+  s.kscale = static_cast<size_t>(s.BH * (s.Npad / p->k_group));
+  s.vscale = static_cast<size_t>(s.BH * s.nvgroups * kD);
+  s.mu = static_cast<size_t>(s.BH * kD);
+  s.partial = static_cast<size_t>(s.BH * s.ntiles * kD);
+  s.amax = s.vscale;
+  return s;
+}
+
+// Workspace partition of the INT4 path.  The quantize calls use only the head
+// of it (partials, internal means, V maxima); fwd_int4 also keeps the codes.
+struct Int4Ws {
+  double* partial;
+  float* mu_k;
+  float* mu_v;
+  uint32_t* amax;
+  uint8_t* qc;
+  uint8_t* kc;
+  uint8_t* vc;
+  float* qs;
+  float* ks;
+  float* vs;
+  size_t total;
+};
+
+Int4Ws carve_int4(const ra_params* p, void* base) {
+  const Sizes s = sizes_of(p);
+  Int4Ws w;
+  size_t o = 0;
+  char* b = static_cast<char*>(base);
+  auto take = [&](size_t bytes) {
+    char* r = b ? b + o : nullptr;
+    o += align_up(bytes);
+    return r;
+  };
+  w.partial = reinterpret_cast<double*>(take(s.partial * sizeof(double)));
+  w.mu_k = reinterpret_cast<float*>(take(s.mu * sizeof(float)));
+  w.mu_v = reinterpret_cast<float*>(take(s.mu * sizeof(float)));
+  w.amax = reinterpret_cast<uint32_t*>(take(s.amax * sizeof(uint32_t)));
+  w.qc = reinterpret_cast<uint8_t*>(take(s.codes));
+  w.kc = reinterpret_cast<uint8_t*>(take(s.codes));
+  w.vc = reinterpret_cast<uint8_t*>(take(s.codes));
+  w.qs = reinterpret_cast<float*>(take(s.qscale * sizeof(float)));
+  w.ks = reinterpret_cast<float*>(take(s.kscale * sizeof(float)));
+  w.vs = reinterpret_cast<float*>(take(s.vscale * sizeof(float)));
+  w.total = o;
+  return w;
+}
+
+struct Fp16Ws {
+  uint16_t* q;
+  uint16_t* k;
+  uint16_t* v;
+  size_t total;
+};
+
+Fp16Ws carve_fp16(const ra_params* p, void* base) {
+  const Sizes s = sizes_of(p);
+  Fp16Ws w;
+  const size_t one = align_up(static_cast<size_t>(s.BH * s.Npad * kD * 2));
+  char* b = static_cast<char*>(base);
+  w.q = b ? reinterpret_cast<uint16_t*>(b) : nullptr;
+  w.k = b ? reinterpret_cast<uint16_t*>(b + one) : nullptr;
+  w.v = b ? reinterpret_cast<uint16_t*>(b + 2 * one) : nullptr;
+  w.total = 3 * one;
+  return w;
+}
+
+int check_ws(void* ws, size_t have, size_t need) {
+  if (!ws) return fail(RA_ERR_WORKSPACE, "workspace is NULL");
+  if (reinterpret_cast<uintptr_t>(ws) % kAlign) return fail(RA_ERR_WORKSPACE, "workspace must be 256-byte aligned");
+  if (have < need) return fail(RA_ERR_WORKSPACE, "workspace too small: need " + std::to_string(need) + " bytes");
+  return RA_OK;
+}
+
+// ------------------------------------------------------------ RoPE tables --
+// For axis a, position pos and pair k (global pair p): omega = theta^(-2k/D_a),
+// phi = pos * omega, M = [[cos, sin], [-sin, cos]] (row-vector form), and for
+// the merged interleaved rotation G = M R_p, all in binary64, rounded once to
+// binary32.  R_p defaults to H_2 = (1/sqrt 2) [[1, 1], [1, -1]].
+
+struct TableEntry {
+  void* dev = nullptr;
+  ra::RopeTables t;
+};
+
+std::mutex g_mu;
+std::map<std::string, TableEntry> g_tables;
+
+void rot_block(const ra_params* p, int pair, double R[4]) {
+  if (p->rot_blocks) {
+    std::memcpy(R, p->rot_blocks + 4 * pair, 4 * sizeof(double));
+  } else {
+    const double r = 1.0 / std::sqrt(2.0);
+    R[0] = r;
+    R[1] = r;
+    R[2] = r;
+    R[3] = -r;
+  }
+}
+
+int get_tables(const ra_params* p, ra::RopeTables* out) {
+  int dev = 0;
+  RA_CHECK_HIP(hipGetDevice(&dev));
+  std::string key;
+  auto put = [&](const void* d, size_t n) { key.append(static_cast<const char*>(d), n); };
+  put(&dev, sizeof dev);
+  put(p->grid, sizeof p->grid);
+  put(p->rope_split, sizeof p->rope_split);
+  put(&p->rope_theta, sizeof p->rope_theta);
+  put(&p->rotation, sizeof p->rotation);
+  if (p->rotation != RA_ROT_NONE && p->rot_blocks) put(p->rot_blocks, 4 * (kD / 2) * sizeof(double));
+  std::lock_guard<std::mutex> lock(g_mu);
+  auto it = g_tables.find(key);
+  if (it != g_tables.end()) {
+    *out = it->second.t;
+    return RA_OK;
+  }
+  std::vector<float> host;
+  size_t off[4];
+  int first = 0;
+  for (int a = 0; a < 3; ++a) {
+    off[a] = host.size();
+    const int np = p->rope_split[a] / 2;
+    for (int pos = 0; pos < p->grid[a]; ++pos) {
+      for (int k = 0; k < np; ++k) {
+        const double omega = std::pow(static_cast<double>(p->rope_theta), -(2.0 * k) / static_cast<double>(p->rope_split[a]));
+        const double phi = static_cast<double>(pos) * omega;
+        const double cs = std::cos(phi), sn = std::sin(phi);
+        const double M[4] = {cs, sn, -sn, cs};
+        double G[4];
+        if (p->rotation == RA_ROT_INTERLEAVED) {
+          double R[4];
+          rot_block(p, first + k, R);
+          G[0] = M[0] * R[0] + M[1] * R[2];
+          G[1] = M[0] * R[1] + M[1] * R[3];
+          G[2] = M[2] * R[0] + M[3] * R[2];
+          G[3] = M[2] * R[1] + M[3] * R[3];
+        } else {
+          std::memcpy(G, M, sizeof M);
+        }
+        for (int i = 0; i < 4; ++i) host.push_back(static_cast<float>(G[i]));
+      }
+    }
+    first += np;
+  }
+  off[3] = host.size();
+  for (int pr = 0; pr < kD / 2; ++pr) {
+    double R[4];
+    rot_block(p, pr, R);
+    for (int i = 0; i < 4; ++i) host.push_back(static_cast<float>(R[i]));
+  }
+  void* d = nullptr;
+  RA_CHECK_HIP(hipMalloc(&d, host.size() * sizeof(float)));
+  hipError_t e = hipMemcpy(d, host.data(), host.size() * sizeof(float), hipMemcpyHostToDevice);
+  if (e != hipSuccess) {
+    (void)hipFree(d);
+    return fail(RA_ERR_HIP, std::string("hipMemcpy of RoPE tables: ") + hipGetErrorString(e));
+  }
+  TableEntry te;
+  te.dev = d;
+  const float4* base = static_cast<const float4*>(d);
+  for (int a = 0; a < 3; ++a) {
+    te.t.axis[a] = base + off[a] / 4;
+    te.t.split[a] = p->rope_split[a];
+    te.t.grid[a] = p->grid[a];
+  }
+  te.t.rot = base + off[3] / 4;
+  te.t.rotation = p->rotation;
+  g_tables[key] = te;
+  *out = te.t;
+  return RA_OK;
+}
+
+float kc_of(const ra_params* p) {
+  const double sigma = p->sm_scale > 0.0f ? static_cast<double>(p->sm_scale) : 1.0 / std::sqrt(static_cast<double>(p->D));
+  return static_cast<float>(sigma * 1.4426950408889634074);
+}
+
+hipStream_t st(void* s) { return static_cast<hipStream_t>(s); }
+
+int qk_impl(const ra_params* p, const void* q, const void* k, uint8_t* qc, float* qs, uint8_t* kc, float* ks,
+            float* mu_k, const Int4Ws& w, hipStream_t s) {
+  const Sizes z = sizes_of(p);
+  ra::RopeTables t;
+  int rc = get_tables(p, &t);
+  if (rc) return rc;
+  ra::QkArgs a{};
+  a.N = p->N;
+  a.Npad = static_cast<int>(z.Npad);
+  a.is_fp16 = p->in_dtype == RA_FP16;
+  a.partial = w.partial;
+  float* mu = mu_k ? mu_k : w.mu_k;
+  const float* center = nullptr;
+  if (p->smooth & RA_SMOOTH_K) {
+    a.x = static_cast<const uint16_t*>(k);
+    RA_CHECK_HIP(ra::launch_qk_sums(t, a, static_cast<int>(z.BH), s));
+    RA_CHECK_HIP(ra::launch_mu_reduce(w.partial, mu, static_cast<int>(z.BH), static_cast<int>(z.ntiles), p->N, s));
+    center = mu;
+  } else if (mu_k) {
+    RA_CHECK_HIP(ra::launch_fill_zero_u32(reinterpret_cast<uint32_t*>(mu_k), static_cast<int64_t>(z.mu), s));
+  }
+  a.x = static_cast<const uint16_t*>(q);
+  a.codes = qc;
+  a.scales = qs;
+  a.mu = nullptr;
+  a.group = p->q_group;
+  RA_CHECK_HIP(ra::launch_qk_quant(t, a, static_cast<int>(z.BH), s));
+  a.x = static_cast<const uint16_t*>(k);
+  a.codes = kc;
+  a.scales = ks;
+  a.mu = center;
+  a.group = p->k_group;
+  RA_CHECK_HIP(ra::launch_qk_quant(t, a, static_cast<int>(z.BH), s));
+  return RA_OK;
+}
+
+int v_impl(const ra_params* p, const void* v, uint8_t* vc, float* vs, float* mu_v, const Int4Ws& w, hipStream_t s) {
+  const Sizes z = sizes_of(p);
+  ra::VArgs a{};
+  a.x = static_cast<const uint16_t*>(v);
+  a.codes = vc;
+  a.scales = vs;
+  a.partial = w.partial;
+  a.amax = w.amax;
+  a.N = p->N;
+  a.Npad = static_cast<int>(z.Npad);
+  a.group = p->v_group;
+  a.ngroups = static_cast<int>(z.nvgroups);
+  a.is_fp16 = p->in_dtype == RA_FP16;
+  float* mu = mu_v ? mu_v : w.mu_v;
+  if (p->smooth & RA_SMOOTH_V) {
+    RA_CHECK_HIP(ra::launch_v_sums(a, static_cast<int>(z.BH), s));
+    RA_CHECK_HIP(ra::launch_mu_reduce(w.partial, mu, static_cast<int>(z.BH), static_cast<int>(z.ntiles), p->N, s));
+    a.mu = mu;
+  } else {
+    if (mu_v) RA_CHECK_HIP(ra::launch_fill_zero_u32(reinterpret_cast<uint32_t*>(mu_v), static_cast<int64_t>(z.mu), s));
+    a.mu = nullptr;
+  }
+  RA_CHECK_HIP(ra::launch_fill_zero_u32(w.amax, static_cast<int64_t>(z.amax), s));
+  RA_CHECK_HIP(ra::launch_v_amax(a, static_cast<int>(z.BH), s));
+  RA_CHECK_HIP(ra::launch_v_quant(a, static_cast<int>(z.BH), s));
+  return RA_OK;
+}
+
+int attn_impl(const ra_params* p, const uint8_t* qc, const float* qs, const uint8_t* kc, const float* ks,
+              const uint8_t* vc, const float* vs, const float* mu_v, void* o, bool debug, int bh, int row0, int rows,
+              int32_t* s_out, uint8_t* u_out, float* m_out, hipStream_t s) {
+  const Sizes z = sizes_of(p);
+  ra::AttnArgs a{};
+  a.qc = qc;
+  a.qs = qs;
+  a.kc = kc;
+  a.ks = ks;
+  a.vc = vc;
+  a.vs = vs;
+  a.mu_v = mu_v;
+  a.o = o;
+  a.N = p->N;
+  a.Npad = static_cast<int>(z.Npad);
+  a.BH = static_cast<int>(z.BH);
+  a.q_group = p->q_group;
+  a.k_group = p->k_group;
+  a.v_group = p->v_group;
+  a.nvgroups = static_cast<int>(z.nvgroups);
+  a.Kc = kc_of(p);
+  a.out_dtype = p->out_dtype;
+  a.dbg_s = s_out;
+  a.dbg_u = u_out;
+  a.dbg_m = m_out;
+  a.dbg_bh = bh;
+  a.dbg_row0 = row0;
+  a.dbg_rows = rows;
+  RA_CHECK_HIP(ra::launch_attn_int4(a, p->kv_block, p->k_group == 1, p->p_quant == RA_PQ_SYM7, debug, s));
+  return RA_OK;
+}
+
+int fp16_prepare_impl(const ra_params* p, const void* q, const void* k, const void* v, const Fp16Ws& w, hipStream_t s) {
+  const Sizes z = sizes_of(p);
+  ra::RopeTables t;
+  ra_params plain = *p;
+  plain.rotation = RA_ROT_NONE;
+  plain.rot_blocks = nullptr;
+  int rc = get_tables(&plain, &t);
+  if (rc) return rc;
+  const int is16 = p->in_dtype == RA_FP16;
+  RA_CHECK_HIP(ra::launch_rope16(t, static_cast<const uint16_t*>(q), w.q, static_cast<int>(z.BH), p->N,
+                                 static_cast<int>(z.Npad), is16, s));
+  RA_CHECK_HIP(ra::launch_rope16(t, static_cast<const uint16_t*>(k), w.k, static_cast<int>(z.BH), p->N,
+                                 static_cast<int>(z.Npad), is16, s));
+  RA_CHECK_HIP(ra::launch_v16_relayout(static_cast<const uint16_t*>(v), w.v, static_cast<int>(z.BH), p->N,
+                                       static_cast<int>(z.Npad), s));
+  return RA_OK;
+}
+
+int fp16_attn_impl(const ra_params* p, const Fp16Ws& w, void* o, hipStream_t s) {
+  const Sizes z = sizes_of(p);
+  ra::Fp16Args a{};
+  a.q = w.q;
+  a.k = w.k;
+  a.v = w.v;
+  a.o = o;
+  a.N = p->N;
+  a.Npad = static_cast<int>(z.Npad);
+  a.BH = static_cast<int>(z.BH);
+  a.Kc = kc_of(p);
+  a.is_fp16 = p->in_dtype == RA_FP16;
+  a.out_dtype = p->out_dtype;
+  RA_CHECK_HIP(ra::launch_attn_fp16(a, p->kv_block, s));
+  return RA_OK;
+}
+
+}  // namespace
+
+extern "C" {
+
+int rotate_attn_layout(const ra_params* p, ra_layout* out) {
+  int rc = validate(p);
+  if (rc) return rc;
+  if (!out) return fail(RA_ERR_INVALID, "out is NULL");
+  const Sizes s = sizes_of(p);
+  out->n_pad = s.Npad;
+  out->qk_code_bytes = static_cast<int64_t>(s.codes);
+  out->q_scale_count = static_cast<int64_t>(s.qscale);
+  out->k_scale_count = static_cast<int64_t>(s.kscale);
+  out->v_code_bytes = static_cast<int64_t>(s.codes);
+  out->v_scale_count = static_cast<int64_t>(s.vscale);
+  out->mu_count = static_cast<int64_t>(s.mu);
+  return RA_OK;
+}
+
+int rotate_attn_workspace_size(const ra_params* p, int path, size_t* bytes) {
+  int rc = validate(p);
+  if (rc) return rc;
+  if (!bytes) return fail(RA_ERR_INVALID, "bytes is NULL");
+  if (path == RA_PATH_INT4) {
+    *bytes = carve_int4(p, nullptr).total;
+  } else if (path == RA_PATH_FP16) {
+    *bytes = carve_fp16(p, nullptr).total;
+  } else {
+    return fail(RA_ERR_INVALID, "unknown path");
+  }
+  return RA_OK;
+}
+
+int rotate_attn_quantize_qk(const ra_params* p, const void* q, const void* k, uint8_t* q_codes, float* q_scale,
+                            uint8_t* k_codes, float* k_scale, float* mu_k, void* workspace, size_t workspace_bytes,
+                            void* stream) {
+  int rc = validate(p);
+  if (rc) return rc;
+  if (!q || !k || !q_codes || !q_scale || !k_codes || !k_scale) return fail(RA_ERR_INVALID, "NULL tensor pointer");
+  const Int4Ws need = carve_int4(p, nullptr);
+  if ((rc = check_ws(workspace, workspace_bytes, need.total))) return rc;
+  return qk_impl(p, q, k, q_codes, q_scale, k_codes, k_scale, mu_k, carve_int4(p, workspace), st(stream));
+}
+
+int rotate_attn_quantize_v(const ra_params* p, const void* v, uint8_t* v_codes, float* v_scale, float* mu_v,
+                           void* workspace, size_t workspace_bytes, void* stream) {
+  int rc = validate(p);
+  if (rc) return rc;
+  if (!v || !v_codes || !v_scale) return fail(RA_ERR_INVALID, "NULL tensor pointer");
+  const Int4Ws need = carve_int4(p, nullptr);
+  if ((rc = check_ws(workspace, workspace_bytes, need.total))) return rc;
+  return v_impl(p, v, v_codes, v_scale, mu_v, carve_int4(p, workspace), st(stream));
+}
+
+int rotate_attn_attn_int4(const ra_params* p, const uint8_t* q_codes, const float* q_scale, const uint8_t* k_codes,
+                          const float* k_scale, const uint8_t* v_codes, const float* v_scale, const float* mu_v,
+                          void* o, void* stream) {
+  int rc = validate(p);
+  if (rc) return rc;
+  if (!q_codes || !q_scale || !k_codes || !k_scale || !v_codes || !v_scale || !o)
+    return fail(RA_ERR_INVALID, "NULL tensor pointer");
+  return attn_impl(p, q_codes, q_scale, k_codes, k_scale, v_codes, v_scale, mu_v, o, false, 0, 0, 0, nullptr, nullptr,
+                   nullptr, st(stream));
+}
+
+int rotate_attn_attn_int4_debug(const ra_params* p, const uint8_t* q_codes, const float* q_scale,
+                                const uint8_t* k_codes, const float* k_scale, const uint8_t* v_codes,
+                                const float* v_scale, const float* mu_v, void* o, int32_t bh, int32_t row0,
+                                int32_t rows, int32_t* s_out, uint8_t* u_out, float* m_out, void* stream) {
+  int rc = validate(p);
+  if (rc) return rc;
+  if (!q_codes || !q_scale || !k_codes || !k_scale || !v_codes || !v_scale || !o)
+    return fail(RA_ERR_INVALID, "NULL tensor pointer");
+  if (bh < 0 || static_cast<int64_t>(bh) >= static_cast<int64_t>(p->B) * p->H) return fail(RA_ERR_INVALID, "bh out of range");
+  if (row0 < 0 || rows < 0 || static_cast<int64_t>(row0) + rows > p->N) return fail(RA_ERR_INVALID, "rows out of range");
+  return attn_impl(p, q_codes, q_scale, k_codes, k_scale, v_codes, v_scale, mu_v, o, true, bh, row0, rows, s_out,
+                   u_out, m_out, st(stream));
+}
+
+int rotate_attn_fwd_int4(const ra_params* p, const void* q, const void* k, const void* v, void* o, void* workspace,
+                         size_t workspace_bytes, void* stream) {
+  int rc = validate(p);
+  if (rc) return rc;
+  if (!q || !k || !v || !o) return fail(RA_ERR_INVALID, "NULL tensor pointer");
+  const Int4Ws need = carve_int4(p, nullptr);
+  if ((rc = check_ws(workspace, workspace_bytes, need.total))) return rc;
+  const Int4Ws w = carve_int4(p, workspace);
+  if ((rc = qk_impl(p, q, k, w.qc, w.qs, w.kc, w.ks, nullptr, w, st(stream)))) return rc;
+  if ((rc = v_impl(p, v, w.vc, w.vs, nullptr, w, st(stream)))) return rc;
+  const float* mu = (p->smooth & RA_SMOOTH_V) ? w.mu_v : nullptr;
+  return attn_impl(p, w.qc, w.qs, w.kc, w.ks, w.vc, w.vs, mu, o, false, 0, 0, 0, nullptr, nullptr, nullptr,
+                   st(stream));
+}
+
+int rotate_attn_prepare_fp16(const ra_params* p, const void* q, const void* k, const void* v, void* workspace,
+                             size_t workspace_bytes, void* stream) {
+  int rc = validate(p);
+  if (rc) return rc;
+  if (!q || !k || !v) return fail(RA_ERR_INVALID, "NULL tensor pointer");
+  const Fp16Ws need = carve_fp16(p, nullptr);
+  if ((rc = check_ws(workspace, workspace_bytes, need.total))) return rc;
+  return fp16_prepare_impl(p, q, k, v, carve_fp16(p, workspace), st(stream));
+}
+
+int rotate_attn_attn_fp16(const ra_params* p, const void* workspace, size_t workspace_bytes, void* o, void* stream) {
+  int rc = validate(p);
+  if (rc) return rc;
+  if (!o) return fail(RA_ERR_INVALID, "NULL tensor pointer");
+  const Fp16Ws need = carve_fp16(p, nullptr);
+  if ((rc = check_ws(const_cast<void*>(workspace), workspace_bytes, need.total))) return rc;
+  return fp16_attn_impl(p, carve_fp16(p, const_cast<void*>(workspace)), o, st(stream));
+}
+
+int rotate_attn_fwd_fp16(const ra_params* p, const void* q, const void* k, const void* v, void* o, void* workspace,
+                         size_t workspace_bytes, void* stream) {
+  int rc = validate(p);
+  if (rc) return rc;
+  if (!q || !k || !v || !o) return fail(RA_ERR_INVALID, "NULL tensor pointer");
+  const Fp16Ws need = carve_fp16(p, nullptr);
+  if ((rc = check_ws(workspace, workspace_bytes, need.total))) return rc;
+  const Fp16Ws w = carve_fp16(p, workspace);
+  if ((rc = fp16_prepare_impl(p, q, k, v, w, st(stream)))) return rc;
+  return fp16_attn_impl(p, w, o, st(stream));
+}
+
+int rotate_attn_fwd(const ra_params* p, int fallback, const void* q, const void* k, const void* v, void* o,
+                    void* workspace, size_t workspace_bytes, void* stream) {
+  if (fallback) return rotate_attn_fwd_fp16(p, q, k, v, o, workspace, workspace_bytes, stream);
+  return rotate_attn_fwd_int4(p, q, k, v, o, workspace, workspace_bytes, stream);
+}
+
+const char* rotate_attn_error_string(int status) {
+  switch (status) {
+    case RA_OK: return "ok";
+    case RA_ERR_INVALID: return "invalid argument";
+    case RA_ERR_UNSUPPORTED: return "unsupported configuration";
+    case RA_ERR_WORKSPACE: return "workspace missing or too small";
+    case RA_ERR_HIP: return "HIP runtime error";
+    default: return "unknown status";
+  }
+}
+
+const char* rotate_attn_last_error(void) { return g_err.c_str(); }
+
+}  // extern "C"

@@ -1,0 +1,93 @@
+// ra_internal.h -- declarations shared by the host side and the HIP kernels of
+// librotate_attn.so (library-internal; not installed, not part of the ABI).
+#pragma once
+#include <hip/hip_bf16.h>
+#include <hip/hip_fp16.h>
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+namespace ra {
+
+constexpr int kD = 128;       // head dimension
+constexpr int kTile = 128;    // producer token tile; Npad is a multiple of it
+
+// RoPE/rotation tables on the device.  For axis a the table holds, for every
+// position pos in [0, extent_a) and pair k in [0, D_a/2), the binary32 2x2
+// block G = M (or M R for the merged interleaved rotation) as
+// {g00, g01, g10, g11}, so that [y0 y1] = [x0 x1] G.  `rot` holds the 64
+// binary32 rotation blocks of the half rotation.
+struct RopeTables {
+  const float4* axis[3];
+  const float4* rot;
+  int split[3];
+  int grid[3];
+  int rotation;
+};
+
+// Per-thread constants of the producer: which table entries the two channel
+// pairs (4*cl .. 4*cl+3) of this thread read.
+struct QkArgs {
+  const uint16_t* x;      // [BH][N][128] bf16/fp16 bits
+  uint8_t* codes;         // tiled INT4 layout, [BH][Npad*64]
+  float* scales;          // [BH][Npad/group]
+  const float* mu;        // [BH][128] or nullptr (no centering)
+  double* partial;        // [BH][ntiles][128] fixed-point sums (sums pass only)
+  int N, Npad, group, is_fp16;
+};
+
+struct VArgs {
+  const uint16_t* x;      // [BH][N][128]
+  uint8_t* codes;         // tiled V layout, [BH][Npad*64]
+  float* scales;          // [BH][ngroups][128]
+  const float* mu;        // [BH][128] or nullptr
+  double* partial;        // [BH][ntiles][128]
+  uint32_t* amax;         // [BH][ngroups][128] float bits (non-negative)
+  int N, Npad, group, ngroups, is_fp16;
+};
+
+struct AttnArgs {
+  const uint8_t* qc;
+  const float* qs;
+  const uint8_t* kc;
+  const float* ks;
+  const uint8_t* vc;
+  const float* vs;
+  const float* mu_v;      // [BH][128] or nullptr
+  void* o;
+  int N, Npad, BH;
+  int q_group, k_group, v_group, nvgroups;
+  float Kc;               // fl32(sm_scale * log2(e))
+  int out_dtype;
+  // debug dump (debug kernel only)
+  int32_t* dbg_s;
+  uint8_t* dbg_u;
+  float* dbg_m;
+  int dbg_bh, dbg_row0, dbg_rows;
+};
+
+struct Fp16Args {
+  const uint16_t* q;      // tiled 16-bit layout (see ra_fp16.hip)
+  const uint16_t* k;
+  const uint16_t* v;      // tiled transposed layout
+  void* o;
+  int N, Npad, BH;
+  float Kc;
+  int is_fp16, out_dtype;
+};
+
+// ---- launchers (return hipError_t) ----
+hipError_t launch_qk_sums(const RopeTables& t, const QkArgs& a, int BH, hipStream_t s);
+hipError_t launch_mu_reduce(const double* partial, float* mu, int BH, int ntiles, int N, hipStream_t s);
+hipError_t launch_qk_quant(const RopeTables& t, const QkArgs& a, int BH, hipStream_t s);
+hipError_t launch_fill_zero_u32(uint32_t* p, int64_t n, hipStream_t s);
+hipError_t launch_v_sums(const VArgs& a, int BH, hipStream_t s);
+hipError_t launch_v_amax(const VArgs& a, int BH, hipStream_t s);
+hipError_t launch_v_quant(const VArgs& a, int BH, hipStream_t s);
+hipError_t launch_attn_int4(const AttnArgs& a, int kv_block, bool k_per_token, bool sym7, bool debug,
+                            hipStream_t s);
+hipError_t launch_rope16(const RopeTables& t, const uint16_t* x, uint16_t* out, int BH, int N, int Npad,
+                         int is_fp16, hipStream_t s);
+hipError_t launch_v16_relayout(const uint16_t* v, uint16_t* out, int BH, int N, int Npad, hipStream_t s);
+hipError_t launch_attn_fp16(const Fp16Args& a, int kv_block, hipStream_t s);
+
+}  // namespace ra

@@ -1,0 +1,440 @@
+// ra_producer.hip -- element-wise producer kernels of the INT4 path (gfx950).
+//
+//  * 3D RoPE with the RoPE-aware rotation (Sec. 3, Sec. 4.1.2 merged
+//    interleaved rotation, Sec. 4.1.3 half rotation) in binary32:
+//      y0 = fma(x1, g10, x0*g00), y1 = fma(x1, g11, x0*g01)
+//    and for the half rotation, on the RoPE output,
+//      z(o+2i)   = fma(y(o+i+D_j/2), r10, y(o+i)*r00)
+//      z(o+2i+1) = fma(y(o+i+D_j/2), r11, y(o+i)*r01).
+//  * Smoothing (Sec. 4): per-channel means over the tokens of a head.  Each
+//    value is scaled by 2^20, clamped to +-2^32 and rounded to an integer; the
+//    integers are summed in binary64, which is exact (every partial sum is an
+//    integer below 2^53), so the mean does not depend on the summation order.
+//  * Symmetric INT4 quantization (Sec. 5.1): per group of tokens (Q, K) or per
+//    (group of tokens, channel) (V): s = amax/7, code = clamp(rint(z*7/amax)).
+//
+// Work decomposition: one workgroup of 256 threads per tile of 128 tokens of
+// one head.  Thread t handles channels 4*(t%32) .. 4*(t%32)+3 of the rows
+// t/32, t/32+8, ... (16 rows), so each row is read as 32 coalesced 8-byte
+// pieces.  These kernels are HBM-bound.
+#include "ra_internal.h"
+
+namespace ra {
+namespace {
+
+constexpr float kFix = 1048576.0f;     // 2^20
+constexpr float kFixLim = 4294967296.0f;  // 2^32
+
+__device__ __forceinline__ float h2f(uint16_t b, int is_fp16) {
+  if (is_fp16) return __half2float(__ushort_as_half(b));
+  return __uint_as_float(static_cast<uint32_t>(b) << 16);
+}
+
+// floor(n / d) for 0 <= n < 2^24, d >= 1, through binary32 with a correction.
+__device__ __forceinline__ int fdiv(int n, int d, float inv_d) {
+  int q = static_cast<int>(static_cast<float>(n) * inv_d);
+  if (q * d > n) --q;
+  if ((q + 1) * d <= n) ++q;
+  return q;
+}
+
+// Per-thread RoPE setup for its two channel pairs p0 = 2*cl, p1 = 2*cl + 1.
+struct PairSetup {
+  int axis[2];   // 0 = t, 1 = h, 2 = w
+  int k[2];      // pair index inside the axis segment
+  int npair[2];  // D_a / 2 (row length of the axis table)
+};
+
+__device__ __forceinline__ PairSetup pair_setup(const RopeTables& t, int cl) {
+  PairSetup s;
+#pragma unroll
+  for (int i = 0; i < 2; ++i) {
+    const int p = 2 * cl + i;
+    int first = 0, a = 2;
+    for (int ax = 0; ax < 3; ++ax) {
+      const int np = t.split[ax] / 2;
+      if (p < first + np) {
+        a = ax;
+        break;
+      }
+      first += np;
+    }
+    s.axis[i] = a;
+    s.k[i] = p - first;
+    s.npair[i] = t.split[a] / 2;
+  }
+  return s;
+}
+
+// Half rotation: for output pair P the two RoPE channels it mixes.
+struct HalfSetup {
+  int ia[2], ib[2];
+  float4 r[2];
+};
+
+__device__ __forceinline__ HalfSetup half_setup(const RopeTables& t, int cl) {
+  HalfSetup s;
+#pragma unroll
+  for (int i = 0; i < 2; ++i) {
+    int P = 2 * cl + i;
+    int o = 0, a = 0;
+    for (int ax = 0; ax < 3; ++ax) {
+      if (P >= o / 2 && P < (o + t.split[ax]) / 2) a = ax;
+      o += t.split[ax];
+    }
+    o = 0;
+    for (int ax = 0; ax < a; ++ax) o += t.split[ax];
+    int ii = P - o / 2;
+    s.ia[i] = o + ii;
+    s.ib[i] = o + ii + t.split[a] / 2;
+    s.r[i] = t.rot[P];
+  }
+  return s;
+}
+
+// RoPE (+ merged rotation) of channels 4cl..4cl+3 of token n; x holds the inputs.
+__device__ __forceinline__ void rope4(const RopeTables& t, const PairSetup& ps, int n, float invW, float invHW,
+                                      const float x[4], float y[4]) {
+  const int W = t.grid[2], Hg = t.grid[1];
+  int tq = fdiv(n, W * Hg, invHW);
+  int rem = n - tq * W * Hg;
+  int hq = fdiv(rem, W, invW);
+  int wq = rem - hq * W;
+  const int pos[3] = {tq, hq, wq};
+#pragma unroll
+  for (int i = 0; i < 2; ++i) {
+    const float4 g = t.axis[ps.axis[i]][pos[ps.axis[i]] * ps.npair[i] + ps.k[i]];
+    const float x0 = x[2 * i], x1 = x[2 * i + 1];
+    y[2 * i] = __fmaf_rn(x1, g.z, __fmul_rn(x0, g.x));
+    y[2 * i + 1] = __fmaf_rn(x1, g.w, __fmul_rn(x0, g.y));
+  }
+}
+
+__device__ __forceinline__ void load4(const uint16_t* row, int cl, int is_fp16, float x[4]) {
+  const uint2 w = *reinterpret_cast<const uint2*>(row + 4 * cl);
+  x[0] = h2f(static_cast<uint16_t>(w.x & 0xffff), is_fp16);
+  x[1] = h2f(static_cast<uint16_t>(w.x >> 16), is_fp16);
+  x[2] = h2f(static_cast<uint16_t>(w.y & 0xffff), is_fp16);
+  x[3] = h2f(static_cast<uint16_t>(w.y >> 16), is_fp16);
+}
+
+// Computes the rotated values z of the thread's 4 channels for the 16 rows of
+// the tile.  Rows beyond N give zeros.  ybuf: [8][128] floats of LDS.
+__device__ __forceinline__ void rope_tile(const RopeTables& t, const QkArgs& a, int bh, int tile, float (*ybuf)[kD],
+                                          float z[16][4]) {
+  const int tid = threadIdx.x, rr = tid >> 5, cl = tid & 31;
+  const PairSetup ps = pair_setup(t, cl);
+  const float invW = 1.0f / static_cast<float>(t.grid[2]);
+  const float invHW = 1.0f / static_cast<float>(t.grid[2] * t.grid[1]);
+  const bool half = t.rotation == 2;
+  HalfSetup hs;
+  if (half) hs = half_setup(t, cl);
+  const uint16_t* xb = a.x + static_cast<size_t>(bh) * a.N * kD;
+  for (int p = 0; p < 16; ++p) {
+    const int n = tile * kTile + p * 8 + rr;
+    float y[4] = {0.f, 0.f, 0.f, 0.f};
+    if (n < a.N) {
+      float x[4];
+      load4(xb + static_cast<size_t>(n) * kD, cl, a.is_fp16, x);
+      rope4(t, ps, n, invW, invHW, x, y);
+    }
+    if (half) {
+      __syncthreads();
+      *reinterpret_cast<float4*>(&ybuf[rr][4 * cl]) = make_float4(y[0], y[1], y[2], y[3]);
+      __syncthreads();
+#pragma unroll
+      for (int i = 0; i < 2; ++i) {
+        const float av = ybuf[rr][hs.ia[i]], bv = ybuf[rr][hs.ib[i]];
+        const float4 r = hs.r[i];
+        y[2 * i] = __fmaf_rn(bv, r.z, __fmul_rn(av, r.x));
+        y[2 * i + 1] = __fmaf_rn(bv, r.w, __fmul_rn(av, r.y));
+      }
+      if (n >= a.N) y[0] = y[1] = y[2] = y[3] = 0.f;
+    }
+#pragma unroll
+    for (int c = 0; c < 4; ++c) z[p][c] = y[c];
+  }
+}
+
+__device__ __forceinline__ double fixq(float v) {
+  float s = __fmul_rn(v, kFix);
+  s = fminf(fmaxf(s, -kFixLim), kFixLim);
+  return static_cast<double>(__builtin_rintf(s));
+}
+
+// Reduces the per-thread fixed-point sums over the 8 row groups and writes the
+// tile's partial sums [128] (binary64 integers).
+__device__ __forceinline__ void write_partial(double acc[4], double* out) {
+  __shared__ double red[8][kD];
+  const int tid = threadIdx.x, rr = tid >> 5, cl = tid & 31;
+#pragma unroll
+  for (int c = 0; c < 4; ++c) red[rr][4 * cl + c] = acc[c];
+  __syncthreads();
+  if (tid < kD) {
+    double s = 0.0;
+#pragma unroll
+    for (int r = 0; r < 8; ++r) s += red[r][tid];
+    out[tid] = s;
+  }
+}
+
+__global__ __launch_bounds__(256) void k_qk_sums(RopeTables t, QkArgs a) {
+  __shared__ float ybuf[8][kD];
+  const int tile = blockIdx.x, bh = blockIdx.y;
+  float z[16][4];
+  rope_tile(t, a, bh, tile, ybuf, z);
+  double acc[4] = {0.0, 0.0, 0.0, 0.0};
+#pragma unroll
+  for (int p = 0; p < 16; ++p)
+#pragma unroll
+    for (int c = 0; c < 4; ++c) acc[c] += fixq(z[p][c]);
+  const int ntiles = a.Npad / kTile;
+  write_partial(acc, a.partial + (static_cast<size_t>(bh) * ntiles + tile) * kD);
+}
+
+__global__ __launch_bounds__(128) void k_mu_reduce(const double* partial, float* mu, int ntiles, int N) {
+  const int bh = blockIdx.x, ch = threadIdx.x;
+  const double* p = partial + static_cast<size_t>(bh) * ntiles * kD + ch;
+  double s = 0.0;
+  for (int i = 0; i < ntiles; ++i) s += p[static_cast<size_t>(i) * kD];
+  mu[bh * kD + ch] = static_cast<float>(s / (static_cast<double>(N) * 1048576.0));
+}
+
+__device__ __forceinline__ int qcode(float z, float inv) {
+  float c = __builtin_rintf(__fmul_rn(z, inv));
+  c = fminf(fmaxf(c, -7.0f), 7.0f);
+  return static_cast<int>(c);
+}
+
+__global__ __launch_bounds__(256) void k_qk_quant(RopeTables t, QkArgs a) {
+  __shared__ float ybuf[8][kD];
+  __shared__ float rowmax[kTile];
+  __shared__ float ginv[kTile];
+  __shared__ __align__(16) uint8_t ctile[kTile * 64];
+  const int tile = blockIdx.x, bh = blockIdx.y;
+  const int tid = threadIdx.x, rr = tid >> 5, cl = tid & 31;
+  float z[16][4];
+  rope_tile(t, a, bh, tile, ybuf, z);
+  if (a.mu) {
+    const float4 m = *reinterpret_cast<const float4*>(a.mu + bh * kD + 4 * cl);
+    for (int p = 0; p < 16; ++p) {
+      const int n = tile * kTile + p * 8 + rr;
+      if (n < a.N) {
+        z[p][0] = __fsub_rn(z[p][0], m.x);
+        z[p][1] = __fsub_rn(z[p][1], m.y);
+        z[p][2] = __fsub_rn(z[p][2], m.z);
+        z[p][3] = __fsub_rn(z[p][3], m.w);
+      }
+    }
+  }
+  // row abs-max over the 128 channels (32 threads of the row)
+  for (int p = 0; p < 16; ++p) {
+    float v = fmaxf(fmaxf(fabsf(z[p][0]), fabsf(z[p][1])), fmaxf(fabsf(z[p][2]), fabsf(z[p][3])));
+#pragma unroll
+    for (int off = 16; off >= 1; off >>= 1) v = fmaxf(v, __shfl_xor(v, off, 32));
+    if (cl == 0) rowmax[p * 8 + rr] = v;
+  }
+  __syncthreads();
+  const int g = a.group, ng = kTile / g;
+  if (tid < ng) {
+    float m = 0.f;
+    for (int i = 0; i < g; ++i) m = fmaxf(m, rowmax[tid * g + i]);
+    float s = 0.f, inv = 0.f;
+    if (m > 0.f) {
+      s = __fdiv_rn(m, 7.0f);
+      inv = __fdiv_rn(7.0f, m);
+    }
+    ginv[tid] = inv;
+    a.scales[static_cast<size_t>(bh) * (a.Npad / g) + tile * ng + tid] = s;
+  }
+  __syncthreads();
+  for (int p = 0; p < 16; ++p) {
+    const int nl = p * 8 + rr;
+    const float inv = ginv[nl / g];
+    const int c0 = qcode(z[p][0], inv), c1 = qcode(z[p][1], inv);
+    const int c2 = qcode(z[p][2], inv), c3 = qcode(z[p][3], inv);
+    const uint32_t b0 = (c0 & 0xF) | ((c1 & 0xF) << 4);
+    const uint32_t b1 = (c2 & 0xF) | ((c3 & 0xF) << 4);
+    // tiled layout: ((chunk*8 + unit)*32 + row)*8 + byte, pair j = 2*cl -> unit cl/4, byte 2*(cl%4)
+    const int off = (((nl >> 5) * 8 + (cl >> 2)) * 32 + (nl & 31)) * 8 + 2 * (cl & 3);
+    *reinterpret_cast<uint16_t*>(&ctile[off]) = static_cast<uint16_t>(b0 | (b1 << 8));
+  }
+  __syncthreads();
+  uint8_t* dst = a.codes + static_cast<size_t>(bh) * a.Npad * 64 + static_cast<size_t>(tile) * kTile * 64;
+#pragma unroll
+  for (int i = 0; i < 2; ++i) {
+    const int o = (i * 256 + tid) * 16;
+    *reinterpret_cast<uint4*>(dst + o) = *reinterpret_cast<const uint4*>(&ctile[o]);
+  }
+}
+
+// ------------------------------------------------------------------ V --
+
+__device__ __forceinline__ void load_v_tile(const VArgs& a, int bh, int tile, float z[16][4]) {
+  const int tid = threadIdx.x, rr = tid >> 5, cl = tid & 31;
+  const uint16_t* xb = a.x + static_cast<size_t>(bh) * a.N * kD;
+  float4 m = make_float4(0.f, 0.f, 0.f, 0.f);
+  if (a.mu) m = *reinterpret_cast<const float4*>(a.mu + bh * kD + 4 * cl);
+  for (int p = 0; p < 16; ++p) {
+    const int n = tile * kTile + p * 8 + rr;
+    if (n < a.N) {
+      float x[4];
+      load4(xb + static_cast<size_t>(n) * kD, cl, a.is_fp16, x);
+      if (a.mu) {
+        x[0] = __fsub_rn(x[0], m.x);
+        x[1] = __fsub_rn(x[1], m.y);
+        x[2] = __fsub_rn(x[2], m.z);
+        x[3] = __fsub_rn(x[3], m.w);
+      }
+#pragma unroll
+      for (int c = 0; c < 4; ++c) z[p][c] = x[c];
+    } else {
+#pragma unroll
+      for (int c = 0; c < 4; ++c) z[p][c] = 0.f;
+    }
+  }
+}
+
+__global__ __launch_bounds__(256) void k_v_sums(VArgs a) {
+  const int tile = blockIdx.x, bh = blockIdx.y;
+  VArgs b = a;
+  b.mu = nullptr;
+  float z[16][4];
+  load_v_tile(b, bh, tile, z);
+  double acc[4] = {0.0, 0.0, 0.0, 0.0};
+#pragma unroll
+  for (int p = 0; p < 16; ++p)
+#pragma unroll
+    for (int c = 0; c < 4; ++c) acc[c] += fixq(z[p][c]);
+  const int ntiles = a.Npad / kTile;
+  write_partial(acc, a.partial + (static_cast<size_t>(bh) * ntiles + tile) * kD);
+}
+
+__device__ __forceinline__ int vgroup_of(const VArgs& a, int n) {
+  int g = n / a.group;
+  return g < a.ngroups ? g : a.ngroups - 1;
+}
+
+// Per (tile half, channel) abs-max, merged into the group maxima with an
+// order-independent atomic max on the float bits (values are >= 0).
+__global__ __launch_bounds__(256) void k_v_amax(VArgs a) {
+  __shared__ float red[8][2][kD];
+  const int tile = blockIdx.x, bh = blockIdx.y;
+  const int tid = threadIdx.x, rr = tid >> 5, cl = tid & 31;
+  float z[16][4];
+  load_v_tile(a, bh, tile, z);
+  float m[2][4] = {{0.f, 0.f, 0.f, 0.f}, {0.f, 0.f, 0.f, 0.f}};
+  for (int p = 0; p < 16; ++p)
+#pragma unroll
+    for (int c = 0; c < 4; ++c) m[p >> 3][c] = fmaxf(m[p >> 3][c], fabsf(z[p][c]));
+#pragma unroll
+  for (int hf = 0; hf < 2; ++hf)
+#pragma unroll
+    for (int c = 0; c < 4; ++c) red[rr][hf][4 * cl + c] = m[hf][c];
+  __syncthreads();
+  const int hf = tid >> 7, ch = tid & 127;
+  const int n0 = tile * kTile + hf * 64;
+  if (n0 < a.N) {
+    float v = 0.f;
+#pragma unroll
+    for (int r = 0; r < 8; ++r) v = fmaxf(v, red[r][hf][ch]);
+    const int g = vgroup_of(a, n0);
+    atomicMax(a.amax + (static_cast<size_t>(bh) * a.ngroups + g) * kD + ch, __float_as_uint(v));
+  }
+}
+
+__global__ __launch_bounds__(256) void k_v_quant(VArgs a) {
+  __shared__ __align__(16) uint8_t ctile[kTile * 64];
+  __shared__ float ginv[2][kD];
+  const int tile = blockIdx.x, bh = blockIdx.y;
+  const int tid = threadIdx.x, rr = tid >> 5, cl = tid & 31;
+  {
+    const int hf = tid >> 7, ch = tid & 127;
+    const int n0 = tile * kTile + hf * 64;
+    const int g = vgroup_of(a, n0 < a.N ? n0 : a.N - 1);
+    const float m = __uint_as_float(a.amax[(static_cast<size_t>(bh) * a.ngroups + g) * kD + ch]);
+    float s = 0.f, inv = 0.f;
+    if (m > 0.f) {
+      s = __fdiv_rn(m, 7.0f);
+      inv = __fdiv_rn(7.0f, m);
+    }
+    ginv[hf][ch] = inv;
+    // the tile half holding the first token of group g writes its scales
+    if (n0 < a.N && g * a.group >= n0 && g * a.group < n0 + 64)
+      a.scales[(static_cast<size_t>(bh) * a.ngroups + g) * kD + ch] = s;
+  }
+  __syncthreads();
+  float z[16][4];
+  load_v_tile(a, bh, tile, z);
+  // token kappa = (p%4)*8 + rr inside chunk p/4; nibble np = 8*(kappa/16) + 2*(kappa%4) + (kappa/8)%2,
+  // half h = (kappa/4)%2; byte ((chunk*2 + h)*128 + ch)*8 + np/2.  Passes p and p+1 (p even)
+  // share every byte (np differs in its low bit only).
+  for (int p = 0; p < 16; p += 2) {
+    const int chunk = p >> 2;
+    const int kap = (p & 3) * 8 + rr;
+    const int np = 8 * (kap >> 4) + 2 * (kap & 3);  // even nibble (pass p), odd = pass p+1
+    const int hh = (kap >> 2) & 1;
+#pragma unroll
+    for (int c = 0; c < 4; ++c) {
+      const int ch = 4 * cl + c;
+      const float inv = ginv[(p * 8) >= 64 ? 1 : 0][ch];
+      const int lo = qcode(z[p][c], inv), hi = qcode(z[p + 1][c], inv);
+      ctile[((chunk * 2 + hh) * kD + ch) * 8 + (np >> 1)] = static_cast<uint8_t>((lo & 0xF) | ((hi & 0xF) << 4));
+    }
+  }
+  __syncthreads();
+  uint8_t* dst = a.codes + static_cast<size_t>(bh) * a.Npad * 64 + static_cast<size_t>(tile) * kTile * 64;
+#pragma unroll
+  for (int i = 0; i < 2; ++i) {
+    const int o = (i * 256 + tid) * 16;
+    *reinterpret_cast<uint4*>(dst + o) = *reinterpret_cast<const uint4*>(&ctile[o]);
+  }
+}
+
+__global__ void k_fill_zero_u32(uint32_t* p, int64_t n) {
+  for (int64_t i = blockIdx.x * static_cast<int64_t>(blockDim.x) + threadIdx.x; i < n;
+       i += static_cast<int64_t>(gridDim.x) * blockDim.x)
+    p[i] = 0u;
+}
+
+}  // namespace
+
+hipError_t launch_qk_sums(const RopeTables& t, const QkArgs& a, int BH, hipStream_t s) {
+  hipLaunchKernelGGL(k_qk_sums, dim3(a.Npad / kTile, BH), dim3(256), 0, s, t, a);
+  return hipGetLastError();
+}
+
+hipError_t launch_mu_reduce(const double* partial, float* mu, int BH, int ntiles, int N, hipStream_t s) {
+  hipLaunchKernelGGL(k_mu_reduce, dim3(BH), dim3(kD), 0, s, partial, mu, ntiles, N);
+  return hipGetLastError();
+}
+
+hipError_t launch_qk_quant(const RopeTables& t, const QkArgs& a, int BH, hipStream_t s) {
+  hipLaunchKernelGGL(k_qk_quant, dim3(a.Npad / kTile, BH), dim3(256), 0, s, t, a);
+  return hipGetLastError();
+}
+
+hipError_t launch_fill_zero_u32(uint32_t* p, int64_t n, hipStream_t s) {
+  int64_t blocks = (n + 255) / 256;
+  if (blocks > 4096) blocks = 4096;
+  if (blocks < 1) blocks = 1;
+  hipLaunchKernelGGL(k_fill_zero_u32, dim3(static_cast<unsigned>(blocks)), dim3(256), 0, s, p, n);
+  return hipGetLastError();
+}
+
+hipError_t launch_v_sums(const VArgs& a, int BH, hipStream_t s) {
+  hipLaunchKernelGGL(k_v_sums, dim3(a.Npad / kTile, BH), dim3(256), 0, s, a);
+  return hipGetLastError();
+}
+
+hipError_t launch_v_amax(const VArgs& a, int BH, hipStream_t s) {
+  hipLaunchKernelGGL(k_v_amax, dim3(a.Npad / kTile, BH), dim3(256), 0, s, a);
+  return hipGetLastError();
+}
+
+hipError_t launch_v_quant(const VArgs& a, int BH, hipStream_t s) {
+  hipLaunchKernelGGL(k_v_quant, dim3(a.Npad / kTile, BH), dim3(256), 0, s, a);
+  return hipGetLastError();
+}
+
+}  // namespace ra

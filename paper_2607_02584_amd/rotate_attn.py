@@ -1,0 +1,218 @@
+"""Thin ctypes binding of librotate_attn.so (argument marshalling only).
+
+Every step of the path runs in the HIP kernels of the library; this module
+only turns torch tensors into device pointers, fills ``ra_params`` and raises
+on a non-zero status.  If the library is not built the import of the first
+call fails loudly: there is no fallback.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+
+import numpy as np
+
+HERE = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(HERE, "librotate_attn.so")
+
+ROT_NONE, ROT_INTERLEAVED, ROT_HALF = 0, 1, 2
+PQ_RANGE15, PQ_SYM7 = 0, 1
+SMOOTH_K, SMOOTH_V = 1, 2
+BF16, FP16, FP32 = 0, 1, 2
+PATH_INT4, PATH_FP16 = 0, 1
+
+
+class RAError(RuntimeError):
+    def __init__(self, status: int, where: str, message: str):
+        super().__init__(f"{where} failed with status {status}: {message}")
+        self.status = status
+
+
+class Params(ctypes.Structure):
+    _fields_ = [
+        ("B", ctypes.c_int32), ("H", ctypes.c_int32), ("N", ctypes.c_int32), ("D", ctypes.c_int32),
+        ("grid", ctypes.c_int32 * 3), ("rope_split", ctypes.c_int32 * 3), ("rope_theta", ctypes.c_float),
+        ("rotation", ctypes.c_int32), ("rot_blocks", ctypes.POINTER(ctypes.c_double)),
+        ("p_quant", ctypes.c_int32), ("smooth", ctypes.c_int32),
+        ("q_group", ctypes.c_int32), ("k_group", ctypes.c_int32), ("v_group", ctypes.c_int32),
+        ("kv_block", ctypes.c_int32), ("sm_scale", ctypes.c_float),
+        ("in_dtype", ctypes.c_int32), ("out_dtype", ctypes.c_int32),
+    ]
+
+
+class Layout(ctypes.Structure):
+    _fields_ = [("n_pad", ctypes.c_int64), ("qk_code_bytes", ctypes.c_int64), ("q_scale_count", ctypes.c_int64),
+                ("k_scale_count", ctypes.c_int64), ("v_code_bytes", ctypes.c_int64),
+                ("v_scale_count", ctypes.c_int64), ("mu_count", ctypes.c_int64)]
+
+
+_lib = None
+
+
+def lib():
+    global _lib
+    if _lib is None:
+        if not os.path.exists(LIB_PATH):
+            raise RuntimeError(f"{LIB_PATH} is missing: build it with __graft_entry__.build() "
+                               "(python -c 'import __graft_entry__ as g; g.build()')")
+        L = ctypes.CDLL(LIB_PATH)
+        P = ctypes.c_void_p
+        PP = ctypes.POINTER(Params)
+        sig = {
+            "rotate_attn_layout": [PP, ctypes.POINTER(Layout)],
+            "rotate_attn_workspace_size": [PP, ctypes.c_int, ctypes.POINTER(ctypes.c_size_t)],
+            "rotate_attn_quantize_qk": [PP, P, P, P, P, P, P, P, P, ctypes.c_size_t, P],
+            "rotate_attn_quantize_v": [PP, P, P, P, P, P, ctypes.c_size_t, P],
+            "rotate_attn_attn_int4": [PP, P, P, P, P, P, P, P, P, P],
+            "rotate_attn_attn_int4_debug": [PP, P, P, P, P, P, P, P, P, ctypes.c_int32, ctypes.c_int32,
+                                            ctypes.c_int32, P, P, P, P],
+            "rotate_attn_fwd_int4": [PP, P, P, P, P, P, ctypes.c_size_t, P],
+            "rotate_attn_prepare_fp16": [PP, P, P, P, P, ctypes.c_size_t, P],
+            "rotate_attn_attn_fp16": [PP, P, ctypes.c_size_t, P, P],
+            "rotate_attn_fwd_fp16": [PP, P, P, P, P, P, ctypes.c_size_t, P],
+            "rotate_attn_fwd": [PP, ctypes.c_int, P, P, P, P, P, ctypes.c_size_t, P],
+        }
+        for name, args in sig.items():
+            fn = getattr(L, name)
+            fn.argtypes = args
+            fn.restype = ctypes.c_int
+        L.rotate_attn_error_string.argtypes = [ctypes.c_int]
+        L.rotate_attn_error_string.restype = ctypes.c_char_p
+        L.rotate_attn_last_error.argtypes = []
+        L.rotate_attn_last_error.restype = ctypes.c_char_p
+        _lib = L
+    return _lib
+
+
+def _check(status: int, where: str):
+    if status != 0:
+        raise RAError(status, where, lib().rotate_attn_last_error().decode())
+
+
+def make_params(B, H, grid, split=(44, 42, 42), theta=10000.0, *, rotation=ROT_INTERLEAVED, rot_blocks=None,
+                p_quant=PQ_RANGE15, smooth=SMOOTH_K | SMOOTH_V, q_group=128, k_group=128, v_group=128,
+                kv_block=128, sm_scale=0.0, in_dtype=BF16, out_dtype=BF16, D=128) -> Params:
+    p = Params()
+    p.B, p.H, p.D = B, H, D
+    p.N = int(grid[0] * grid[1] * grid[2])
+    p.grid[:] = [int(g) for g in grid]
+    p.rope_split[:] = [int(s) for s in split]
+    p.rope_theta = float(theta)
+    p.rotation = rotation
+    if rot_blocks is not None:
+        arr = np.ascontiguousarray(rot_blocks, dtype=np.float64).reshape(D // 2, 2, 2)
+        p._rot_keep = arr  # keep alive with the struct
+        p.rot_blocks = arr.ctypes.data_as(ctypes.POINTER(ctypes.c_double))
+    p.p_quant, p.smooth = p_quant, smooth
+    p.q_group, p.k_group, p.v_group, p.kv_block = q_group, k_group, v_group, kv_block
+    p.sm_scale = float(sm_scale)
+    p.in_dtype, p.out_dtype = in_dtype, out_dtype
+    return p
+
+
+def layout(p: Params) -> dict:
+    out = Layout()
+    _check(lib().rotate_attn_layout(ctypes.byref(p), ctypes.byref(out)), "rotate_attn_layout")
+    return {f: getattr(out, f) for f, _ in Layout._fields_}
+
+
+def workspace_size(p: Params, path: int) -> int:
+    n = ctypes.c_size_t()
+    _check(lib().rotate_attn_workspace_size(ctypes.byref(p), path, ctypes.byref(n)), "rotate_attn_workspace_size")
+    return n.value
+
+
+def _ptr(t):
+    if t is None:
+        return None
+    return ctypes.c_void_p(t.data_ptr())
+
+
+def _stream(stream):
+    if stream is not None:
+        return ctypes.c_void_p(stream)
+    import torch
+    return ctypes.c_void_p(torch.cuda.current_stream().cuda_stream)
+
+
+def _nbytes(t) -> int:
+    return t.numel() * t.element_size()
+
+
+def quantize_qk(p, q, k, q_codes, q_scale, k_codes, k_scale, mu_k, ws, stream=None):
+    _check(lib().rotate_attn_quantize_qk(ctypes.byref(p), _ptr(q), _ptr(k), _ptr(q_codes), _ptr(q_scale),
+                                         _ptr(k_codes), _ptr(k_scale), _ptr(mu_k), _ptr(ws), _nbytes(ws),
+                                         _stream(stream)), "rotate_attn_quantize_qk")
+
+
+def quantize_v(p, v, v_codes, v_scale, mu_v, ws, stream=None):
+    _check(lib().rotate_attn_quantize_v(ctypes.byref(p), _ptr(v), _ptr(v_codes), _ptr(v_scale), _ptr(mu_v),
+                                        _ptr(ws), _nbytes(ws), _stream(stream)), "rotate_attn_quantize_v")
+
+
+def attn_int4(p, q_codes, q_scale, k_codes, k_scale, v_codes, v_scale, mu_v, o, stream=None):
+    _check(lib().rotate_attn_attn_int4(ctypes.byref(p), _ptr(q_codes), _ptr(q_scale), _ptr(k_codes), _ptr(k_scale),
+                                       _ptr(v_codes), _ptr(v_scale), _ptr(mu_v), _ptr(o), _stream(stream)),
+           "rotate_attn_attn_int4")
+
+
+def attn_int4_debug(p, q_codes, q_scale, k_codes, k_scale, v_codes, v_scale, mu_v, o, bh, row0, rows,
+                    s_out=None, u_out=None, m_out=None, stream=None):
+    _check(lib().rotate_attn_attn_int4_debug(ctypes.byref(p), _ptr(q_codes), _ptr(q_scale), _ptr(k_codes),
+                                             _ptr(k_scale), _ptr(v_codes), _ptr(v_scale), _ptr(mu_v), _ptr(o),
+                                             bh, row0, rows, _ptr(s_out), _ptr(u_out), _ptr(m_out),
+                                             _stream(stream)), "rotate_attn_attn_int4_debug")
+
+
+def fwd_int4(p, q, k, v, o, ws, stream=None):
+    _check(lib().rotate_attn_fwd_int4(ctypes.byref(p), _ptr(q), _ptr(k), _ptr(v), _ptr(o), _ptr(ws), _nbytes(ws),
+                                      _stream(stream)), "rotate_attn_fwd_int4")
+
+
+def prepare_fp16(p, q, k, v, ws, stream=None):
+    _check(lib().rotate_attn_prepare_fp16(ctypes.byref(p), _ptr(q), _ptr(k), _ptr(v), _ptr(ws), _nbytes(ws),
+                                          _stream(stream)), "rotate_attn_prepare_fp16")
+
+
+def attn_fp16(p, ws, o, stream=None):
+    _check(lib().rotate_attn_attn_fp16(ctypes.byref(p), _ptr(ws), _nbytes(ws), _ptr(o), _stream(stream)),
+           "rotate_attn_attn_fp16")
+
+
+def fwd_fp16(p, q, k, v, o, ws, stream=None):
+    _check(lib().rotate_attn_fwd_fp16(ctypes.byref(p), _ptr(q), _ptr(k), _ptr(v), _ptr(o), _ptr(ws), _nbytes(ws),
+                                      _stream(stream)), "rotate_attn_fwd_fp16")
+
+
+def fwd(p, fallback, q, k, v, o, ws, stream=None):
+    _check(lib().rotate_attn_fwd(ctypes.byref(p), int(bool(fallback)), _ptr(q), _ptr(k), _ptr(v), _ptr(o), _ptr(ws),
+                                 _nbytes(ws), _stream(stream)), "rotate_attn_fwd")
+
+
+# ---------------------------------------------------------------- helpers --
+
+def alloc_int4(p: Params, device="cuda"):
+    """Caller-side buffers for the quantize / attention entry points."""
+    import torch
+    L = layout(p)
+    return dict(
+        q_codes=torch.zeros(L["qk_code_bytes"], dtype=torch.uint8, device=device),
+        k_codes=torch.zeros(L["qk_code_bytes"], dtype=torch.uint8, device=device),
+        v_codes=torch.zeros(L["v_code_bytes"], dtype=torch.uint8, device=device),
+        q_scale=torch.zeros(L["q_scale_count"], dtype=torch.float32, device=device),
+        k_scale=torch.zeros(L["k_scale_count"], dtype=torch.float32, device=device),
+        v_scale=torch.zeros(L["v_scale_count"], dtype=torch.float32, device=device),
+        mu_k=torch.zeros(L["mu_count"], dtype=torch.float32, device=device),
+        mu_v=torch.zeros(L["mu_count"], dtype=torch.float32, device=device),
+    )
+
+
+def workspace(p: Params, path: int, device="cuda"):
+    import torch
+    return torch.empty(max(workspace_size(p, path), 256), dtype=torch.uint8, device=device)
+
+
+def to_device_bits(x_bits: np.ndarray, device="cuda"):
+    """uint16 bit patterns -> int16 device tensor holding the same bits."""
+    import torch
+    return torch.from_numpy(np.ascontiguousarray(x_bits).view(np.int16)).to(device)

@@ -1,0 +1,103 @@
+"""C ABI checks that need no GPU: the library loads, exports every function the
+header declares, and rejects bad arguments before any HIP call."""
+import ctypes
+import os
+import re
+
+import pytest
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "rotate_attn.h")
+
+
+def _ra():
+    from paper_2607_02584_amd import rotate_attn as ra
+    if not os.path.exists(ra.LIB_PATH):
+        pytest.skip("library not built")
+    return ra
+
+
+def declared_functions():
+    text = open(HEADER).read()
+    return sorted(set(re.findall(r"^(?:int|const char\*)\s+(rotate_attn_\w+)\(", text, re.M)))
+
+
+def test_header_declares_the_entry_points():
+    names = declared_functions()
+    for n in ["rotate_attn_quantize_qk", "rotate_attn_fwd_int4", "rotate_attn_fwd_fp16", "rotate_attn_quantize_v",
+              "rotate_attn_attn_int4", "rotate_attn_fwd", "rotate_attn_workspace_size"]:
+        assert n in names
+
+
+def test_library_exports_every_declared_symbol():
+    ra = _ra()
+    L = ctypes.CDLL(ra.LIB_PATH)
+    for n in declared_functions():
+        assert hasattr(L, n), n
+
+
+def _base(ra, **kw):
+    return ra.make_params(1, 2, (4, 16, 16), **kw)
+
+
+@pytest.mark.parametrize("field,value,status", [
+    ("D", 64, -2),
+    ("N", 1000, -1),           # T*Hg*W != N
+    ("B", 0, -1),
+    ("rope_split", (44, 42, 40), -1),
+    ("rope_split", (43, 43, 42), -1),
+    ("rope_theta", 0.0, -1),
+    ("rotation", 3, -1),
+    ("p_quant", 5, -1),
+    ("smooth", 4, -1),
+    ("q_group", 3, -2),
+    ("k_group", 16, -2),
+    ("kv_block", 32, -2),
+    ("v_group", 96, -2),       # not a multiple of kv_block and < N
+    ("in_dtype", 2, -1),
+    ("out_dtype", 7, -1),
+    ("sm_scale", -1.0, -1),
+])
+def test_validation_rejects(field, value, status):
+    ra = _ra()
+    p = _base(ra)
+    if field == "rope_split":
+        p.rope_split[:] = list(value)
+    else:
+        setattr(p, field, value)
+    with pytest.raises(ra.RAError) as e:
+        ra.layout(p)
+    assert e.value.status == status
+
+
+def test_validation_accepts_defaults_and_reports_sizes():
+    ra = _ra()
+    p = _base(ra)
+    L = ra.layout(p)
+    assert L["n_pad"] == 1024 and L["qk_code_bytes"] == 2 * 1024 * 64 and L["v_scale_count"] == 2 * 8 * 128
+    assert ra.workspace_size(p, ra.PATH_INT4) > 3 * L["qk_code_bytes"]
+    assert ra.workspace_size(p, ra.PATH_FP16) >= 3 * 2 * 1024 * 128 * 2
+    p2 = ra.make_params(1, 1, (3, 7, 11), v_group=10 ** 6)
+    assert ra.layout(p2)["n_pad"] == 256 and ra.layout(p2)["v_scale_count"] == 128
+
+
+def test_null_pointers_and_workspace_errors_before_gpu():
+    ra = _ra()
+    L = ra.lib()
+    p = _base(ra)
+    P = ctypes.c_void_p
+    # NULL tensors -> RA_ERR_INVALID; no GPU call happens on this path
+    st = L.rotate_attn_fwd_int4(ctypes.byref(p), None, None, None, None, None, 0, None)
+    assert st == -1 and b"NULL" in L.rotate_attn_last_error()
+    fake = P(0x1000)
+    st = L.rotate_attn_fwd_int4(ctypes.byref(p), fake, fake, fake, fake, None, 0, None)
+    assert st == -3
+    st = L.rotate_attn_fwd_int4(ctypes.byref(p), fake, fake, fake, fake, P(0x1001), 1 << 30, None)
+    assert st == -3  # misaligned
+    st = L.rotate_attn_fwd_fp16(ctypes.byref(p), fake, fake, fake, fake, P(0x1000), 16, None)
+    assert st == -3  # too small
+    st = L.rotate_attn_attn_int4_debug(ctypes.byref(p), fake, fake, fake, fake, fake, fake, None, fake, 5, 0, 1,
+                                       None, None, None, None)
+    assert st == -1  # bh out of range
+    assert L.rotate_attn_error_string(-4) == b"HIP runtime error"
+    assert L.rotate_attn_fwd_int4(None, fake, fake, fake, fake, fake, 1 << 30, None) == -1

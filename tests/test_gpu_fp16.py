@@ -1,0 +1,71 @@
+"""GPU parity of the BF16/FP16 fallback attention against the CPU oracle."""
+import numpy as np
+import pytest
+
+pytestmark = pytest.mark.gpu
+
+O_TOL = 2e-3
+
+
+def _torch():
+    import torch
+    if not torch.cuda.is_available():
+        pytest.skip("no GPU")
+    return torch
+
+
+def _ra():
+    from paper_2607_02584_amd import rotate_attn as ra
+    ra.lib()
+    return ra
+
+
+def _f32_to_f16_bits(x):
+    return np.asarray(x, np.float32).astype(np.float16).view(np.uint16)
+
+
+@pytest.mark.parametrize("wname,dtype", [("c1", "bf16"), ("ragged", "bf16"), ("c1", "fp16")])
+def test_fp16_fallback_parity(ora, wname, dtype):
+    torch, ra = _torch(), _ra()
+    from paper_2607_02584_amd import datagen as dg
+    w = dg.WORKLOADS["c1"] if wname == "c1" else dg.small_workload("ragged", 3, 7, 11, H=2, seed=21)
+    print(f"[fp16 parity] {wname} {dtype} N={w.N}", flush=True)
+    q, k, v = dg.make_inputs(w)
+    if dtype == "fp16":
+        # fp16 inputs: the same values expressed in binary16 (bf16 values fit exactly unless tiny)
+        q, k, v = (_f32_to_f16_bits(dg.bf16_bits_to_f32(x)) for x in (q, k, v))
+    p = ra.make_params(w.B, w.H, (w.T, w.Hg, w.W), w.split, w.theta, rotation=0, in_dtype=ra.FP16 if dtype == "fp16"
+                       else ra.BF16, out_dtype=ra.FP32)
+    ws = ra.workspace(p, ra.PATH_FP16)
+    qd, kd, vd = (ra.to_device_bits(x) for x in (q, k, v))
+    o = torch.empty((w.B * w.H, w.N, 128), dtype=torch.float32, device="cuda")
+    ra.fwd_fp16(p, qd, kd, vd, o, ws)
+    o2 = torch.empty_like(o)
+    ra.fwd(p, True, qd, kd, vd, o2, ws)
+    torch.cuda.synchronize()
+    assert torch.equal(o, o2)
+    geo = ora.Geometry(w.T, w.Hg, w.W, w.split, w.theta)
+    for hh in range(w.H):
+        if dtype == "fp16":
+            # oracle on the fp16 inputs: RoPE in binary32, rounded to fp16, fp64 attention with P rounded to fp16
+            O_ref = _oracle_fp16(ora, geo, q[0, hh], k[0, hh], v[0, hh])
+        else:
+            O_ref = ora.fwd_fp16_head(geo, q[0, hh], k[0, hh], v[0, hh], kv_block=64)
+        og = o[hh].cpu().numpy()
+        err = np.abs(og - O_ref).max() / np.abs(O_ref).max()
+        print(f"  head {hh}: O rel err {err:.3e}", flush=True)
+        assert err <= O_TOL
+
+
+def _oracle_fp16(ora, geo, q16, k16, v16):
+    """fp16 inputs: reuse the oracle's binary32 RoPE on the exactly converted
+    values and an fp64 softmax; P rounded to fp16 is within the bf16 bound."""
+    from paper_2607_02584_amd import datagen as dg
+    qf = np.asarray(q16).view(np.float16).astype(np.float32)
+    kf = np.asarray(k16).view(np.float16).astype(np.float32)
+    vf = np.asarray(v16).view(np.float16).astype(np.float64)
+    # the binary16 values of these inputs are exactly bf16 values (they came from bf16)
+    qb, kb = dg.f32_to_bf16_bits(qf), dg.f32_to_bf16_bits(kf)
+    yq = ora.rope_rot_f32(geo, qb, ora.ROT_NONE).astype(np.float16).astype(np.float64)
+    yk = ora.rope_rot_f32(geo, kb, ora.ROT_NONE).astype(np.float16).astype(np.float64)
+    return ora.attn_ref_f64(yq, yk, vf)

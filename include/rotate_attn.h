@@ -37,6 +37,7 @@
  *  Npad = N rounded up to a multiple of 128; tokens n >= N hold zero codes.
  *  A code is a 4-bit two's-complement nibble in [-7, 7].
  *
+ *  INT4 container (code_format == RA_CODES_INT4):
  *  Q/K codes, per head (Npad * 64 bytes, heads contiguous, head bh at
  *  bh * Npad * 64): token n = 32*c + r, channel pair j (channels 2j and 2j+1)
  *  lives in byte ((c*8 + j/8)*32 + r)*8 + (j%8); channel 2j in the low nibble,
@@ -47,6 +48,15 @@
  *  nibble index is np = 8a + 2s + b; the code lives in byte
  *  ((c*2 + h)*128 + ch)*8 + np/2, low nibble when np is even.
  *  (This order makes each 32-token chunk an operand of the int8 matrix core.)
+ *
+ *  E2M3 container (code_format == RA_CODES_E2M3), Npad * 96 bytes per head.
+ *  A code c is the 6-bit E2M3 float equal to c (sign in bit 5, exponent bias 1,
+ *  3 mantissa bits); 32 codes form a 24-byte record, code f at bits [6f, 6f+6)
+ *  of the little-endian record.
+ *   Q/K: token n = 32*c + r, channel ch: record ((c*2 + ch/64)*2 + (ch/32)%2)*32 + r,
+ *        field ch%32.
+ *   V:   token n = 64*g + kappa, channel ch: record ((g*4 + ch/32)*2 + (kappa/4)%2)*32
+ *        + ch%32, field 8*(kappa%4) + 2*((kappa/8)%4) + kappa/32.
  *
  *  Scales are binary32.  Q scales: [B*H][Npad/q_group]; K scales:
  *  [B*H][Npad/k_group]; V scales: [B*H][ceil(N/v_group)][128].  Q/K groups
@@ -87,6 +97,11 @@ extern "C" {
 #define RA_FP16 1
 #define RA_FP32 2
 
+/* container of the INT4 codes (the code values are the same in both) */
+#define RA_CODES_INT4 0 /* two's-complement nibbles, two per byte (int8 matrix-core kernel) */
+#define RA_CODES_E2M3 1 /* each code as a 6-bit E2M3 float, the operand format of the
+                           FP6 matrix core: exact for integers in [-7, 7], twice the int8 rate */
+
 /* which forward a workspace is sized for */
 #define RA_PATH_INT4 0
 #define RA_PATH_FP16 1
@@ -107,6 +122,7 @@ typedef struct ra_params {
   float sm_scale;          /* softmax scale; 0 = 1/sqrt(D) */
   int32_t in_dtype;        /* RA_BF16 | RA_FP16 */
   int32_t out_dtype;       /* RA_BF16 | RA_FP16 | RA_FP32 */
+  int32_t code_format;     /* RA_CODES_*: container of the codes quantize_* write and attn_int4 reads */
 } ra_params;
 
 /* Sizes of the caller-visible INT4 buffers for these parameters. */

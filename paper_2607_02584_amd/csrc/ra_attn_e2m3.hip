@@ -1,0 +1,333 @@
+// ra_attn_e2m3.hip -- INT4 FlashAttention forward on the FP6 matrix core (gfx950).
+//
+// Same computation as the int8 kernel (the paper's Sec. 4.2 blockwise online
+// softmax with the Range-optimized P quantization over INT4 Q, K, V codes),
+// but every INT4 code is carried as the 6-bit E2M3 float of the same value.
+// E2M3 represents the integers -7..7 and the half-integers u/2, u = 0..15,
+// exactly, and the products and 64-term sums of the matrix core stay integer
+// multiples of 1/2 below 2^24, so
+//   S  = Q~ K~^T                         is the exact integer score, and
+//   O' += V~^T (u/2)                     is exact per block,
+// on v_mfma_scale_f32_32x32x64_f8f6f4, which runs at twice the int8 rate and
+// accumulates in binary32: PV accumulates straight into the output tile.
+//
+// Per block of KV keys (ascending):
+//   m_new = max(m, rowmax fl(S * c)),  x = fma(S, c, -m_new),  P = 2^x,
+//   u = rint(15 P),  l = alpha l + sum P,  alpha = 2^(m - m_new),
+//   O' = O' * alpha * (w_old / w_new) + V~^T (u/2)   (w = V scale of the block's group)
+// and finally O = O' * 2 w / 15 / l + mu_v.
+//
+// Matrix-core mapping (one wave = 32 queries): S^T = K Q^T (A = 32 keys x 64
+// channels of K, B = Q^T), so a lane holds 16 scores of one query per 32-key
+// chunk.  The P codes of two chunks (64 keys) are packed by
+// v_cvt_scalef32_2xpk16_fp6_f32 into the B operand of O^T = V^T P^T; the V
+// records are stored in the key order that packing produces.
+#include "ra_internal.h"
+
+namespace ra {
+namespace {
+
+typedef int v8i __attribute__((ext_vector_type(8)));
+typedef int v6i __attribute__((ext_vector_type(6)));
+typedef float v16f __attribute__((ext_vector_type(16)));
+
+constexpr int kBlockM = 128;  // queries per workgroup (4 waves x 32)
+constexpr int kScaleOne = 127;  // E8M0 block scale 2^0
+
+__device__ __forceinline__ v16f mfma6(v8i a, v8i b, v16f c) {
+  return __builtin_amdgcn_mfma_scale_f32_32x32x64_f8f6f4(a, b, c, 2, 2, 0, kScaleOne, 0, kScaleOne);
+}
+
+// 24-byte record -> operand registers (6 used dwords)
+__device__ __forceinline__ v8i load_rec(const uint8_t* p) {
+  const uint2 a = *reinterpret_cast<const uint2*>(p);
+  const uint2 b = *reinterpret_cast<const uint2*>(p + 8);
+  const uint2 c = *reinterpret_cast<const uint2*>(p + 16);
+  return v8i{static_cast<int>(a.x), static_cast<int>(a.y), static_cast<int>(b.x), static_cast<int>(b.y),
+             static_cast<int>(c.x), static_cast<int>(c.y), 0, 0};
+}
+
+template <int KV, bool KTOK, bool SYM7, bool DEBUG>
+__global__ __launch_bounds__(256, 2) void k_attn_e2m3(AttnArgs a) {
+  constexpr int NCH = KV / 32;   // 32-key chunks
+  constexpr int NG = KV / 64;    // 64-key groups (one PV instruction each)
+  constexpr int KB = KV * 96;    // bytes of K (and of V) codes per block
+  constexpr int NLD = (KB / 16 + 255) / 256;
+  __shared__ __align__(16) uint8_t sK[2][KB];
+  __shared__ __align__(16) uint8_t sV[2][KB];
+  __shared__ __align__(16) float sR[2][kD];   // V scale ratio w_old / w_new for the block
+  __shared__ __align__(16) float sW[kD];      // final V scale per channel
+  __shared__ __align__(16) float sKs[2][KTOK ? KV : 1];
+
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int hh = lane >> 5, j = lane & 31;
+  const int bh = blockIdx.y;
+  const int qrow = blockIdx.x * kBlockM + wave * 32 + j;
+  const int N = a.N;
+  const int nblocks = (N + KV - 1) / KV;
+  const int kstride = a.Npad / a.k_group;
+  const float pscale = SYM7 ? 7.0f : 15.0f;
+  const size_t hcode = static_cast<size_t>(bh) * a.Npad * 96;
+
+  // ---- Q operand (B of S^T = K Q^T) ----
+  v8i qop[2];
+  {
+    const uint8_t* qp = a.qc + hcode;
+#pragma unroll
+    for (int kc = 0; kc < 2; ++kc) {
+      const int rec = (((qrow >> 5) * 2 + kc) * 2 + hh) * 32 + (qrow & 31);
+      qop[kc] = load_rec(qp + static_cast<size_t>(rec) * 24);
+    }
+  }
+  const float cq = __fmul_rn(a.qs[static_cast<size_t>(bh) * (a.Npad / a.q_group) + qrow / a.q_group], a.Kc);
+
+  // V scale bookkeeping: thread ch < 128 owns channel ch's working scale w.
+  float wcur = 1.0f;
+  auto stage_aux = [&](int jb, int buf) {
+    if (tid < kD) {
+      int g = (jb * KV) / a.v_group;
+      if (g >= a.nvgroups) g = a.nvgroups - 1;
+      const float s = a.vs[(static_cast<size_t>(bh) * a.nvgroups + g) * kD + tid];
+      float r = 1.0f;
+      if (s > 0.0f) {
+        r = (jb == 0) ? 1.0f : __fdiv_rn(wcur, s);
+        wcur = s;
+      }
+      sR[buf][tid] = r;
+    }
+    if (KTOK && tid < KV) sKs[buf][tid] = a.ks[static_cast<size_t>(bh) * kstride + jb * KV + tid];
+  };
+
+  uint4 stk[NLD], stv[NLD];
+  auto load = [&](int jb) {
+    const uint8_t* kb = a.kc + hcode + static_cast<size_t>(jb) * KB;
+    const uint8_t* vb = a.vc + hcode + static_cast<size_t>(jb) * KB;
+#pragma unroll
+    for (int i = 0; i < NLD; ++i) {
+      const int o = (i * 256 + tid) * 16;
+      if (o < KB) {
+        stk[i] = *reinterpret_cast<const uint4*>(kb + o);
+        stv[i] = *reinterpret_cast<const uint4*>(vb + o);
+      }
+    }
+  };
+  auto store = [&](int buf) {
+#pragma unroll
+    for (int i = 0; i < NLD; ++i) {
+      const int o = (i * 256 + tid) * 16;
+      if (o < KB) {
+        *reinterpret_cast<uint4*>(&sK[buf][o]) = stk[i];
+        *reinterpret_cast<uint4*>(&sV[buf][o]) = stv[i];
+      }
+    }
+  };
+
+  v16f of[4];
+#pragma unroll
+  for (int mt = 0; mt < 4; ++mt)
+#pragma unroll
+    for (int r = 0; r < 16; ++r) of[mt][r] = 0.f;
+  float m = -INFINITY, l = 0.f;
+
+  load(0);
+  store(0);
+  stage_aux(0, 0);
+  __syncthreads();
+
+  for (int jb = 0; jb < nblocks; ++jb) {
+    const int buf = jb & 1;
+    const bool more = jb + 1 < nblocks;
+    if (more) load(jb + 1);
+    const int key0 = jb * KV;
+    const bool last = key0 + KV > N;
+
+    // ---- S^T = K Q^T: exact integer scores in binary32 ----
+    v16f s[NCH];
+#pragma unroll
+    for (int ch = 0; ch < NCH; ++ch) {
+#pragma unroll
+      for (int r = 0; r < 16; ++r) s[ch][r] = 0.f;
+#pragma unroll
+      for (int kc = 0; kc < 2; ++kc) {
+        const v8i A = load_rec(&sK[buf][((((ch * 2) + kc) * 2 + hh) * 32 + j) * 24]);
+        s[ch] = mfma6(A, qop[kc], s[ch]);
+      }
+    }
+
+    // key of accumulator register r in chunk ch: key0 + 32*ch + 8*(r/4) + 4*hh + r%4
+    float cch[NCH];
+    float tmax = -INFINITY;
+    if (!KTOK) {
+#pragma unroll
+      for (int ch = 0; ch < NCH; ++ch) {
+        const int kbase = key0 + ch * 32;
+        cch[ch] = __fmul_rn(cq, a.ks[static_cast<size_t>(bh) * kstride + kbase / a.k_group]);
+        if (kbase < N) {
+          float mx = -INFINITY;
+#pragma unroll
+          for (int r = 0; r < 16; ++r) {
+            const int key = kbase + 8 * (r >> 2) + 4 * hh + (r & 3);
+            if (!last || key < N) mx = fmaxf(mx, s[ch][r]);
+          }
+          if (mx != -INFINITY) tmax = fmaxf(tmax, __fmul_rn(mx, cch[ch]));
+        }
+      }
+    } else {
+#pragma unroll
+      for (int ch = 0; ch < NCH; ++ch)
+#pragma unroll
+        for (int r = 0; r < 16; ++r) {
+          const int kl = ch * 32 + 8 * (r >> 2) + 4 * hh + (r & 3);
+          if (!last || key0 + kl < N) tmax = fmaxf(tmax, __fmul_rn(s[ch][r], __fmul_rn(cq, sKs[buf][kl])));
+        }
+    }
+    tmax = fmaxf(tmax, __shfl_xor(tmax, 32));
+    const float mnew = fmaxf(m, tmax);
+    const float alpha = __builtin_amdgcn_exp2f(m - mnew);
+    m = mnew;
+
+    // ---- rescale O' for the new maximum and the block's V scale ----
+    const bool vchange = jb > 0 && a.nvgroups > 1 && ((jb * KV) % a.v_group) == 0;
+    if (vchange) {
+#pragma unroll
+      for (int mt = 0; mt < 4; ++mt)
+#pragma unroll
+        for (int rq = 0; rq < 4; ++rq) {
+          const float4 rr = *reinterpret_cast<const float4*>(&sR[buf][mt * 32 + 8 * rq + 4 * hh]);
+          of[mt][4 * rq + 0] = __fmul_rn(of[mt][4 * rq + 0], __fmul_rn(rr.x, alpha));
+          of[mt][4 * rq + 1] = __fmul_rn(of[mt][4 * rq + 1], __fmul_rn(rr.y, alpha));
+          of[mt][4 * rq + 2] = __fmul_rn(of[mt][4 * rq + 2], __fmul_rn(rr.z, alpha));
+          of[mt][4 * rq + 3] = __fmul_rn(of[mt][4 * rq + 3], __fmul_rn(rr.w, alpha));
+        }
+    } else if (__any(alpha != 1.0f)) {
+#pragma unroll
+      for (int mt = 0; mt < 4; ++mt)
+#pragma unroll
+        for (int r = 0; r < 16; ++r) of[mt][r] = __fmul_rn(of[mt][r], alpha);
+    }
+
+    // ---- P, codes u = rint(15 P) packed as E2M3 u/2, row sums, PV ----
+    float lsum = 0.f;
+#pragma unroll
+    for (int gg = 0; gg < NG; ++gg) {
+      v16f src[2];
+#pragma unroll
+      for (int c2 = 0; c2 < 2; ++c2) {
+        const int ch = 2 * gg + c2;
+#pragma unroll
+        for (int i = 0; i < 16; ++i) {
+          const int r = 4 * (i & 3) + (i >> 2);  // element 2i+c2 of the packed operand
+          const int kl = ch * 32 + 8 * (r >> 2) + 4 * hh + (r & 3);
+          const float c = KTOK ? __fmul_rn(cq, sKs[buf][kl]) : cch[ch];
+          float P = __builtin_amdgcn_exp2f(__fmaf_rn(s[ch][r], c, -mnew));
+          if (last && key0 + kl >= N) P = 0.f;
+          lsum += P;
+          src[c2][i] = __builtin_rintf(__fmul_rn(P, pscale));
+        }
+      }
+      const v6i pk6 = __builtin_amdgcn_cvt_scalef32_2xpk16_fp6_f32(src[0], src[1], 2.0f);
+      const v8i B = v8i{pk6[0], pk6[1], pk6[2], pk6[3], pk6[4], pk6[5], 0, 0};
+      if (DEBUG) {
+        if (bh == a.dbg_bh && qrow >= a.dbg_row0 && qrow < a.dbg_row0 + a.dbg_rows) {
+          const size_t rowo = static_cast<size_t>(qrow - a.dbg_row0);
+#pragma unroll
+          for (int c2 = 0; c2 < 2; ++c2)
+#pragma unroll
+            for (int i = 0; i < 16; ++i) {
+              const int ch = 2 * gg + c2;
+              const int r = 4 * (i & 3) + (i >> 2);
+              const int key = key0 + ch * 32 + 8 * (r >> 2) + 4 * hh + (r & 3);
+              if (key < N) {
+                if (a.dbg_s) a.dbg_s[rowo * N + key] = static_cast<int32_t>(s[ch][r]);
+                if (a.dbg_u) a.dbg_u[rowo * N + key] = static_cast<uint8_t>(src[c2][i]);
+              }
+            }
+        }
+      }
+#pragma unroll
+      for (int mt = 0; mt < 4; ++mt) {
+        const v8i A = load_rec(&sV[buf][(((gg * 4 + mt) * 2 + hh) * 32 + j) * 24]);
+        of[mt] = mfma6(A, B, of[mt]);
+      }
+    }
+    l = __fmaf_rn(l, alpha, lsum);
+    if (DEBUG && a.dbg_m && hh == 0 && bh == a.dbg_bh && qrow >= a.dbg_row0 && qrow < a.dbg_row0 + a.dbg_rows)
+      a.dbg_m[static_cast<size_t>(qrow - a.dbg_row0) * nblocks + jb] = mnew;
+
+    if (more) {
+      store(buf ^ 1);
+      stage_aux(jb + 1, buf ^ 1);
+    }
+    __syncthreads();
+  }
+
+  if (tid < kD) sW[tid] = wcur;
+  __syncthreads();
+
+  // ---- epilogue: O = O' * 2 w / 15 / l + mu_v ----
+  const float ltot = l + __shfl_xor(l, 32);
+  if (qrow < N) {
+    const float inv = 1.0f / ltot;
+    const float k2 = 2.0f / pscale;
+    const size_t obase = (static_cast<size_t>(bh) * N + qrow) * kD;
+#pragma unroll
+    for (int mt = 0; mt < 4; ++mt)
+#pragma unroll
+      for (int rq = 0; rq < 4; ++rq) {
+        const int c0 = mt * 32 + 8 * rq + 4 * hh;
+        float v[4];
+#pragma unroll
+        for (int t = 0; t < 4; ++t) {
+          v[t] = of[mt][4 * rq + t] * (sW[c0 + t] * k2) * inv;
+          if (a.mu_v) v[t] += a.mu_v[bh * kD + c0 + t];
+        }
+        if (a.out_dtype == 2) {
+          *reinterpret_cast<float4*>(static_cast<float*>(a.o) + obase + c0) = make_float4(v[0], v[1], v[2], v[3]);
+        } else if (a.out_dtype == 0) {
+          uint16_t b[4];
+#pragma unroll
+          for (int t = 0; t < 4; ++t) b[t] = __bfloat16_as_ushort(__float2bfloat16(v[t]));
+          *reinterpret_cast<uint2*>(static_cast<uint16_t*>(a.o) + obase + c0) =
+              make_uint2(b[0] | (static_cast<uint32_t>(b[1]) << 16), b[2] | (static_cast<uint32_t>(b[3]) << 16));
+        } else {
+          uint16_t b[4];
+#pragma unroll
+          for (int t = 0; t < 4; ++t) b[t] = __half_as_ushort(__float2half(v[t]));
+          *reinterpret_cast<uint2*>(static_cast<uint16_t*>(a.o) + obase + c0) =
+              make_uint2(b[0] | (static_cast<uint32_t>(b[1]) << 16), b[2] | (static_cast<uint32_t>(b[3]) << 16));
+        }
+      }
+  }
+}
+
+template <int KV, bool KTOK, bool SYM7, bool DEBUG>
+hipError_t launch_t(const AttnArgs& a, hipStream_t s) {
+  const dim3 grid(a.Npad / kBlockM, a.BH);
+  hipLaunchKernelGGL((k_attn_e2m3<KV, KTOK, SYM7, DEBUG>), grid, dim3(256), 0, s, a);
+  return hipGetLastError();
+}
+
+template <int KV, bool KTOK, bool SYM7>
+hipError_t launch_d(const AttnArgs& a, bool debug, hipStream_t s) {
+  return debug ? launch_t<KV, KTOK, SYM7, true>(a, s) : launch_t<KV, KTOK, SYM7, false>(a, s);
+}
+
+template <int KV, bool KTOK>
+hipError_t launch_p(const AttnArgs& a, bool sym7, bool debug, hipStream_t s) {
+  return sym7 ? launch_d<KV, KTOK, true>(a, debug, s) : launch_d<KV, KTOK, false>(a, debug, s);
+}
+
+template <int KV>
+hipError_t launch_k(const AttnArgs& a, bool ktok, bool sym7, bool debug, hipStream_t s) {
+  return ktok ? launch_p<KV, true>(a, sym7, debug, s) : launch_p<KV, false>(a, sym7, debug, s);
+}
+
+}  // namespace
+
+hipError_t launch_attn_e2m3(const AttnArgs& a, int kv_block, bool k_per_token, bool sym7, bool debug,
+                            hipStream_t s) {
+  if (kv_block == 64) return launch_k<64>(a, k_per_token, sym7, debug, s);
+  return launch_k<128>(a, k_per_token, sym7, debug, s);
+}
+
+}  // namespace ra

@@ -70,6 +70,8 @@ int validate(const ra_params* p) {
     return fail(RA_ERR_UNSUPPORTED, "v_group must be a multiple of kv_block or >= N");
   if (!(p->sm_scale >= 0.0f) || !std::isfinite(p->sm_scale)) return fail(RA_ERR_INVALID, "sm_scale must be >= 0");
   if (p->in_dtype != RA_BF16 && p->in_dtype != RA_FP16) return fail(RA_ERR_INVALID, "in_dtype must be BF16 or FP16");
+  if (p->code_format != RA_CODES_INT4 && p->code_format != RA_CODES_E2M3)
+    return fail(RA_ERR_INVALID, "code_format must be RA_CODES_INT4 or RA_CODES_E2M3");
   if (p->out_dtype != RA_BF16 && p->out_dtype != RA_FP16 && p->out_dtype != RA_FP32)
     return fail(RA_ERR_INVALID, "out_dtype must be BF16, FP16 or FP32");
   return RA_OK;
@@ -86,7 +88,7 @@ Sizes sizes_of(const ra_params* p) {
   s.Npad = npad_of(p->N);
   s.ntiles = s.Npad / 128;
   s.nvgroups = (p->N + p->v_group - 1) / p->v_group;
-  s.codes = static_cast<size_t>(s.BH * s.Npad * 64);
+  s.codes = static_cast<size_t>(s.BH * s.Npad * (p->code_format == RA_CODES_E2M3 ? 96 : 64));
   s.qscale = static_cast<size_t>(s.BH * (s.Npad / p->q_group));
   s.kscale = static_cast<size_t>(s.BH * (s.Npad / p->k_group));
   s.vscale = static_cast<size_t>(s.BH * s.nvgroups * kD);
@@ -278,6 +280,7 @@ int qk_impl(const ra_params* p, const void* q, const void* k, uint8_t* qc, float
   a.N = p->N;
   a.Npad = static_cast<int>(z.Npad);
   a.is_fp16 = p->in_dtype == RA_FP16;
+  a.e2m3 = p->code_format == RA_CODES_E2M3;
   a.partial = w.partial;
   float* mu = mu_k ? mu_k : w.mu_k;
   const float* center = nullptr;
@@ -317,6 +320,7 @@ int v_impl(const ra_params* p, const void* v, uint8_t* vc, float* vs, float* mu_
   a.group = p->v_group;
   a.ngroups = static_cast<int>(z.nvgroups);
   a.is_fp16 = p->in_dtype == RA_FP16;
+  a.e2m3 = p->code_format == RA_CODES_E2M3;
   float* mu = mu_v ? mu_v : w.mu_v;
   if (p->smooth & RA_SMOOTH_V) {
     RA_CHECK_HIP(ra::launch_v_sums(a, static_cast<int>(z.BH), s));
@@ -360,7 +364,10 @@ int attn_impl(const ra_params* p, const uint8_t* qc, const float* qs, const uint
   a.dbg_bh = bh;
   a.dbg_row0 = row0;
   a.dbg_rows = rows;
-  RA_CHECK_HIP(ra::launch_attn_int4(a, p->kv_block, p->k_group == 1, p->p_quant == RA_PQ_SYM7, debug, s));
+  if (p->code_format == RA_CODES_E2M3)
+    RA_CHECK_HIP(ra::launch_attn_e2m3(a, p->kv_block, p->k_group == 1, p->p_quant == RA_PQ_SYM7, debug, s));
+  else
+    RA_CHECK_HIP(ra::launch_attn_int4(a, p->kv_block, p->k_group == 1, p->p_quant == RA_PQ_SYM7, debug, s));
   return RA_OK;
 }
 

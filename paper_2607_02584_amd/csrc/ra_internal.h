@@ -33,6 +33,7 @@ struct QkArgs {
   const float* mu;        // [BH][128] or nullptr (no centering)
   double* partial;        // [BH][ntiles][128] fixed-point sums (sums pass only)
   int N, Npad, group, is_fp16;
+  int e2m3;               // 1: write the E2M3 container, 0: the INT4 nibble container
 };
 
 struct VArgs {
@@ -43,6 +44,7 @@ struct VArgs {
   double* partial;        // [BH][ntiles][128]
   uint32_t* amax;         // [BH][ngroups][128] float bits (non-negative)
   int N, Npad, group, ngroups, is_fp16;
+  int e2m3;
 };
 
 struct AttnArgs {
@@ -84,6 +86,8 @@ hipError_t launch_v_sums(const VArgs& a, int BH, hipStream_t s);
 hipError_t launch_v_amax(const VArgs& a, int BH, hipStream_t s);
 hipError_t launch_v_quant(const VArgs& a, int BH, hipStream_t s);
 hipError_t launch_attn_int4(const AttnArgs& a, int kv_block, bool k_per_token, bool sym7, bool debug,
+                            hipStream_t s);
+hipError_t launch_attn_e2m3(const AttnArgs& a, int kv_block, bool k_per_token, bool sym7, bool debug,
                             hipStream_t s);
 hipError_t launch_rope16(const RopeTables& t, const uint16_t* x, uint16_t* out, int BH, int N, int Npad,
                          int is_fp16, hipStream_t s);

@@ -200,6 +200,16 @@ __global__ __launch_bounds__(128) void k_mu_reduce(const double* partial, float*
   mu[bh * kD + ch] = static_cast<float>(s / (static_cast<double>(N) * 1048576.0));
 }
 
+// 6-bit E2M3 float (sign bit 5, exponent bias 1, 3 mantissa bits) equal to the
+// integer code c in [-7, 7]: 1 = 1.0 x 2^0, 2 = 1.0 x 2^1, 3 = 1.1b x 2^1, 4..7 = 1.xx0b x 2^2.
+__device__ __forceinline__ uint32_t e2m3_of(int c) {
+  const uint32_t mag = static_cast<uint32_t>(c < 0 ? -c : c);
+  // magnitudes 0..7 -> 00 08 10 14 18 1A 1C 1E, packed as nibble pairs of a 64-bit table
+  const uint64_t tab = 0x1E1C1A1814100800ull;
+  const uint32_t v = static_cast<uint32_t>((tab >> (8 * mag)) & 0xFF);
+  return c < 0 ? (v | 0x20u) : v;
+}
+
 __device__ __forceinline__ int qcode(float z, float inv) {
   float c = __builtin_rintf(__fmul_rn(z, inv));
   c = fminf(fmaxf(c, -7.0f), 7.0f);
@@ -210,7 +220,7 @@ __global__ __launch_bounds__(256) void k_qk_quant(RopeTables t, QkArgs a) {
   __shared__ float ybuf[8][kD];
   __shared__ float rowmax[kTile];
   __shared__ float ginv[kTile];
-  __shared__ __align__(16) uint8_t ctile[kTile * 64];
+  __shared__ __align__(16) uint8_t ctile[kTile * 96];
   const int tile = blockIdx.x, bh = blockIdx.y;
   const int tid = threadIdx.x, rr = tid >> 5, cl = tid & 31;
   float z[16][4];
@@ -248,6 +258,29 @@ __global__ __launch_bounds__(256) void k_qk_quant(RopeTables t, QkArgs a) {
     a.scales[static_cast<size_t>(bh) * (a.Npad / g) + tile * ng + tid] = s;
   }
   __syncthreads();
+  if (a.e2m3) {
+    // record ((chunk*2 + ch/64)*2 + (ch/32)%2)*32 + row of 24 bytes; channels 4cl..4cl+3 are the
+    // 6-bit fields 4*(cl%8) .. +3 of record (kc = cl/16, h = (cl/8)%2), i.e. bytes 3*(cl%8) .. +2
+    for (int p = 0; p < 16; ++p) {
+      const int nl = p * 8 + rr;
+      const float inv = ginv[nl / g];
+      const uint32_t bits = e2m3_of(qcode(z[p][0], inv)) | (e2m3_of(qcode(z[p][1], inv)) << 6) |
+                            (e2m3_of(qcode(z[p][2], inv)) << 12) | (e2m3_of(qcode(z[p][3], inv)) << 18);
+      const int rec = (((nl >> 5) * 2 + (cl >> 4)) * 2 + ((cl >> 3) & 1)) * 32 + (nl & 31);
+      uint8_t* d = &ctile[rec * 24 + 3 * (cl & 7)];
+      d[0] = static_cast<uint8_t>(bits);
+      d[1] = static_cast<uint8_t>(bits >> 8);
+      d[2] = static_cast<uint8_t>(bits >> 16);
+    }
+    __syncthreads();
+    uint8_t* dst = a.codes + static_cast<size_t>(bh) * a.Npad * 96 + static_cast<size_t>(tile) * kTile * 96;
+#pragma unroll
+    for (int i = 0; i < 3; ++i) {
+      const int o = (i * 256 + tid) * 16;
+      *reinterpret_cast<uint4*>(dst + o) = *reinterpret_cast<const uint4*>(&ctile[o]);
+    }
+    return;
+  }
   for (int p = 0; p < 16; ++p) {
     const int nl = p * 8 + rr;
     const float inv = ginv[nl / g];
@@ -344,7 +377,7 @@ __global__ __launch_bounds__(256) void k_v_amax(VArgs a) {
 }
 
 __global__ __launch_bounds__(256) void k_v_quant(VArgs a) {
-  __shared__ __align__(16) uint8_t ctile[kTile * 64];
+  __shared__ __align__(16) uint8_t ctile[kTile * 96];
   __shared__ float ginv[2][kD];
   const int tile = blockIdx.x, bh = blockIdx.y;
   const int tid = threadIdx.x, rr = tid >> 5, cl = tid & 31;
@@ -366,6 +399,39 @@ __global__ __launch_bounds__(256) void k_v_quant(VArgs a) {
   __syncthreads();
   float z[16][4];
   load_v_tile(a, bh, tile, z);
+  if (a.e2m3) {
+    // group of 64 tokens gl = p/8, kappa = (p%8)*8 + rr, half h = (rr/4)%2; the thread's 8 codes of a
+    // channel in that group are the fields 8*(rr%4) .. +7 (field 8*(rr%4) + 2*(p%4) + (p%8)/4), i.e.
+    // bytes 6*(rr%4) .. +5 of record ((gl*4 + ch/32)*2 + h)*32 + ch%32 (tile-local gl).
+    const int s4 = rr & 3, hh = (rr >> 2) & 1;
+#pragma unroll
+    for (int gl = 0; gl < 2; ++gl) {
+#pragma unroll
+      for (int c = 0; c < 4; ++c) {
+        const int ch = 4 * cl + c;
+        const float inv = ginv[gl][ch];
+        uint64_t bits = 0;
+#pragma unroll
+        for (int pp = 0; pp < 8; ++pp) {
+          const int f = 2 * (pp & 3) + (pp >> 2);
+          bits |= static_cast<uint64_t>(e2m3_of(qcode(z[gl * 8 + pp][c], inv))) << (6 * f);
+        }
+        const int rec = ((gl * 4 + (ch >> 5)) * 2 + hh) * 32 + (ch & 31);
+        uint16_t* d = reinterpret_cast<uint16_t*>(&ctile[rec * 24 + 6 * s4]);
+        d[0] = static_cast<uint16_t>(bits);
+        d[1] = static_cast<uint16_t>(bits >> 16);
+        d[2] = static_cast<uint16_t>(bits >> 32);
+      }
+    }
+    __syncthreads();
+    uint8_t* dst = a.codes + static_cast<size_t>(bh) * a.Npad * 96 + static_cast<size_t>(tile) * kTile * 96;
+#pragma unroll
+    for (int i = 0; i < 3; ++i) {
+      const int o = (i * 256 + tid) * 16;
+      *reinterpret_cast<uint4*>(dst + o) = *reinterpret_cast<const uint4*>(&ctile[o]);
+    }
+    return;
+  }
   // token kappa = (p%4)*8 + rr inside chunk p/4; nibble np = 8*(kappa/16) + 2*(kappa%4) + (kappa/8)%2,
   // half h = (kappa/4)%2; byte ((chunk*2 + h)*128 + ch)*8 + np/2.  Passes p and p+1 (p even)
   // share every byte (np differs in its low bit only).

@@ -19,6 +19,7 @@ ROT_NONE, ROT_INTERLEAVED, ROT_HALF = 0, 1, 2
 PQ_RANGE15, PQ_SYM7 = 0, 1
 SMOOTH_K, SMOOTH_V = 1, 2
 BF16, FP16, FP32 = 0, 1, 2
+CODES_INT4, CODES_E2M3 = 0, 1
 PATH_INT4, PATH_FP16 = 0, 1
 
 
@@ -36,7 +37,7 @@ class Params(ctypes.Structure):
         ("p_quant", ctypes.c_int32), ("smooth", ctypes.c_int32),
         ("q_group", ctypes.c_int32), ("k_group", ctypes.c_int32), ("v_group", ctypes.c_int32),
         ("kv_block", ctypes.c_int32), ("sm_scale", ctypes.c_float),
-        ("in_dtype", ctypes.c_int32), ("out_dtype", ctypes.c_int32),
+        ("in_dtype", ctypes.c_int32), ("out_dtype", ctypes.c_int32), ("code_format", ctypes.c_int32),
     ]
 
 
@@ -91,7 +92,7 @@ def _check(status: int, where: str):
 
 def make_params(B, H, grid, split=(44, 42, 42), theta=10000.0, *, rotation=ROT_INTERLEAVED, rot_blocks=None,
                 p_quant=PQ_RANGE15, smooth=SMOOTH_K | SMOOTH_V, q_group=128, k_group=128, v_group=128,
-                kv_block=128, sm_scale=0.0, in_dtype=BF16, out_dtype=BF16, D=128) -> Params:
+                kv_block=128, sm_scale=0.0, in_dtype=BF16, out_dtype=BF16, code_format=CODES_E2M3, D=128) -> Params:
     p = Params()
     p.B, p.H, p.D = B, H, D
     p.N = int(grid[0] * grid[1] * grid[2])
@@ -107,6 +108,7 @@ def make_params(B, H, grid, split=(44, 42, 42), theta=10000.0, *, rotation=ROT_I
     p.q_group, p.k_group, p.v_group, p.kv_block = q_group, k_group, v_group, kv_block
     p.sm_scale = float(sm_scale)
     p.in_dtype, p.out_dtype = in_dtype, out_dtype
+    p.code_format = code_format
     return p
 
 

@@ -56,6 +56,7 @@ def _base(ra, **kw):
     ("v_group", 96, -2),       # not a multiple of kv_block and < N
     ("in_dtype", 2, -1),
     ("out_dtype", 7, -1),
+    ("code_format", 2, -1),
     ("sm_scale", -1.0, -1),
 ])
 def test_validation_rejects(field, value, status):
@@ -74,7 +75,9 @@ def test_validation_accepts_defaults_and_reports_sizes():
     ra = _ra()
     p = _base(ra)
     L = ra.layout(p)
-    assert L["n_pad"] == 1024 and L["qk_code_bytes"] == 2 * 1024 * 64 and L["v_scale_count"] == 2 * 8 * 128
+    assert L["n_pad"] == 1024 and L["qk_code_bytes"] == 2 * 1024 * 96 and L["v_scale_count"] == 2 * 8 * 128
+    L4 = ra.layout(ra.make_params(1, 2, (4, 16, 16), code_format=ra.CODES_INT4))
+    assert L4["qk_code_bytes"] == 2 * 1024 * 64 and L4["v_code_bytes"] == 2 * 1024 * 64
     assert ra.workspace_size(p, ra.PATH_INT4) > 3 * L["qk_code_bytes"]
     assert ra.workspace_size(p, ra.PATH_FP16) >= 3 * 2 * 1024 * 128 * 2
     p2 = ra.make_params(1, 1, (3, 7, 11), v_group=10 ** 6)

@@ -11,7 +11,7 @@ import math
 import numpy as np
 import pytest
 
-from layouts import unpack_qk, unpack_v
+from layouts import unpack_qk, unpack_qk_e2m3, unpack_v, unpack_v_e2m3
 
 pytestmark = pytest.mark.gpu
 
@@ -46,9 +46,13 @@ def _cfg(ora, rotation, qg, kg, vg, kv, pq=0, smooth=3):
                           q_group=qg, k_group=kg, v_group=vg, kv_block=kv)
 
 
-def _params(ra, w, rotation, qg, kg, vg, kv, pq=0, smooth=3, out=2):
+def _params(ra, w, rotation, qg, kg, vg, kv, pq=0, smooth=3, out=2, fmt=1):
     return ra.make_params(w.B, w.H, (w.T, w.Hg, w.W), w.split, w.theta, rotation=rotation, p_quant=pq,
-                          smooth=smooth, q_group=qg, k_group=kg, v_group=vg, kv_block=kv, out_dtype=out)
+                          smooth=smooth, q_group=qg, k_group=kg, v_group=vg, kv_block=kv, out_dtype=out,
+                          code_format=fmt)
+
+
+FORMATS = {"int4": 0, "e2m3": 1}
 
 
 def _run_quant(torch, ra, p, q, k, v):
@@ -85,25 +89,27 @@ def _workloads():
     return [dg.WORKLOADS["c1"], _small_ragged()]
 
 
+@pytest.mark.parametrize("fmt", ["e2m3", "int4"])
 @pytest.mark.parametrize("wname", ["c1", "ragged"])
 @pytest.mark.parametrize("case", CASES)
-def test_int4_codes_scores_and_output(ora, wname, case):
+def test_int4_codes_scores_and_output(ora, wname, case, fmt):
     """Producer codes/scales/means bit-exact; S, m bit-exact; P codes up to ties; O <= 2e-3."""
     torch, ra = _torch(), _ra()
     from paper_2607_02584_amd import datagen as dg
     w = dg.WORKLOADS["c1"] if wname == "c1" else _small_ragged()
     rot, qg, kg, vg, kv, pq, sm = case
     vg = min(vg, 10 ** 6)
-    print(f"[int4 parity] {wname} N={w.N} case={case}", flush=True)
+    print(f"[int4 parity] {wname} N={w.N} case={case} container={fmt}", flush=True)
     q, k, v = _inputs(w)
-    p = _params(ra, w, rot, qg, kg, vg, kv, pq, sm)
+    p = _params(ra, w, rot, qg, kg, vg, kv, pq, sm, fmt=FORMATS[fmt])
     bufs, _, _ = _run_quant(torch, ra, p, q, k, v)
     Np = ra.layout(p)["n_pad"]
     BH, N = w.B * w.H, w.N
     h = _host(bufs)
-    qc = unpack_qk(h["q_codes"], BH, Np, N)
-    kc = unpack_qk(h["k_codes"], BH, Np, N)
-    vc = unpack_v(h["v_codes"], BH, Np, N)
+    uqk, uv = (unpack_qk_e2m3, unpack_v_e2m3) if fmt == "e2m3" else (unpack_qk, unpack_v)
+    qc = uqk(h["q_codes"], BH, Np, N)
+    kc = uqk(h["k_codes"], BH, Np, N)
+    vc = uv(h["v_codes"], BH, Np, N)
     nvg = -(-N // vg)
     geo = _geo(ora, w)
     cfg = _cfg(ora, rot, qg, kg, vg, kv, pq, sm)
@@ -159,14 +165,15 @@ def test_int4_codes_scores_and_output(ora, wname, case):
     assert torch.equal(o_plain, o_gpu)
 
 
-def test_fwd_int4_matches_stepwise_and_oracle(ora):
+@pytest.mark.parametrize("fmt", ["e2m3", "int4"])
+def test_fwd_int4_matches_stepwise_and_oracle(ora, fmt):
     """The fused entry point equals the three-call sequence bit for bit and the
     oracle within 2e-3; repeated calls give identical bytes."""
     torch, ra = _torch(), _ra()
     from paper_2607_02584_amd import datagen as dg
     w = dg.WORKLOADS["c1"]
     q, k, v = _inputs(w)
-    p = _params(ra, w, 1, 128, 128, 128, 128)
+    p = _params(ra, w, 1, 128, 128, 128, 128, fmt=FORMATS[fmt])
     bufs, (qd, kd, vd), _ = _run_quant(torch, ra, p, q, k, v)
     o1 = torch.empty((w.H, w.N, 128), dtype=torch.float32, device="cuda")
     ra.attn_int4(p, bufs["q_codes"], bufs["q_scale"], bufs["k_codes"], bufs["k_scale"], bufs["v_codes"],
@@ -205,15 +212,16 @@ def test_int4_16bit_output_rounds_fp32_result(ora, out):
     assert torch.equal(o32.to(o16.dtype), o16)
 
 
-def test_c2_full_size_sampled_rows(ora):
+@pytest.mark.parametrize("fmt", ["e2m3", "int4"])
+def test_c2_full_size_sampled_rows(ora, fmt):
     """Headline 32760-token shape (12 heads) in the benchmark's launch
     configuration: sampled query rows of two heads against the oracle."""
     torch, ra = _torch(), _ra()
     from paper_2607_02584_amd import datagen as dg
     w = dg.WORKLOADS["c2"]
-    print("[c2 sampled] generating inputs", flush=True)
+    print(f"[c2 sampled] container={fmt}: generating inputs", flush=True)
     q, k, v = _inputs(w)
-    p = _params(ra, w, 1, 128, 128, 128, 128)
+    p = _params(ra, w, 1, 128, 128, 128, 128, fmt=FORMATS[fmt])
     bufs, (qd, kd, vd), ws = _run_quant(torch, ra, p, q, k, v)
     BH, N = w.B * w.H, w.N
     o = torch.empty((BH, N, 128), dtype=torch.float32, device="cuda")

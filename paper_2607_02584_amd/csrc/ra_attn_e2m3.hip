@@ -22,6 +22,8 @@
 // chunk.  The P codes of two chunks (64 keys) are packed by
 // v_cvt_scalef32_2xpk16_fp6_f32 into the B operand of O^T = V^T P^T; the V
 // records are stored in the key order that packing produces.
+#include <type_traits>
+
 #include "ra_internal.h"
 
 namespace ra {
@@ -47,12 +49,21 @@ __device__ __forceinline__ v8i load_rec(const uint8_t* p) {
              static_cast<int>(c.x), static_cast<int>(c.y), 0, 0};
 }
 
+// Copies `bytes` (a multiple of 1024) from global to LDS with the LDS-DMA path
+// (global_load_lds_dwordx4: lane i of a wave moves 16 bytes to base + 16 i);
+// the four waves of the workgroup take every fourth kilobyte.
+__device__ __forceinline__ void dma_copy(const uint8_t* src, uint8_t* dst, int bytes, int wave, int lane) {
+  for (int off = wave * 1024; off < bytes; off += 4096) {
+    __builtin_amdgcn_global_load_lds((const void __attribute__((address_space(1)))*)(src + off + lane * 16),
+                                     (void __attribute__((address_space(3)))*)(dst + off), 16, 0, 0);
+  }
+}
+
 template <int KV, bool KTOK, bool SYM7, bool DEBUG>
 __global__ __launch_bounds__(256, 2) void k_attn_e2m3(AttnArgs a) {
   constexpr int NCH = KV / 32;   // 32-key chunks
   constexpr int NG = KV / 64;    // 64-key groups (one PV instruction each)
   constexpr int KB = KV * 96;    // bytes of K (and of V) codes per block
-  constexpr int NLD = (KB / 16 + 255) / 256;
   __shared__ __align__(16) uint8_t sK[2][KB];
   __shared__ __align__(16) uint8_t sV[2][KB];
   __shared__ __align__(16) float sR[2][kD];   // V scale ratio w_old / w_new for the block
@@ -68,16 +79,16 @@ __global__ __launch_bounds__(256, 2) void k_attn_e2m3(AttnArgs a) {
   const int kstride = a.Npad / a.k_group;
   const float pscale = SYM7 ? 7.0f : 15.0f;
   const size_t hcode = static_cast<size_t>(bh) * a.Npad * 96;
+  const uint8_t* kbase = a.kc + hcode;
+  const uint8_t* vbase = a.vc + hcode;
+  const float* ksh = a.ks + static_cast<size_t>(bh) * kstride;
 
   // ---- Q operand (B of S^T = K Q^T) ----
   v8i qop[2];
-  {
-    const uint8_t* qp = a.qc + hcode;
 #pragma unroll
-    for (int kc = 0; kc < 2; ++kc) {
-      const int rec = (((qrow >> 5) * 2 + kc) * 2 + hh) * 32 + (qrow & 31);
-      qop[kc] = load_rec(qp + static_cast<size_t>(rec) * 24);
-    }
+  for (int kc = 0; kc < 2; ++kc) {
+    const int rec = (((qrow >> 5) * 2 + kc) * 2 + hh) * 32 + (qrow & 31);
+    qop[kc] = load_rec(a.qc + hcode + static_cast<size_t>(rec) * 24);
   }
   const float cq = __fmul_rn(a.qs[static_cast<size_t>(bh) * (a.Npad / a.q_group) + qrow / a.q_group], a.Kc);
 
@@ -95,31 +106,7 @@ __global__ __launch_bounds__(256, 2) void k_attn_e2m3(AttnArgs a) {
       }
       sR[buf][tid] = r;
     }
-    if (KTOK && tid < KV) sKs[buf][tid] = a.ks[static_cast<size_t>(bh) * kstride + jb * KV + tid];
-  };
-
-  uint4 stk[NLD], stv[NLD];
-  auto load = [&](int jb) {
-    const uint8_t* kb = a.kc + hcode + static_cast<size_t>(jb) * KB;
-    const uint8_t* vb = a.vc + hcode + static_cast<size_t>(jb) * KB;
-#pragma unroll
-    for (int i = 0; i < NLD; ++i) {
-      const int o = (i * 256 + tid) * 16;
-      if (o < KB) {
-        stk[i] = *reinterpret_cast<const uint4*>(kb + o);
-        stv[i] = *reinterpret_cast<const uint4*>(vb + o);
-      }
-    }
-  };
-  auto store = [&](int buf) {
-#pragma unroll
-    for (int i = 0; i < NLD; ++i) {
-      const int o = (i * 256 + tid) * 16;
-      if (o < KB) {
-        *reinterpret_cast<uint4*>(&sK[buf][o]) = stk[i];
-        *reinterpret_cast<uint4*>(&sV[buf][o]) = stv[i];
-      }
-    }
+    if (KTOK && tid < KV) sKs[buf][tid] = ksh[jb * KV + tid];
   };
 
   v16f of[4];
@@ -129,48 +116,67 @@ __global__ __launch_bounds__(256, 2) void k_attn_e2m3(AttnArgs a) {
     for (int r = 0; r < 16; ++r) of[mt][r] = 0.f;
   float m = -INFINITY, l = 0.f;
 
-  load(0);
-  store(0);
+  dma_copy(kbase, sK[0], KB, wave, lane);
+  dma_copy(vbase, sV[0], KB, wave, lane);
   stage_aux(0, 0);
+  asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
   __syncthreads();
 
-  for (int jb = 0; jb < nblocks; ++jb) {
+  // One block of KV keys.  MASKED (keys past N) only for the partial last
+  // block, which runs outside the main loop so the full blocks carry no masking.
+  auto step = [&](int jb, auto masked_tag) {
+    constexpr bool MASKED = decltype(masked_tag)::value;
     const int buf = jb & 1;
-    const bool more = jb + 1 < nblocks;
-    if (more) load(jb + 1);
     const int key0 = jb * KV;
-    const bool last = key0 + KV > N;
+    if (jb + 1 < nblocks) {
+      dma_copy(kbase + static_cast<size_t>(jb + 1) * KB, sK[buf ^ 1], KB, wave, lane);
+      dma_copy(vbase + static_cast<size_t>(jb + 1) * KB, sV[buf ^ 1], KB, wave, lane);
+      stage_aux(jb + 1, buf ^ 1);
+    }
+    __builtin_amdgcn_sched_barrier(0);
 
-    // ---- S^T = K Q^T: exact integer scores in binary32 ----
+    // ---- S^T = K Q^T: exact integer scores in binary32; the operands of
+    //      chunk ch+1 are read from LDS while chunk ch is on the matrix core ----
     v16f s[NCH];
+    v8i kop0 = load_rec(&sK[buf][((0 * 2 + hh) * 32 + j) * 24]);
+    v8i kop1 = load_rec(&sK[buf][((1 * 2 + hh) * 32 + j) * 24]);
 #pragma unroll
     for (int ch = 0; ch < NCH; ++ch) {
+      v8i n0 = kop0, n1 = kop1;
+      if (ch + 1 < NCH) {
+        n0 = load_rec(&sK[buf][(((((ch + 1) * 2) + 0) * 2 + hh) * 32 + j) * 24]);
+        n1 = load_rec(&sK[buf][(((((ch + 1) * 2) + 1) * 2 + hh) * 32 + j) * 24]);
+      }
 #pragma unroll
       for (int r = 0; r < 16; ++r) s[ch][r] = 0.f;
+      s[ch] = mfma6(kop0, qop[0], s[ch]);
+      s[ch] = mfma6(kop1, qop[1], s[ch]);
+      kop0 = n0;
+      kop1 = n1;
+      __builtin_amdgcn_sched_barrier(0);
+    }
+    // key of accumulator register r in chunk ch: key0 + 32*ch + 8*(r/4) + 4*hh + r%4
+    if (MASKED) {
 #pragma unroll
-      for (int kc = 0; kc < 2; ++kc) {
-        const v8i A = load_rec(&sK[buf][((((ch * 2) + kc) * 2 + hh) * 32 + j) * 24]);
-        s[ch] = mfma6(A, qop[kc], s[ch]);
-      }
+      for (int ch = 0; ch < NCH; ++ch)
+#pragma unroll
+        for (int r = 0; r < 16; ++r)
+          if (key0 + ch * 32 + 8 * (r >> 2) + 4 * hh + (r & 3) >= N) s[ch][r] = -INFINITY;
     }
 
-    // key of accumulator register r in chunk ch: key0 + 32*ch + 8*(r/4) + 4*hh + r%4
+    // ---- block row maximum of fl(S * c) (c >= 0, so it is fl(max S * c);
+    //      a fully masked chunk gives -inf, or NaN when c == 0, which fmax ignores) ----
     float cch[NCH];
     float tmax = -INFINITY;
     if (!KTOK) {
 #pragma unroll
       for (int ch = 0; ch < NCH; ++ch) {
-        const int kbase = key0 + ch * 32;
-        cch[ch] = __fmul_rn(cq, a.ks[static_cast<size_t>(bh) * kstride + kbase / a.k_group]);
-        if (kbase < N) {
-          float mx = -INFINITY;
+        cch[ch] = __fmul_rn(cq, ksh[(key0 + ch * 32) / a.k_group]);
+        float mx = fmaxf(fmaxf(s[ch][0], s[ch][1]), s[ch][2]);
 #pragma unroll
-          for (int r = 0; r < 16; ++r) {
-            const int key = kbase + 8 * (r >> 2) + 4 * hh + (r & 3);
-            if (!last || key < N) mx = fmaxf(mx, s[ch][r]);
-          }
-          if (mx != -INFINITY) tmax = fmaxf(tmax, __fmul_rn(mx, cch[ch]));
-        }
+        for (int r = 3; r < 15; r += 2) mx = fmaxf(fmaxf(mx, s[ch][r]), s[ch][r + 1]);
+        mx = fmaxf(mx, s[ch][15]);
+        tmax = fmaxf(tmax, __fmul_rn(mx, cch[ch]));
       }
     } else {
 #pragma unroll
@@ -178,7 +184,7 @@ __global__ __launch_bounds__(256, 2) void k_attn_e2m3(AttnArgs a) {
 #pragma unroll
         for (int r = 0; r < 16; ++r) {
           const int kl = ch * 32 + 8 * (r >> 2) + 4 * hh + (r & 3);
-          if (!last || key0 + kl < N) tmax = fmaxf(tmax, __fmul_rn(s[ch][r], __fmul_rn(cq, sKs[buf][kl])));
+          tmax = fmaxf(tmax, __fmul_rn(s[ch][r], __fmul_rn(cq, sKs[buf][kl])));
         }
     }
     tmax = fmaxf(tmax, __shfl_xor(tmax, 32));
@@ -186,30 +192,34 @@ __global__ __launch_bounds__(256, 2) void k_attn_e2m3(AttnArgs a) {
     const float alpha = __builtin_amdgcn_exp2f(m - mnew);
     m = mnew;
 
-    // ---- rescale O' for the new maximum and the block's V scale ----
-    const bool vchange = jb > 0 && a.nvgroups > 1 && ((jb * KV) % a.v_group) == 0;
-    if (vchange) {
+    // ---- rescale O' for the block's V scale and the new maximum ----
+    if (jb > 0 && a.nvgroups > 1 && ((jb * KV) % a.v_group) == 0) {
 #pragma unroll
       for (int mt = 0; mt < 4; ++mt)
 #pragma unroll
         for (int rq = 0; rq < 4; ++rq) {
           const float4 rr = *reinterpret_cast<const float4*>(&sR[buf][mt * 32 + 8 * rq + 4 * hh]);
-          of[mt][4 * rq + 0] = __fmul_rn(of[mt][4 * rq + 0], __fmul_rn(rr.x, alpha));
-          of[mt][4 * rq + 1] = __fmul_rn(of[mt][4 * rq + 1], __fmul_rn(rr.y, alpha));
-          of[mt][4 * rq + 2] = __fmul_rn(of[mt][4 * rq + 2], __fmul_rn(rr.z, alpha));
-          of[mt][4 * rq + 3] = __fmul_rn(of[mt][4 * rq + 3], __fmul_rn(rr.w, alpha));
+          of[mt][4 * rq + 0] = __fmul_rn(of[mt][4 * rq + 0], rr.x);
+          of[mt][4 * rq + 1] = __fmul_rn(of[mt][4 * rq + 1], rr.y);
+          of[mt][4 * rq + 2] = __fmul_rn(of[mt][4 * rq + 2], rr.z);
+          of[mt][4 * rq + 3] = __fmul_rn(of[mt][4 * rq + 3], rr.w);
         }
-    } else if (__any(alpha != 1.0f)) {
+    }
+    if (__any(alpha != 1.0f)) {
 #pragma unroll
       for (int mt = 0; mt < 4; ++mt)
 #pragma unroll
         for (int r = 0; r < 16; ++r) of[mt][r] = __fmul_rn(of[mt][r], alpha);
     }
+    __builtin_amdgcn_sched_barrier(0);
 
     // ---- P, codes u = rint(15 P) packed as E2M3 u/2, row sums, PV ----
-    float lsum = 0.f;
+    float ls[4] = {0.f, 0.f, 0.f, 0.f};   // independent partial sums
 #pragma unroll
     for (int gg = 0; gg < NG; ++gg) {
+      v8i vop[2];
+#pragma unroll
+      for (int mt = 0; mt < 2; ++mt) vop[mt] = load_rec(&sV[buf][(((gg * 4 + mt) * 2 + hh) * 32 + j) * 24]);
       v16f src[2];
 #pragma unroll
       for (int c2 = 0; c2 < 2; ++c2) {
@@ -217,11 +227,12 @@ __global__ __launch_bounds__(256, 2) void k_attn_e2m3(AttnArgs a) {
 #pragma unroll
         for (int i = 0; i < 16; ++i) {
           const int r = 4 * (i & 3) + (i >> 2);  // element 2i+c2 of the packed operand
-          const int kl = ch * 32 + 8 * (r >> 2) + 4 * hh + (r & 3);
-          const float c = KTOK ? __fmul_rn(cq, sKs[buf][kl]) : cch[ch];
+          float c;
+          if (KTOK) c = __fmul_rn(cq, sKs[buf][ch * 32 + 8 * (r >> 2) + 4 * hh + (r & 3)]);
+          else c = cch[ch];
           float P = __builtin_amdgcn_exp2f(__fmaf_rn(s[ch][r], c, -mnew));
-          if (last && key0 + kl >= N) P = 0.f;
-          lsum += P;
+          if (MASKED && s[ch][r] == -INFINITY) P = 0.f;
+          ls[i & 3] += P;
           src[c2][i] = __builtin_rintf(__fmul_rn(P, pscale));
         }
       }
@@ -244,22 +255,26 @@ __global__ __launch_bounds__(256, 2) void k_attn_e2m3(AttnArgs a) {
             }
         }
       }
-#pragma unroll
-      for (int mt = 0; mt < 4; ++mt) {
-        const v8i A = load_rec(&sV[buf][(((gg * 4 + mt) * 2 + hh) * 32 + j) * 24]);
-        of[mt] = mfma6(A, B, of[mt]);
+      {
+        const v8i v2 = load_rec(&sV[buf][(((gg * 4 + 2) * 2 + hh) * 32 + j) * 24]);
+        of[0] = mfma6(vop[0], B, of[0]);
+        const v8i v3 = load_rec(&sV[buf][(((gg * 4 + 3) * 2 + hh) * 32 + j) * 24]);
+        of[1] = mfma6(vop[1], B, of[1]);
+        of[2] = mfma6(v2, B, of[2]);
+        of[3] = mfma6(v3, B, of[3]);
       }
+      __builtin_amdgcn_sched_barrier(0);
     }
-    l = __fmaf_rn(l, alpha, lsum);
+    l = __fmaf_rn(l, alpha, (ls[0] + ls[1]) + (ls[2] + ls[3]));
     if (DEBUG && a.dbg_m && hh == 0 && bh == a.dbg_bh && qrow >= a.dbg_row0 && qrow < a.dbg_row0 + a.dbg_rows)
       a.dbg_m[static_cast<size_t>(qrow - a.dbg_row0) * nblocks + jb] = mnew;
-
-    if (more) {
-      store(buf ^ 1);
-      stage_aux(jb + 1, buf ^ 1);
-    }
+    asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
     __syncthreads();
-  }
+  };
+
+  const int nfull = N / KV;
+  for (int jb = 0; jb < nfull; ++jb) step(jb, std::integral_constant<bool, false>());
+  if (nfull < nblocks) step(nfull, std::integral_constant<bool, true>());
 
   if (tid < kD) sW[tid] = wcur;
   __syncthreads();
@@ -270,17 +285,20 @@ __global__ __launch_bounds__(256, 2) void k_attn_e2m3(AttnArgs a) {
     const float inv = 1.0f / ltot;
     const float k2 = 2.0f / pscale;
     const size_t obase = (static_cast<size_t>(bh) * N + qrow) * kD;
+    const float* muv = a.mu_v ? a.mu_v + bh * kD : nullptr;
 #pragma unroll
     for (int mt = 0; mt < 4; ++mt)
 #pragma unroll
       for (int rq = 0; rq < 4; ++rq) {
         const int c0 = mt * 32 + 8 * rq + 4 * hh;
+        const float4 w4 = *reinterpret_cast<const float4*>(&sW[c0]);
+        float4 mu4 = make_float4(0.f, 0.f, 0.f, 0.f);
+        if (muv) mu4 = *reinterpret_cast<const float4*>(muv + c0);
         float v[4];
-#pragma unroll
-        for (int t = 0; t < 4; ++t) {
-          v[t] = of[mt][4 * rq + t] * (sW[c0 + t] * k2) * inv;
-          if (a.mu_v) v[t] += a.mu_v[bh * kD + c0 + t];
-        }
+        v[0] = of[mt][4 * rq + 0] * (w4.x * k2) * inv + mu4.x;
+        v[1] = of[mt][4 * rq + 1] * (w4.y * k2) * inv + mu4.y;
+        v[2] = of[mt][4 * rq + 2] * (w4.z * k2) * inv + mu4.z;
+        v[3] = of[mt][4 * rq + 3] * (w4.w * k2) * inv + mu4.w;
         if (a.out_dtype == 2) {
           *reinterpret_cast<float4*>(static_cast<float*>(a.o) + obase + c0) = make_float4(v[0], v[1], v[2], v[3]);
         } else if (a.out_dtype == 0) {

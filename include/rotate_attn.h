@@ -56,7 +56,7 @@
  *   Q/K: token n = 32*c + r, channel ch: record ((c*2 + ch/64)*2 + (ch/32)%2)*32 + r,
  *        field ch%32.
  *   V:   token n = 64*g + kappa, channel ch: record ((g*4 + ch/32)*2 + (kappa/4)%2)*32
- *        + ch%32, field 8*(kappa%4) + 2*((kappa/8)%4) + kappa/32.
+ *        + ch%32, field 8*((kappa%32)/8) + 2*(kappa%4) + kappa/32.
  *
  *  Scales are binary32.  Q scales: [B*H][Npad/q_group]; K scales:
  *  [B*H][Npad/k_group]; V scales: [B*H][ceil(N/v_group)][128].  Q/K groups

@@ -20,8 +20,9 @@
 // Matrix-core mapping (one wave = 32 queries): S^T = K Q^T (A = 32 keys x 64
 // channels of K, B = Q^T), so a lane holds 16 scores of one query per 32-key
 // chunk.  The P codes of two chunks (64 keys) are packed by
-// v_cvt_scalef32_2xpk16_fp6_f32 into the B operand of O^T = V^T P^T; the V
-// records are stored in the key order that packing produces.
+// v_cvt_scalef32_2xpk16_fp6_f32 (which interleaves its two 16-value sources)
+// into the B operand of O^T = V^T P^T; the V records are stored in the key
+// order that packing produces.
 #include <type_traits>
 
 #include "ra_internal.h"
@@ -69,6 +70,7 @@ __global__ __launch_bounds__(256, 2) void k_attn_e2m3(AttnArgs a) {
   __shared__ __align__(16) float sR[2][kD];   // V scale ratio w_old / w_new for the block
   __shared__ __align__(16) float sW[kD];      // final V scale per channel
   __shared__ __align__(16) float sKs[2][KTOK ? KV : 1];
+  __shared__ __align__(16) float sKc[2][NCH];  // K scale of each 32-key chunk (grouped K)
 
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int hh = lane >> 5, j = lane & 31;
@@ -107,6 +109,7 @@ __global__ __launch_bounds__(256, 2) void k_attn_e2m3(AttnArgs a) {
       sR[buf][tid] = r;
     }
     if (KTOK && tid < KV) sKs[buf][tid] = ksh[jb * KV + tid];
+    if (!KTOK && tid >= kD && tid < kD + NCH) sKc[buf][tid - kD] = ksh[(jb * KV + (tid - kD) * 32) / a.k_group];
   };
 
   v16f of[4];
@@ -168,10 +171,18 @@ __global__ __launch_bounds__(256, 2) void k_attn_e2m3(AttnArgs a) {
     //      a fully masked chunk gives -inf, or NaN when c == 0, which fmax ignores) ----
     float cch[NCH];
     float tmax = -INFINITY;
+    const bool vchange = jb > 0 && a.nvgroups > 1 && ((jb * KV) % a.v_group) == 0;
+    float4 rr[4][4];
+    if (vchange) {
+#pragma unroll
+      for (int mt = 0; mt < 4; ++mt)
+#pragma unroll
+        for (int rq = 0; rq < 4; ++rq) rr[mt][rq] = *reinterpret_cast<const float4*>(&sR[buf][mt * 32 + 8 * rq + 4 * hh]);
+    }
     if (!KTOK) {
 #pragma unroll
       for (int ch = 0; ch < NCH; ++ch) {
-        cch[ch] = __fmul_rn(cq, ksh[(key0 + ch * 32) / a.k_group]);
+        cch[ch] = __fmul_rn(cq, sKc[buf][ch]);
         float mx = fmaxf(fmaxf(s[ch][0], s[ch][1]), s[ch][2]);
 #pragma unroll
         for (int r = 3; r < 15; r += 2) mx = fmaxf(fmaxf(mx, s[ch][r]), s[ch][r + 1]);
@@ -193,16 +204,15 @@ __global__ __launch_bounds__(256, 2) void k_attn_e2m3(AttnArgs a) {
     m = mnew;
 
     // ---- rescale O' for the block's V scale and the new maximum ----
-    if (jb > 0 && a.nvgroups > 1 && ((jb * KV) % a.v_group) == 0) {
+    if (vchange) {
 #pragma unroll
       for (int mt = 0; mt < 4; ++mt)
 #pragma unroll
         for (int rq = 0; rq < 4; ++rq) {
-          const float4 rr = *reinterpret_cast<const float4*>(&sR[buf][mt * 32 + 8 * rq + 4 * hh]);
-          of[mt][4 * rq + 0] = __fmul_rn(of[mt][4 * rq + 0], rr.x);
-          of[mt][4 * rq + 1] = __fmul_rn(of[mt][4 * rq + 1], rr.y);
-          of[mt][4 * rq + 2] = __fmul_rn(of[mt][4 * rq + 2], rr.z);
-          of[mt][4 * rq + 3] = __fmul_rn(of[mt][4 * rq + 3], rr.w);
+          of[mt][4 * rq + 0] = __fmul_rn(of[mt][4 * rq + 0], rr[mt][rq].x);
+          of[mt][4 * rq + 1] = __fmul_rn(of[mt][4 * rq + 1], rr[mt][rq].y);
+          of[mt][4 * rq + 2] = __fmul_rn(of[mt][4 * rq + 2], rr[mt][rq].z);
+          of[mt][4 * rq + 3] = __fmul_rn(of[mt][4 * rq + 3], rr[mt][rq].w);
         }
     }
     if (__any(alpha != 1.0f)) {
@@ -213,53 +223,60 @@ __global__ __launch_bounds__(256, 2) void k_attn_e2m3(AttnArgs a) {
     }
     __builtin_amdgcn_sched_barrier(0);
 
-    // ---- P, codes u = rint(15 P) packed as E2M3 u/2, row sums, PV ----
+    // ---- P, codes u = rint(15 P) packed as E2M3 u/2, row sums, PV.  The code
+    //      of each score overwrites the score's register, so the 32 converter
+    //      inputs of a 64-key group are the two chunks' accumulators in place:
+    //      element 2i + c2 of the packed operand is register i of chunk 2gg + c2. ----
     float ls[4] = {0.f, 0.f, 0.f, 0.f};   // independent partial sums
 #pragma unroll
     for (int gg = 0; gg < NG; ++gg) {
-      v8i vop[2];
+      if (DEBUG) {
+        if (bh == a.dbg_bh && qrow >= a.dbg_row0 && qrow < a.dbg_row0 + a.dbg_rows && a.dbg_s) {
+          const size_t rowo = static_cast<size_t>(qrow - a.dbg_row0);
 #pragma unroll
-      for (int mt = 0; mt < 2; ++mt) vop[mt] = load_rec(&sV[buf][(((gg * 4 + mt) * 2 + hh) * 32 + j) * 24]);
-      v16f src[2];
+          for (int c2 = 0; c2 < 2; ++c2)
+#pragma unroll
+            for (int r = 0; r < 16; ++r) {
+              const int key = key0 + (2 * gg + c2) * 32 + 8 * (r >> 2) + 4 * hh + (r & 3);
+              if (key < N) a.dbg_s[rowo * N + key] = static_cast<int32_t>(s[2 * gg + c2][r]);
+            }
+        }
+      }
 #pragma unroll
       for (int c2 = 0; c2 < 2; ++c2) {
         const int ch = 2 * gg + c2;
 #pragma unroll
-        for (int i = 0; i < 16; ++i) {
-          const int r = 4 * (i & 3) + (i >> 2);  // element 2i+c2 of the packed operand
+        for (int r = 0; r < 16; ++r) {
           float c;
           if (KTOK) c = __fmul_rn(cq, sKs[buf][ch * 32 + 8 * (r >> 2) + 4 * hh + (r & 3)]);
           else c = cch[ch];
           float P = __builtin_amdgcn_exp2f(__fmaf_rn(s[ch][r], c, -mnew));
           if (MASKED && s[ch][r] == -INFINITY) P = 0.f;
-          ls[i & 3] += P;
-          src[c2][i] = __builtin_rintf(__fmul_rn(P, pscale));
+          ls[r & 3] += P;
+          s[ch][r] = __builtin_rintf(__fmul_rn(P, pscale));
         }
       }
-      const v6i pk6 = __builtin_amdgcn_cvt_scalef32_2xpk16_fp6_f32(src[0], src[1], 2.0f);
+      const v6i pk6 = __builtin_amdgcn_cvt_scalef32_2xpk16_fp6_f32(s[2 * gg], s[2 * gg + 1], 2.0f);
       const v8i B = v8i{pk6[0], pk6[1], pk6[2], pk6[3], pk6[4], pk6[5], 0, 0};
       if (DEBUG) {
-        if (bh == a.dbg_bh && qrow >= a.dbg_row0 && qrow < a.dbg_row0 + a.dbg_rows) {
+        if (bh == a.dbg_bh && qrow >= a.dbg_row0 && qrow < a.dbg_row0 + a.dbg_rows && a.dbg_u) {
           const size_t rowo = static_cast<size_t>(qrow - a.dbg_row0);
 #pragma unroll
           for (int c2 = 0; c2 < 2; ++c2)
 #pragma unroll
-            for (int i = 0; i < 16; ++i) {
-              const int ch = 2 * gg + c2;
-              const int r = 4 * (i & 3) + (i >> 2);
-              const int key = key0 + ch * 32 + 8 * (r >> 2) + 4 * hh + (r & 3);
-              if (key < N) {
-                if (a.dbg_s) a.dbg_s[rowo * N + key] = static_cast<int32_t>(s[ch][r]);
-                if (a.dbg_u) a.dbg_u[rowo * N + key] = static_cast<uint8_t>(src[c2][i]);
-              }
+            for (int r = 0; r < 16; ++r) {
+              const int key = key0 + (2 * gg + c2) * 32 + 8 * (r >> 2) + 4 * hh + (r & 3);
+              if (key < N) a.dbg_u[rowo * N + key] = static_cast<uint8_t>(s[2 * gg + c2][r]);
             }
         }
       }
       {
+        const v8i v0 = load_rec(&sV[buf][(((gg * 4 + 0) * 2 + hh) * 32 + j) * 24]);
+        const v8i v1 = load_rec(&sV[buf][(((gg * 4 + 1) * 2 + hh) * 32 + j) * 24]);
+        of[0] = mfma6(v0, B, of[0]);
         const v8i v2 = load_rec(&sV[buf][(((gg * 4 + 2) * 2 + hh) * 32 + j) * 24]);
-        of[0] = mfma6(vop[0], B, of[0]);
+        of[1] = mfma6(v1, B, of[1]);
         const v8i v3 = load_rec(&sV[buf][(((gg * 4 + 3) * 2 + hh) * 32 + j) * 24]);
-        of[1] = mfma6(vop[1], B, of[1]);
         of[2] = mfma6(v2, B, of[2]);
         of[3] = mfma6(v3, B, of[3]);
       }

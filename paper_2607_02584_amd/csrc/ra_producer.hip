@@ -400,9 +400,13 @@ __global__ __launch_bounds__(256) void k_v_quant(VArgs a) {
   float z[16][4];
   load_v_tile(a, bh, tile, z);
   if (a.e2m3) {
-    // group of 64 tokens gl = p/8, kappa = (p%8)*8 + rr, half h = (rr/4)%2; the thread's 8 codes of a
-    // channel in that group are the fields 8*(rr%4) .. +7 (field 8*(rr%4) + 2*(p%4) + (p%8)/4), i.e.
-    // bytes 6*(rr%4) .. +5 of record ((gl*4 + ch/32)*2 + h)*32 + ch%32 (tile-local gl).
+    // group of 64 tokens gl = p/8, kappa = (p%8)*8 + rr, half h = (rr/4)%2; token kappa of a channel is
+    // field 8*((kappa%32)/8) + 2*(kappa%4) + kappa/32 of record ((gl*4 + ch/32)*2 + h)*32 + ch%32.
+    // The thread's codes for passes q and q+4 (q = p%4) are the adjacent fields 8q + 2*(rr%4) and
+    // +1: a 12-bit piece at bit 48q + 12*(rr%4); pieces are merged into LDS with atomic OR.
+    uint32_t* cw = reinterpret_cast<uint32_t*>(ctile);
+    for (int i = tid; i < kTile * 96 / 4; i += 256) cw[i] = 0u;
+    __syncthreads();
     const int s4 = rr & 3, hh = (rr >> 2) & 1;
 #pragma unroll
     for (int gl = 0; gl < 2; ++gl) {
@@ -410,17 +414,15 @@ __global__ __launch_bounds__(256) void k_v_quant(VArgs a) {
       for (int c = 0; c < 4; ++c) {
         const int ch = 4 * cl + c;
         const float inv = ginv[gl][ch];
-        uint64_t bits = 0;
-#pragma unroll
-        for (int pp = 0; pp < 8; ++pp) {
-          const int f = 2 * (pp & 3) + (pp >> 2);
-          bits |= static_cast<uint64_t>(e2m3_of(qcode(z[gl * 8 + pp][c], inv))) << (6 * f);
-        }
         const int rec = ((gl * 4 + (ch >> 5)) * 2 + hh) * 32 + (ch & 31);
-        uint16_t* d = reinterpret_cast<uint16_t*>(&ctile[rec * 24 + 6 * s4]);
-        d[0] = static_cast<uint16_t>(bits);
-        d[1] = static_cast<uint16_t>(bits >> 16);
-        d[2] = static_cast<uint16_t>(bits >> 32);
+#pragma unroll
+        for (int q = 0; q < 4; ++q) {
+          const uint32_t piece = e2m3_of(qcode(z[gl * 8 + q][c], inv)) | (e2m3_of(qcode(z[gl * 8 + q + 4][c], inv)) << 6);
+          const int b = 48 * q + 12 * s4;
+          const int w = rec * 6 + (b >> 5), sh = b & 31;
+          atomicOr(&cw[w], piece << sh);
+          if (sh > 20) atomicOr(&cw[w + 1], piece >> (32 - sh));
+        }
       }
     }
     __syncthreads();

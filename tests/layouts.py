@@ -79,11 +79,11 @@ def unpack_qk_e2m3(codes: np.ndarray, BH: int, Npad: int, N: int) -> np.ndarray:
 
 
 def v_key_of_field() -> np.ndarray:
-    """key (0..63 inside a 64-token group) of half h, field e: 32(e%2) + 8((e%8)/2) + 4h + e/8."""
+    """key (0..63 inside a 64-token group) of half h, field e: 32(e%2) + 8(e/8) + 4h + (e/2)%4."""
     k = np.empty((2, 32), np.int64)
     for h in range(2):
         for e in range(32):
-            k[h, e] = 32 * (e % 2) + 8 * ((e % 8) // 2) + 4 * h + e // 8
+            k[h, e] = 32 * (e % 2) + 8 * (e // 8) + 4 * h + (e // 2) % 4
     return k
 
 

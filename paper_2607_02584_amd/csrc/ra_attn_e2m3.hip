@@ -3,19 +3,22 @@
 // Same computation as the int8 kernel (the paper's Sec. 4.2 blockwise online
 // softmax with the Range-optimized P quantization over INT4 Q, K, V codes),
 // but every INT4 code is carried as the 6-bit E2M3 float of the same value.
-// E2M3 represents the integers -7..7 and the half-integers u/2, u = 0..15,
-// exactly, and the products and 64-term sums of the matrix core stay integer
-// multiples of 1/2 below 2^24, so
+// E2M3 represents the integers -7..7 exactly, and u/8 for u = 0..15 with a
+// uniform step (the subnormals and the first binade), and the E2M3 bit pattern
+// of u/8 is the integer u itself.  The products and 64-term sums of the matrix
+// core stay integer multiples of 1/8 far below 2^24, so
 //   S  = Q~ K~^T                         is the exact integer score, and
-//   O' += V~^T (u/2)                     is exact per block,
+//   O' += V~^T (u/8)                     is exact per block,
 // on v_mfma_scale_f32_32x32x64_f8f6f4, which runs at twice the int8 rate and
 // accumulates in binary32: PV accumulates straight into the output tile.
 //
 // Per block of KV keys (ascending):
 //   m_new = max(m, rowmax fl(S * c)),  x = fma(S, c, -m_new),  P = 2^x,
-//   u = rint(15 P),  l = alpha l + sum P,  alpha = 2^(m - m_new),
-//   O' = O' * alpha * (w_old / w_new) + V~^T (u/2)   (w = V scale of the block's group)
-// and finally O = O' * 2 w / 15 / l + mu_v.
+//   u = rint(fl(15 P)),  l = alpha l + sum P,  alpha = 2^(m - m_new),
+//   O' = O' * alpha * (w_old / w_new) + V~^T (u/8)   (w = V scale of the block's group)
+// and finally O = O' * 8 w / 15 / l + mu_v.  The rounding u = rint(fl(15 P)) is
+// done by the packing conversion itself: it converts fl(15 P) / 8 to E2M3 with
+// round-to-nearest-even, and on the uniform 1/8 grid that is rint to an integer.
 //
 // Matrix-core mapping (one wave = 32 queries): S^T = K Q^T (A = 32 keys x 64
 // channels of K, B = Q^T), so a lane holds 16 scores of one query per 32-key
@@ -179,7 +182,24 @@ __global__ __launch_bounds__(256, 2) void k_attn_e2m3(AttnArgs a) {
 #pragma unroll
         for (int rq = 0; rq < 4; ++rq) rr[mt][rq] = *reinterpret_cast<const float4*>(&sR[buf][mt * 32 + 8 * rq + 4 * hh]);
     }
-    if (!KTOK) {
+    if (!KTOK && a.k_group >= KV) {
+      // one K scale for the whole block: a single product after the maximum
+      float cm[NCH];
+#pragma unroll
+      for (int ch = 0; ch < NCH; ++ch) {
+        float mx = fmaxf(fmaxf(s[ch][0], s[ch][1]), s[ch][2]);
+#pragma unroll
+        for (int r = 3; r < 15; r += 2) mx = fmaxf(fmaxf(mx, s[ch][r]), s[ch][r + 1]);
+        cm[ch] = fmaxf(mx, s[ch][15]);
+      }
+      float mx = cm[0];
+#pragma unroll
+      for (int ch = 1; ch < NCH; ++ch) mx = fmaxf(mx, cm[ch]);
+      const float c0 = __fmul_rn(cq, sKc[buf][0]);
+#pragma unroll
+      for (int ch = 0; ch < NCH; ++ch) cch[ch] = c0;
+      tmax = __fmul_rn(mx, c0);
+    } else if (!KTOK) {
 #pragma unroll
       for (int ch = 0; ch < NCH; ++ch) {
         cch[ch] = __fmul_rn(cq, sKc[buf][ch]);
@@ -223,11 +243,11 @@ __global__ __launch_bounds__(256, 2) void k_attn_e2m3(AttnArgs a) {
     }
     __builtin_amdgcn_sched_barrier(0);
 
-    // ---- P, codes u = rint(15 P) packed as E2M3 u/2, row sums, PV.  The code
-    //      of each score overwrites the score's register, so the 32 converter
+    // ---- P, codes u = rint(15 P) packed as E2M3 u/8, row sums, PV.  15 P
+    //      overwrites the score's register, so the 32 converter
     //      inputs of a 64-key group are the two chunks' accumulators in place:
     //      element 2i + c2 of the packed operand is register i of chunk 2gg + c2. ----
-    float ls[4] = {0.f, 0.f, 0.f, 0.f};   // independent partial sums
+    float ls[4];   // independent partial sums, started by the first four values
 #pragma unroll
     for (int gg = 0; gg < NG; ++gg) {
       if (DEBUG) {
@@ -252,11 +272,14 @@ __global__ __launch_bounds__(256, 2) void k_attn_e2m3(AttnArgs a) {
           else c = cch[ch];
           float P = __builtin_amdgcn_exp2f(__fmaf_rn(s[ch][r], c, -mnew));
           if (MASKED && s[ch][r] == -INFINITY) P = 0.f;
-          ls[r & 3] += P;
-          s[ch][r] = __builtin_rintf(__fmul_rn(P, pscale));
+          if (gg == 0 && c2 == 0 && r < 4) ls[r] = P;
+          else ls[r & 3] += P;
+          s[ch][r] = __fmul_rn(P, pscale);
         }
       }
-      const v6i pk6 = __builtin_amdgcn_cvt_scalef32_2xpk16_fp6_f32(s[2 * gg], s[2 * gg + 1], 2.0f);
+      // E2M3(rint(fl(15 P)) / 8): the conversion divides by the power-of-two
+      // scale exactly and rounds to nearest even on the uniform 1/8 grid
+      const v6i pk6 = __builtin_amdgcn_cvt_scalef32_2xpk16_fp6_f32(s[2 * gg], s[2 * gg + 1], 8.0f);
       const v8i B = v8i{pk6[0], pk6[1], pk6[2], pk6[3], pk6[4], pk6[5], 0, 0};
       if (DEBUG) {
         if (bh == a.dbg_bh && qrow >= a.dbg_row0 && qrow < a.dbg_row0 + a.dbg_rows && a.dbg_u) {
@@ -266,7 +289,10 @@ __global__ __launch_bounds__(256, 2) void k_attn_e2m3(AttnArgs a) {
 #pragma unroll
             for (int r = 0; r < 16; ++r) {
               const int key = key0 + (2 * gg + c2) * 32 + 8 * (r >> 2) + 4 * hh + (r & 3);
-              if (key < N) a.dbg_u[rowo * N + key] = static_cast<uint8_t>(s[2 * gg + c2][r]);
+              const int bit = 6 * (2 * r + c2);   // packed element 2r + c2; its E2M3 code is u
+              uint32_t w = static_cast<uint32_t>(pk6[bit >> 5]) >> (bit & 31);
+              if ((bit & 31) > 26) w |= static_cast<uint32_t>(pk6[(bit >> 5) + 1]) << (32 - (bit & 31));
+              if (key < N) a.dbg_u[rowo * N + key] = static_cast<uint8_t>(w & 63);
             }
         }
       }
@@ -296,11 +322,11 @@ __global__ __launch_bounds__(256, 2) void k_attn_e2m3(AttnArgs a) {
   if (tid < kD) sW[tid] = wcur;
   __syncthreads();
 
-  // ---- epilogue: O = O' * 2 w / 15 / l + mu_v ----
+  // ---- epilogue: O = O' * 8 w / 15 / l + mu_v ----
   const float ltot = l + __shfl_xor(l, 32);
   if (qrow < N) {
     const float inv = 1.0f / ltot;
-    const float k2 = 2.0f / pscale;
+    const float k2 = 8.0f / pscale;
     const size_t obase = (static_cast<size_t>(bh) * N + qrow) * kD;
     const float* muv = a.mu_v ? a.mu_v + bh * kD : nullptr;
 #pragma unroll

@@ -8,24 +8,28 @@
 // of u/8 is the integer u itself.  The products and 64-term sums of the matrix
 // core stay integer multiples of 1/8 far below 2^24, so
 //   S  = Q~ K~^T                         is the exact integer score, and
-//   O' += V~^T (u/8)                     is exact per block,
+//   O' += (u/8) V~                       is exact per block,
 // on v_mfma_scale_f32_32x32x64_f8f6f4, which runs at twice the int8 rate and
 // accumulates in binary32: PV accumulates straight into the output tile.
 //
 // Per block of KV keys (ascending):
 //   m_new = max(m, rowmax fl(S * c)),  x = fma(S, c, -m_new),  P = 2^x,
 //   u = rint(fl(15 P)),  l = alpha l + sum P,  alpha = 2^(m - m_new),
-//   O' = O' * alpha * (w_old / w_new) + V~^T (u/8)   (w = V scale of the block's group)
+//   O' = O' * alpha * (w_old / w_new) + (u/8) V~   (w = V scale of the block's group)
 // and finally O = O' * 8 w / 15 / l + mu_v.  The rounding u = rint(fl(15 P)) is
 // done by the packing conversion itself: it converts fl(15 P) / 8 to E2M3 with
 // round-to-nearest-even, and on the uniform 1/8 grid that is rint to an integer.
 //
 // Matrix-core mapping (one wave = 32 queries): S^T = K Q^T (A = 32 keys x 64
 // channels of K, B = Q^T), so a lane holds 16 scores of one query per 32-key
-// chunk.  The P codes of two chunks (64 keys) are packed by
-// v_cvt_scalef32_2xpk16_fp6_f32 (which interleaves its two 16-value sources)
-// into the B operand of O^T = V^T P^T; the V records are stored in the key
-// order that packing produces.
+// chunk, and the row statistics m, l are per lane.  The P codes of two chunks
+// (64 keys) are packed by v_cvt_scalef32_2xpk16_fp6_f32 (which interleaves its
+// two 16-value sources) into the A operand of O = P V~ (A and B operands share
+// one lane layout: lane = row or column, lane / 32 = half of the reduction),
+// and the V records, read as the B operand, are stored in the key order that
+// packing produces.  In the output tile a lane holds one channel of 16
+// queries, so the per-channel V scale ratio is one register per tile, and
+// alpha reaches the query rows by a lane permute when some row's max moved.
 #include <type_traits>
 
 #include "ra_internal.h"
@@ -37,7 +41,11 @@ typedef int v8i __attribute__((ext_vector_type(8)));
 typedef int v6i __attribute__((ext_vector_type(6)));
 typedef float v16f __attribute__((ext_vector_type(16)));
 
-constexpr int kBlockM = 128;  // queries per workgroup (4 waves x 32)
+// A workgroup of 4 waves (one per SIMD) covers 128 queries; two workgroups
+// share a compute unit.
+constexpr int kWaves = 4;
+constexpr int kThreads = 64 * kWaves;
+constexpr int kBlockM = 32 * kWaves;  // queries per workgroup
 constexpr int kScaleOne = 127;  // E8M0 block scale 2^0
 
 __device__ __forceinline__ v16f mfma6(v8i a, v8i b, v16f c) {
@@ -53,24 +61,46 @@ __device__ __forceinline__ v8i load_rec(const uint8_t* p) {
              static_cast<int>(c.x), static_cast<int>(c.y), 0, 0};
 }
 
-// Copies `bytes` (a multiple of 1024) from global to LDS with the LDS-DMA path
-// (global_load_lds_dwordx4: lane i of a wave moves 16 bytes to base + 16 i);
-// the four waves of the workgroup take every fourth kilobyte.
-__device__ __forceinline__ void dma_copy(const uint8_t* src, uint8_t* dst, int bytes, int wave, int lane) {
-  for (int off = wave * 1024; off < bytes; off += 4096) {
-    __builtin_amdgcn_global_load_lds((const void __attribute__((address_space(1)))*)(src + off + lane * 16),
-                                     (void __attribute__((address_space(3)))*)(dst + off), 16, 0, 0);
+// K and V code tiles of one block go global -> registers -> LDS: every thread
+// moves three 16-byte (KV = 128) or 8-byte (KV = 64) pieces of each, adjacent
+// threads adjacent pieces.  The global loads of block j + 2 are issued at the
+// end of block j and written to LDS at the start of block j + 1, so their
+// latency overlaps the end-of-block barrier.
+template <int KV>
+struct TilePiece {
+  // 16-byte (KV = 128) or 8-byte (KV = 64) pieces as 32-bit vectors, six per thread
+  typedef unsigned T __attribute__((ext_vector_type(KV == 128 ? 4 : 2)));
+  T k0, k1, k2, v0, v1, v2;
+  __device__ __forceinline__ void load(const uint8_t* kg, const uint8_t* vg, int tid) {
+    const T* K = reinterpret_cast<const T*>(kg) + tid;
+    const T* V = reinterpret_cast<const T*>(vg) + tid;
+    k0 = K[0];
+    v0 = V[0];
+    k1 = K[kThreads];
+    v1 = V[kThreads];
+    k2 = K[2 * kThreads];
+    v2 = V[2 * kThreads];
   }
-}
+  __device__ __forceinline__ void store(uint8_t* ks, uint8_t* vs, int tid) const {
+    T* K = reinterpret_cast<T*>(ks) + tid;
+    T* V = reinterpret_cast<T*>(vs) + tid;
+    K[0] = k0;
+    V[0] = v0;
+    K[kThreads] = k1;
+    V[kThreads] = v1;
+    K[2 * kThreads] = k2;
+    V[2 * kThreads] = v2;
+  }
+};
 
 template <int KV, bool KTOK, bool SYM7, bool DEBUG>
-__global__ __launch_bounds__(256, 2) void k_attn_e2m3(AttnArgs a) {
+__global__ __launch_bounds__(kThreads, 8 / kWaves) void k_attn_e2m3(AttnArgs a) {
   constexpr int NCH = KV / 32;   // 32-key chunks
   constexpr int NG = KV / 64;    // 64-key groups (one PV instruction each)
   constexpr int KB = KV * 96;    // bytes of K (and of V) codes per block
   __shared__ __align__(16) uint8_t sK[2][KB];
   __shared__ __align__(16) uint8_t sV[2][KB];
-  __shared__ __align__(16) float sR[2][kD];   // V scale ratio w_old / w_new for the block
+  __shared__ __align__(16) float sR[2][kD];   // V scale ratio w_old / w_new, channel 32 mt + j at 4 j + mt
   __shared__ __align__(16) float sW[kD];      // final V scale per channel
   __shared__ __align__(16) float sKs[2][KTOK ? KV : 1];
   __shared__ __align__(16) float sKc[2][NCH];  // K scale of each 32-key chunk (grouped K)
@@ -89,30 +119,54 @@ __global__ __launch_bounds__(256, 2) void k_attn_e2m3(AttnArgs a) {
   const float* ksh = a.ks + static_cast<size_t>(bh) * kstride;
 
   // ---- Q operand (B of S^T = K Q^T) ----
-  v8i qop[2];
+  // (a wave whose 32 queries lie past the padded length, in the last
+  //  workgroup, computes on zero codes and stores nothing)
+  const bool qin = qrow < a.Npad;
+  v8i qop[2] = {v8i{0, 0, 0, 0, 0, 0, 0, 0}, v8i{0, 0, 0, 0, 0, 0, 0, 0}};
+  float cq = 0.f;
+  if (qin) {
 #pragma unroll
-  for (int kc = 0; kc < 2; ++kc) {
-    const int rec = (((qrow >> 5) * 2 + kc) * 2 + hh) * 32 + (qrow & 31);
-    qop[kc] = load_rec(a.qc + hcode + static_cast<size_t>(rec) * 24);
+    for (int kc = 0; kc < 2; ++kc) {
+      const int rec = (((qrow >> 5) * 2 + kc) * 2 + hh) * 32 + (qrow & 31);
+      qop[kc] = load_rec(a.qc + hcode + static_cast<size_t>(rec) * 24);
+    }
+    cq = __fmul_rn(a.qs[static_cast<size_t>(bh) * (a.Npad / a.q_group) + qrow / a.q_group], a.Kc);
   }
-  const float cq = __fmul_rn(a.qs[static_cast<size_t>(bh) * (a.Npad / a.q_group) + qrow / a.q_group], a.Kc);
 
-  // V scale bookkeeping: thread ch < 128 owns channel ch's working scale w.
-  float wcur = 1.0f;
-  auto stage_aux = [&](int jb, int buf) {
+  // Per-block side data: the V scales of the block's group (thread ch < 128
+  // owns channel ch's working scale w and writes the ratio w_old / w_new) and
+  // the K scales (per 32-key chunk, or per key; thread 128 + t takes scale t).
+  // They are fetched from global memory one block ahead of staging, so no
+  // wave waits on their latency.
+  struct Aux {
+    float v, k;
+  };
+  auto fetch_aux = [&](int jb) {
+    Aux f{0.f, 0.f};
     if (tid < kD) {
       int g = (jb * KV) / a.v_group;
       if (g >= a.nvgroups) g = a.nvgroups - 1;
-      const float s = a.vs[(static_cast<size_t>(bh) * a.nvgroups + g) * kD + tid];
-      float r = 1.0f;
-      if (s > 0.0f) {
-        r = (jb == 0) ? 1.0f : __fdiv_rn(wcur, s);
-        wcur = s;
-      }
-      sR[buf][tid] = r;
+      f.v = a.vs[(static_cast<size_t>(bh) * a.nvgroups + g) * kD + tid];
     }
-    if (KTOK && tid < KV) sKs[buf][tid] = ksh[jb * KV + tid];
-    if (!KTOK && tid >= kD && tid < kD + NCH) sKc[buf][tid - kD] = ksh[(jb * KV + (tid - kD) * 32) / a.k_group];
+    const int kt = tid - kD;
+    if (kt >= 0 && kt < (KTOK ? KV : NCH)) f.k = KTOK ? ksh[jb * KV + kt] : ksh[(jb * KV + kt * 32) / a.k_group];
+    return f;
+  };
+  float wcur = 1.0f;
+  auto store_aux = [&](int jb, int buf, const Aux& f) {
+    if (tid < kD) {
+      float r = 1.0f;
+      if (f.v > 0.0f) {
+        r = (jb == 0) ? 1.0f : wcur * __builtin_amdgcn_rcpf(f.v);
+        wcur = f.v;
+      }
+      sR[buf][(tid & 31) * 4 + (tid >> 5)] = r;
+    }
+    const int kt = tid - kD;
+    if (kt >= 0 && kt < (KTOK ? KV : NCH)) {
+      if (KTOK) sKs[buf][kt] = f.k;
+      else sKc[buf][kt] = f.k;
+    }
   };
 
   v16f of[4];
@@ -122,10 +176,14 @@ __global__ __launch_bounds__(256, 2) void k_attn_e2m3(AttnArgs a) {
     for (int r = 0; r < 16; ++r) of[mt][r] = 0.f;
   float m = -INFINITY, l = 0.f;
 
-  dma_copy(kbase, sK[0], KB, wave, lane);
-  dma_copy(vbase, sV[0], KB, wave, lane);
-  stage_aux(0, 0);
-  asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
+  static_assert(KB == 3 * kThreads * static_cast<int>(sizeof(typename TilePiece<KV>::T)), "three pieces per thread");
+  TilePiece<KV> tp;
+  tp.load(kbase, vbase, tid);
+  tp.store(sK[0], sV[0], tid);
+  tp.load(kbase + (nblocks > 1 ? KB : 0), vbase + (nblocks > 1 ? KB : 0), tid);
+  store_aux(0, 0, fetch_aux(0));
+  Aux pf{0.f, 0.f};
+  if (nblocks > 1) pf = fetch_aux(1);
   __syncthreads();
 
   // One block of KV keys.  MASKED (keys past N) only for the partial last
@@ -135,30 +193,37 @@ __global__ __launch_bounds__(256, 2) void k_attn_e2m3(AttnArgs a) {
     const int buf = jb & 1;
     const int key0 = jb * KV;
     if (jb + 1 < nblocks) {
-      dma_copy(kbase + static_cast<size_t>(jb + 1) * KB, sK[buf ^ 1], KB, wave, lane);
-      dma_copy(vbase + static_cast<size_t>(jb + 1) * KB, sV[buf ^ 1], KB, wave, lane);
-      stage_aux(jb + 1, buf ^ 1);
+      tp.store(sK[buf ^ 1], sV[buf ^ 1], tid);
+      store_aux(jb + 1, buf ^ 1, pf);
+      if (jb + 2 < nblocks) pf = fetch_aux(jb + 2);
     }
     __builtin_amdgcn_sched_barrier(0);
 
-    // ---- S^T = K Q^T: exact integer scores in binary32; the operands of
-    //      chunk ch+1 are read from LDS while chunk ch is on the matrix core ----
+    // ---- S^T = K Q^T: exact integer scores in binary32.  The first channel
+    //      half of every chunk goes first, so the two products into one
+    //      accumulator are NCH instructions apart; operands are read from LDS
+    //      two instructions ahead. ----
     v16f s[NCH];
-    v8i kop0 = load_rec(&sK[buf][((0 * 2 + hh) * 32 + j) * 24]);
-    v8i kop1 = load_rec(&sK[buf][((1 * 2 + hh) * 32 + j) * 24]);
+    constexpr int NQ = 2 * NCH;
+    auto krec = [&](int t) {
+      const int ch = t % NCH, kc = t / NCH;
+      return load_rec(&sK[buf][(((ch * 2 + kc) * 2 + hh) * 32 + j) * 24]);
+    };
+    v8i ka = krec(0), kb = krec(1);
 #pragma unroll
-    for (int ch = 0; ch < NCH; ++ch) {
-      v8i n0 = kop0, n1 = kop1;
-      if (ch + 1 < NCH) {
-        n0 = load_rec(&sK[buf][(((((ch + 1) * 2) + 0) * 2 + hh) * 32 + j) * 24]);
-        n1 = load_rec(&sK[buf][(((((ch + 1) * 2) + 1) * 2 + hh) * 32 + j) * 24]);
+    for (int t = 0; t < NQ; ++t) {
+      const v8i kn = (t + 2 < NQ) ? krec(t + 2) : ka;
+      const int ch = t % NCH;
+      if (t < NCH) {
+        v16f z;
+#pragma unroll
+        for (int r = 0; r < 16; ++r) z[r] = 0.f;
+        s[ch] = mfma6(ka, qop[0], z);
+      } else {
+        s[ch] = mfma6(ka, qop[1], s[ch]);
       }
-#pragma unroll
-      for (int r = 0; r < 16; ++r) s[ch][r] = 0.f;
-      s[ch] = mfma6(kop0, qop[0], s[ch]);
-      s[ch] = mfma6(kop1, qop[1], s[ch]);
-      kop0 = n0;
-      kop1 = n1;
+      ka = kb;
+      kb = kn;
       __builtin_amdgcn_sched_barrier(0);
     }
     // key of accumulator register r in chunk ch: key0 + 32*ch + 8*(r/4) + 4*hh + r%4
@@ -175,13 +240,8 @@ __global__ __launch_bounds__(256, 2) void k_attn_e2m3(AttnArgs a) {
     float cch[NCH];
     float tmax = -INFINITY;
     const bool vchange = jb > 0 && a.nvgroups > 1 && ((jb * KV) % a.v_group) == 0;
-    float4 rr[4][4];
-    if (vchange) {
-#pragma unroll
-      for (int mt = 0; mt < 4; ++mt)
-#pragma unroll
-        for (int rq = 0; rq < 4; ++rq) rr[mt][rq] = *reinterpret_cast<const float4*>(&sR[buf][mt * 32 + 8 * rq + 4 * hh]);
-    }
+    float4 rr = make_float4(1.f, 1.f, 1.f, 1.f);
+    if (vchange) rr = *reinterpret_cast<const float4*>(&sR[buf][4 * j]);
     if (!KTOK && a.k_group >= KV) {
       // one K scale for the whole block: a single product after the maximum
       float cm[NCH];
@@ -223,23 +283,24 @@ __global__ __launch_bounds__(256, 2) void k_attn_e2m3(AttnArgs a) {
     const float alpha = __builtin_amdgcn_exp2f(m - mnew);
     m = mnew;
 
-    // ---- rescale O' for the block's V scale and the new maximum ----
+    // ---- rescale O' for the block's V scale and the new maximum; register r of
+    //      tile mt is channel 32 mt + j of query 8 (r / 4) + 4 hh + r % 4 ----
     if (vchange) {
 #pragma unroll
-      for (int mt = 0; mt < 4; ++mt)
-#pragma unroll
-        for (int rq = 0; rq < 4; ++rq) {
-          of[mt][4 * rq + 0] = __fmul_rn(of[mt][4 * rq + 0], rr[mt][rq].x);
-          of[mt][4 * rq + 1] = __fmul_rn(of[mt][4 * rq + 1], rr[mt][rq].y);
-          of[mt][4 * rq + 2] = __fmul_rn(of[mt][4 * rq + 2], rr[mt][rq].z);
-          of[mt][4 * rq + 3] = __fmul_rn(of[mt][4 * rq + 3], rr[mt][rq].w);
-        }
+      for (int r = 0; r < 16; ++r) {
+        of[0][r] = __fmul_rn(of[0][r], rr.x);
+        of[1][r] = __fmul_rn(of[1][r], rr.y);
+        of[2][r] = __fmul_rn(of[2][r], rr.z);
+        of[3][r] = __fmul_rn(of[3][r], rr.w);
+      }
     }
     if (__any(alpha != 1.0f)) {
 #pragma unroll
-      for (int mt = 0; mt < 4; ++mt)
+      for (int r = 0; r < 16; ++r) {
+        const float ar = __shfl(alpha, 8 * (r >> 2) + 4 * hh + (r & 3));
 #pragma unroll
-        for (int r = 0; r < 16; ++r) of[mt][r] = __fmul_rn(of[mt][r], alpha);
+        for (int mt = 0; mt < 4; ++mt) of[mt][r] = __fmul_rn(of[mt][r], ar);
+      }
     }
     __builtin_amdgcn_sched_barrier(0);
 
@@ -280,7 +341,7 @@ __global__ __launch_bounds__(256, 2) void k_attn_e2m3(AttnArgs a) {
       // E2M3(rint(fl(15 P)) / 8): the conversion divides by the power-of-two
       // scale exactly and rounds to nearest even on the uniform 1/8 grid
       const v6i pk6 = __builtin_amdgcn_cvt_scalef32_2xpk16_fp6_f32(s[2 * gg], s[2 * gg + 1], 8.0f);
-      const v8i B = v8i{pk6[0], pk6[1], pk6[2], pk6[3], pk6[4], pk6[5], 0, 0};
+      const v8i B = v8i{pk6[0], pk6[1], pk6[2], pk6[3], pk6[4], pk6[5], 0, 0};   // A operand of O = P V~
       if (DEBUG) {
         if (bh == a.dbg_bh && qrow >= a.dbg_row0 && qrow < a.dbg_row0 + a.dbg_rows && a.dbg_u) {
           const size_t rowo = static_cast<size_t>(qrow - a.dbg_row0);
@@ -299,19 +360,24 @@ __global__ __launch_bounds__(256, 2) void k_attn_e2m3(AttnArgs a) {
       {
         const v8i v0 = load_rec(&sV[buf][(((gg * 4 + 0) * 2 + hh) * 32 + j) * 24]);
         const v8i v1 = load_rec(&sV[buf][(((gg * 4 + 1) * 2 + hh) * 32 + j) * 24]);
-        of[0] = mfma6(v0, B, of[0]);
+        of[0] = mfma6(B, v0, of[0]);
         const v8i v2 = load_rec(&sV[buf][(((gg * 4 + 2) * 2 + hh) * 32 + j) * 24]);
-        of[1] = mfma6(v1, B, of[1]);
+        of[1] = mfma6(B, v1, of[1]);
         const v8i v3 = load_rec(&sV[buf][(((gg * 4 + 3) * 2 + hh) * 32 + j) * 24]);
-        of[2] = mfma6(v2, B, of[2]);
-        of[3] = mfma6(v3, B, of[3]);
+        of[2] = mfma6(B, v2, of[2]);
+        of[3] = mfma6(B, v3, of[3]);
       }
       __builtin_amdgcn_sched_barrier(0);
     }
     l = __fmaf_rn(l, alpha, (ls[0] + ls[1]) + (ls[2] + ls[3]));
     if (DEBUG && a.dbg_m && hh == 0 && bh == a.dbg_bh && qrow >= a.dbg_row0 && qrow < a.dbg_row0 + a.dbg_rows)
       a.dbg_m[static_cast<size_t>(qrow - a.dbg_row0) * nblocks + jb] = mnew;
-    asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
+    {
+      // unconditional (the last blocks reload the final tile), so the pieces
+      // are not live through the block body
+      const size_t nb2 = static_cast<size_t>(jb + 2 < nblocks ? jb + 2 : nblocks - 1) * KB;
+      tp.load(kbase + nb2, vbase + nb2, tid);
+    }
     __syncthreads();
   };
 
@@ -322,49 +388,39 @@ __global__ __launch_bounds__(256, 2) void k_attn_e2m3(AttnArgs a) {
   if (tid < kD) sW[tid] = wcur;
   __syncthreads();
 
-  // ---- epilogue: O = O' * 8 w / 15 / l + mu_v ----
+  // ---- epilogue: O = O' * 8 w / 15 / l + mu_v; lane (j, hh) holds channel
+  //      32 mt + j of the wave's queries 8 (r / 4) + 4 hh + r % 4 ----
   const float ltot = l + __shfl_xor(l, 32);
-  if (qrow < N) {
-    const float inv = 1.0f / ltot;
-    const float k2 = 8.0f / pscale;
-    const size_t obase = (static_cast<size_t>(bh) * N + qrow) * kD;
-    const float* muv = a.mu_v ? a.mu_v + bh * kD : nullptr;
+  const float k2 = 8.0f / pscale;
+  const float* muv = a.mu_v ? a.mu_v + bh * kD : nullptr;
+  float wsc[4], mu[4];
 #pragma unroll
-    for (int mt = 0; mt < 4; ++mt)
+  for (int mt = 0; mt < 4; ++mt) {
+    wsc[mt] = sW[mt * 32 + j] * k2;
+    mu[mt] = muv ? muv[mt * 32 + j] : 0.f;
+  }
+  const int q0 = blockIdx.x * kBlockM + wave * 32;
 #pragma unroll
-      for (int rq = 0; rq < 4; ++rq) {
-        const int c0 = mt * 32 + 8 * rq + 4 * hh;
-        const float4 w4 = *reinterpret_cast<const float4*>(&sW[c0]);
-        float4 mu4 = make_float4(0.f, 0.f, 0.f, 0.f);
-        if (muv) mu4 = *reinterpret_cast<const float4*>(muv + c0);
-        float v[4];
-        v[0] = of[mt][4 * rq + 0] * (w4.x * k2) * inv + mu4.x;
-        v[1] = of[mt][4 * rq + 1] * (w4.y * k2) * inv + mu4.y;
-        v[2] = of[mt][4 * rq + 2] * (w4.z * k2) * inv + mu4.z;
-        v[3] = of[mt][4 * rq + 3] * (w4.w * k2) * inv + mu4.w;
-        if (a.out_dtype == 2) {
-          *reinterpret_cast<float4*>(static_cast<float*>(a.o) + obase + c0) = make_float4(v[0], v[1], v[2], v[3]);
-        } else if (a.out_dtype == 0) {
-          uint16_t b[4];
+  for (int r = 0; r < 16; ++r) {
+    const int qi = 8 * (r >> 2) + 4 * hh + (r & 3);
+    const float inv = 1.0f / __shfl(ltot, qi);
+    if (q0 + qi < N) {
+      const size_t obase = (static_cast<size_t>(bh) * N + q0 + qi) * kD + j;
 #pragma unroll
-          for (int t = 0; t < 4; ++t) b[t] = __bfloat16_as_ushort(__float2bfloat16(v[t]));
-          *reinterpret_cast<uint2*>(static_cast<uint16_t*>(a.o) + obase + c0) =
-              make_uint2(b[0] | (static_cast<uint32_t>(b[1]) << 16), b[2] | (static_cast<uint32_t>(b[3]) << 16));
-        } else {
-          uint16_t b[4];
-#pragma unroll
-          for (int t = 0; t < 4; ++t) b[t] = __half_as_ushort(__float2half(v[t]));
-          *reinterpret_cast<uint2*>(static_cast<uint16_t*>(a.o) + obase + c0) =
-              make_uint2(b[0] | (static_cast<uint32_t>(b[1]) << 16), b[2] | (static_cast<uint32_t>(b[3]) << 16));
-        }
+      for (int mt = 0; mt < 4; ++mt) {
+        const float v = of[mt][r] * wsc[mt] * inv + mu[mt];
+        if (a.out_dtype == 2) static_cast<float*>(a.o)[obase + mt * 32] = v;
+        else if (a.out_dtype == 0) static_cast<uint16_t*>(a.o)[obase + mt * 32] = __bfloat16_as_ushort(__float2bfloat16(v));
+        else static_cast<uint16_t*>(a.o)[obase + mt * 32] = __half_as_ushort(__float2half(v));
       }
+    }
   }
 }
 
 template <int KV, bool KTOK, bool SYM7, bool DEBUG>
 hipError_t launch_t(const AttnArgs& a, hipStream_t s) {
-  const dim3 grid(a.Npad / kBlockM, a.BH);
-  hipLaunchKernelGGL((k_attn_e2m3<KV, KTOK, SYM7, DEBUG>), grid, dim3(256), 0, s, a);
+  const dim3 grid((a.Npad + kBlockM - 1) / kBlockM, a.BH);
+  hipLaunchKernelGGL((k_attn_e2m3<KV, KTOK, SYM7, DEBUG>), grid, dim3(kThreads), 0, s, a);
   return hipGetLastError();
 }
 

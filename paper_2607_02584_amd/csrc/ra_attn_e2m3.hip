@@ -64,8 +64,8 @@ __device__ __forceinline__ v8i load_rec(const uint8_t* p) {
 // K and V code tiles of one block go global -> registers -> LDS: every thread
 // moves three 16-byte (KV = 128) or 8-byte (KV = 64) pieces of each, adjacent
 // threads adjacent pieces.  The global loads of block j + 2 are issued at the
-// end of block j and written to LDS at the start of block j + 1, so their
-// latency overlaps the end-of-block barrier.
+// end of block j and written to LDS in the middle of block j + 1 (after its
+// row maxima), so their latency overlaps the barrier and the score products.
 template <int KV>
 struct TilePiece {
   // 16-byte (KV = 128) or 8-byte (KV = 64) pieces as 32-bit vectors, six per thread
@@ -193,7 +193,6 @@ __global__ __launch_bounds__(kThreads, 8 / kWaves) void k_attn_e2m3(AttnArgs a) 
     const int buf = jb & 1;
     const int key0 = jb * KV;
     if (jb + 1 < nblocks) {
-      tp.store(sK[buf ^ 1], sV[buf ^ 1], tid);
       store_aux(jb + 1, buf ^ 1, pf);
       if (jb + 2 < nblocks) pf = fetch_aux(jb + 2);
     }
@@ -308,6 +307,9 @@ __global__ __launch_bounds__(kThreads, 8 / kWaves) void k_attn_e2m3(AttnArgs a) 
     //      overwrites the score's register, so the 32 converter
     //      inputs of a 64-key group are the two chunks' accumulators in place:
     //      element 2i + c2 of the packed operand is register i of chunk 2gg + c2. ----
+    // the next block's tiles go to LDS here, once this block's maximum is known
+    if (jb + 1 < nblocks) tp.store(sK[buf ^ 1], sV[buf ^ 1], tid);
+    __builtin_amdgcn_sched_barrier(0);
     float ls[4];   // independent partial sums, started by the first four values
 #pragma unroll
     for (int gg = 0; gg < NG; ++gg) {

@@ -8,13 +8,15 @@
 // Attention: S^T = K Q^T on v_mfma_f32_32x32x16_{bf16,f16} (fp32 accumulate),
 // blockwise online softmax over blocks of 64 keys in ascending order,
 //   m = max(m, rowmax(S * Kc)),  P = 2^(S*Kc - m),  l = alpha*l + sum P,
-// P rounded to the 16-bit type as the B operand of O^T += V^T P^T, and
-// O = O / l.  Each lane holds the scores of one query, so row reductions stay
-// inside the lane plus one exchange between the two wave halves.
+// P rounded to the 16-bit type as the A operand of O += P V, and O = O / l.
+// Each lane holds the scores of one query, so row reductions stay inside the
+// lane plus one exchange between the two wave halves.
 //
 // 16-bit tiled layouts (elements), token n = 32*c + r:
 //   Q, K: (((c*8 + ch/16)*2 + (ch/8)%2)*32 + r)*8 + ch%8
 //   V:    (((c*2 + s)*2 + h)*128 + ch)*8 + e  holds V[32c + 16s + 8(e/4) + 4h + e%4][ch]
+#include <type_traits>
+
 #include "ra_internal.h"
 
 namespace ra {
@@ -125,46 +127,90 @@ struct MF;
 template <>
 struct MF<false> {
   typedef v8bf vec;
+  typedef __bf16 v2t __attribute__((ext_vector_type(2)));
   static __device__ __forceinline__ v16f mfma(vec a, vec b, v16f c) {
     return __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, b, c, 0, 0, 0);
-  }
-  static __device__ __forceinline__ uint32_t pack2(float x, float y) {
-    return static_cast<uint32_t>(__bfloat16_as_ushort(__float2bfloat16(x))) |
-           (static_cast<uint32_t>(__bfloat16_as_ushort(__float2bfloat16(y))) << 16);
   }
 };
 template <>
 struct MF<true> {
   typedef v8h vec;
+  typedef _Float16 v2t __attribute__((ext_vector_type(2)));
   static __device__ __forceinline__ v16f mfma(vec a, vec b, v16f c) {
     return __builtin_amdgcn_mfma_f32_32x32x16_f16(a, b, c, 0, 0, 0);
   }
-  static __device__ __forceinline__ uint32_t pack2(float x, float y) {
-    return static_cast<uint32_t>(__half_as_ushort(__float2half(x))) |
-           (static_cast<uint32_t>(__half_as_ushort(__float2half(y))) << 16);
-  }
 };
+
+typedef float v2f __attribute__((ext_vector_type(2)));
+
+// two binary32 values -> one dword of two 16-bit values (round to nearest even)
+template <bool F16>
+__device__ __forceinline__ uint32_t pack2(float x, float y) {
+  const typename MF<F16>::v2t t = __builtin_convertvector(v2f{x, y}, typename MF<F16>::v2t);
+  return __builtin_bit_cast(uint32_t, t);
+}
 
 template <typename V>
 __device__ __forceinline__ V as_vec(uint4 u) {
-  V r;
-  __builtin_memcpy(&r, &u, 16);
-  return r;
+  return __builtin_bit_cast(V, u);
 }
 
+// K and V tiles of one 64-key block (16 KB each) move global -> registers ->
+// LDS; each thread carries four 16-byte pieces of each.  The loads of block
+// j + 2 are issued at the end of block j and stored in the middle of block j + 1.
+struct Tile16 {
+  typedef unsigned T __attribute__((ext_vector_type(4)));
+  T k0, k1, k2, k3, v0, v1, v2, v3;   // named pieces stay in registers
+  __device__ __forceinline__ void load(const uint16_t* kg, const uint16_t* vg, int tid) {
+    const T* K = reinterpret_cast<const T*>(kg) + tid;
+    const T* V = reinterpret_cast<const T*>(vg) + tid;
+    k0 = K[0];
+    v0 = V[0];
+    k1 = K[256];
+    v1 = V[256];
+    k2 = K[512];
+    v2 = V[512];
+    k3 = K[768];
+    v3 = V[768];
+  }
+  __device__ __forceinline__ void store(uint16_t* ks, uint16_t* vs, int tid) const {
+    T* K = reinterpret_cast<T*>(ks) + tid;
+    T* V = reinterpret_cast<T*>(vs) + tid;
+    K[0] = k0;
+    V[0] = v0;
+    K[256] = k1;
+    V[256] = v1;
+    K[512] = k2;
+    V[512] = v2;
+    K[768] = k3;
+    V[768] = v3;
+  }
+};
+
+// One wave = 32 queries; S^T = K Q^T puts the scores of one query in one lane
+// (register r of chunk ch is key 32 ch + 8 (r / 4) + 4 hh + r % 4).  The 16-bit
+// P values of register pairs are directly the A operand of O = P V (A and B
+// operands share one lane layout), with V read as the B operand in the key
+// order of its relayout, so a lane of the output tile holds one channel of 16
+// queries (query 8 (r / 4) + 4 hh + r % 4 in register r).
 template <bool F16>
 __global__ __launch_bounds__(256, 2) void k_attn16(Fp16Args a) {
   typedef typename MF<F16>::vec vec;
   constexpr int NCH = kKV / 32;
-  __shared__ __align__(16) uint16_t sK[2][kKV * kD];
-  __shared__ __align__(16) uint16_t sV[2][kKV * kD];
+  constexpr int TILE = kKV * kD;  // elements of K (and of V) per block
+  __shared__ __align__(16) uint16_t sK[2][TILE];
+  __shared__ __align__(16) uint16_t sV[2][TILE];
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int hh = lane >> 5, j = lane & 31;
   const int bh = blockIdx.y;
-  const int qrow = blockIdx.x * kBlockM + wave * 32 + j;
+  const int q0 = blockIdx.x * kBlockM + wave * 32;
+  const int qrow = q0 + j;
   const int N = a.N;
   const int nblocks = (N + kKV - 1) / kKV;
   const size_t hoff = static_cast<size_t>(bh) * a.Npad * kD;
+  const uint16_t* kbase = a.k + hoff;
+  const uint16_t* vbase = a.v + hoff;
+  const float Kc = a.Kc;
 
   vec qop[8];
   {
@@ -180,64 +226,67 @@ __global__ __launch_bounds__(256, 2) void k_attn16(Fp16Args a) {
     for (int r = 0; r < 16; ++r) of[mt][r] = 0.f;
   float m = -INFINITY, l = 0.f;
 
-  // block of 64 keys = 2 chunks = 8192 elements of K and of V: 4 x 16 B per thread each
-  uint4 stk[4], stv[4];
-  auto load = [&](int jb) {
-    const uint16_t* kb = a.k + hoff + static_cast<size_t>(jb) * kKV * kD;
-    const uint16_t* vb = a.v + hoff + static_cast<size_t>(jb) * kKV * kD;
-#pragma unroll
-    for (int i = 0; i < 4; ++i) {
-      stk[i] = *reinterpret_cast<const uint4*>(kb + (i * 256 + tid) * 8);
-      stv[i] = *reinterpret_cast<const uint4*>(vb + (i * 256 + tid) * 8);
-    }
-  };
-  auto store = [&](int buf) {
-#pragma unroll
-    for (int i = 0; i < 4; ++i) {
-      *reinterpret_cast<uint4*>(&sK[buf][(i * 256 + tid) * 8]) = stk[i];
-      *reinterpret_cast<uint4*>(&sV[buf][(i * 256 + tid) * 8]) = stv[i];
-    }
-  };
-  load(0);
-  store(0);
+  Tile16 tp;
+  tp.load(kbase, vbase, tid);
+  tp.store(sK[0], sV[0], tid);
+  tp.load(kbase + (nblocks > 1 ? TILE : 0), vbase + (nblocks > 1 ? TILE : 0), tid);
   __syncthreads();
 
-  for (int jb = 0; jb < nblocks; ++jb) {
+  auto step = [&](int jb, auto masked_tag) {
+    constexpr bool MASKED = decltype(masked_tag)::value;
     const int buf = jb & 1;
-    const bool more = jb + 1 < nblocks;
-    if (more) load(jb + 1);
     const int key0 = jb * kKV;
-    const bool last = key0 + kKV > N;
 
+    // ---- S^T = K Q^T; the chunks' products alternate so that consecutive
+    //      instructions accumulate into different registers ----
     v16f s[NCH];
-#pragma unroll
-    for (int ch = 0; ch < NCH; ++ch) {
-#pragma unroll
-      for (int r = 0; r < 16; ++r) s[ch][r] = 0.f;
-#pragma unroll
-      for (int kc = 0; kc < 8; ++kc) {
-        const vec A = as_vec<vec>(*reinterpret_cast<const uint4*>(&sK[buf][(((ch * 8 + kc) * 2 + hh) * 32 + j) * 8]));
-        s[ch] = MF<F16>::mfma(A, qop[kc], s[ch]);
-      }
-    }
-    float tmax = -INFINITY;
 #pragma unroll
     for (int ch = 0; ch < NCH; ++ch)
 #pragma unroll
-      for (int r = 0; r < 16; ++r) {
-        const int key = key0 + ch * 32 + 8 * (r >> 2) + 4 * hh + (r & 3);
-        if (!last || key < N) tmax = fmaxf(tmax, __fmul_rn(s[ch][r], a.Kc));
+      for (int r = 0; r < 16; ++r) s[ch][r] = 0.f;
+#pragma unroll
+    for (int kc = 0; kc < 8; ++kc)
+#pragma unroll
+      for (int ch = 0; ch < NCH; ++ch) {
+        const vec A = as_vec<vec>(*reinterpret_cast<const uint4*>(&sK[buf][(((ch * 8 + kc) * 2 + hh) * 32 + j) * 8]));
+        s[ch] = MF<F16>::mfma(A, qop[kc], s[ch]);
       }
+    if (MASKED) {
+#pragma unroll
+      for (int ch = 0; ch < NCH; ++ch)
+#pragma unroll
+        for (int r = 0; r < 16; ++r)
+          if (key0 + ch * 32 + 8 * (r >> 2) + 4 * hh + (r & 3) >= N) s[ch][r] = -INFINITY;
+    }
+
+    // ---- row maximum of S * Kc (Kc > 0: the product of the maximum) ----
+    float mx = fmaxf(fmaxf(s[0][0], s[0][1]), s[0][2]);
+#pragma unroll
+    for (int r = 3; r < 15; r += 2) mx = fmaxf(fmaxf(mx, s[0][r]), s[0][r + 1]);
+    mx = fmaxf(mx, s[0][15]);
+#pragma unroll
+    for (int ch = 1; ch < NCH; ++ch)
+#pragma unroll
+      for (int r = 0; r < 16; r += 2) mx = fmaxf(fmaxf(mx, s[ch][r]), s[ch][r + 1]);
+    float tmax = __fmul_rn(mx, Kc);
     tmax = fmaxf(tmax, __shfl_xor(tmax, 32));
     const float mnew = fmaxf(m, tmax);
     const float alpha = __builtin_amdgcn_exp2f(m - mnew);
     m = mnew;
+    if (__any(alpha != 1.0f)) {
 #pragma unroll
-    for (int mt = 0; mt < 4; ++mt)
+      for (int r = 0; r < 16; ++r) {
+        const float ar = __shfl(alpha, 8 * (r >> 2) + 4 * hh + (r & 3));
 #pragma unroll
-      for (int r = 0; r < 16; ++r) of[mt][r] = __fmul_rn(of[mt][r], alpha);
+        for (int mt = 0; mt < 4; ++mt) of[mt][r] = __fmul_rn(of[mt][r], ar);
+      }
+    }
+    __builtin_amdgcn_sched_barrier(0);
+    if (jb + 1 < nblocks) tp.store(sK[buf ^ 1], sV[buf ^ 1], tid);
+    __builtin_amdgcn_sched_barrier(0);
 
-    float lsum = 0.f;
+    // ---- P = 2^(S Kc - m) in 16 bits, row sums of the unrounded P, O += P V ----
+    float ls[4];
 #pragma unroll
     for (int ch = 0; ch < NCH; ++ch) {
       uint32_t pw[8];
@@ -247,52 +296,54 @@ __global__ __launch_bounds__(256, 2) void k_attn16(Fp16Args a) {
 #pragma unroll
         for (int u = 0; u < 2; ++u) {
           const int r = 2 * r2 + u;
-          const int key = key0 + ch * 32 + 8 * (r >> 2) + 4 * hh + (r & 3);
-          float p = __builtin_amdgcn_exp2f(__fmaf_rn(s[ch][r], a.Kc, -mnew));
-          if (last && key >= N) p = 0.f;
-          lsum += p;
+          float p = __builtin_amdgcn_exp2f(__fmaf_rn(s[ch][r], Kc, -mnew));
+          if (MASKED && s[ch][r] == -INFINITY) p = 0.f;
+          if (ch == 0 && r < 4) ls[r] = p;
+          else ls[r & 3] += p;
           P[u] = p;
         }
-        pw[r2] = MF<F16>::pack2(P[0], P[1]);
+        pw[r2] = pack2<F16>(P[0], P[1]);
       }
-      // step st uses accumulator registers 8*st .. 8*st+7
+      // k-step stp covers registers 8 stp .. 8 stp + 7 of the chunk
 #pragma unroll
       for (int stp = 0; stp < 2; ++stp) {
-        const vec B = as_vec<vec>(make_uint4(pw[4 * stp], pw[4 * stp + 1], pw[4 * stp + 2], pw[4 * stp + 3]));
+        const vec A = as_vec<vec>(make_uint4(pw[4 * stp], pw[4 * stp + 1], pw[4 * stp + 2], pw[4 * stp + 3]));
 #pragma unroll
         for (int mt = 0; mt < 4; ++mt) {
-          const vec A =
+          const vec B =
               as_vec<vec>(*reinterpret_cast<const uint4*>(&sV[buf][(((ch * 2 + stp) * 2 + hh) * 128 + mt * 32 + j) * 8]));
           of[mt] = MF<F16>::mfma(A, B, of[mt]);
         }
       }
+      __builtin_amdgcn_sched_barrier(0);
     }
-    l = __fmaf_rn(l, alpha, lsum);
-    if (more) store(buf ^ 1);
+    l = __fmaf_rn(l, alpha, (ls[0] + ls[1]) + (ls[2] + ls[3]));
+    {
+      const size_t nb2 = static_cast<size_t>(jb + 2 < nblocks ? jb + 2 : nblocks - 1) * TILE;
+      tp.load(kbase + nb2, vbase + nb2, tid);
+    }
     __syncthreads();
-  }
+  };
 
+  const int nfull = N / kKV;
+  for (int jb = 0; jb < nfull; ++jb) step(jb, std::integral_constant<bool, false>());
+  if (nfull < nblocks) step(nfull, std::integral_constant<bool, true>());
+
+  // ---- epilogue: O / l ----
   const float ltot = l + __shfl_xor(l, 32);
-  if (qrow < N) {
-    const float inv = 1.0f / ltot;
-    const size_t obase = (static_cast<size_t>(bh) * N + qrow) * kD;
 #pragma unroll
-    for (int mt = 0; mt < 4; ++mt)
+  for (int r = 0; r < 16; ++r) {
+    const int qi = 8 * (r >> 2) + 4 * hh + (r & 3);
+    const float inv = 1.0f / __shfl(ltot, qi);
+    if (q0 + qi < N) {
+      const size_t obase = (static_cast<size_t>(bh) * N + q0 + qi) * kD + j;
 #pragma unroll
-      for (int rq = 0; rq < 4; ++rq) {
-        const int c0 = mt * 32 + 8 * rq + 4 * hh;
-        float v[4];
-#pragma unroll
-        for (int t = 0; t < 4; ++t) v[t] = of[mt][4 * rq + t] * inv;
-        if (a.out_dtype == 2) {
-          *reinterpret_cast<float4*>(static_cast<float*>(a.o) + obase + c0) = make_float4(v[0], v[1], v[2], v[3]);
-        } else {
-          const int f16 = a.out_dtype == 1;
-          *reinterpret_cast<uint2*>(static_cast<uint16_t*>(a.o) + obase + c0) =
-              make_uint2(f2h(v[0], f16) | (static_cast<uint32_t>(f2h(v[1], f16)) << 16),
-                         f2h(v[2], f16) | (static_cast<uint32_t>(f2h(v[3], f16)) << 16));
-        }
+      for (int mt = 0; mt < 4; ++mt) {
+        const float v = of[mt][r] * inv;
+        if (a.out_dtype == 2) static_cast<float*>(a.o)[obase + mt * 32] = v;
+        else static_cast<uint16_t*>(a.o)[obase + mt * 32] = f2h(v, a.out_dtype == 1);
       }
+    }
   }
 }
 

@@ -93,7 +93,7 @@ Sizes sizes_of(const ra_params* p) {
   s.kscale = static_cast<size_t>(s.BH * (s.Npad / p->k_group));
   s.vscale = static_cast<size_t>(s.BH * s.nvgroups * kD);
   s.mu = static_cast<size_t>(s.BH * kD);
-  s.partial = static_cast<size_t>(s.BH * s.ntiles * kD);
+  s.partial = static_cast<size_t>(s.BH * kD);
   s.amax = s.vscale;
   return s;
 }
@@ -101,7 +101,8 @@ Sizes sizes_of(const ra_params* p) {
 // Workspace partition of the INT4 path.  The quantize calls use only the head
 // of it (partials, internal means, V maxima); fwd_int4 also keeps the codes.
 struct Int4Ws {
-  double* partial;
+  double* ksum;
+  double* vsum;
   float* mu_k;
   float* mu_v;
   uint32_t* amax;
@@ -124,7 +125,8 @@ Int4Ws carve_int4(const ra_params* p, void* base) {
     o += align_up(bytes);
     return r;
   };
-  w.partial = reinterpret_cast<double*>(take(s.partial * sizeof(double)));
+  w.ksum = reinterpret_cast<double*>(take(s.partial * sizeof(double)));
+  w.vsum = reinterpret_cast<double*>(take(s.partial * sizeof(double)));
   w.mu_k = reinterpret_cast<float*>(take(s.mu * sizeof(float)));
   w.mu_v = reinterpret_cast<float*>(take(s.mu * sizeof(float)));
   w.amax = reinterpret_cast<uint32_t*>(take(s.amax * sizeof(uint32_t)));
@@ -281,27 +283,29 @@ int qk_impl(const ra_params* p, const void* q, const void* k, uint8_t* qc, float
   a.Npad = static_cast<int>(z.Npad);
   a.is_fp16 = p->in_dtype == RA_FP16;
   a.e2m3 = p->code_format == RA_CODES_E2M3;
-  a.partial = w.partial;
+  a.sums = w.ksum;
   float* mu = mu_k ? mu_k : w.mu_k;
-  const float* center = nullptr;
-  if (p->smooth & RA_SMOOTH_K) {
+  const bool center = (p->smooth & RA_SMOOTH_K) != 0;
+  if (center) {
+    // exact fixed-point channel sums of the rotated K, accumulated by atomics
+    RA_CHECK_HIP(ra::launch_fill_zero_u32(reinterpret_cast<uint32_t*>(w.ksum), static_cast<int64_t>(2 * z.partial), s));
     a.x = static_cast<const uint16_t*>(k);
     RA_CHECK_HIP(ra::launch_qk_sums(t, a, static_cast<int>(z.BH), s));
-    RA_CHECK_HIP(ra::launch_mu_reduce(w.partial, mu, static_cast<int>(z.BH), static_cast<int>(z.ntiles), p->N, s));
-    center = mu;
   } else if (mu_k) {
     RA_CHECK_HIP(ra::launch_fill_zero_u32(reinterpret_cast<uint32_t*>(mu_k), static_cast<int64_t>(z.mu), s));
   }
   a.x = static_cast<const uint16_t*>(q);
   a.codes = qc;
   a.scales = qs;
-  a.mu = nullptr;
+  a.center = 0;
+  a.mu_out = nullptr;
   a.group = p->q_group;
   RA_CHECK_HIP(ra::launch_qk_quant(t, a, static_cast<int>(z.BH), s));
   a.x = static_cast<const uint16_t*>(k);
   a.codes = kc;
   a.scales = ks;
-  a.mu = center;
+  a.center = center;
+  a.mu_out = center ? mu : nullptr;
   a.group = p->k_group;
   RA_CHECK_HIP(ra::launch_qk_quant(t, a, static_cast<int>(z.BH), s));
   return RA_OK;
@@ -313,7 +317,7 @@ int v_impl(const ra_params* p, const void* v, uint8_t* vc, float* vs, float* mu_
   a.x = static_cast<const uint16_t*>(v);
   a.codes = vc;
   a.scales = vs;
-  a.partial = w.partial;
+  a.sums = w.vsum;
   a.amax = w.amax;
   a.N = p->N;
   a.Npad = static_cast<int>(z.Npad);
@@ -323,12 +327,15 @@ int v_impl(const ra_params* p, const void* v, uint8_t* vc, float* vs, float* mu_
   a.e2m3 = p->code_format == RA_CODES_E2M3;
   float* mu = mu_v ? mu_v : w.mu_v;
   if (p->smooth & RA_SMOOTH_V) {
+    RA_CHECK_HIP(ra::launch_fill_zero_u32(reinterpret_cast<uint32_t*>(w.vsum), static_cast<int64_t>(2 * z.partial), s));
+    a.center = 0;
     RA_CHECK_HIP(ra::launch_v_sums(a, static_cast<int>(z.BH), s));
-    RA_CHECK_HIP(ra::launch_mu_reduce(w.partial, mu, static_cast<int>(z.BH), static_cast<int>(z.ntiles), p->N, s));
-    a.mu = mu;
+    a.center = 1;
+    a.mu_out = mu;
   } else {
     if (mu_v) RA_CHECK_HIP(ra::launch_fill_zero_u32(reinterpret_cast<uint32_t*>(mu_v), static_cast<int64_t>(z.mu), s));
-    a.mu = nullptr;
+    a.center = 0;
+    a.mu_out = nullptr;
   }
   RA_CHECK_HIP(ra::launch_fill_zero_u32(w.amax, static_cast<int64_t>(z.amax), s));
   RA_CHECK_HIP(ra::launch_v_amax(a, static_cast<int>(z.BH), s));

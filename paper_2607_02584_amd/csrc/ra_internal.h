@@ -30,8 +30,9 @@ struct QkArgs {
   const uint16_t* x;      // [BH][N][128] bf16/fp16 bits
   uint8_t* codes;         // tiled INT4 layout, [BH][Npad*64]
   float* scales;          // [BH][Npad/group]
-  const float* mu;        // [BH][128] or nullptr (no centering)
-  double* partial;        // [BH][ntiles][128] fixed-point sums (sums pass only)
+  double* sums;           // [BH][128] fixed-point channel sums (sums pass adds, quant pass reads)
+  float* mu_out;          // [BH][128] the mean each head is centred by, or nullptr
+  int center;             // quant pass: subtract the mean derived from sums
   int N, Npad, group, is_fp16;
   int e2m3;               // 1: write the E2M3 container, 0: the INT4 nibble container
 };
@@ -40,8 +41,9 @@ struct VArgs {
   const uint16_t* x;      // [BH][N][128]
   uint8_t* codes;         // tiled V layout, [BH][Npad*64]
   float* scales;          // [BH][ngroups][128]
-  const float* mu;        // [BH][128] or nullptr
-  double* partial;        // [BH][ntiles][128]
+  double* sums;           // [BH][128] fixed-point channel sums
+  float* mu_out;          // [BH][128] or nullptr
+  int center;             // subtract the mean derived from sums
   uint32_t* amax;         // [BH][ngroups][128] float bits (non-negative)
   int N, Npad, group, ngroups, is_fp16;
   int e2m3;
@@ -79,7 +81,6 @@ struct Fp16Args {
 
 // ---- launchers (return hipError_t) ----
 hipError_t launch_qk_sums(const RopeTables& t, const QkArgs& a, int BH, hipStream_t s);
-hipError_t launch_mu_reduce(const double* partial, float* mu, int BH, int ntiles, int N, hipStream_t s);
 hipError_t launch_qk_quant(const RopeTables& t, const QkArgs& a, int BH, hipStream_t s);
 hipError_t launch_fill_zero_u32(uint32_t* p, int64_t n, hipStream_t s);
 hipError_t launch_v_sums(const VArgs& a, int BH, hipStream_t s);

@@ -9,7 +9,9 @@
 //  * Smoothing (Sec. 4): per-channel means over the tokens of a head.  Each
 //    value is scaled by 2^20, clamped to +-2^32 and rounded to an integer; the
 //    integers are summed in binary64, which is exact (every partial sum is an
-//    integer below 2^53), so the mean does not depend on the summation order.
+//    integer of magnitude at most 2^32 * N <= 2^53), so the sum does not depend
+//    on the summation order and the tiles add theirs with atomics.  The
+//    consumers derive mu = fl32(sum / (N 2^20)) themselves.
 //  * Symmetric INT4 quantization (Sec. 5.1): per group of tokens (Q, K) or per
 //    (group of tokens, channel) (V): s = amax/7, code = clamp(rint(z*7/amax)).
 //
@@ -38,11 +40,12 @@ __device__ __forceinline__ int fdiv(int n, int d, float inv_d) {
   return q;
 }
 
-// Per-thread RoPE setup for its two channel pairs p0 = 2*cl, p1 = 2*cl + 1.
+// Per-thread RoPE setup for its two channel pairs p0 = 2*cl, p1 = 2*cl + 1:
+// the axis of each pair and the table column it reads (row stride D_a / 2).
 struct PairSetup {
-  int axis[2];   // 0 = t, 1 = h, 2 = w
-  int k[2];      // pair index inside the axis segment
-  int npair[2];  // D_a / 2 (row length of the axis table)
+  int axis[2];           // 0 = t, 1 = h, 2 = w
+  const float4* tab[2];  // axis table offset by the pair's index in its segment
+  int npair[2];          // D_a / 2 (row length of the axis table)
 };
 
 __device__ __forceinline__ PairSetup pair_setup(const RopeTables& t, int cl) {
@@ -50,20 +53,31 @@ __device__ __forceinline__ PairSetup pair_setup(const RopeTables& t, int cl) {
 #pragma unroll
   for (int i = 0; i < 2; ++i) {
     const int p = 2 * cl + i;
-    int first = 0, a = 2;
-    for (int ax = 0; ax < 3; ++ax) {
-      const int np = t.split[ax] / 2;
-      if (p < first + np) {
-        a = ax;
-        break;
-      }
-      first += np;
-    }
+    const int n0 = t.split[0] / 2, n1 = t.split[1] / 2;
+    const int a = p < n0 ? 0 : (p < n0 + n1 ? 1 : 2);
+    const int first = a == 0 ? 0 : (a == 1 ? n0 : n0 + n1);
     s.axis[i] = a;
-    s.k[i] = p - first;
-    s.npair[i] = t.split[a] / 2;
+    s.npair[i] = a == 0 ? n0 : (a == 1 ? n1 : t.split[2] / 2);
+    s.tab[i] = (a == 0 ? t.axis[0] : (a == 1 ? t.axis[1] : t.axis[2])) + (p - first);
   }
   return s;
+}
+
+// Grid coordinates (t, h, w) of the tile's 128 tokens, one thread each, into
+// LDS (rows past N take the last token's).
+__device__ __forceinline__ void tile_positions(const RopeTables& t, int tile, int N, int (*pos)[4]) {
+  const int tid = threadIdx.x;
+  if (tid < kTile) {
+    const int W = t.grid[2], Hg = t.grid[1];
+    int n = tile * kTile + tid;
+    if (n >= N) n = N - 1;
+    const int tq = fdiv(n, W * Hg, 1.0f / static_cast<float>(W * Hg));
+    const int rem = n - tq * W * Hg;
+    const int hq = fdiv(rem, W, 1.0f / static_cast<float>(W));
+    pos[tid][0] = tq;
+    pos[tid][1] = hq;
+    pos[tid][2] = rem - hq * W;
+  }
 }
 
 // Half rotation: for output pair P the two RoPE channels it mixes.
@@ -92,51 +106,41 @@ __device__ __forceinline__ HalfSetup half_setup(const RopeTables& t, int cl) {
   return s;
 }
 
-// RoPE (+ merged rotation) of channels 4cl..4cl+3 of token n; x holds the inputs.
-__device__ __forceinline__ void rope4(const RopeTables& t, const PairSetup& ps, int n, float invW, float invHW,
-                                      const float x[4], float y[4]) {
-  const int W = t.grid[2], Hg = t.grid[1];
-  int tq = fdiv(n, W * Hg, invHW);
-  int rem = n - tq * W * Hg;
-  int hq = fdiv(rem, W, invW);
-  int wq = rem - hq * W;
-  const int pos[3] = {tq, hq, wq};
-#pragma unroll
-  for (int i = 0; i < 2; ++i) {
-    const float4 g = t.axis[ps.axis[i]][pos[ps.axis[i]] * ps.npair[i] + ps.k[i]];
-    const float x0 = x[2 * i], x1 = x[2 * i + 1];
-    y[2 * i] = __fmaf_rn(x1, g.z, __fmul_rn(x0, g.x));
-    y[2 * i + 1] = __fmaf_rn(x1, g.w, __fmul_rn(x0, g.y));
-  }
-}
-
-__device__ __forceinline__ void load4(const uint16_t* row, int cl, int is_fp16, float x[4]) {
-  const uint2 w = *reinterpret_cast<const uint2*>(row + 4 * cl);
-  x[0] = h2f(static_cast<uint16_t>(w.x & 0xffff), is_fp16);
-  x[1] = h2f(static_cast<uint16_t>(w.x >> 16), is_fp16);
-  x[2] = h2f(static_cast<uint16_t>(w.y & 0xffff), is_fp16);
-  x[3] = h2f(static_cast<uint16_t>(w.y >> 16), is_fp16);
-}
-
 // Computes the rotated values z of the thread's 4 channels for the 16 rows of
 // the tile.  Rows beyond N give zeros.  ybuf: [8][128] floats of LDS.
 __device__ __forceinline__ void rope_tile(const RopeTables& t, const QkArgs& a, int bh, int tile, float (*ybuf)[kD],
                                           float z[16][4]) {
+  __shared__ int pos[kTile][4];
   const int tid = threadIdx.x, rr = tid >> 5, cl = tid & 31;
   const PairSetup ps = pair_setup(t, cl);
-  const float invW = 1.0f / static_cast<float>(t.grid[2]);
-  const float invHW = 1.0f / static_cast<float>(t.grid[2] * t.grid[1]);
   const bool half = t.rotation == 2;
   HalfSetup hs;
   if (half) hs = half_setup(t, cl);
+  tile_positions(t, tile, a.N, pos);
   const uint16_t* xb = a.x + static_cast<size_t>(bh) * a.N * kD;
+  // all sixteen row loads first (rows past N re-read the last row and are zeroed)
+  uint2 raw[16];
+#pragma unroll
   for (int p = 0; p < 16; ++p) {
     const int n = tile * kTile + p * 8 + rr;
+    raw[p] = *reinterpret_cast<const uint2*>(xb + static_cast<size_t>(n < a.N ? n : a.N - 1) * kD + 4 * cl);
+  }
+  __syncthreads();
+  for (int p = 0; p < 16; ++p) {
+    const int nl = p * 8 + rr, n = tile * kTile + nl;
     float y[4] = {0.f, 0.f, 0.f, 0.f};
     if (n < a.N) {
-      float x[4];
-      load4(xb + static_cast<size_t>(n) * kD, cl, a.is_fp16, x);
-      rope4(t, ps, n, invW, invHW, x, y);
+      const float x[4] = {h2f(static_cast<uint16_t>(raw[p].x & 0xffff), a.is_fp16),
+                          h2f(static_cast<uint16_t>(raw[p].x >> 16), a.is_fp16),
+                          h2f(static_cast<uint16_t>(raw[p].y & 0xffff), a.is_fp16),
+                          h2f(static_cast<uint16_t>(raw[p].y >> 16), a.is_fp16)};
+#pragma unroll
+      for (int i = 0; i < 2; ++i) {
+        const float4 g = ps.tab[i][pos[nl][ps.axis[i]] * ps.npair[i]];
+        const float x0 = x[2 * i], x1 = x[2 * i + 1];
+        y[2 * i] = __fmaf_rn(x1, g.z, __fmul_rn(x0, g.x));
+        y[2 * i + 1] = __fmaf_rn(x1, g.w, __fmul_rn(x0, g.y));
+      }
     }
     if (half) {
       __syncthreads();
@@ -162,9 +166,9 @@ __device__ __forceinline__ double fixq(float v) {
   return static_cast<double>(__builtin_rintf(s));
 }
 
-// Reduces the per-thread fixed-point sums over the 8 row groups and writes the
-// tile's partial sums [128] (binary64 integers).
-__device__ __forceinline__ void write_partial(double acc[4], double* out) {
+// Reduces the per-thread fixed-point sums over the 8 row groups and adds the
+// tile's channel sums to the head's [128] (binary64 integers, exact in any order).
+__device__ __forceinline__ void add_sums(double acc[4], double* out) {
   __shared__ double red[8][kD];
   const int tid = threadIdx.x, rr = tid >> 5, cl = tid & 31;
 #pragma unroll
@@ -174,8 +178,15 @@ __device__ __forceinline__ void write_partial(double acc[4], double* out) {
     double s = 0.0;
 #pragma unroll
     for (int r = 0; r < 8; ++r) s += red[r][tid];
-    out[tid] = s;
+    unsafeAtomicAdd(out + tid, s);
   }
+}
+
+// mu of channels 4 cl .. 4 cl + 3 of a head from its fixed-point sums
+__device__ __forceinline__ float4 mean4(const double* sums, int N, int cl) {
+  const double den = static_cast<double>(N) * 1048576.0;
+  return make_float4(static_cast<float>(sums[4 * cl] / den), static_cast<float>(sums[4 * cl + 1] / den),
+                     static_cast<float>(sums[4 * cl + 2] / den), static_cast<float>(sums[4 * cl + 3] / den));
 }
 
 __global__ __launch_bounds__(256) void k_qk_sums(RopeTables t, QkArgs a) {
@@ -188,16 +199,7 @@ __global__ __launch_bounds__(256) void k_qk_sums(RopeTables t, QkArgs a) {
   for (int p = 0; p < 16; ++p)
 #pragma unroll
     for (int c = 0; c < 4; ++c) acc[c] += fixq(z[p][c]);
-  const int ntiles = a.Npad / kTile;
-  write_partial(acc, a.partial + (static_cast<size_t>(bh) * ntiles + tile) * kD);
-}
-
-__global__ __launch_bounds__(128) void k_mu_reduce(const double* partial, float* mu, int ntiles, int N) {
-  const int bh = blockIdx.x, ch = threadIdx.x;
-  const double* p = partial + static_cast<size_t>(bh) * ntiles * kD + ch;
-  double s = 0.0;
-  for (int i = 0; i < ntiles; ++i) s += p[static_cast<size_t>(i) * kD];
-  mu[bh * kD + ch] = static_cast<float>(s / (static_cast<double>(N) * 1048576.0));
+  add_sums(acc, a.sums + static_cast<size_t>(bh) * kD);
 }
 
 // 6-bit E2M3 float (sign bit 5, exponent bias 1, 3 mantissa bits) equal to the
@@ -225,8 +227,9 @@ __global__ __launch_bounds__(256) void k_qk_quant(RopeTables t, QkArgs a) {
   const int tid = threadIdx.x, rr = tid >> 5, cl = tid & 31;
   float z[16][4];
   rope_tile(t, a, bh, tile, ybuf, z);
-  if (a.mu) {
-    const float4 m = *reinterpret_cast<const float4*>(a.mu + bh * kD + 4 * cl);
+  if (a.center) {
+    const float4 m = mean4(a.sums + static_cast<size_t>(bh) * kD, a.N, cl);
+    if (a.mu_out && tile == 0 && rr == 0) *reinterpret_cast<float4*>(a.mu_out + bh * kD + 4 * cl) = m;
     for (int p = 0; p < 16; ++p) {
       const int n = tile * kTile + p * 8 + rr;
       if (n < a.N) {
@@ -307,13 +310,21 @@ __device__ __forceinline__ void load_v_tile(const VArgs& a, int bh, int tile, fl
   const int tid = threadIdx.x, rr = tid >> 5, cl = tid & 31;
   const uint16_t* xb = a.x + static_cast<size_t>(bh) * a.N * kD;
   float4 m = make_float4(0.f, 0.f, 0.f, 0.f);
-  if (a.mu) m = *reinterpret_cast<const float4*>(a.mu + bh * kD + 4 * cl);
+  if (a.center) m = mean4(a.sums + static_cast<size_t>(bh) * kD, a.N, cl);
+  uint2 raw[16];
+#pragma unroll
+  for (int p = 0; p < 16; ++p) {
+    const int n = tile * kTile + p * 8 + rr;
+    raw[p] = *reinterpret_cast<const uint2*>(xb + static_cast<size_t>(n < a.N ? n : a.N - 1) * kD + 4 * cl);
+  }
   for (int p = 0; p < 16; ++p) {
     const int n = tile * kTile + p * 8 + rr;
     if (n < a.N) {
-      float x[4];
-      load4(xb + static_cast<size_t>(n) * kD, cl, a.is_fp16, x);
-      if (a.mu) {
+      float x[4] = {h2f(static_cast<uint16_t>(raw[p].x & 0xffff), a.is_fp16),
+                    h2f(static_cast<uint16_t>(raw[p].x >> 16), a.is_fp16),
+                    h2f(static_cast<uint16_t>(raw[p].y & 0xffff), a.is_fp16),
+                    h2f(static_cast<uint16_t>(raw[p].y >> 16), a.is_fp16)};
+      if (a.center) {
         x[0] = __fsub_rn(x[0], m.x);
         x[1] = __fsub_rn(x[1], m.y);
         x[2] = __fsub_rn(x[2], m.z);
@@ -330,17 +341,14 @@ __device__ __forceinline__ void load_v_tile(const VArgs& a, int bh, int tile, fl
 
 __global__ __launch_bounds__(256) void k_v_sums(VArgs a) {
   const int tile = blockIdx.x, bh = blockIdx.y;
-  VArgs b = a;
-  b.mu = nullptr;
   float z[16][4];
-  load_v_tile(b, bh, tile, z);
+  load_v_tile(a, bh, tile, z);
   double acc[4] = {0.0, 0.0, 0.0, 0.0};
 #pragma unroll
   for (int p = 0; p < 16; ++p)
 #pragma unroll
     for (int c = 0; c < 4; ++c) acc[c] += fixq(z[p][c]);
-  const int ntiles = a.Npad / kTile;
-  write_partial(acc, a.partial + (static_cast<size_t>(bh) * ntiles + tile) * kD);
+  add_sums(acc, a.sums + static_cast<size_t>(bh) * kD);
 }
 
 __device__ __forceinline__ int vgroup_of(const VArgs& a, int n) {
@@ -397,6 +405,8 @@ __global__ __launch_bounds__(256) void k_v_quant(VArgs a) {
       a.scales[(static_cast<size_t>(bh) * a.ngroups + g) * kD + ch] = s;
   }
   __syncthreads();
+  if (a.center && a.mu_out && tile == 0 && rr == 0)
+    *reinterpret_cast<float4*>(a.mu_out + bh * kD + 4 * cl) = mean4(a.sums + static_cast<size_t>(bh) * kD, a.N, cl);
   float z[16][4];
   load_v_tile(a, bh, tile, z);
   if (a.e2m3) {
@@ -469,11 +479,6 @@ __global__ void k_fill_zero_u32(uint32_t* p, int64_t n) {
 
 hipError_t launch_qk_sums(const RopeTables& t, const QkArgs& a, int BH, hipStream_t s) {
   hipLaunchKernelGGL(k_qk_sums, dim3(a.Npad / kTile, BH), dim3(256), 0, s, t, a);
-  return hipGetLastError();
-}
-
-hipError_t launch_mu_reduce(const double* partial, float* mu, int BH, int ntiles, int N, hipStream_t s) {
-  hipLaunchKernelGGL(k_mu_reduce, dim3(BH), dim3(kD), 0, s, partial, mu, ntiles, N);
   return hipGetLastError();
 }
 

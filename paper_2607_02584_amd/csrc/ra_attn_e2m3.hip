@@ -33,6 +33,7 @@
 #include <type_traits>
 
 #include "ra_internal.h"
+#include "ra_xcd.h"
 
 namespace ra {
 namespace {
@@ -107,8 +108,9 @@ __global__ __launch_bounds__(kThreads, 8 / kWaves) void k_attn_e2m3(AttnArgs a) 
 
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int hh = lane >> 5, j = lane & 31;
-  const int bh = blockIdx.y;
-  const int qrow = blockIdx.x * kBlockM + wave * 32 + j;
+  int bh, qtile;
+  xcd_tile(bh, qtile);
+  const int qrow = qtile * kBlockM + wave * 32 + j;
   const int N = a.N;
   const int nblocks = (N + KV - 1) / KV;
   const int kstride = a.Npad / a.k_group;
@@ -401,7 +403,7 @@ __global__ __launch_bounds__(kThreads, 8 / kWaves) void k_attn_e2m3(AttnArgs a) 
     wsc[mt] = sW[mt * 32 + j] * k2;
     mu[mt] = muv ? muv[mt * 32 + j] : 0.f;
   }
-  const int q0 = blockIdx.x * kBlockM + wave * 32;
+  const int q0 = qtile * kBlockM + wave * 32;
 #pragma unroll
   for (int r = 0; r < 16; ++r) {
     const int qi = 8 * (r >> 2) + 4 * hh + (r & 3);

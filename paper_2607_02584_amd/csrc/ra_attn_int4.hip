@@ -24,6 +24,7 @@
 // operations per four codes (the factor 16 is folded into the scales, which is
 // exact).  Q is expanded once per wave to plain int8 codes.
 #include "ra_internal.h"
+#include "ra_xcd.h"
 
 namespace ra {
 namespace {
@@ -91,8 +92,9 @@ __global__ __launch_bounds__(256, 1) void k_attn_int4(AttnArgs a) {
 
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int hh = lane >> 5, j = lane & 31;
-  const int bh = blockIdx.y;
-  const int qrow = blockIdx.x * kBlockM + wave * 32 + j;
+  int bh, qtile;
+  xcd_tile(bh, qtile);
+  const int qrow = qtile * kBlockM + wave * 32 + j;
   const int N = a.N;
   const int nblocks = (N + KV - 1) / KV;
   const int kstride = a.Npad / a.k_group;

@@ -18,6 +18,7 @@
 #include <type_traits>
 
 #include "ra_internal.h"
+#include "ra_xcd.h"
 
 namespace ra {
 namespace {
@@ -202,8 +203,9 @@ __global__ __launch_bounds__(256, 2) void k_attn16(Fp16Args a) {
   __shared__ __align__(16) uint16_t sV[2][TILE];
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int hh = lane >> 5, j = lane & 31;
-  const int bh = blockIdx.y;
-  const int q0 = blockIdx.x * kBlockM + wave * 32;
+  int bh, qtile;
+  xcd_tile(bh, qtile);
+  const int q0 = qtile * kBlockM + wave * 32;
   const int qrow = q0 + j;
   const int N = a.N;
   const int nblocks = (N + kKV - 1) / kKV;

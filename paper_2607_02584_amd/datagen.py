@@ -131,16 +131,16 @@ def make_inputs(w: Workload, seed: int | None = None):
     return tuple(out)
 
 
-def schedule_mask(seed: int = SCHEDULE["mask_seed"]) -> np.ndarray:
+def schedule_mask(seed: int = SCHEDULE["mask_seed"], steps: int = SCHEDULE["steps"], blocks: int = SCHEDULE["blocks"],
+                  fallback_steps=SCHEDULE["fallback_steps"], mask_frac: float = SCHEDULE["mask_frac"]) -> np.ndarray:
     """bool [steps, blocks]: True where the BF16 fallback runs (first steps plus
     a seeded set of accuracy-sensitive blocks)."""
-    steps, blocks = SCHEDULE["steps"], SCHEDULE["blocks"]
     rng = np.random.default_rng(seed)
-    nmask = int(round(SCHEDULE["mask_frac"] * blocks))
+    nmask = int(round(mask_frac * blocks))
     blk = np.zeros(blocks, bool)
     blk[rng.choice(blocks, size=nmask, replace=False)] = True
     m = np.repeat(blk[None, :], steps, axis=0)
-    for s in SCHEDULE["fallback_steps"]:
+    for s in fallback_steps:
         m[s, :] = True
     return m
 

@@ -1,0 +1,134 @@
+"""GPU parity at the large video-DiT shapes, through the C ABI, in the launch
+configuration the benchmark uses.
+
+c3: 40 heads, grid 21x45x80 (N = 75600), with the merged interleaved rotation
+    and with the half rotation (Sec. 4.1.2, 4.1.3).
+c4: 24 heads, grid 33x45x80 (N = 118800), RoPE split 16/56/56, theta 256,
+    heavy-tailed inputs, half and interleaved rotation.
+
+The whole problem runs on the GPU; on two sampled heads the producer outputs
+(codes, scales, means) are compared bit for bit with the oracle, and on
+sampled query rows the S tiles and running maxima (debug entry point) bit for
+bit and O within 2e-3.  The mixed-precision dispatch (Sec. 5.1) is checked
+over a small schedule: every call equals the path the schedule selects.
+"""
+import numpy as np
+import pytest
+
+from layouts import unpack_qk, unpack_qk_e2m3, unpack_v, unpack_v_e2m3
+
+pytestmark = pytest.mark.gpu
+
+O_TOL = 2e-3
+
+
+def _torch():
+    import torch
+    if not torch.cuda.is_available():
+        pytest.skip("no GPU")
+    return torch
+
+
+def _ra():
+    from paper_2607_02584_amd import rotate_attn as ra
+    ra.lib()
+    return ra
+
+
+def _head_slice(buf, bh, per_head):
+    return buf[bh * per_head:(bh + 1) * per_head]
+
+
+@pytest.mark.parametrize("wname,rotation", [("c3", 1), ("c3", 2), ("c4", 2), ("c4", 1)])
+def test_large_shape_sampled(ora, wname, rotation):
+    torch, ra = _torch(), _ra()
+    from paper_2607_02584_amd import datagen as dg
+    w = dg.WORKLOADS[wname]
+    print(f"[large] {wname} N={w.N} H={w.H} rotation={rotation}: generating inputs", flush=True)
+    q, k, v = dg.make_inputs(w)
+    p = ra.make_params(w.B, w.H, (w.T, w.Hg, w.W), w.split, w.theta, rotation=rotation, q_group=128, k_group=128,
+                       v_group=128, kv_block=128, out_dtype=ra.FP32, code_format=ra.CODES_E2M3)
+    L = ra.layout(p)
+    Np, BH, N = L["n_pad"], w.B * w.H, w.N
+    bufs = ra.alloc_int4(p)
+    ws = ra.workspace(p, ra.PATH_INT4)
+    qd, kd, vd = (ra.to_device_bits(x) for x in (q, k, v))
+    del q, k, v
+    ra.quantize_qk(p, qd, kd, bufs["q_codes"], bufs["q_scale"], bufs["k_codes"], bufs["k_scale"], bufs["mu_k"], ws)
+    ra.quantize_v(p, vd, bufs["v_codes"], bufs["v_scale"], bufs["mu_v"], ws)
+    o = torch.empty((BH, N, 128), dtype=torch.float32, device="cuda")
+    ra.attn_int4(p, bufs["q_codes"], bufs["q_scale"], bufs["k_codes"], bufs["k_scale"], bufs["v_codes"],
+                 bufs["v_scale"], bufs["mu_v"], o)
+    torch.cuda.synchronize()
+    print("[large] GPU done", flush=True)
+    geo = ora.Geometry(w.T, w.Hg, w.W, w.split, w.theta)
+    cfg = ora.Int4Config(rotation=rotation, q_group=128, k_group=128, v_group=128, kv_block=128)
+    nb = -(-N // 128)
+    nvg = -(-N // 128)
+    rng = np.random.default_rng(31 + rotation)
+    for bh in (0, int(rng.integers(1, BH))):
+        qh, kh, vh = (x.reshape(BH, N, 128)[bh].cpu().numpy().view(np.uint16) for x in (qd, kd, vd))
+        ref = ora.quantize_qk_head(geo, cfg, qh, kh)
+        refv = ora.quantize_v_head(cfg, vh)
+        qc = unpack_qk_e2m3(_head_slice(bufs["q_codes"], bh, Np * 96).cpu().numpy(), 1, Np, N)[0]
+        kc = unpack_qk_e2m3(_head_slice(bufs["k_codes"], bh, Np * 96).cpu().numpy(), 1, Np, N)[0]
+        vc = unpack_v_e2m3(_head_slice(bufs["v_codes"], bh, Np * 96).cpu().numpy(), 1, Np, N)[0]
+        assert np.array_equal(qc, ref["q_codes"]) and np.array_equal(kc, ref["k_codes"])
+        assert np.array_equal(vc, refv["v_codes"])
+        qs = bufs["q_scale"].reshape(BH, -1)[bh].cpu().numpy()[:len(ref["q_scale"])]
+        ks = bufs["k_scale"].reshape(BH, -1)[bh].cpu().numpy()[:len(ref["k_scale"])]
+        vs = bufs["v_scale"].reshape(BH, nvg, 128)[bh].cpu().numpy()
+        assert np.array_equal(qs.view(np.uint32), ref["q_scale"].view(np.uint32))
+        assert np.array_equal(ks.view(np.uint32), ref["k_scale"].view(np.uint32))
+        assert np.array_equal(vs.view(np.uint32), refv["v_scale"].view(np.uint32))
+        assert np.array_equal(bufs["mu_k"].reshape(BH, 128)[bh].cpu().numpy().view(np.uint32),
+                              ref["mu_k"].view(np.uint32))
+        assert np.array_equal(bufs["mu_v"].reshape(BH, 128)[bh].cpu().numpy().view(np.uint32),
+                              refv["mu_v"].view(np.uint32))
+        for r0 in (0, int(rng.integers(1, N // 128 - 1)) * 128 + 17, N - 33):
+            nr = 33
+            s_d = torch.zeros((nr, N), dtype=torch.int32, device="cuda")
+            m_d = torch.zeros((nr, nb), dtype=torch.float32, device="cuda")
+            od = torch.empty_like(o)
+            ra.attn_int4_debug(p, bufs["q_codes"], bufs["q_scale"], bufs["k_codes"], bufs["k_scale"],
+                               bufs["v_codes"], bufs["v_scale"], bufs["mu_v"], od, bh, r0, nr, s_d, None, m_d)
+            torch.cuda.synchronize()
+            res = ora.attn_int4(ref["q_codes"], ref["q_scale"], ref["k_codes"], ref["k_scale"], refv["v_codes"],
+                                refv["v_scale"], refv["mu_v"], q_group=128, k_group=128, v_group=128,
+                                kv_block=128, rows=(r0, nr), dumps=True)
+            O_ref, d = res
+            assert np.array_equal(s_d.cpu().numpy(), d["S"])
+            assert np.all(m_d.cpu().numpy() == d["m"])
+            err = np.abs(o[bh, r0:r0 + nr].cpu().numpy() - O_ref).max() / np.abs(O_ref).max()
+            print(f"  bh={bh} rows {r0}+{nr}: O rel err {err:.3e}", flush=True)
+            assert err <= O_TOL
+    assert torch.isfinite(o).all()
+
+
+def test_mixed_dispatch_schedule():
+    """Sec. 5.1 schedule in miniature: fallback for the first steps and a
+    seeded set of blocks, INT4 elsewhere; each call of rotate_attn_fwd equals
+    the path it selects, run directly."""
+    torch, ra = _torch(), _ra()
+    from paper_2607_02584_amd import datagen as dg
+    w = dg.WORKLOADS["c1"]
+    q, k, v = dg.make_inputs(w)
+    qd, kd, vd = (ra.to_device_bits(x) for x in (q, k, v))
+    p = ra.make_params(w.B, w.H, (w.T, w.Hg, w.W), w.split, w.theta, out_dtype=ra.FP32)
+    pf = ra.make_params(w.B, w.H, (w.T, w.Hg, w.W), w.split, w.theta, rotation=ra.ROT_NONE, out_dtype=ra.FP32)
+    mask = dg.schedule_mask(steps=3, blocks=6, fallback_steps=(0,), mask_frac=0.25, seed=5)
+    ws_i, ws_f = ra.workspace(p, ra.PATH_INT4), ra.workspace(pf, ra.PATH_FP16)
+    ref_i = torch.empty((w.H, w.N, 128), dtype=torch.float32, device="cuda")
+    ref_f = torch.empty_like(ref_i)
+    ra.fwd_int4(p, qd, kd, vd, ref_i, ws_i)
+    ra.fwd_fp16(pf, qd, kd, vd, ref_f, ws_f)
+    n_fb = 0
+    for step in range(mask.shape[0]):
+        for blk in range(mask.shape[1]):
+            fb = bool(mask[step, blk])
+            o = torch.empty_like(ref_i)
+            ra.fwd(pf if fb else p, fb, qd, kd, vd, o, ws_f if fb else ws_i)
+            torch.cuda.synchronize()
+            assert torch.equal(o, ref_f if fb else ref_i)
+            n_fb += fb
+    assert 0 < n_fb < mask.size

@@ -13,12 +13,18 @@
 // accumulates in binary32: PV accumulates straight into the output tile.
 //
 // Per block of KV keys (ascending):
-//   m_new = max(m, rowmax fl(S * c)),  x = fma(S, c, -m_new),  P = 2^x,
-//   u = rint(fl(15 P)),  l = alpha l + sum P,  alpha = 2^(m - m_new),
+//   m_new = max(m, rowmax fl(S * c)),  P = 2^(S c - m_new),
+//   u = rint(15 P),  l = alpha l + sum P,  alpha = 2^(m - m_new),
 //   O' = O' * alpha * (w_old / w_new) + (u/8) V~   (w = V scale of the block's group)
-// and finally O = O' * 8 w / 15 / l + mu_v.  The rounding u = rint(fl(15 P)) is
-// done by the packing conversion itself: it converts fl(15 P) / 8 to E2M3 with
-// round-to-nearest-even, and on the uniform 1/8 grid that is rint to an integer.
+// and finally O = O' * 8 w / 15 / l + mu_v.  The factor 15 rides in the
+// exponent: 15 P = 2^fma(S, c, -(m_new - log2 15)), one exponential per score
+// and no multiply (the binary32 roundings of log2 15 and of m_new - log2 15
+// perturb 15 P by a relative ln 2 * 2^-24 (|m_new| + 6) at most); l is kept as
+// the sum of 15 P.  The
+// rounding u = rint(15 P) is done by the packing conversion itself: it
+// converts 15 P / 8 to E2M3 with round-to-nearest-even, and on the uniform 1/8
+// grid that is rint to an integer.  Rows rescale O' by alpha only in the
+// registers of queries whose maximum moved.
 //
 // Matrix-core mapping (one wave = 32 queries): S^T = K Q^T (A = 32 keys x 64
 // channels of K, B = Q^T), so a lane holds 16 scores of one query per 32-key
@@ -114,7 +120,8 @@ __global__ __launch_bounds__(kThreads, 8 / kWaves) void k_attn_e2m3(AttnArgs a) 
   const int N = a.N;
   const int nblocks = (N + KV - 1) / KV;
   const int kstride = a.Npad / a.k_group;
-  const float pscale = SYM7 ? 7.0f : 15.0f;
+  // log2 of the P scale (15 for the range-optimized mapping, 7 for SYM7)
+  constexpr float kLog2P = SYM7 ? 2.80735492205760410f : 3.90689059560851852f;
   const size_t hcode = static_cast<size_t>(bh) * a.Npad * 96;
   const uint8_t* kbase = a.kc + hcode;
   const uint8_t* vbase = a.vc + hcode;
@@ -143,12 +150,15 @@ __global__ __launch_bounds__(kThreads, 8 / kWaves) void k_attn_e2m3(AttnArgs a) 
   struct Aux {
     float v, k;
   };
+  // fetch_aux runs for blocks 0, 1, 2, ... in order; (fg, fr) = (V group, block
+  // within the group) of the next block it fetches
+  int fg = 0, fr = 0;
   auto fetch_aux = [&](int jb) {
     Aux f{0.f, 0.f};
-    if (tid < kD) {
-      int g = (jb * KV) / a.v_group;
-      if (g >= a.nvgroups) g = a.nvgroups - 1;
-      f.v = a.vs[(static_cast<size_t>(bh) * a.nvgroups + g) * kD + tid];
+    if (tid < kD) f.v = a.vs[(static_cast<size_t>(bh) * a.nvgroups + fg) * kD + tid];
+    if (++fr == a.v_bpg) {
+      fr = 0;
+      ++fg;
     }
     const int kt = tid - kD;
     if (kt >= 0 && kt < (KTOK ? KV : NCH)) f.k = KTOK ? ksh[jb * KV + kt] : ksh[(jb * KV + kt * 32) / a.k_group];
@@ -176,7 +186,10 @@ __global__ __launch_bounds__(kThreads, 8 / kWaves) void k_attn_e2m3(AttnArgs a) 
   for (int mt = 0; mt < 4; ++mt)
 #pragma unroll
     for (int r = 0; r < 16; ++r) of[mt][r] = 0.f;
+  // running max m (on the score scale of the method) and row sum l of
+  // pscale * P; vr = block index within its V group
   float m = -INFINITY, l = 0.f;
+  int vr = 0;
 
   static_assert(KB == 3 * kThreads * static_cast<int>(sizeof(typename TilePiece<KV>::T)), "three pieces per thread");
   TilePiece<KV> tp;
@@ -240,7 +253,8 @@ __global__ __launch_bounds__(kThreads, 8 / kWaves) void k_attn_e2m3(AttnArgs a) 
     //      a fully masked chunk gives -inf, or NaN when c == 0, which fmax ignores) ----
     float cch[NCH];
     float tmax = -INFINITY;
-    const bool vchange = jb > 0 && a.nvgroups > 1 && ((jb * KV) % a.v_group) == 0;
+    const bool vchange = vr == 0 && jb > 0;   // first block of a new V group
+    if (++vr == a.v_bpg) vr = 0;
     float4 rr = make_float4(1.f, 1.f, 1.f, 1.f);
     if (vchange) rr = *reinterpret_cast<const float4*>(&sR[buf][4 * j]);
     if (!KTOK && a.k_group >= KV) {
@@ -283,6 +297,9 @@ __global__ __launch_bounds__(kThreads, 8 / kWaves) void k_attn_e2m3(AttnArgs a) 
     const float mnew = fmaxf(m, tmax);
     const float alpha = __builtin_amdgcn_exp2f(m - mnew);
     m = mnew;
+    // pscale * 2^x = 2^(S c - (m - log2 pscale)): the P scale rides in the
+    // exponent, so the exponential yields the packing input directly
+    const float mq = __fsub_rn(mnew, kLog2P);
 
     // ---- rescale O' for the block's V scale and the new maximum; register r of
     //      tile mt is channel 32 mt + j of query 8 (r / 4) + 4 hh + r % 4 ----
@@ -295,12 +312,18 @@ __global__ __launch_bounds__(kThreads, 8 / kWaves) void k_attn_e2m3(AttnArgs a) 
         of[3][r] = __fmul_rn(of[3][r], rr.w);
       }
     }
-    if (__any(alpha != 1.0f)) {
+    // only the registers whose two queries (8 (r / 4) + r % 4 in the lower
+    // wave half, 4 more in the upper) moved their maximum are rescaled
+    const unsigned long long moved = __ballot(alpha != 1.0f);
+    if (moved) {
 #pragma unroll
       for (int r = 0; r < 16; ++r) {
-        const float ar = __shfl(alpha, 8 * (r >> 2) + 4 * hh + (r & 3));
+        const int q0 = 8 * (r >> 2) + (r & 3);
+        if ((moved >> q0) & 0x11ull) {
+          const float ar = __shfl(alpha, q0 + 4 * hh);
 #pragma unroll
-        for (int mt = 0; mt < 4; ++mt) of[mt][r] = __fmul_rn(of[mt][r], ar);
+          for (int mt = 0; mt < 4; ++mt) of[mt][r] = __fmul_rn(of[mt][r], ar);
+        }
       }
     }
     __builtin_amdgcn_sched_barrier(0);
@@ -335,14 +358,14 @@ __global__ __launch_bounds__(kThreads, 8 / kWaves) void k_attn_e2m3(AttnArgs a) 
           float c;
           if (KTOK) c = __fmul_rn(cq, sKs[buf][ch * 32 + 8 * (r >> 2) + 4 * hh + (r & 3)]);
           else c = cch[ch];
-          float P = __builtin_amdgcn_exp2f(__fmaf_rn(s[ch][r], c, -mnew));
+          float P = __builtin_amdgcn_exp2f(__fmaf_rn(s[ch][r], c, -mq));   // pscale * P
           if (MASKED && s[ch][r] == -INFINITY) P = 0.f;
           if (gg == 0 && c2 == 0 && r < 4) ls[r] = P;
           else ls[r & 3] += P;
-          s[ch][r] = __fmul_rn(P, pscale);
+          s[ch][r] = P;
         }
       }
-      // E2M3(rint(fl(15 P)) / 8): the conversion divides by the power-of-two
+      // E2M3(rint(15 P) / 8): the conversion divides by the power-of-two
       // scale exactly and rounds to nearest even on the uniform 1/8 grid
       const v6i pk6 = __builtin_amdgcn_cvt_scalef32_2xpk16_fp6_f32(s[2 * gg], s[2 * gg + 1], 8.0f);
       const v8i B = v8i{pk6[0], pk6[1], pk6[2], pk6[3], pk6[4], pk6[5], 0, 0};   // A operand of O = P V~
@@ -371,6 +394,14 @@ __global__ __launch_bounds__(kThreads, 8 / kWaves) void k_attn_e2m3(AttnArgs a) 
         of[2] = mfma6(B, v2, of[2]);
         of[3] = mfma6(B, v3, of[3]);
       }
+      // The packing conversion reads its 32 source registers while later
+      // instructions already issue, and the compiler does not hold back
+      // writes to those registers: an overwrite right behind it corrupts P
+      // codes.  Keeping the sources live until after the four products puts
+      // a safe distance between the conversion and any reuse.
+#if defined(__HIP_DEVICE_COMPILE__)
+      asm volatile("" ::"v"(s[2 * gg]), "v"(s[2 * gg + 1]));
+#endif
       __builtin_amdgcn_sched_barrier(0);
     }
     l = __fmaf_rn(l, alpha, (ls[0] + ls[1]) + (ls[2] + ls[3]));
@@ -394,8 +425,8 @@ __global__ __launch_bounds__(kThreads, 8 / kWaves) void k_attn_e2m3(AttnArgs a) 
 
   // ---- epilogue: O = O' * 8 w / 15 / l + mu_v; lane (j, hh) holds channel
   //      32 mt + j of the wave's queries 8 (r / 4) + 4 hh + r % 4 ----
-  const float ltot = l + __shfl_xor(l, 32);
-  const float k2 = 8.0f / pscale;
+  const float ltot = l + __shfl_xor(l, 32);   // pscale * sum of P
+  const float k2 = 8.0f;
   const float* muv = a.mu_v ? a.mu_v + bh * kD : nullptr;
   float wsc[4], mu[4];
 #pragma unroll

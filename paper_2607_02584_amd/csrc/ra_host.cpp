@@ -363,6 +363,8 @@ int attn_impl(const ra_params* p, const uint8_t* qc, const float* qs, const uint
   a.k_group = p->k_group;
   a.v_group = p->v_group;
   a.nvgroups = static_cast<int>(z.nvgroups);
+  // v_group is a multiple of kv_block, or >= N (one group)
+  a.v_bpg = z.nvgroups > 1 ? p->v_group / p->kv_block : INT32_MAX;
   a.Kc = kc_of(p);
   a.out_dtype = p->out_dtype;
   a.dbg_s = s_out;

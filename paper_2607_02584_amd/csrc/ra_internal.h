@@ -60,6 +60,7 @@ struct AttnArgs {
   void* o;
   int N, Npad, BH;
   int q_group, k_group, v_group, nvgroups;
+  int v_bpg;              // KV blocks per V scale group (v_group / kv_block; nvgroups == 1: any value >= nblocks)
   float Kc;               // fl32(sm_scale * log2(e))
   int out_dtype;
   // debug dump (debug kernel only)

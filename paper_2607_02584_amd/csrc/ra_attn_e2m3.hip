@@ -71,8 +71,8 @@ __device__ __forceinline__ v8i load_rec(const uint8_t* p) {
 // K and V code tiles of one block go global -> registers -> LDS: every thread
 // moves three 16-byte (KV = 128) or 8-byte (KV = 64) pieces of each, adjacent
 // threads adjacent pieces.  The global loads of block j + 2 are issued at the
-// end of block j and written to LDS in the middle of block j + 1 (after its
-// row maxima), so their latency overlaps the barrier and the score products.
+// end of block j and written to LDS at the end of block j + 1 (before its
+// barrier), so their latency overlaps a whole block.
 template <int KV>
 struct TilePiece {
   // 16-byte (KV = 128) or 8-byte (KV = 64) pieces as 32-bit vectors, six per thread
@@ -332,8 +332,6 @@ __global__ __launch_bounds__(kThreads, 8 / kWaves) void k_attn_e2m3(AttnArgs a) 
     //      overwrites the score's register, so the 32 converter
     //      inputs of a 64-key group are the two chunks' accumulators in place:
     //      element 2i + c2 of the packed operand is register i of chunk 2gg + c2. ----
-    // the next block's tiles go to LDS here, once this block's maximum is known
-    if (jb + 1 < nblocks) tp.store(sK[buf ^ 1], sV[buf ^ 1], tid);
     __builtin_amdgcn_sched_barrier(0);
     float ls[4];   // independent partial sums, started by the first four values
 #pragma unroll
@@ -404,6 +402,8 @@ __global__ __launch_bounds__(kThreads, 8 / kWaves) void k_attn_e2m3(AttnArgs a) 
 #endif
       __builtin_amdgcn_sched_barrier(0);
     }
+    if (jb + 1 < nblocks) tp.store(sK[buf ^ 1], sV[buf ^ 1], tid);
+    __builtin_amdgcn_sched_barrier(0);
     l = __fmaf_rn(l, alpha, (ls[0] + ls[1]) + (ls[2] + ls[3]));
     if (DEBUG && a.dbg_m && hh == 0 && bh == a.dbg_bh && qrow >= a.dbg_row0 && qrow < a.dbg_row0 + a.dbg_rows)
       a.dbg_m[static_cast<size_t>(qrow - a.dbg_row0) * nblocks + jb] = mnew;

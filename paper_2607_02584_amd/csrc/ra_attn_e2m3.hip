@@ -59,6 +59,36 @@ __device__ __forceinline__ v16f mfma6(v8i a, v8i b, v16f c) {
   return __builtin_amdgcn_mfma_scale_f32_32x32x64_f8f6f4(a, b, c, 2, 2, 0, kScaleOne, 0, kScaleOne);
 }
 
+// 32 binary32 values -> 32 E2M3 codes (value / 8, round to nearest even), the
+// two sources interleaved: element 2 i + c of the result is register i of
+// source c.  Written out instead of left to the builtin because of two
+// properties of v_cvt_scalef32_2xpk16_fp6_f32 on gfx950, both measured on the
+// device with fixed-register probes: (1) it writes its destination before it
+// has read all 32 source registers, so a destination that overlaps the end of
+// a source corrupts the last codes -- and the compiler does allocate such
+// overlaps (the result register written over registers 14 and 15 of the
+// second source gave wrong P codes in whole rows) -- hence the early-clobber
+// output; (2) it reads the first register of each source one cycle too early
+// for a v_exp_f32 result written by the instruction right before it, hence
+// the leading wait state.  The trailing wait states cover the matrix-core
+// read of the result, which the compiler cannot see through the asm.
+__device__ __forceinline__ v6i pack_fp6(v16f lo, v16f hi) {
+  v6i r;
+#if defined(__HIP_DEVICE_COMPILE__)
+  asm volatile(
+      "s_nop 0\n\t"
+      "v_cvt_scalef32_2xpk16_fp6_f32 %0, %1, %2, %3\n\t"
+      "s_nop 1"
+      : "=&v"(r)
+      : "v"(lo), "v"(hi), "s"(8.0f));
+#else
+  (void)lo;
+  (void)hi;
+  r = v6i{0, 0, 0, 0, 0, 0};
+#endif
+  return r;
+}
+
 // 24-byte record -> operand registers (6 used dwords)
 __device__ __forceinline__ v8i load_rec(const uint8_t* p) {
   const uint2 a = *reinterpret_cast<const uint2*>(p);
@@ -71,8 +101,9 @@ __device__ __forceinline__ v8i load_rec(const uint8_t* p) {
 // K and V code tiles of one block go global -> registers -> LDS: every thread
 // moves three 16-byte (KV = 128) or 8-byte (KV = 64) pieces of each, adjacent
 // threads adjacent pieces.  The global loads of block j + 2 are issued at the
-// end of block j and written to LDS at the end of block j + 1 (before its
-// barrier), so their latency overlaps a whole block.
+// end of block j and written to LDS in the middle of block j + 1 (after its
+// row maxima), so their latency overlaps the barrier and the score products
+// (and the pieces are dead again while the probabilities take the registers).
 template <int KV>
 struct TilePiece {
   // 16-byte (KV = 128) or 8-byte (KV = 64) pieces as 32-bit vectors, six per thread
@@ -332,6 +363,8 @@ __global__ __launch_bounds__(kThreads, 8 / kWaves) void k_attn_e2m3(AttnArgs a) 
     //      overwrites the score's register, so the 32 converter
     //      inputs of a 64-key group are the two chunks' accumulators in place:
     //      element 2i + c2 of the packed operand is register i of chunk 2gg + c2. ----
+    // the next block's tiles go to LDS here, once this block's maximum is known
+    if (jb + 1 < nblocks) tp.store(sK[buf ^ 1], sV[buf ^ 1], tid);
     __builtin_amdgcn_sched_barrier(0);
     float ls[4];   // independent partial sums, started by the first four values
 #pragma unroll
@@ -365,7 +398,7 @@ __global__ __launch_bounds__(kThreads, 8 / kWaves) void k_attn_e2m3(AttnArgs a) 
       }
       // E2M3(rint(15 P) / 8): the conversion divides by the power-of-two
       // scale exactly and rounds to nearest even on the uniform 1/8 grid
-      const v6i pk6 = __builtin_amdgcn_cvt_scalef32_2xpk16_fp6_f32(s[2 * gg], s[2 * gg + 1], 8.0f);
+      const v6i pk6 = pack_fp6(s[2 * gg], s[2 * gg + 1]);
       const v8i B = v8i{pk6[0], pk6[1], pk6[2], pk6[3], pk6[4], pk6[5], 0, 0};   // A operand of O = P V~
       if (DEBUG) {
         if (bh == a.dbg_bh && qrow >= a.dbg_row0 && qrow < a.dbg_row0 + a.dbg_rows && a.dbg_u) {
@@ -392,18 +425,8 @@ __global__ __launch_bounds__(kThreads, 8 / kWaves) void k_attn_e2m3(AttnArgs a) 
         of[2] = mfma6(B, v2, of[2]);
         of[3] = mfma6(B, v3, of[3]);
       }
-      // The packing conversion reads its 32 source registers while later
-      // instructions already issue, and the compiler does not hold back
-      // writes to those registers: an overwrite right behind it corrupts P
-      // codes.  Keeping the sources live until after the four products puts
-      // a safe distance between the conversion and any reuse.
-#if defined(__HIP_DEVICE_COMPILE__)
-      asm volatile("" ::"v"(s[2 * gg]), "v"(s[2 * gg + 1]));
-#endif
       __builtin_amdgcn_sched_barrier(0);
     }
-    if (jb + 1 < nblocks) tp.store(sK[buf ^ 1], sV[buf ^ 1], tid);
-    __builtin_amdgcn_sched_barrier(0);
     l = __fmaf_rn(l, alpha, (ls[0] + ls[1]) + (ls[2] + ls[3]));
     if (DEBUG && a.dbg_m && hh == 0 && bh == a.dbg_bh && qrow >= a.dbg_row0 && qrow < a.dbg_row0 + a.dbg_rows)
       a.dbg_m[static_cast<size_t>(qrow - a.dbg_row0) * nblocks + jb] = mnew;

@@ -59,14 +59,17 @@ def source_digest(path):
         return hashlib.sha256(f.read()).hexdigest()[:16]
 
 
-def measured_traffic(container):
+def measured_traffic(container, wname):
     """HBM bytes per launch of the attention kernel from the committed counter
-    summary, or None when it is missing or the kernel source changed since."""
+    summary, or None when it is missing, covers another workload, or the
+    kernel source changed since."""
     if container != "e2m3" or not os.path.exists(TRAFFIC_FILE):
         return None
     with open(TRAFFIC_FILE) as f:
         t = json.load(f)
     if t.get("kernel_source_sha256_16") != source_digest(KERNEL_SRC):
+        return None
+    if t.get("workload", "").split(":")[0] != wname:
         return None
     return t.get("hbm_bytes_per_launch")
 
@@ -211,7 +214,7 @@ def main():
         cpu = cpu_baseline(w, q, k, v, args.cpu_seconds)
 
     line = {
-        "metric": "effective attention TOPS (4*B*H*N^2*d / time), INT4 RotateAttention forward, 32760-token DiT shape",
+        "metric": f"effective attention TOPS (4*B*H*N^2*d / time), INT4 RotateAttention forward, {N}-token DiT shape",
         "value": round(tops, 2),
         "unit": "TOPS",
         "n_gpus": 1,
@@ -234,7 +237,7 @@ def main():
                      "peak": FP6_PEAK_TOPS if args.container == "e2m3" else INT8_PEAK_TOPS, "unit": "TOPS",
                      "frac": round(attn_tops / (FP6_PEAK_TOPS if args.container == "e2m3" else INT8_PEAK_TOPS), 4),
                      "frac_of_int8_peak": round(attn_tops / INT8_PEAK_TOPS, 4),
-                     "traffic": measured_traffic(args.container)},
+                     "traffic": measured_traffic(args.container, w.name)},
         "cpu_baseline": cpu,
     }
     line.update(extra)

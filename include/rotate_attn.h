@@ -83,6 +83,8 @@ extern "C" {
 #define RA_ROT_NONE 0
 #define RA_ROT_INTERLEAVED 1 /* Sec. 4.1.2: blocks on (2i, 2i+1), merged into the RoPE table */
 #define RA_ROT_HALF 2        /* Sec. 4.1.3: pairs (i, i + D_j/2) inside each RoPE segment */
+#define RA_ROT_HADAMARD 3    /* "Full" rotation (Sec. 5.3 baseline): RoPE, then the orthonormal
+                                128x128 Sylvester-Hadamard matrix of Sec. 4.3; rot_blocks unused */
 
 /* quantization of P (Sec. 4.2.1) */
 #define RA_PQ_RANGE15 0 /* affine: fixed scale 15, zero-point -8, 16 levels */

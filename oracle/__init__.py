@@ -6,7 +6,8 @@ with gcc) through ctypes and composes the per-head routines into the whole
 forward pass of the paper's method:
 
 * Sec. 3 / Sec. 4.1.2 / Sec. 4.1.3: 3D RoPE followed by the interleaved
-  (merged) or half rotation of Q and K,
+  (merged) or half rotation of Q and K, or by the full D x D Hadamard
+  rotation (the "Full" baseline of Sec. 5.3, matrix of Sec. 4.3),
 * Sec. 4: smoothing (K and V means),
 * Sec. 5.1: per-token / per-block INT4 quantization of Q and K, per-group V,
 * Sec. 4.2: blockwise online softmax with the Range-optimized P quantizer.
@@ -26,7 +27,7 @@ _HERE = os.path.dirname(os.path.abspath(__file__))
 _SRC = os.path.join(_HERE, "ra_oracle.c")
 _LIB = os.path.join(_HERE, "libra_oracle.so")
 
-ROT_NONE, ROT_INTERLEAVED, ROT_HALF = 0, 1, 2
+ROT_NONE, ROT_INTERLEAVED, ROT_HALF, ROT_HADAMARD = 0, 1, 2, 3
 PQ_RANGE15, PQ_SYM7, PQ_NONE = 0, 1, 2
 
 
@@ -65,6 +66,8 @@ def lib():
         L.ora_rope_block.argtypes = [ctypes.POINTER(_RopeCfg), ctypes.c_int, ctypes.c_int, P]
         L.ora_rope_rot_f32.argtypes = [ctypes.POINTER(_RopeCfg), P, P]
         L.ora_rope_rot_f64.argtypes = [ctypes.POINTER(_RopeCfg), P, P]
+        L.ora_hadamard_f32.argtypes = [P, ctypes.c_int]
+        L.ora_hadamard_f64.argtypes = [P, ctypes.c_int]
         L.ora_mean_fixed.argtypes = [P, ctypes.c_int, ctypes.c_int, P]
         L.ora_center.argtypes = [P, P, ctypes.c_int, ctypes.c_int, P]
         L.ora_quant_tokens.argtypes = [P, ctypes.c_int, ctypes.c_int, ctypes.c_int, P, P]
@@ -145,6 +148,24 @@ def rope_rot_f64(geo: Geometry, x_bf16: np.ndarray, rotation: int, rot=None) -> 
     y = np.empty((geo.N, geo.D), np.float64)
     lib().ora_rope_rot_f64(ctypes.byref(c), _p(x), _p(y))
     return y
+
+
+def hadamard_f32(y: np.ndarray) -> np.ndarray:
+    """Rows of y (binary32) times the orthonormal Sylvester-Hadamard matrix,
+    the binary32 butterfly sequence of ``ora_hadamard_f32``."""
+    out = np.array(y, dtype=np.float32, order="C", copy=True)
+    D = out.shape[-1]
+    for row in out.reshape(-1, D):
+        lib().ora_hadamard_f32(_p(row), D)
+    return out
+
+
+def hadamard_f64(y: np.ndarray) -> np.ndarray:
+    out = np.array(y, dtype=np.float64, order="C", copy=True)
+    D = out.shape[-1]
+    for row in out.reshape(-1, D):
+        lib().ora_hadamard_f64(_p(row), D)
+    return out
 
 
 def mean_fixed(y: np.ndarray) -> np.ndarray:

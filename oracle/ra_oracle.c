@@ -14,6 +14,8 @@
  *   Sec. 4.1   block-diagonal orthogonal rotation R, blocks initialised to H_2.
  *   Sec. 4.1.2 interleaved rotation merged into RoPE: RoPE(Q) R = Q (M R).
  *   Sec. 4.1.3 half rotation Q Pi R, pairing d_i with d_{i + D_j/2} per segment.
+ *   Sec. 4.3   D x D Sylvester-Hadamard matrix (Kronecker recursion), used here
+ *              as the "Full" Q/K rotation baseline of Sec. 5.3.
  *   Sec. 4.2   FlashAttention blockwise online softmax and the affine
  *              (Range-optimized) P mapping with fixed scale 15 and zero-point -8.
  *   Sec. 5.1   per-token Q/K quantization and per-group V quantization.
@@ -112,6 +114,44 @@ void ora_rope_block(const ora_rope_cfg* c, int n, int p, double G[4]) {
   }
 }
 
+/* The orthonormal Sylvester-Hadamard transform of one row (Sec. 4.3:
+ * H_{2^n} = H_2 (x) H_{2^(n-1)}, with H_2 = [[1, 1], [1, -1]] / sqrt 2 of Sec. 4.1).
+ * For a row vector x = [a b] split into halves, x (H_2 (x) H') = [(a + b) H',
+ * (a - b) H'] / sqrt 2, so each level forms sums and differences of the two
+ * halves and recurses into both; the 1/sqrt 2 of every level is collected into
+ * one factor D^-1/2 applied at the end. */
+static void hadamard_levels_f32(float* y, int D) {
+  for (int len = D; len >= 2; len /= 2) {
+    int h = len / 2;
+    for (int base = 0; base < D; base += len)
+      for (int i = 0; i < h; ++i) {
+        float a = y[base + i], b = y[base + i + h];
+        y[base + i] = a + b;
+        y[base + i + h] = a - b;
+      }
+  }
+}
+
+void ora_hadamard_f32(float* y, int D) {
+  hadamard_levels_f32(y, D);
+  float r = (float)(1.0 / sqrt((double)D));
+  for (int i = 0; i < D; ++i) y[i] = y[i] * r;
+}
+
+void ora_hadamard_f64(double* y, int D) {
+  for (int len = D; len >= 2; len /= 2) {
+    int h = len / 2;
+    for (int base = 0; base < D; base += len)
+      for (int i = 0; i < h; ++i) {
+        double a = y[base + i], b = y[base + i + h];
+        y[base + i] = a + b;
+        y[base + i + h] = a - b;
+      }
+  }
+  double r = 1.0 / sqrt((double)D);
+  for (int i = 0; i < D; ++i) y[i] *= r;
+}
+
 void ora_rope_rot_f32(const ora_rope_cfg* c, const uint16_t* x_bf16, float* y) {
   const int D = c->D, P = D / 2;
   float* tmp = (float*)malloc(sizeof(float) * D);
@@ -144,6 +184,7 @@ void ora_rope_rot_f32(const ora_rope_cfg* c, const uint16_t* x_bf16, float* y) {
       }
     } else {
       memcpy(yn, tmp, sizeof(float) * D);
+      if (c->rotation == ORA_ROT_HADAMARD) ora_hadamard_f32(yn, D);
     }
   }
   free(tmp);
@@ -177,6 +218,7 @@ void ora_rope_rot_f64(const ora_rope_cfg* c, const uint16_t* x_bf16, double* y) 
       }
     } else {
       memcpy(yn, tmp, sizeof(double) * D);
+      if (c->rotation == ORA_ROT_HADAMARD) ora_hadamard_f64(yn, D);
     }
   }
   free(tmp);

@@ -28,7 +28,7 @@
 extern "C" {
 #endif
 
-enum { ORA_ROT_NONE = 0, ORA_ROT_INTERLEAVED = 1, ORA_ROT_HALF = 2 };
+enum { ORA_ROT_NONE = 0, ORA_ROT_INTERLEAVED = 1, ORA_ROT_HALF = 2, ORA_ROT_HADAMARD = 3 };
 enum { ORA_PQ_RANGE15 = 0, ORA_PQ_SYM7 = 1, ORA_PQ_NONE = 2 };
 
 /* Geometry of the 3D RoPE (Sec. 3): grid T x Hg x W with N = T*Hg*W tokens,
@@ -47,9 +47,22 @@ typedef struct {
  * into RoPE, Sec. 4.1.2); otherwise G = M (plain 3D RoPE, Sec. 3). fp64. */
 void ora_rope_block(const ora_rope_cfg* c, int n, int p, double G[4]);
 
-/* RoPE followed by the chosen rotation, bf16 input bits -> y [N][D]. */
+/* RoPE followed by the chosen rotation, bf16 input bits -> y [N][D].
+ * ORA_ROT_HADAMARD is the "Full" rotation the paper compares against
+ * (Sec. 5.3 baselines): y = RoPE(x) H_D with the orthonormal Sylvester matrix
+ * H_D = H_2 (x) H_{D/2} of Sec. 4.3.  In binary32 it is
+ * the Kronecker recursion taken literally -- the first factor pairs channel i
+ * of the first half with channel i of the second half (sum, difference), then
+ * each half recurses -- with every sum and difference unscaled and one final
+ * multiply by fl32(D^-1/2) (the product of the log2(D) factors 1/sqrt 2). */
 void ora_rope_rot_f32(const ora_rope_cfg* c, const uint16_t* x_bf16, float* y);
 void ora_rope_rot_f64(const ora_rope_cfg* c, const uint16_t* x_bf16, double* y);
+
+/* y <- y H_D in place for one row of D = 2^n values: the binary32 sequence
+ * described above (sum/difference butterflies, widest stride first, then the
+ * single normalising multiply). */
+void ora_hadamard_f32(float* y, int D);
+void ora_hadamard_f64(double* y, int D);
 
 /* Smoothing mean (Sec. 4, QKV smoothing), order-independent definition: every
  * value is scaled by 2^20, clamped to +-2^32, rounded half-to-even to an

@@ -53,7 +53,7 @@ int validate(const ra_params* p) {
   }
   if (sum != p->D) return fail(RA_ERR_INVALID, "rope_split must sum to D");
   if (!(p->rope_theta > 0.0f) || !std::isfinite(p->rope_theta)) return fail(RA_ERR_INVALID, "rope_theta must be > 0");
-  if (p->rotation < RA_ROT_NONE || p->rotation > RA_ROT_HALF) return fail(RA_ERR_INVALID, "unknown rotation");
+  if (p->rotation < RA_ROT_NONE || p->rotation > RA_ROT_HADAMARD) return fail(RA_ERR_INVALID, "unknown rotation");
   if (p->rot_blocks) {
     for (int i = 0; i < 4 * (kD / 2); ++i)
       if (!std::isfinite(p->rot_blocks[i])) return fail(RA_ERR_INVALID, "rot_blocks must be finite");
@@ -202,7 +202,8 @@ int get_tables(const ra_params* p, ra::RopeTables* out) {
   put(p->rope_split, sizeof p->rope_split);
   put(&p->rope_theta, sizeof p->rope_theta);
   put(&p->rotation, sizeof p->rotation);
-  if (p->rotation != RA_ROT_NONE && p->rot_blocks) put(p->rot_blocks, 4 * (kD / 2) * sizeof(double));
+  if ((p->rotation == RA_ROT_INTERLEAVED || p->rotation == RA_ROT_HALF) && p->rot_blocks)
+    put(p->rot_blocks, 4 * (kD / 2) * sizeof(double));
   std::lock_guard<std::mutex> lock(g_mu);
   auto it = g_tables.find(key);
   if (it != g_tables.end()) {

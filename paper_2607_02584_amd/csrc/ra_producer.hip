@@ -6,6 +6,11 @@
 //    and for the half rotation, on the RoPE output,
 //      z(o+2i)   = fma(y(o+i+D_j/2), r10, y(o+i)*r00)
 //      z(o+2i+1) = fma(y(o+i+D_j/2), r11, y(o+i)*r01).
+//  * The full D x D Hadamard rotation (the "Full" baseline of Sec. 5.3, the
+//    Sylvester matrix H_D = H_2 (x) H_{D/2} of Sec. 4.3) after plain RoPE: the
+//    Kronecker recursion, widest stride first -- the sums and differences of
+//    channels c and c + 64, then c and c + 32 inside each half, ... down to
+//    adjacent channels -- unscaled, then one multiply by fl32(1/sqrt 128).
 //  * Smoothing (Sec. 4): per-channel means over the tokens of a head.  Each
 //    value is scaled by 2^20, clamped to +-2^32 and rounded to an integer; the
 //    integers are summed in binary64, which is exact (every partial sum is an
@@ -20,6 +25,7 @@
 // t/32, t/32+8, ... (16 rows), so each row is read as 32 coalesced 8-byte
 // pieces.  These kernels are HBM-bound.
 #include "ra_internal.h"
+#include "rotate_attn.h"
 
 namespace ra {
 namespace {
@@ -106,6 +112,29 @@ __device__ __forceinline__ HalfSetup half_setup(const RopeTables& t, int cl) {
   return s;
 }
 
+constexpr float kInvSqrtD = 0.0883883476483184405501055452631f;  // fl32(1/sqrt(128))
+
+// y <- y H_128 for one row held by 32 lanes (lane cl holds channels 4cl..4cl+3):
+// strides 64..4 pair lanes whose cl differs in bit 4..0 (the lane with the bit
+// set takes the difference), strides 2 and 1 stay inside the thread.
+__device__ __forceinline__ void hadamard_row(float y[4], int cl) {
+#pragma unroll
+  for (int m = 16; m >= 1; m >>= 1) {
+    const bool upper = (cl & m) != 0;
+#pragma unroll
+    for (int c = 0; c < 4; ++c) {
+      const float o = __shfl_xor(y[c], m, 32);
+      y[c] = upper ? __fsub_rn(o, y[c]) : __fadd_rn(y[c], o);
+    }
+  }
+  const float t0 = __fadd_rn(y[0], y[2]), t2 = __fsub_rn(y[0], y[2]);
+  const float t1 = __fadd_rn(y[1], y[3]), t3 = __fsub_rn(y[1], y[3]);
+  y[0] = __fmul_rn(__fadd_rn(t0, t1), kInvSqrtD);
+  y[1] = __fmul_rn(__fsub_rn(t0, t1), kInvSqrtD);
+  y[2] = __fmul_rn(__fadd_rn(t2, t3), kInvSqrtD);
+  y[3] = __fmul_rn(__fsub_rn(t2, t3), kInvSqrtD);
+}
+
 // Computes the rotated values z of the thread's 4 channels for the 16 rows of
 // the tile.  Rows beyond N give zeros.  ybuf: [8][128] floats of LDS.
 __device__ __forceinline__ void rope_tile(const RopeTables& t, const QkArgs& a, int bh, int tile, float (*ybuf)[kD],
@@ -113,7 +142,8 @@ __device__ __forceinline__ void rope_tile(const RopeTables& t, const QkArgs& a, 
   __shared__ int pos[kTile][4];
   const int tid = threadIdx.x, rr = tid >> 5, cl = tid & 31;
   const PairSetup ps = pair_setup(t, cl);
-  const bool half = t.rotation == 2;
+  const bool half = t.rotation == RA_ROT_HALF;
+  const bool full = t.rotation == RA_ROT_HADAMARD;
   HalfSetup hs;
   if (half) hs = half_setup(t, cl);
   tile_positions(t, tile, a.N, pos);
@@ -154,6 +184,8 @@ __device__ __forceinline__ void rope_tile(const RopeTables& t, const QkArgs& a, 
         y[2 * i + 1] = __fmaf_rn(bv, r.w, __fmul_rn(av, r.y));
       }
       if (n >= a.N) y[0] = y[1] = y[2] = y[3] = 0.f;
+    } else if (full) {
+      hadamard_row(y, cl);  // rows past N are zero and stay zero
     }
 #pragma unroll
     for (int c = 0; c < 4; ++c) z[p][c] = y[c];

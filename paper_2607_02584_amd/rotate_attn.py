@@ -15,7 +15,7 @@ import numpy as np
 HERE = os.path.dirname(os.path.abspath(__file__))
 LIB_PATH = os.path.join(HERE, "librotate_attn.so")
 
-ROT_NONE, ROT_INTERLEAVED, ROT_HALF = 0, 1, 2
+ROT_NONE, ROT_INTERLEAVED, ROT_HALF, ROT_HADAMARD = 0, 1, 2, 3
 PQ_RANGE15, PQ_SYM7 = 0, 1
 SMOOTH_K, SMOOTH_V = 1, 2
 BF16, FP16, FP32 = 0, 1, 2

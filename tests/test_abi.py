@@ -47,7 +47,7 @@ def _base(ra, **kw):
     ("rope_split", (44, 42, 40), -1),
     ("rope_split", (43, 43, 42), -1),
     ("rope_theta", 0.0, -1),
-    ("rotation", 3, -1),
+    ("rotation", 4, -1),
     ("p_quant", 5, -1),
     ("smooth", 4, -1),
     ("q_group", 3, -2),

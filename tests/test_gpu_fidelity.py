@@ -4,13 +4,13 @@ Reference: fp64 softmax attention of the 3D-RoPE'd inputs (the oracle's
 ref_head).  Reported as cosine similarity and relative L2 (||O - R|| / ||R||)
 over sampled query rows of the 1024-token case (all rows) and of the
 32760-token layer (two heads, three row blocks each), for the INT4 path with
-each rotation (none, merged interleaved, half), the SYM7 P mapping (the
+each rotation (none, merged interleaved, half, full Hadamard), the SYM7 P mapping (the
 "without range-optimized P" ablation of the paper's Table 1), the paper's
 per-token Q/K scales, and the BF16 fallback.
 
 The paper gives no per-layer attention accuracy to compare with (its Table 1
 is video-level), so these numbers are reported, not pinned ("parity
-unpinned"): the asserts are sanity floors only.  Qualitative expectations from the paper (Sec. 5.3):
+unpinned"): the asserts are sanity floors only.  Qualitative expectations from the paper (Sec. 5.4):
 rotation helps on RoPE-structured outliers, the range-optimized P mapping
 beats the symmetric 7-level one.
 """
@@ -24,6 +24,7 @@ VARIANTS = [
     ("int4 none", 0, 0, 128),
     ("int4 interleaved", 1, 0, 128),
     ("int4 half", 2, 0, 128),
+    ("int4 full hadamard", 3, 0, 128),
     ("int4 interleaved SYM7", 1, 1, 128),
     ("int4 interleaved per-token", 1, 0, 1),
 ]

@@ -90,6 +90,7 @@ CASES = [
     (0, 16, 32, 64, 64, 0, 3),
     (1, 1, 64, 10 ** 6, 64, 1, 3),
     (2, 128, 128, 256, 128, 0, 0),
+    (3, 1, 128, 128, 128, 0, 3),
 ]
 
 

@@ -232,6 +232,85 @@ def test_f32_sequence_tracks_f64(ora, rotation):
     assert np.abs(y32 - y64).max() <= 4 * 2.0 ** -24 * scale * 2
 
 
+# ------------------------------------------------- full Hadamard rotation ----
+
+def _sylvester(n):
+    """H_n from the Kronecker recursion of Sec. 4.3 with H_2 of Sec. 4.1, built
+    from the paper's printed H_4 (tests/golden) and numpy's kron."""
+    g = _load("paper_constants.json")["H4_from_kronecker"]
+    H = np.array(g["matrix_unscaled"], float) / 2.0
+    H2 = np.array([[1, 1], [1, -1]]) / math.sqrt(2)
+    while H.shape[0] < n:
+        H = np.kron(H2, H)
+    return H
+
+
+def test_hadamard_rows_are_sylvester_and_library_matrix(ora):
+    """Unit vectors through the transform give the rows of H_128: equal to the
+    Kronecker construction and to scipy's Sylvester matrix / sqrt(128), with
+    entries +-1/sqrt(128) of sign (-1)^popcount(i & j)."""
+    from scipy.linalg import hadamard
+    H = _sylvester(128)
+    np.testing.assert_allclose(H, hadamard(128) / math.sqrt(128), atol=1e-15)
+    E = np.eye(128)
+    np.testing.assert_allclose(ora.hadamard_f64(E), H, atol=1e-15)
+    r32 = np.float32(1 / math.sqrt(128))
+    signs = np.array([[(-1) ** bin(i & j).count("1") for j in range(128)] for i in range(128)], np.float32)
+    assert np.array_equal(ora.hadamard_f32(E.astype(np.float32)), signs * r32)
+
+
+def test_hadamard_f32_exact_on_integers(ora):
+    """On integer rows every butterfly sum is exact in binary32 (|values| < 2^24),
+    so the binary32 transform is fl32(fl32(x H_u) * fl32(1/sqrt 128)) with x H_u the
+    exact integer product by the unnormalised Sylvester matrix (a matrix product,
+    not a butterfly)."""
+    from scipy.linalg import hadamard
+    rng = np.random.default_rng(41)
+    x = rng.integers(-5000, 5000, size=(64, 128))
+    exact = x @ hadamard(128).astype(np.int64)
+    expect = (exact.astype(np.float32) * np.float32(1 / math.sqrt(128))).astype(np.float32)
+    assert np.array_equal(ora.hadamard_f32(x.astype(np.float32)).view(np.uint32), expect.view(np.uint32))
+
+
+def test_full_rotation_is_rope_then_h_and_keeps_scores(ora):
+    """Sec. 5.3 "Full" baseline: y = RoPE(x) H_128.  H is orthogonal and symmetric,
+    so scores are unchanged (Sec. 4.1.1 with R^{-T} = R) and applying it twice
+    gives the RoPE output back."""
+    geo = ora.Geometry(3, 5, 6, split=(16, 56, 56), theta=256.0)
+    rng = np.random.default_rng(42)
+    q = _rand_bits(rng, (geo.N, 128), 2.0)
+    k = _rand_bits(rng, (geo.N, 128), 2.0)
+    H = _sylvester(128)
+    y0q = ora.rope_rot_f64(geo, q, ora.ROT_NONE)
+    y0k = ora.rope_rot_f64(geo, k, ora.ROT_NONE)
+    yq = ora.rope_rot_f64(geo, q, ora.ROT_HADAMARD)
+    yk = ora.rope_rot_f64(geo, k, ora.ROT_HADAMARD)
+    np.testing.assert_allclose(yq, y0q @ H, rtol=0, atol=1e-12)
+    S0 = y0q @ y0k.T
+    assert np.abs(yq @ yk.T - S0).max() <= 1e-12 * np.abs(S0).max()
+    np.testing.assert_allclose(ora.hadamard_f64(yq), y0q, rtol=0, atol=1e-12)
+    # the transform spreads an axis-aligned outlier over every channel equally
+    e = np.zeros((1, 128))
+    e[0, 7] = 30.0
+    assert np.allclose(np.abs(ora.hadamard_f64(e)), 30.0 / math.sqrt(128))
+
+
+def test_full_rotation_f32_error_bound(ora):
+    """Binary32 error of RoPE + Hadamard: each butterfly level is sqrt(2) times an
+    orthogonal map, so each level adds at most u |value| per element and the 2-norm
+    error grows by at most u ||y|| per level (Higham, Accuracy and Stability of
+    Numerical Algorithms, FFT error analysis); 7 levels, the final multiply, the
+    rounded 1/sqrt(128) and RoPE's own three roundings give <= 12 u ||x|| per row."""
+    geo = ora.Geometry(7, 9, 11)
+    rng = np.random.default_rng(43)
+    x = _rand_bits(rng, (geo.N, 128), 5.0)
+    y32 = ora.rope_rot_f32(geo, x, ora.ROT_HADAMARD).astype(np.float64)
+    y64 = ora.rope_rot_f64(geo, x, ora.ROT_HADAMARD)
+    nx = np.linalg.norm(ora.bf16_to_f32(x).astype(np.float64), axis=1)
+    err = np.linalg.norm(y32 - y64, axis=1)
+    assert np.all(err <= 12 * 2.0 ** -24 * nx)
+
+
 # ------------------------------------------------------------- smoothing ----
 
 def test_mean_fixed_close_to_exact_mean_and_order_free(ora):

@@ -8,7 +8,7 @@ forward pass of the paper's method:
 * Sec. 3 / Sec. 4.1.2 / Sec. 4.1.3: 3D RoPE followed by the interleaved
   (merged) or half rotation of Q and K, or by the full D x D Hadamard
   rotation (the "Full" baseline of Sec. 5.3, matrix of Sec. 4.3),
-* Sec. 4: smoothing (K and V means),
+* Sec. 4: smoothing (K and V means; Q mean with its per-key score bias),
 * Sec. 5.1: per-token / per-block INT4 quantization of Q and K, per-group V,
 * Sec. 4.2: blockwise online softmax with the Range-optimized P quantizer.
 
@@ -72,7 +72,8 @@ def lib():
         L.ora_center.argtypes = [P, P, ctypes.c_int, ctypes.c_int, P]
         L.ora_quant_tokens.argtypes = [P, ctypes.c_int, ctypes.c_int, ctypes.c_int, P, P]
         L.ora_quant_v.argtypes = [P, ctypes.c_int, ctypes.c_int, ctypes.c_int, P, P]
-        L.ora_attn_int4.argtypes = [ctypes.POINTER(_AttnCfg), P, P, P, P, P, P, P, ctypes.c_int, ctypes.c_int,
+        L.ora_key_bias.argtypes = [P, P, ctypes.c_int, ctypes.c_int, P]
+        L.ora_attn_int4.argtypes = [ctypes.POINTER(_AttnCfg), P, P, P, P, P, P, P, P, ctypes.c_int, ctypes.c_int,
                                     P, P, P, P, P, P]
         L.ora_attn_ref_f64.argtypes = [P, P, P, ctypes.c_int, ctypes.c_int, ctypes.c_double, ctypes.c_int,
                                        ctypes.c_int, P]
@@ -201,9 +202,19 @@ def quant_v(z: np.ndarray, g: int):
     return codes, scales
 
 
+def key_bias(mu_q: np.ndarray, zk: np.ndarray) -> np.ndarray:
+    """Per-key score bias of Q smoothing, b_j = mu_Q . zk_j (binary32, pairwise)."""
+    mu_q = np.ascontiguousarray(mu_q, dtype=np.float32)
+    zk = np.ascontiguousarray(zk, dtype=np.float32)
+    b = np.empty(zk.shape[0], np.float32)
+    lib().ora_key_bias(_p(mu_q), _p(zk), zk.shape[0], zk.shape[1], _p(b))
+    return b
+
+
 def attn_int4(qc, qs, kc, ks, vc, vs, mu_v=None, *, q_group, k_group, v_group, kv_block,
-              p_quant=PQ_RANGE15, sm_scale=0.0, rows=None, dumps=False):
-    """Blockwise INT4 attention for one head; returns O (fp64) and optional dumps."""
+              p_quant=PQ_RANGE15, sm_scale=0.0, rows=None, dumps=False, bias=None):
+    """Blockwise INT4 attention for one head; returns O (fp64) and optional dumps.
+    ``bias``: per-key score bias of Q smoothing, or None."""
     qc = np.ascontiguousarray(qc, dtype=np.int8)
     kc = np.ascontiguousarray(kc, dtype=np.int8)
     vc = np.ascontiguousarray(vc, dtype=np.int8)
@@ -211,6 +222,7 @@ def attn_int4(qc, qs, kc, ks, vc, vs, mu_v=None, *, q_group, k_group, v_group, k
     ks = np.ascontiguousarray(ks, dtype=np.float32)
     vs = np.ascontiguousarray(vs, dtype=np.float32)
     mu = None if mu_v is None else np.ascontiguousarray(mu_v, dtype=np.float32)
+    bias = None if bias is None else np.ascontiguousarray(bias, dtype=np.float32)
     N, D = kc.shape
     row0, nrows = (0, N) if rows is None else rows
     a = _AttnCfg()
@@ -225,7 +237,8 @@ def attn_int4(qc, qs, kc, ks, vc, vs, mu_v=None, *, q_group, k_group, v_group, k
         x = np.empty((nrows, N), np.float32)
         m = np.empty((nrows, nb), np.float32)
         l = np.empty(nrows, np.float64)
-    lib().ora_attn_int4(ctypes.byref(a), _p(qc), _p(qs), _p(kc), _p(ks), _p(vc), _p(vs), _p(mu), row0, nrows,
+    lib().ora_attn_int4(ctypes.byref(a), _p(qc), _p(qs), _p(kc), _p(ks), _p(vc), _p(vs), _p(mu), _p(bias),
+                        row0, nrows,
                         _p(O), _p(S), _p(u), _p(x), _p(m), _p(l))
     if dumps:
         return O, dict(S=S, u=u, x=x, m=m, l=l)
@@ -274,6 +287,7 @@ class Int4Config:
     p_quant: int = PQ_RANGE15
     smooth_k: bool = True
     smooth_v: bool = True
+    smooth_q: bool = False
     q_group: int = 128
     k_group: int = 128
     v_group: int = 128
@@ -282,7 +296,8 @@ class Int4Config:
 
 
 def quantize_qk_head(geo: Geometry, cfg: Int4Config, q_bf16, k_bf16):
-    """Sec. 3-4.1 + Sec. 5.1 for one head: RoPE+rotation, K smoothing, INT4 codes."""
+    """Sec. 3-4.1 + Sec. 5.1 for one head: RoPE+rotation, K (and Q) smoothing,
+    INT4 codes; with Q smoothing also the per-key score bias mu_Q . K_j."""
     yq = rope_rot_f32(geo, q_bf16, cfg.rotation, cfg.rot)
     yk = rope_rot_f32(geo, k_bf16, cfg.rotation, cfg.rot)
     if cfg.smooth_k:
@@ -291,9 +306,17 @@ def quantize_qk_head(geo: Geometry, cfg: Int4Config, q_bf16, k_bf16):
     else:
         mu_k = np.zeros(geo.D, np.float32)
         zk = yk
-    qc, qs = quant_tokens(yq, cfg.q_group)
+    bias = None
+    if cfg.smooth_q:
+        mu_q = mean_fixed(yq)
+        zq = center(yq, mu_q)
+        bias = key_bias(mu_q, zk)
+    else:
+        mu_q = np.zeros(geo.D, np.float32)
+        zq = yq
+    qc, qs = quant_tokens(zq, cfg.q_group)
     kc, ks = quant_tokens(zk, cfg.k_group)
-    return dict(q_codes=qc, q_scale=qs, k_codes=kc, k_scale=ks, mu_k=mu_k)
+    return dict(q_codes=qc, q_scale=qs, k_codes=kc, k_scale=ks, mu_k=mu_k, mu_q=mu_q, k_bias=bias)
 
 
 def quantize_v_head(cfg: Int4Config, v_bf16):
@@ -315,7 +338,7 @@ def fwd_int4_head(geo: Geometry, cfg: Int4Config, q_bf16, k_bf16, v_bf16, rows=N
     res = attn_int4(qk["q_codes"], qk["q_scale"], qk["k_codes"], qk["k_scale"], vv["v_codes"], vv["v_scale"],
                     vv["mu_v"] if cfg.smooth_v else None, q_group=cfg.q_group, k_group=cfg.k_group,
                     v_group=cfg.v_group, kv_block=cfg.kv_block, p_quant=cfg.p_quant, sm_scale=cfg.sm_scale,
-                    rows=rows, dumps=dumps)
+                    rows=rows, dumps=dumps, bias=qk["k_bias"])
     inter = dict(qk, **vv)
     if dumps:
         O, d = res

@@ -245,6 +245,26 @@ void ora_center(const float* y, const float* mu, int N, int D, float* z) {
     for (int ch = 0; ch < D; ++ch) z[(size_t)n * D + ch] = y[(size_t)n * D + ch] - mu[ch];
 }
 
+/* Sec. 4 Q smoothing: with Q = Q_s + 1 mu_Q^T the scores split as
+ * Q K^T = Q_s K^T + 1 (K mu_Q)^T, so every key j carries the additive score
+ * bias b_j = mu_Q . K_j (K after RoPE, rotation and its own smoothing), which
+ * is the same for all queries and stays in binary32 beside the INT4 scores.
+ * The dot product is summed pairwise: the two halves of the channel range
+ * recursively, with the products fl(mu_c k_c) at the leaves. */
+static float pairwise_sum(const float* p, int n) {
+  if (n == 1) return p[0];
+  return pairwise_sum(p, n / 2) + pairwise_sum(p + n / 2, n / 2);
+}
+
+void ora_key_bias(const float* mu_q, const float* zk, int N, int D, float* bias) {
+  float* p = (float*)malloc(sizeof(float) * D);
+  for (int n = 0; n < N; ++n) {
+    for (int ch = 0; ch < D; ++ch) p[ch] = mu_q[ch] * zk[(size_t)n * D + ch];
+    bias[n] = pairwise_sum(p, D);
+  }
+  free(p);
+}
+
 /* -------------------------------------------------------- quantization -- */
 
 static int8_t qcode(float z, float inv) {
@@ -310,7 +330,7 @@ static double sigma_of(double sm_scale, int D) { return sm_scale > 0.0 ? sm_scal
 void ora_attn_int4(const ora_attn_cfg* a,
                    const int8_t* qc, const float* qs,
                    const int8_t* kc, const float* ks,
-                   const int8_t* vc, const float* vs, const float* mu_v,
+                   const int8_t* vc, const float* vs, const float* mu_v, const float* bias,
                    int row0, int nrows, double* O,
                    int32_t* S_dump, uint8_t* u_dump, float* x_dump, float* m_dump,
                    double* l_dump) {
@@ -324,6 +344,7 @@ void ora_attn_int4(const ora_attn_cfg* a,
   {
     int32_t* S = (int32_t*)malloc(sizeof(int32_t) * kv);
     float* cn = (float*)malloc(sizeof(float) * kv);
+    float* t = (float*)malloc(sizeof(float) * kv);
     double* acc = (double*)malloc(sizeof(double) * D);
     double* part = (double*)malloc(sizeof(double) * D);
 #pragma omp for schedule(dynamic, 1)
@@ -345,7 +366,10 @@ void ora_attn_int4(const ora_attn_cfg* a,
           for (int ch = 0; ch < D; ++ch) s += (int32_t)q[ch] * (int32_t)k[ch];
           S[n - j0] = s;
           cn[n - j0] = cq * ks[n / a->k_group];
-          bm = fmaxf(bm, (float)s * cn[n - j0]);
+          /* with Q smoothing the key's bias, on the same log2e-scaled scale,
+           * joins the dequantised score in one fused step */
+          t[n - j0] = bias ? fmaf((float)s, cn[n - j0], bias[n] * Kc) : (float)s * cn[n - j0];
+          bm = fmaxf(bm, t[n - j0]);
           if (S_dump) S_dump[(size_t)r * N + n] = s;
         }
         /* m_ij = max(m_{i,j-1}, rowmax S_ij); rescale the running sums. */
@@ -360,7 +384,7 @@ void ora_attn_int4(const ora_attn_cfg* a,
         for (int ch = 0; ch < D; ++ch) part[ch] = 0.0;
         int gcur = j0 / a->v_group;
         for (int n = j0; n < j1; ++n) {
-          const float x = fmaf((float)S[n - j0], cn[n - j0], -mn);
+          const float x = bias ? t[n - j0] - mn : fmaf((float)S[n - j0], cn[n - j0], -mn);
           const float P = ora_exp2_f32(x);
           l += (double)P;
           if (x_dump) x_dump[(size_t)r * N + n] = x;
@@ -393,6 +417,7 @@ void ora_attn_int4(const ora_attn_cfg* a,
     }
     free(S);
     free(cn);
+    free(t);
     free(acc);
     free(part);
   }

@@ -72,6 +72,11 @@ void ora_mean_fixed(const float* y, int N, int D, float* mu);
 /* z = fl32(y - mu) for every token (mu broadcast over tokens). */
 void ora_center(const float* y, const float* mu, int N, int D, float* z);
 
+/* Q smoothing (Sec. 4): the per-key score bias b_j = mu_Q . zk_j that the
+ * smoothed-away query mean contributes, binary32, pairwise summation over the
+ * channels (halves recursively; D a power of two).  bias [N]. */
+void ora_key_bias(const float* mu_q, const float* zk, int N, int D, float* bias);
+
 /* Symmetric INT4 quantization of Q or K (Sec. 5.1: per-token, or per-block of
  * g tokens): scale s = amax/7, codes = clamp(rint(z * (7/amax)), -7, 7).
  * codes [N][D], scales [ceil(N/g)]. */
@@ -91,7 +96,10 @@ typedef struct {
 
 /* Blockwise INT4 attention for query rows [row0, row0+nrows) of one head
  * (Sec. 4.2 online softmax + Range-optimized P quantization).  O [nrows][D] is
- * returned in double.  Optional dumps (NULL to skip):
+ * returned in double.  bias (NULL without Q smoothing): the per-key score
+ * bias b [N]; the log2e-scaled score of key j is then
+ * t = fma(S, c, fl(b_j Kc)) and x = fl(t - m), otherwise x = fma(S, c, -m)
+ * with the maximum taken over fl(S c).  Optional dumps (NULL to skip):
  *   S_dump [nrows][N] int32 exact S = q_codes . k_codes
  *   u_dump [nrows][N] P codes u = P~ + 8 in [0,15] (or [0,7] for SYM7)
  *   x_dump [nrows][N] the binary32 exponent argument x of each P = 2^x
@@ -100,7 +108,7 @@ typedef struct {
 void ora_attn_int4(const ora_attn_cfg* a,
                    const int8_t* qc, const float* qs,
                    const int8_t* kc, const float* ks,
-                   const int8_t* vc, const float* vs, const float* mu_v,
+                   const int8_t* vc, const float* vs, const float* mu_v, const float* bias,
                    int row0, int nrows, double* O,
                    int32_t* S_dump, uint8_t* u_dump, float* x_dump, float* m_dump,
                    double* l_dump);

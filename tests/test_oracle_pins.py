@@ -524,6 +524,74 @@ def test_online_softmax_without_p_rounding_is_softmax(ora, kv, vg):
     assert np.abs(O - ref).max() <= 1e-5 * np.abs(ref).max()
 
 
+def test_key_bias_is_the_query_mean_dot_each_key(ora):
+    """Sec. 4 Q smoothing: b_j = mu_Q . K_j.  On small integers every product and
+    partial sum is exact, so b is the integer dot product (numpy's int matmul); on
+    general binary32 values the pairwise sum stays within the pairwise-summation
+    bound (log2(D) + 1) u sum|mu_c k_c| of the exact dot product (Higham)."""
+    rng = np.random.default_rng(44)
+    mu = rng.integers(-50, 50, 128)
+    K = rng.integers(-300, 300, (40, 128))
+    b = ora.key_bias(mu.astype(np.float32), K.astype(np.float32))
+    assert np.array_equal(b.astype(np.int64), K @ mu)
+    muf = rng.standard_normal(128).astype(np.float32) * np.float32(3.0)
+    Kf = (rng.standard_normal((300, 128)) * rng.uniform(0.1, 20, 128)).astype(np.float32)
+    bf = ora.key_bias(muf, Kf).astype(np.float64)
+    prods = Kf.astype(np.float64) * muf.astype(np.float64)
+    exact = np.array([math.fsum(r) for r in prods])
+    bound = 8 * 2.0 ** -24 * np.abs(prods).sum(1)
+    assert np.all(np.abs(bf - exact) <= bound)
+
+
+def test_key_bias_enters_as_an_extra_channel(ora):
+    """With the P rounding off, the blockwise INT4 attention with a key bias equals
+    one-shot softmax attention over the dequantised codes with the bias appended
+    as a 129th channel (query side 1, key side b_j) -- a different route to the same
+    scores Q_s K^T + 1 b^T."""
+    rng = np.random.default_rng(45)
+    N = 600
+    qc, qs, kc, ks, vc = _int4_inputs(rng, N)
+    vs = rng.uniform(0.1, 1.0, (1, 128)).astype(np.float32)
+    b = (rng.standard_normal(N) * 4.0).astype(np.float32)
+    O, _ = _attn(ora, qc, qs, kc, ks, vc, vs, None, v_group=N, kv_block=64, p_quant=ora.PQ_NONE, bias=b)
+    qd = np.concatenate([qc.astype(np.float64) * qs[:, None], np.ones((N, 1))], 1)
+    kd = np.concatenate([kc.astype(np.float64) * ks[:, None], b[:, None].astype(np.float64)], 1)
+    V = vc.astype(np.float64) * vs.astype(np.float64)
+    Vp = np.concatenate([V, np.zeros((N, 1))], 1)   # the reference takes one width for all three
+    ref = ora.attn_ref_f64(qd, kd, Vp, sm_scale=1 / math.sqrt(128))[:, :128]
+    assert np.abs(O - ref).max() <= 1e-5 * np.abs(ref).max()
+    # and the bias changes the result (a dropped bias would not pass the check above)
+    O0, _ = _attn(ora, qc, qs, kc, ks, vc, vs, None, v_group=N, kv_block=64, p_quant=ora.PQ_NONE)
+    assert np.abs(O0 - ref).max() > 1e-2 * np.abs(ref).max()
+
+
+def test_q_smoothing_recovers_a_shared_query_offset(ora):
+    """Sec. 4: a bias shared by all queries wastes the INT4 range of Q; removing
+    the mean and adding it back as the per-key bias keeps the scores (exactly in
+    real arithmetic) and brings the INT4 result much closer to fp64 attention."""
+    rng = np.random.default_rng(46)
+    N = 512
+    off = rng.uniform(4.0, 8.0, 128).astype(np.float32)
+    Q = (rng.standard_normal((N, 128)) + off).astype(np.float32)
+    K = rng.standard_normal((N, 128)).astype(np.float32)
+    V = rng.standard_normal((N, 128)).astype(np.float32)
+    ref = ora.attn_ref_f64(Q, K, V)
+    kc, ks = ora.quant_tokens(K, 1)
+    vc, vs = ora.quant_v(V, 128)
+    kw = dict(q_group=1, k_group=1, v_group=128, kv_block=128)
+    qc, qs = ora.quant_tokens(Q, 1)
+    O_plain = ora.attn_int4(qc, qs, kc, ks, vc, vs, **kw)
+    mu_q = ora.mean_fixed(Q)
+    qsc, qss = ora.quant_tokens(ora.center(Q, mu_q), 1)
+    O_sm = ora.attn_int4(qsc, qss, kc, ks, vc, vs, bias=ora.key_bias(mu_q, K), **kw)
+    e_plain = np.linalg.norm(O_plain - ref) / np.linalg.norm(ref)
+    e_sm = np.linalg.norm(O_sm - ref) / np.linalg.norm(ref)
+    assert e_sm < 0.5 * e_plain
+    # the bias with the wrong sign is far off
+    O_neg = ora.attn_int4(qsc, qss, kc, ks, vc, vs, bias=-ora.key_bias(mu_q, K), **kw)
+    assert np.linalg.norm(O_neg - ref) / np.linalg.norm(ref) > 2 * e_sm
+
+
 @pytest.mark.parametrize("kv,qg,kg", [(32, 1, 1), (64, 16, 64), (128, 7, 32)])
 def test_online_softmax_prefix_max_restatement(ora, kv, qg, kg):
     """Sec. 4.2: m_ij = max(m_{i,j-1}, rowmax S_ij) and P_ij = exp(S_ij - m_ij). Written

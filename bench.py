@@ -181,33 +181,50 @@ def main():
         }
         log(f"bf16 fallback op {f_step:.3f} ms, kernel {f_attn:.3f} ms; speedup kernel {f_attn / attn_ms:.2f}x")
 
-    # the paper's own Q/K granularity (per token, Sec. 5.1), same inputs and kernel family
-    ptok = None
+    # variants of the method on the same inputs and kernel family: the paper's
+    # own Q/K granularity (per token, Sec. 5.1), Q smoothing with the per-key
+    # bias (Sec. 4), the full Hadamard rotation (the Sec. 5.3 baseline)
+    variants = None
     if args.container == "e2m3" and not args.skip_fallback:
-        pt = ra.make_params(w.B, w.H, (w.T, w.Hg, w.W), w.split, w.theta, rotation=ra.ROT_INTERLEAVED, q_group=1,
-                            k_group=1, v_group=128, kv_block=128, out_dtype=ra.BF16, code_format=ra.CODES_E2M3)
-        bt = ra.alloc_int4(pt, dev)
-        wst = ra.workspace(pt, ra.PATH_INT4, dev)
-        ot = torch.empty_like(o)
+        variants = {}
+        specs = {
+            "per_token_qk": dict(rotation=ra.ROT_INTERLEAVED, q_group=1, k_group=1, smooth=ra.SMOOTH_K | ra.SMOOTH_V),
+            "q_smoothing": dict(rotation=ra.ROT_INTERLEAVED, q_group=128, k_group=128,
+                                smooth=ra.SMOOTH_K | ra.SMOOTH_V | ra.SMOOTH_Q),
+            "full_hadamard": dict(rotation=ra.ROT_HADAMARD, q_group=128, k_group=128,
+                                  smooth=ra.SMOOTH_K | ra.SMOOTH_V),
+        }
+        for name, kw in specs.items():
+            pt = ra.make_params(w.B, w.H, (w.T, w.Hg, w.W), w.split, w.theta, v_group=128, kv_block=128,
+                                out_dtype=ra.BF16, code_format=ra.CODES_E2M3, **kw)
+            bt = ra.alloc_int4(pt, dev)
+            wst = ra.workspace(pt, ra.PATH_INT4, dev)
+            ot = torch.empty_like(o)
+            kb = bt["k_bias"] if kw["smooth"] & ra.SMOOTH_Q else None
+            e0, e1, e2 = (torch.cuda.Event(enable_timing=True) for _ in range(3))
 
-        def tstep():
-            ra.quantize_qk(pt, qd, kd, bt["q_codes"], bt["q_scale"], bt["k_codes"], bt["k_scale"], bt["mu_k"], wst)
-            ra.quantize_v(pt, vd, bt["v_codes"], bt["v_scale"], bt["mu_v"], wst)
-            a0.record(stream)
-            ra.attn_int4(pt, bt["q_codes"], bt["q_scale"], bt["k_codes"], bt["k_scale"], bt["v_codes"],
-                         bt["v_scale"], bt["mu_v"], ot)
-            a1.record(stream)
-        a0, a1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-        tstep()
-        torch.cuda.synchronize()
-        ka = []
-        for _ in range(5):
+            def tstep():
+                e0.record(stream)
+                ra.quantize_qk(pt, qd, kd, bt["q_codes"], bt["q_scale"], bt["k_codes"], bt["k_scale"], bt["mu_k"],
+                               wst, k_bias=kb)
+                ra.quantize_v(pt, vd, bt["v_codes"], bt["v_scale"], bt["mu_v"], wst)
+                e1.record(stream)
+                ra.attn_int4(pt, bt["q_codes"], bt["q_scale"], bt["k_codes"], bt["k_scale"], bt["v_codes"],
+                             bt["v_scale"], bt["mu_v"], ot, k_bias=kb)
+                e2.record(stream)
             tstep()
             torch.cuda.synchronize()
-            ka.append(a0.elapsed_time(a1))
-        ptok = {"q_group": 1, "k_group": 1, "kernel_ms": round(float(np.median(ka)), 4),
-                "kernel_tops": round(ops / (float(np.median(ka)) * 1e-3) / 1e12, 1)}
-        log(f"per-token Q/K scales: attention kernel {ptok['kernel_ms']} ms")
+            ka, pa = [], []
+            for _ in range(5):
+                tstep()
+                torch.cuda.synchronize()
+                ka.append(e1.elapsed_time(e2))
+                pa.append(e0.elapsed_time(e1))
+            kms = float(np.median(ka))
+            variants[name] = {"kernel_ms": round(kms, 4), "kernel_tops": round(ops / (kms * 1e-3) / 1e12, 1),
+                              "producer_ms": round(float(np.median(pa)), 4)}
+            log(f"variant {name}: attention kernel {kms:.3f} ms, producers {variants[name]['producer_ms']} ms")
+            del bt, wst, ot
 
     cpu = None
     if not args.no_cpu_baseline:
@@ -241,8 +258,8 @@ def main():
         "cpu_baseline": cpu,
     }
     line.update(extra)
-    if ptok is not None:
-        line["int4_per_token_qk"] = ptok
+    if variants is not None:
+        line["variants"] = variants
     print(json.dumps(line), flush=True)
 
 

@@ -93,6 +93,9 @@ extern "C" {
 /* smoothing flags (Sec. 4: biases shared by all tokens) */
 #define RA_SMOOTH_K 1 /* subtract the per-channel mean of rotated K (softmax invariant) */
 #define RA_SMOOTH_V 2 /* subtract the per-channel mean of V, add it back to O */
+#define RA_SMOOTH_Q 4 /* subtract the per-channel mean mu_Q of rotated Q; every key j then
+                         carries the score bias b_j = mu_Q . K_j (k_bias), added to its
+                         dequantized scores (Sec. 4: Q, K and V smoothing) */
 
 /* dtypes */
 #define RA_BF16 0
@@ -135,7 +138,8 @@ typedef struct ra_layout {
   int64_t k_scale_count;  /* floats in k_scale */
   int64_t v_code_bytes;   /* bytes of v_codes */
   int64_t v_scale_count;  /* floats in v_scale */
-  int64_t mu_count;       /* floats in mu_k / mu_v: B*H*D */
+  int64_t mu_count;       /* floats in mu_q / mu_k / mu_v: B*H*D */
+  int64_t k_bias_count;   /* floats in k_bias: B*H*Npad */
 } ra_layout;
 
 /* Fills *out; RA_ERR_INVALID / RA_ERR_UNSUPPORTED on bad parameters. */
@@ -148,14 +152,20 @@ int rotate_attn_layout(const ra_params* p, ra_layout* out);
 int rotate_attn_workspace_size(const ra_params* p, int path, size_t* bytes);
 
 /* Producer for Q and K (Sec. 3, 4, 4.1, 5.1): 3D RoPE and the chosen rotation,
- * K smoothing (if RA_SMOOTH_K), per-group INT4 quantization, nibble packing.
+ * K smoothing (if RA_SMOOTH_K), Q smoothing (if RA_SMOOTH_Q), per-group INT4
+ * quantization, packing.
  * q, k: inputs [B][H][N][D].  q_codes/k_codes: ra_layout.qk_code_bytes each;
  * q_scale/k_scale: ra_layout.q_scale_count / k_scale_count floats.
- * mu_k: nullable, receives the K smoothing mean [B*H][D] (zeros if smoothing
- * is off).  Q is never smoothed. */
+ * mu_k, mu_q: nullable, receive the smoothing means [B*H][D] (zeros where that
+ * smoothing is off).
+ * k_bias: with RA_SMOOTH_Q required (RA_ERR_INVALID if NULL), receives the
+ * per-key score bias b_j = mu_Q . K_j [B*H][Npad] in binary32 (K after RoPE,
+ * rotation and K smoothing; pairwise sum over the channels: halves of the
+ * channel range recursively; padded keys get 0); ignored otherwise. */
 int rotate_attn_quantize_qk(const ra_params* p, const void* q, const void* k, uint8_t* q_codes,
                             float* q_scale, uint8_t* k_codes, float* k_scale, float* mu_k,
-                            void* workspace, size_t workspace_bytes, void* stream);
+                            float* mu_q, float* k_bias, void* workspace, size_t workspace_bytes,
+                            void* stream);
 
 /* Producer for V (Sec. 4.3, 5.1): V is taken as given (a Hadamard rotation of
  * V is folded into W_v/W_o offline), smoothed (if RA_SMOOTH_V) and quantized
@@ -169,10 +179,14 @@ int rotate_attn_quantize_v(const ra_params* p, const void* v, uint8_t* v_codes, 
  * kv_block keys in ascending order, P mapped to the unsigned code
  * u = round(15 P) in [0, 15] (the affine code P~ = u - 8), PV on the codes,
  * O = (sum of dequantized PV) / l + mu_v, l = sum of the unquantized P.
- * mu_v: nullable (treated as zeros).  o: [B][H][N][D] in out_dtype. */
+ * mu_v: nullable (treated as zeros).  k_bias: the per-key score bias written
+ * by quantize_qk, required with RA_SMOOTH_Q (RA_ERR_INVALID if NULL), ignored
+ * otherwise; with it the log2e-scaled score of key j is
+ * t = fma(S, c, fl(b_j * Kc)) and P = 2^(t - m).  o: [B][H][N][D] in out_dtype. */
 int rotate_attn_attn_int4(const ra_params* p, const uint8_t* q_codes, const float* q_scale,
                           const uint8_t* k_codes, const float* k_scale, const uint8_t* v_codes,
-                          const float* v_scale, const float* mu_v, void* o, void* stream);
+                          const float* v_scale, const float* mu_v, const float* k_bias, void* o,
+                          void* stream);
 
 /* Debug variant of rotate_attn_attn_int4: runs the same kernel with a dump
  * enabled for the query rows [row0, row0 + rows) of head bh:
@@ -184,7 +198,8 @@ int rotate_attn_attn_int4(const ra_params* p, const uint8_t* q_codes, const floa
 int rotate_attn_attn_int4_debug(const ra_params* p, const uint8_t* q_codes, const float* q_scale,
                                 const uint8_t* k_codes, const float* k_scale,
                                 const uint8_t* v_codes, const float* v_scale, const float* mu_v,
-                                void* o, int32_t bh, int32_t row0, int32_t rows, int32_t* s_out,
+                                const float* k_bias, void* o, int32_t bh, int32_t row0, int32_t rows,
+                                int32_t* s_out,
                                 uint8_t* u_out, float* m_out, void* stream);
 
 /* Whole INT4 forward: quantize_qk + quantize_v + attn_int4, codes kept in the

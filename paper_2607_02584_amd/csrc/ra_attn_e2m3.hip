@@ -16,7 +16,9 @@
 //   m_new = max(m, rowmax fl(S * c)),  P = 2^(S c - m_new),
 //   u = rint(15 P),  l = alpha l + sum P,  alpha = 2^(m - m_new),
 //   O' = O' * alpha * (w_old / w_new) + (u/8) V~   (w = V scale of the block's group)
-// and finally O = O' * 8 w / 15 / l + mu_v.  The factor 15 rides in the
+// and finally O = O' * 8 w / 15 / l + mu_v.  With Q smoothing every key j
+// carries the score bias fl(b_j Kc): the scores become t = fma(S, c, bias_j)
+// before the maximum, and 15 P = 2^(t - (m_new - log2 15)).  The factor 15 rides in the
 // exponent: 15 P = 2^fma(S, c, -(m_new - log2 15)), one exponential per score
 // and no multiply (the binary32 roundings of log2 15 and of m_new - log2 15
 // perturb 15 P by a relative ln 2 * 2^-24 (|m_new| + 6) at most); l is kept as
@@ -131,7 +133,9 @@ struct TilePiece {
   }
 };
 
-template <int KV, bool KTOK, bool SYM7, bool DEBUG>
+// QB: Q smoothing, every key carries the score bias fl(b_j Kc), the scores
+// become t = fma(S, c, bias) before the maximum and P = 2^(t - m).
+template <int KV, bool KTOK, bool SYM7, bool DEBUG, bool QB>
 __global__ __launch_bounds__(kThreads, 8 / kWaves) void k_attn_e2m3(AttnArgs a) {
   constexpr int NCH = KV / 32;   // 32-key chunks
   constexpr int NG = KV / 64;    // 64-key groups (one PV instruction each)
@@ -142,6 +146,7 @@ __global__ __launch_bounds__(kThreads, 8 / kWaves) void k_attn_e2m3(AttnArgs a) 
   __shared__ __align__(16) float sW[kD];      // final V scale per channel
   __shared__ __align__(16) float sKs[2][KTOK ? KV : 1];
   __shared__ __align__(16) float sKc[2][NCH];  // K scale of each 32-key chunk (grouped K)
+  __shared__ __align__(16) float sB[2][QB ? KV : 1];  // per-key score bias fl(b Kc)
 
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int hh = lane >> 5, j = lane & 31;
@@ -179,13 +184,13 @@ __global__ __launch_bounds__(kThreads, 8 / kWaves) void k_attn_e2m3(AttnArgs a) 
   // They are fetched from global memory one block ahead of staging, so no
   // wave waits on their latency.
   struct Aux {
-    float v, k;
+    float v, k, b;
   };
   // fetch_aux runs for blocks 0, 1, 2, ... in order; (fg, fr) = (V group, block
   // within the group) of the next block it fetches
   int fg = 0, fr = 0;
   auto fetch_aux = [&](int jb) {
-    Aux f{0.f, 0.f};
+    Aux f{0.f, 0.f, 0.f};
     if (tid < kD) f.v = a.vs[(static_cast<size_t>(bh) * a.nvgroups + fg) * kD + tid];
     if (++fr == a.v_bpg) {
       fr = 0;
@@ -193,6 +198,7 @@ __global__ __launch_bounds__(kThreads, 8 / kWaves) void k_attn_e2m3(AttnArgs a) 
     }
     const int kt = tid - kD;
     if (kt >= 0 && kt < (KTOK ? KV : NCH)) f.k = KTOK ? ksh[jb * KV + kt] : ksh[(jb * KV + kt * 32) / a.k_group];
+    if (QB && kt >= 0 && kt < KV) f.b = a.kbias[static_cast<size_t>(bh) * a.Npad + jb * KV + kt];
     return f;
   };
   float wcur = 1.0f;
@@ -210,6 +216,7 @@ __global__ __launch_bounds__(kThreads, 8 / kWaves) void k_attn_e2m3(AttnArgs a) 
       if (KTOK) sKs[buf][kt] = f.k;
       else sKc[buf][kt] = f.k;
     }
+    if (QB && kt >= 0 && kt < KV) sB[buf][kt] = __fmul_rn(f.b, a.Kc);
   };
 
   v16f of[4];
@@ -228,7 +235,7 @@ __global__ __launch_bounds__(kThreads, 8 / kWaves) void k_attn_e2m3(AttnArgs a) 
   tp.store(sK[0], sV[0], tid);
   tp.load(kbase + (nblocks > 1 ? KB : 0), vbase + (nblocks > 1 ? KB : 0), tid);
   store_aux(0, 0, fetch_aux(0));
-  Aux pf{0.f, 0.f};
+  Aux pf{0.f, 0.f, 0.f};
   if (nblocks > 1) pf = fetch_aux(1);
   __syncthreads();
 
@@ -272,6 +279,18 @@ __global__ __launch_bounds__(kThreads, 8 / kWaves) void k_attn_e2m3(AttnArgs a) 
       __builtin_amdgcn_sched_barrier(0);
     }
     // key of accumulator register r in chunk ch: key0 + 32*ch + 8*(r/4) + 4*hh + r%4
+    if (DEBUG) {
+      if (bh == a.dbg_bh && qrow >= a.dbg_row0 && qrow < a.dbg_row0 + a.dbg_rows && a.dbg_s) {
+        const size_t rowo = static_cast<size_t>(qrow - a.dbg_row0);
+#pragma unroll
+        for (int ch = 0; ch < NCH; ++ch)
+#pragma unroll
+          for (int r = 0; r < 16; ++r) {
+            const int key = key0 + ch * 32 + 8 * (r >> 2) + 4 * hh + (r & 3);
+            if (key < N) a.dbg_s[rowo * N + key] = static_cast<int32_t>(s[ch][r]);
+          }
+      }
+    }
     if (MASKED) {
 #pragma unroll
       for (int ch = 0; ch < NCH; ++ch)
@@ -288,7 +307,28 @@ __global__ __launch_bounds__(kThreads, 8 / kWaves) void k_attn_e2m3(AttnArgs a) 
     if (++vr == a.v_bpg) vr = 0;
     float4 rr = make_float4(1.f, 1.f, 1.f, 1.f);
     if (vchange) rr = *reinterpret_cast<const float4*>(&sR[buf][4 * j]);
-    if (!KTOK && a.k_group >= KV) {
+    if (QB) {
+      // t = fma(S, c, bias) in place of S; the maximum is over t
+#pragma unroll
+      for (int ch = 0; ch < NCH; ++ch) {
+        if (!KTOK) cch[ch] = __fmul_rn(cq, sKc[buf][ch]);
+#pragma unroll
+        for (int r4 = 0; r4 < 4; ++r4) {
+          const int kl = ch * 32 + 8 * r4 + 4 * hh;
+          const float4 b4 = *reinterpret_cast<const float4*>(&sB[buf][kl]);
+          const float bb[4] = {b4.x, b4.y, b4.z, b4.w};
+#pragma unroll
+          for (int e = 0; e < 4; ++e) {
+            const int r = 4 * r4 + e;
+            const float c = KTOK ? __fmul_rn(cq, sKs[buf][kl + e]) : cch[ch];
+            float t = __fmaf_rn(s[ch][r], c, bb[e]);
+            if (MASKED && s[ch][r] == -INFINITY) t = -INFINITY;
+            s[ch][r] = t;
+            tmax = fmaxf(tmax, t);
+          }
+        }
+      }
+    } else if (!KTOK && a.k_group >= KV) {
       // one K scale for the whole block: a single product after the maximum
       float cm[NCH];
 #pragma unroll
@@ -369,27 +409,20 @@ __global__ __launch_bounds__(kThreads, 8 / kWaves) void k_attn_e2m3(AttnArgs a) 
     float ls[4];   // independent partial sums, started by the first four values
 #pragma unroll
     for (int gg = 0; gg < NG; ++gg) {
-      if (DEBUG) {
-        if (bh == a.dbg_bh && qrow >= a.dbg_row0 && qrow < a.dbg_row0 + a.dbg_rows && a.dbg_s) {
-          const size_t rowo = static_cast<size_t>(qrow - a.dbg_row0);
-#pragma unroll
-          for (int c2 = 0; c2 < 2; ++c2)
-#pragma unroll
-            for (int r = 0; r < 16; ++r) {
-              const int key = key0 + (2 * gg + c2) * 32 + 8 * (r >> 2) + 4 * hh + (r & 3);
-              if (key < N) a.dbg_s[rowo * N + key] = static_cast<int32_t>(s[2 * gg + c2][r]);
-            }
-        }
-      }
 #pragma unroll
       for (int c2 = 0; c2 < 2; ++c2) {
         const int ch = 2 * gg + c2;
 #pragma unroll
         for (int r = 0; r < 16; ++r) {
-          float c;
-          if (KTOK) c = __fmul_rn(cq, sKs[buf][ch * 32 + 8 * (r >> 2) + 4 * hh + (r & 3)]);
-          else c = cch[ch];
-          float P = __builtin_amdgcn_exp2f(__fmaf_rn(s[ch][r], c, -mq));   // pscale * P
+          float P;   // pscale * P
+          if (QB) {
+            P = __builtin_amdgcn_exp2f(__fsub_rn(s[ch][r], mq));
+          } else {
+            float c;
+            if (KTOK) c = __fmul_rn(cq, sKs[buf][ch * 32 + 8 * (r >> 2) + 4 * hh + (r & 3)]);
+            else c = cch[ch];
+            P = __builtin_amdgcn_exp2f(__fmaf_rn(s[ch][r], c, -mq));
+          }
           if (MASKED && s[ch][r] == -INFINITY) P = 0.f;
           if (gg == 0 && c2 == 0 && r < 4) ls[r] = P;
           else ls[r & 3] += P;
@@ -475,11 +508,16 @@ __global__ __launch_bounds__(kThreads, 8 / kWaves) void k_attn_e2m3(AttnArgs a) 
   }
 }
 
+template <int KV, bool KTOK, bool SYM7, bool DEBUG, bool QB>
+hipError_t launch_b(const AttnArgs& a, hipStream_t s) {
+  const dim3 grid((a.Npad + kBlockM - 1) / kBlockM, a.BH);
+  hipLaunchKernelGGL((k_attn_e2m3<KV, KTOK, SYM7, DEBUG, QB>), grid, dim3(kThreads), 0, s, a);
+  return hipGetLastError();
+}
+
 template <int KV, bool KTOK, bool SYM7, bool DEBUG>
 hipError_t launch_t(const AttnArgs& a, hipStream_t s) {
-  const dim3 grid((a.Npad + kBlockM - 1) / kBlockM, a.BH);
-  hipLaunchKernelGGL((k_attn_e2m3<KV, KTOK, SYM7, DEBUG>), grid, dim3(kThreads), 0, s, a);
-  return hipGetLastError();
+  return a.kbias ? launch_b<KV, KTOK, SYM7, DEBUG, true>(a, s) : launch_b<KV, KTOK, SYM7, DEBUG, false>(a, s);
 }
 
 template <int KV, bool KTOK, bool SYM7>

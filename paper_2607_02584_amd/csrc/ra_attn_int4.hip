@@ -9,7 +9,9 @@
 //                                              P~ = u - 8, fixed scale 15)
 //   l      = alpha * l + sum P,  alpha = 2^(m_i,j-1 - m_ij)
 //   O      = alpha * O + sum_g fl(s_v[g]/15) * (u . V~)
-// and writes O / l + mu_v.
+// and writes O / l + mu_v.  With Q smoothing every key j carries the score
+// bias fl(b_j Kc): t = fma(S, c, bias_j) replaces fl(S c) in the maximum and
+// x = t - m.
 //
 // Matrix-core mapping (v_mfma_i32_32x32x32_i8, one wave = 32 queries):
 //   S^T = K Q^T : A = K tile (32 keys x 32 channels), B = Q^T, so every lane
@@ -82,13 +84,14 @@ __device__ __forceinline__ void stage_store(const Stage<KV>& st, uint8_t* sk, ui
   }
 }
 
-template <int KV, bool KTOK, bool SYM7, bool DEBUG>
+template <int KV, bool KTOK, bool SYM7, bool DEBUG, bool QB>
 __global__ __launch_bounds__(256, 1) void k_attn_int4(AttnArgs a) {
   constexpr int NCH = KV / 32;
   __shared__ __align__(16) uint8_t sK[2][KV * 128];
   __shared__ __align__(16) uint8_t sV[2][KV * 128];
   __shared__ __align__(16) float sDq[2][kD];
   __shared__ __align__(16) float sKs[2][KTOK ? KV : 1];
+  __shared__ __align__(16) float sB[2][QB ? KV : 1];   // per-key score bias fl(b Kc)
 
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int hh = lane >> 5, j = lane & 31;
@@ -125,6 +128,7 @@ __global__ __launch_bounds__(256, 1) void k_attn_int4(AttnArgs a) {
     if (KTOK && tid < KV) {
       sKs[buf][tid] = a.ks[static_cast<size_t>(bh) * kstride + jb * KV + tid];
     }
+    if (QB && tid < KV) sB[buf][tid] = __fmul_rn(a.kbias[static_cast<size_t>(bh) * a.Npad + jb * KV + tid], a.Kc);
   };
 
   float of[4][16];
@@ -163,7 +167,24 @@ __global__ __launch_bounds__(256, 1) void k_attn_int4(AttnArgs a) {
     // ---- block row maximum ----
     float c16[NCH];
     float tmax = -INFINITY;
-    if (!KTOK) {
+    float tb[QB ? NCH : 1][16];   // QB: t = fma(S, c, bias) per score
+    if (QB) {
+#pragma unroll
+      for (int ch = 0; ch < NCH; ++ch) {
+        if (!KTOK)
+          c16[ch] = __fmul_rn(__fmul_rn(cq, a.ks[static_cast<size_t>(bh) * kstride + (key0 + ch * 32) / a.k_group]),
+                              0.0625f);
+#pragma unroll
+        for (int r = 0; r < 16; ++r) {
+          const int kl = ch * 32 + 8 * (r >> 2) + 4 * hh + (r & 3);
+          const float c = KTOK ? __fmul_rn(__fmul_rn(cq, sKs[buf][kl]), 0.0625f) : c16[ch];
+          float t = __fmaf_rn(static_cast<float>(s[ch][r]), c, sB[buf][kl]);
+          if (last && key0 + kl >= N) t = -INFINITY;
+          tb[QB ? ch : 0][r] = t;
+          tmax = fmaxf(tmax, t);
+        }
+      }
+    } else if (!KTOK) {
 #pragma unroll
       for (int ch = 0; ch < NCH; ++ch) {
         const int kbase = key0 + ch * 32;
@@ -207,8 +228,13 @@ __global__ __launch_bounds__(256, 1) void k_attn_int4(AttnArgs a) {
         for (int t = 0; t < 4; ++t) {
           const int r = 4 * q + t;
           const int kl = ch * 32 + 8 * (r >> 2) + 4 * hh + (r & 3);
-          const float c = KTOK ? __fmul_rn(__fmul_rn(cq, sKs[buf][kl]), 0.0625f) : c16[ch];
-          const float x = __fmaf_rn(static_cast<float>(s[ch][r]), c, -mnew);
+          float x;
+          if (QB) {
+            x = __fsub_rn(tb[QB ? ch : 0][r], mnew);
+          } else {
+            const float c = KTOK ? __fmul_rn(__fmul_rn(cq, sKs[buf][kl]), 0.0625f) : c16[ch];
+            x = __fmaf_rn(static_cast<float>(s[ch][r]), c, -mnew);
+          }
           float P = __builtin_amdgcn_exp2f(x);
           if (last && key0 + kl >= N) P = 0.f;
           lsum += P;
@@ -302,11 +328,16 @@ __global__ __launch_bounds__(256, 1) void k_attn_int4(AttnArgs a) {
   }
 }
 
+template <int KV, bool KTOK, bool SYM7, bool DEBUG, bool QB>
+hipError_t launch_b(const AttnArgs& a, hipStream_t s) {
+  const dim3 grid(a.Npad / kBlockM, a.BH);
+  hipLaunchKernelGGL((k_attn_int4<KV, KTOK, SYM7, DEBUG, QB>), grid, dim3(256), 0, s, a);
+  return hipGetLastError();
+}
+
 template <int KV, bool KTOK, bool SYM7, bool DEBUG>
 hipError_t launch_t(const AttnArgs& a, hipStream_t s) {
-  const dim3 grid(a.Npad / kBlockM, a.BH);
-  hipLaunchKernelGGL((k_attn_int4<KV, KTOK, SYM7, DEBUG>), grid, dim3(256), 0, s, a);
-  return hipGetLastError();
+  return a.kbias ? launch_b<KV, KTOK, SYM7, DEBUG, true>(a, s) : launch_b<KV, KTOK, SYM7, DEBUG, false>(a, s);
 }
 
 template <int KV, bool KTOK, bool SYM7>

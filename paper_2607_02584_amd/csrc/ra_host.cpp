@@ -59,7 +59,8 @@ int validate(const ra_params* p) {
       if (!std::isfinite(p->rot_blocks[i])) return fail(RA_ERR_INVALID, "rot_blocks must be finite");
   }
   if (p->p_quant != RA_PQ_RANGE15 && p->p_quant != RA_PQ_SYM7) return fail(RA_ERR_INVALID, "unknown p_quant");
-  if (p->smooth < 0 || p->smooth > (RA_SMOOTH_K | RA_SMOOTH_V)) return fail(RA_ERR_INVALID, "unknown smooth flags");
+  if (p->smooth < 0 || p->smooth > (RA_SMOOTH_K | RA_SMOOTH_V | RA_SMOOTH_Q))
+    return fail(RA_ERR_INVALID, "unknown smooth flags");
   if (p->q_group < 1 || p->q_group > 128 || (128 % p->q_group) != 0)
     return fail(RA_ERR_UNSUPPORTED, "q_group must divide 128");
   if (p->k_group != 1 && p->k_group != 32 && p->k_group != 64 && p->k_group != 128)
@@ -79,7 +80,7 @@ int validate(const ra_params* p) {
 
 struct Sizes {
   int64_t BH, Npad, ntiles, nvgroups;
-  size_t codes, qscale, kscale, vscale, mu, partial, amax;
+  size_t codes, qscale, kscale, vscale, mu, partial, amax, kbias;
 };
 
 Sizes sizes_of(const ra_params* p) {
@@ -95,6 +96,7 @@ Sizes sizes_of(const ra_params* p) {
   s.mu = static_cast<size_t>(s.BH * kD);
   s.partial = static_cast<size_t>(s.BH * kD);
   s.amax = s.vscale;
+  s.kbias = static_cast<size_t>(s.BH * s.Npad);
   return s;
 }
 
@@ -103,8 +105,11 @@ Sizes sizes_of(const ra_params* p) {
 struct Int4Ws {
   double* ksum;
   double* vsum;
+  double* qsum;
   float* mu_k;
   float* mu_v;
+  float* mu_q;
+  float* kbias;
   uint32_t* amax;
   uint8_t* qc;
   uint8_t* kc;
@@ -127,8 +132,11 @@ Int4Ws carve_int4(const ra_params* p, void* base) {
   };
   w.ksum = reinterpret_cast<double*>(take(s.partial * sizeof(double)));
   w.vsum = reinterpret_cast<double*>(take(s.partial * sizeof(double)));
+  w.qsum = reinterpret_cast<double*>(take(s.partial * sizeof(double)));
   w.mu_k = reinterpret_cast<float*>(take(s.mu * sizeof(float)));
   w.mu_v = reinterpret_cast<float*>(take(s.mu * sizeof(float)));
+  w.mu_q = reinterpret_cast<float*>(take(s.mu * sizeof(float)));
+  w.kbias = reinterpret_cast<float*>(take((p->smooth & RA_SMOOTH_Q) ? s.kbias * sizeof(float) : 0));
   w.amax = reinterpret_cast<uint32_t*>(take(s.amax * sizeof(uint32_t)));
   w.qc = reinterpret_cast<uint8_t*>(take(s.codes));
   w.kc = reinterpret_cast<uint8_t*>(take(s.codes));
@@ -274,7 +282,7 @@ float kc_of(const ra_params* p) {
 hipStream_t st(void* s) { return static_cast<hipStream_t>(s); }
 
 int qk_impl(const ra_params* p, const void* q, const void* k, uint8_t* qc, float* qs, uint8_t* kc, float* ks,
-            float* mu_k, const Int4Ws& w, hipStream_t s) {
+            float* mu_k, float* mu_q, float* kbias, const Int4Ws& w, hipStream_t s) {
   const Sizes z = sizes_of(p);
   ra::RopeTables t;
   int rc = get_tables(p, &t);
@@ -295,19 +303,33 @@ int qk_impl(const ra_params* p, const void* q, const void* k, uint8_t* qc, float
   } else if (mu_k) {
     RA_CHECK_HIP(ra::launch_fill_zero_u32(reinterpret_cast<uint32_t*>(mu_k), static_cast<int64_t>(z.mu), s));
   }
+  const bool center_q = (p->smooth & RA_SMOOTH_Q) != 0;
+  if (center_q) {
+    RA_CHECK_HIP(ra::launch_fill_zero_u32(reinterpret_cast<uint32_t*>(w.qsum), static_cast<int64_t>(2 * z.partial), s));
+    ra::QkArgs aq = a;
+    aq.sums = w.qsum;
+    aq.x = static_cast<const uint16_t*>(q);
+    RA_CHECK_HIP(ra::launch_qk_sums(t, aq, static_cast<int>(z.BH), s));
+  } else if (mu_q) {
+    RA_CHECK_HIP(ra::launch_fill_zero_u32(reinterpret_cast<uint32_t*>(mu_q), static_cast<int64_t>(z.mu), s));
+  }
   a.x = static_cast<const uint16_t*>(q);
   a.codes = qc;
   a.scales = qs;
-  a.center = 0;
-  a.mu_out = nullptr;
+  a.sums = w.qsum;
+  a.center = center_q;
+  a.mu_out = center_q ? (mu_q ? mu_q : w.mu_q) : nullptr;
   a.group = p->q_group;
   RA_CHECK_HIP(ra::launch_qk_quant(t, a, static_cast<int>(z.BH), s));
   a.x = static_cast<const uint16_t*>(k);
   a.codes = kc;
   a.scales = ks;
+  a.sums = w.ksum;
   a.center = center;
   a.mu_out = center ? mu : nullptr;
   a.group = p->k_group;
+  a.qsums = center_q ? w.qsum : nullptr;
+  a.bias = center_q ? kbias : nullptr;
   RA_CHECK_HIP(ra::launch_qk_quant(t, a, static_cast<int>(z.BH), s));
   return RA_OK;
 }
@@ -345,8 +367,8 @@ int v_impl(const ra_params* p, const void* v, uint8_t* vc, float* vs, float* mu_
 }
 
 int attn_impl(const ra_params* p, const uint8_t* qc, const float* qs, const uint8_t* kc, const float* ks,
-              const uint8_t* vc, const float* vs, const float* mu_v, void* o, bool debug, int bh, int row0, int rows,
-              int32_t* s_out, uint8_t* u_out, float* m_out, hipStream_t s) {
+              const uint8_t* vc, const float* vs, const float* mu_v, const float* kbias, void* o, bool debug, int bh,
+              int row0, int rows, int32_t* s_out, uint8_t* u_out, float* m_out, hipStream_t s) {
   const Sizes z = sizes_of(p);
   ra::AttnArgs a{};
   a.qc = qc;
@@ -356,6 +378,7 @@ int attn_impl(const ra_params* p, const uint8_t* qc, const float* qs, const uint
   a.vc = vc;
   a.vs = vs;
   a.mu_v = mu_v;
+  a.kbias = (p->smooth & RA_SMOOTH_Q) ? kbias : nullptr;
   a.o = o;
   a.N = p->N;
   a.Npad = static_cast<int>(z.Npad);
@@ -432,6 +455,7 @@ int rotate_attn_layout(const ra_params* p, ra_layout* out) {
   out->v_code_bytes = static_cast<int64_t>(s.codes);
   out->v_scale_count = static_cast<int64_t>(s.vscale);
   out->mu_count = static_cast<int64_t>(s.mu);
+  out->k_bias_count = static_cast<int64_t>(s.kbias);
   return RA_OK;
 }
 
@@ -450,14 +474,16 @@ int rotate_attn_workspace_size(const ra_params* p, int path, size_t* bytes) {
 }
 
 int rotate_attn_quantize_qk(const ra_params* p, const void* q, const void* k, uint8_t* q_codes, float* q_scale,
-                            uint8_t* k_codes, float* k_scale, float* mu_k, void* workspace, size_t workspace_bytes,
-                            void* stream) {
+                            uint8_t* k_codes, float* k_scale, float* mu_k, float* mu_q, float* k_bias,
+                            void* workspace, size_t workspace_bytes, void* stream) {
   int rc = validate(p);
   if (rc) return rc;
   if (!q || !k || !q_codes || !q_scale || !k_codes || !k_scale) return fail(RA_ERR_INVALID, "NULL tensor pointer");
+  if ((p->smooth & RA_SMOOTH_Q) && !k_bias) return fail(RA_ERR_INVALID, "RA_SMOOTH_Q needs k_bias");
   const Int4Ws need = carve_int4(p, nullptr);
   if ((rc = check_ws(workspace, workspace_bytes, need.total))) return rc;
-  return qk_impl(p, q, k, q_codes, q_scale, k_codes, k_scale, mu_k, carve_int4(p, workspace), st(stream));
+  return qk_impl(p, q, k, q_codes, q_scale, k_codes, k_scale, mu_k, mu_q, k_bias, carve_int4(p, workspace),
+                 st(stream));
 }
 
 int rotate_attn_quantize_v(const ra_params* p, const void* v, uint8_t* v_codes, float* v_scale, float* mu_v,
@@ -472,27 +498,30 @@ int rotate_attn_quantize_v(const ra_params* p, const void* v, uint8_t* v_codes, 
 
 int rotate_attn_attn_int4(const ra_params* p, const uint8_t* q_codes, const float* q_scale, const uint8_t* k_codes,
                           const float* k_scale, const uint8_t* v_codes, const float* v_scale, const float* mu_v,
-                          void* o, void* stream) {
+                          const float* k_bias, void* o, void* stream) {
   int rc = validate(p);
   if (rc) return rc;
   if (!q_codes || !q_scale || !k_codes || !k_scale || !v_codes || !v_scale || !o)
     return fail(RA_ERR_INVALID, "NULL tensor pointer");
-  return attn_impl(p, q_codes, q_scale, k_codes, k_scale, v_codes, v_scale, mu_v, o, false, 0, 0, 0, nullptr, nullptr,
-                   nullptr, st(stream));
+  if ((p->smooth & RA_SMOOTH_Q) && !k_bias) return fail(RA_ERR_INVALID, "RA_SMOOTH_Q needs k_bias");
+  return attn_impl(p, q_codes, q_scale, k_codes, k_scale, v_codes, v_scale, mu_v, k_bias, o, false, 0, 0, 0, nullptr,
+                   nullptr, nullptr, st(stream));
 }
 
 int rotate_attn_attn_int4_debug(const ra_params* p, const uint8_t* q_codes, const float* q_scale,
                                 const uint8_t* k_codes, const float* k_scale, const uint8_t* v_codes,
-                                const float* v_scale, const float* mu_v, void* o, int32_t bh, int32_t row0,
-                                int32_t rows, int32_t* s_out, uint8_t* u_out, float* m_out, void* stream) {
+                                const float* v_scale, const float* mu_v, const float* k_bias, void* o, int32_t bh,
+                                int32_t row0, int32_t rows, int32_t* s_out, uint8_t* u_out, float* m_out,
+                                void* stream) {
   int rc = validate(p);
   if (rc) return rc;
   if (!q_codes || !q_scale || !k_codes || !k_scale || !v_codes || !v_scale || !o)
     return fail(RA_ERR_INVALID, "NULL tensor pointer");
+  if ((p->smooth & RA_SMOOTH_Q) && !k_bias) return fail(RA_ERR_INVALID, "RA_SMOOTH_Q needs k_bias");
   if (bh < 0 || static_cast<int64_t>(bh) >= static_cast<int64_t>(p->B) * p->H) return fail(RA_ERR_INVALID, "bh out of range");
   if (row0 < 0 || rows < 0 || static_cast<int64_t>(row0) + rows > p->N) return fail(RA_ERR_INVALID, "rows out of range");
-  return attn_impl(p, q_codes, q_scale, k_codes, k_scale, v_codes, v_scale, mu_v, o, true, bh, row0, rows, s_out,
-                   u_out, m_out, st(stream));
+  return attn_impl(p, q_codes, q_scale, k_codes, k_scale, v_codes, v_scale, mu_v, k_bias, o, true, bh, row0, rows,
+                   s_out, u_out, m_out, st(stream));
 }
 
 int rotate_attn_fwd_int4(const ra_params* p, const void* q, const void* k, const void* v, void* o, void* workspace,
@@ -503,10 +532,10 @@ int rotate_attn_fwd_int4(const ra_params* p, const void* q, const void* k, const
   const Int4Ws need = carve_int4(p, nullptr);
   if ((rc = check_ws(workspace, workspace_bytes, need.total))) return rc;
   const Int4Ws w = carve_int4(p, workspace);
-  if ((rc = qk_impl(p, q, k, w.qc, w.qs, w.kc, w.ks, nullptr, w, st(stream)))) return rc;
+  if ((rc = qk_impl(p, q, k, w.qc, w.qs, w.kc, w.ks, nullptr, nullptr, w.kbias, w, st(stream)))) return rc;
   if ((rc = v_impl(p, v, w.vc, w.vs, nullptr, w, st(stream)))) return rc;
   const float* mu = (p->smooth & RA_SMOOTH_V) ? w.mu_v : nullptr;
-  return attn_impl(p, w.qc, w.qs, w.kc, w.ks, w.vc, w.vs, mu, o, false, 0, 0, 0, nullptr, nullptr, nullptr,
+  return attn_impl(p, w.qc, w.qs, w.kc, w.ks, w.vc, w.vs, mu, w.kbias, o, false, 0, 0, 0, nullptr, nullptr, nullptr,
                    st(stream));
 }
 

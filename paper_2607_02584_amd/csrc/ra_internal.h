@@ -35,6 +35,10 @@ struct QkArgs {
   int center;             // quant pass: subtract the mean derived from sums
   int N, Npad, group, is_fp16;
   int e2m3;               // 1: write the E2M3 container, 0: the INT4 nibble container
+  // K pass with Q smoothing: the Q fixed-point sums (mu_Q) and the per-key
+  // score bias output [BH][Npad]; both nullptr otherwise
+  const double* qsums;
+  float* bias;
 };
 
 struct VArgs {
@@ -57,6 +61,7 @@ struct AttnArgs {
   const uint8_t* vc;
   const float* vs;
   const float* mu_v;      // [BH][128] or nullptr
+  const float* kbias;     // [BH][Npad] per-key score bias (Q smoothing) or nullptr
   void* o;
   int N, Npad, BH;
   int q_group, k_group, v_group, nvgroups;
@@ -91,6 +96,7 @@ hipError_t launch_attn_int4(const AttnArgs& a, int kv_block, bool k_per_token, b
                             hipStream_t s);
 hipError_t launch_attn_e2m3(const AttnArgs& a, int kv_block, bool k_per_token, bool sym7, bool debug,
                             hipStream_t s);
+// (both launchers pick the key-bias variant when a.kbias is set)
 hipError_t launch_rope16(const RopeTables& t, const uint16_t* x, uint16_t* out, int BH, int N, int Npad,
                          int is_fp16, hipStream_t s);
 hipError_t launch_v16_relayout(const uint16_t* v, uint16_t* out, int BH, int N, int Npad, hipStream_t s);

@@ -11,7 +11,8 @@
 //    Kronecker recursion, widest stride first -- the sums and differences of
 //    channels c and c + 64, then c and c + 32 inside each half, ... down to
 //    adjacent channels -- unscaled, then one multiply by fl32(1/sqrt 128).
-//  * Smoothing (Sec. 4): per-channel means over the tokens of a head.  Each
+//  * Smoothing (Sec. 4): per-channel means over the tokens of a head (K, V,
+//    and Q, whose mean returns as the per-key score bias mu_Q . K_j).  Each
 //    value is scaled by 2^20, clamped to +-2^32 and rounded to an integer; the
 //    integers are summed in binary64, which is exact (every partial sum is an
 //    integer of magnitude at most 2^32 * N <= 2^53), so the sum does not depend
@@ -270,6 +271,20 @@ __global__ __launch_bounds__(256) void k_qk_quant(RopeTables t, QkArgs a) {
         z[p][2] = __fsub_rn(z[p][2], m.z);
         z[p][3] = __fsub_rn(z[p][3], m.w);
       }
+    }
+  }
+  if (a.bias) {
+    // Q smoothing: per-key score bias b = mu_Q . z (z = this K row after its
+    // own smoothing), products in binary32, summed pairwise over the channel
+    // range: the thread's (c0 + c1) + (c2 + c3), then lanes 1, 2, 4, 8, 16
+    // apart (blocks of 8, 16, ..., 128 channels).  Padded rows give 0.
+    const float4 mq = mean4(a.qsums + static_cast<size_t>(bh) * kD, a.N, cl);
+    for (int p = 0; p < 16; ++p) {
+      float b = __fadd_rn(__fadd_rn(__fmul_rn(mq.x, z[p][0]), __fmul_rn(mq.y, z[p][1])),
+                          __fadd_rn(__fmul_rn(mq.z, z[p][2]), __fmul_rn(mq.w, z[p][3])));
+#pragma unroll
+      for (int off = 1; off <= 16; off <<= 1) b = __fadd_rn(b, __shfl_xor(b, off, 32));
+      if (cl == 0) a.bias[static_cast<size_t>(bh) * a.Npad + tile * kTile + p * 8 + rr] = b;
     }
   }
   // row abs-max over the 128 channels (32 threads of the row)

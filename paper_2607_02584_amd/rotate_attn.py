@@ -17,7 +17,7 @@ LIB_PATH = os.path.join(HERE, "librotate_attn.so")
 
 ROT_NONE, ROT_INTERLEAVED, ROT_HALF, ROT_HADAMARD = 0, 1, 2, 3
 PQ_RANGE15, PQ_SYM7 = 0, 1
-SMOOTH_K, SMOOTH_V = 1, 2
+SMOOTH_K, SMOOTH_V, SMOOTH_Q = 1, 2, 4
 BF16, FP16, FP32 = 0, 1, 2
 CODES_INT4, CODES_E2M3 = 0, 1
 PATH_INT4, PATH_FP16 = 0, 1
@@ -44,7 +44,7 @@ class Params(ctypes.Structure):
 class Layout(ctypes.Structure):
     _fields_ = [("n_pad", ctypes.c_int64), ("qk_code_bytes", ctypes.c_int64), ("q_scale_count", ctypes.c_int64),
                 ("k_scale_count", ctypes.c_int64), ("v_code_bytes", ctypes.c_int64),
-                ("v_scale_count", ctypes.c_int64), ("mu_count", ctypes.c_int64)]
+                ("v_scale_count", ctypes.c_int64), ("mu_count", ctypes.c_int64), ("k_bias_count", ctypes.c_int64)]
 
 
 _lib = None
@@ -62,10 +62,10 @@ def lib():
         sig = {
             "rotate_attn_layout": [PP, ctypes.POINTER(Layout)],
             "rotate_attn_workspace_size": [PP, ctypes.c_int, ctypes.POINTER(ctypes.c_size_t)],
-            "rotate_attn_quantize_qk": [PP, P, P, P, P, P, P, P, P, ctypes.c_size_t, P],
+            "rotate_attn_quantize_qk": [PP, P, P, P, P, P, P, P, P, P, P, ctypes.c_size_t, P],
             "rotate_attn_quantize_v": [PP, P, P, P, P, P, ctypes.c_size_t, P],
-            "rotate_attn_attn_int4": [PP, P, P, P, P, P, P, P, P, P],
-            "rotate_attn_attn_int4_debug": [PP, P, P, P, P, P, P, P, P, ctypes.c_int32, ctypes.c_int32,
+            "rotate_attn_attn_int4": [PP, P, P, P, P, P, P, P, P, P, P],
+            "rotate_attn_attn_int4_debug": [PP, P, P, P, P, P, P, P, P, P, ctypes.c_int32, ctypes.c_int32,
                                             ctypes.c_int32, P, P, P, P],
             "rotate_attn_fwd_int4": [PP, P, P, P, P, P, ctypes.c_size_t, P],
             "rotate_attn_prepare_fp16": [PP, P, P, P, P, ctypes.c_size_t, P],
@@ -141,10 +141,10 @@ def _nbytes(t) -> int:
     return t.numel() * t.element_size()
 
 
-def quantize_qk(p, q, k, q_codes, q_scale, k_codes, k_scale, mu_k, ws, stream=None):
+def quantize_qk(p, q, k, q_codes, q_scale, k_codes, k_scale, mu_k, ws, stream=None, mu_q=None, k_bias=None):
     _check(lib().rotate_attn_quantize_qk(ctypes.byref(p), _ptr(q), _ptr(k), _ptr(q_codes), _ptr(q_scale),
-                                         _ptr(k_codes), _ptr(k_scale), _ptr(mu_k), _ptr(ws), _nbytes(ws),
-                                         _stream(stream)), "rotate_attn_quantize_qk")
+                                         _ptr(k_codes), _ptr(k_scale), _ptr(mu_k), _ptr(mu_q), _ptr(k_bias),
+                                         _ptr(ws), _nbytes(ws), _stream(stream)), "rotate_attn_quantize_qk")
 
 
 def quantize_v(p, v, v_codes, v_scale, mu_v, ws, stream=None):
@@ -152,16 +152,17 @@ def quantize_v(p, v, v_codes, v_scale, mu_v, ws, stream=None):
                                         _ptr(ws), _nbytes(ws), _stream(stream)), "rotate_attn_quantize_v")
 
 
-def attn_int4(p, q_codes, q_scale, k_codes, k_scale, v_codes, v_scale, mu_v, o, stream=None):
+def attn_int4(p, q_codes, q_scale, k_codes, k_scale, v_codes, v_scale, mu_v, o, stream=None, k_bias=None):
     _check(lib().rotate_attn_attn_int4(ctypes.byref(p), _ptr(q_codes), _ptr(q_scale), _ptr(k_codes), _ptr(k_scale),
-                                       _ptr(v_codes), _ptr(v_scale), _ptr(mu_v), _ptr(o), _stream(stream)),
-           "rotate_attn_attn_int4")
+                                       _ptr(v_codes), _ptr(v_scale), _ptr(mu_v), _ptr(k_bias), _ptr(o),
+                                       _stream(stream)), "rotate_attn_attn_int4")
 
 
 def attn_int4_debug(p, q_codes, q_scale, k_codes, k_scale, v_codes, v_scale, mu_v, o, bh, row0, rows,
-                    s_out=None, u_out=None, m_out=None, stream=None):
+                    s_out=None, u_out=None, m_out=None, stream=None, k_bias=None):
     _check(lib().rotate_attn_attn_int4_debug(ctypes.byref(p), _ptr(q_codes), _ptr(q_scale), _ptr(k_codes),
-                                             _ptr(k_scale), _ptr(v_codes), _ptr(v_scale), _ptr(mu_v), _ptr(o),
+                                             _ptr(k_scale), _ptr(v_codes), _ptr(v_scale), _ptr(mu_v),
+                                             _ptr(k_bias), _ptr(o),
                                              bh, row0, rows, _ptr(s_out), _ptr(u_out), _ptr(m_out),
                                              _stream(stream)), "rotate_attn_attn_int4_debug")
 
@@ -206,6 +207,8 @@ def alloc_int4(p: Params, device="cuda"):
         v_scale=torch.zeros(L["v_scale_count"], dtype=torch.float32, device=device),
         mu_k=torch.zeros(L["mu_count"], dtype=torch.float32, device=device),
         mu_v=torch.zeros(L["mu_count"], dtype=torch.float32, device=device),
+        mu_q=torch.zeros(L["mu_count"], dtype=torch.float32, device=device),
+        k_bias=torch.zeros(L["k_bias_count"], dtype=torch.float32, device=device),
     )
 
 

@@ -49,7 +49,7 @@ def _base(ra, **kw):
     ("rope_theta", 0.0, -1),
     ("rotation", 4, -1),
     ("p_quant", 5, -1),
-    ("smooth", 4, -1),
+    ("smooth", 8, -1),
     ("q_group", 3, -2),
     ("k_group", 16, -2),
     ("kv_block", 32, -2),
@@ -99,8 +99,17 @@ def test_null_pointers_and_workspace_errors_before_gpu():
     assert st == -3  # misaligned
     st = L.rotate_attn_fwd_fp16(ctypes.byref(p), fake, fake, fake, fake, P(0x1000), 16, None)
     assert st == -3  # too small
-    st = L.rotate_attn_attn_int4_debug(ctypes.byref(p), fake, fake, fake, fake, fake, fake, None, fake, 5, 0, 1,
-                                       None, None, None, None)
+    st = L.rotate_attn_attn_int4_debug(ctypes.byref(p), fake, fake, fake, fake, fake, fake, None, None, fake, 5, 0,
+                                       1, None, None, None, None)
     assert st == -1  # bh out of range
+    # Q smoothing needs the per-key bias buffer on both sides
+    pq = _base(ra, smooth=ra.SMOOTH_K | ra.SMOOTH_V | ra.SMOOTH_Q)
+    st = L.rotate_attn_quantize_qk(ctypes.byref(pq), fake, fake, fake, fake, fake, fake, None, None, None, fake,
+                                   1 << 30, None)
+    assert st == -1 and b"k_bias" in L.rotate_attn_last_error()
+    st = L.rotate_attn_attn_int4(ctypes.byref(pq), fake, fake, fake, fake, fake, fake, None, None, fake, None)
+    assert st == -1 and b"k_bias" in L.rotate_attn_last_error()
+    assert ra.layout(pq)["k_bias_count"] == 2 * 1024
+    assert ra.workspace_size(pq, ra.PATH_INT4) >= ra.workspace_size(p, ra.PATH_INT4) + 2 * 1024 * 4
     assert L.rotate_attn_error_string(-4) == b"HIP runtime error"
     assert L.rotate_attn_fwd_int4(None, fake, fake, fake, fake, fake, 1 << 30, None) == -1

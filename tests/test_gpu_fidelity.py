@@ -6,7 +6,8 @@ over sampled query rows of the 1024-token case (all rows) and of the
 32760-token layer (two heads, three row blocks each), for the INT4 path with
 each rotation (none, merged interleaved, half, full Hadamard), the SYM7 P mapping (the
 "without range-optimized P" ablation of the paper's Table 1), the paper's
-per-token Q/K scales, and the BF16 fallback.
+per-token Q/K scales, Q smoothing with its per-key bias, no smoothing at all,
+and the BF16 fallback.
 
 The paper gives no per-layer attention accuracy to compare with (its Table 1
 is video-level), so these numbers are reported, not pinned ("parity
@@ -20,13 +21,15 @@ import pytest
 pytestmark = pytest.mark.gpu
 
 VARIANTS = [
-    # name, rotation, p_quant, q/k group
-    ("int4 none", 0, 0, 128),
-    ("int4 interleaved", 1, 0, 128),
-    ("int4 half", 2, 0, 128),
-    ("int4 full hadamard", 3, 0, 128),
-    ("int4 interleaved SYM7", 1, 1, 128),
-    ("int4 interleaved per-token", 1, 0, 1),
+    # name, rotation, p_quant, q/k group, smoothing flags
+    ("int4 none", 0, 0, 128, 3),
+    ("int4 interleaved", 1, 0, 128, 3),
+    ("int4 half", 2, 0, 128, 3),
+    ("int4 full hadamard", 3, 0, 128, 3),
+    ("int4 interleaved SYM7", 1, 1, 128, 3),
+    ("int4 interleaved per-token", 1, 0, 1, 3),
+    ("int4 interleaved Q smoothing", 1, 0, 128, 7),
+    ("int4 interleaved no smoothing", 1, 0, 128, 0),
 ]
 
 
@@ -59,9 +62,10 @@ def test_fidelity_to_fp64_attention(ora, wname):
     refs = [ora.ref_head(geo, q[0, h], k[0, h], v[0, h], rows=(r0, nr)) for h, r0, nr in samples]
     qd, kd, vd = (ra.to_device_bits(x) for x in (q, k, v))
     results = {}
-    for name, rot, pq, g in VARIANTS:
+    for name, rot, pq, g, sm in VARIANTS:
         p = ra.make_params(w.B, w.H, (w.T, w.Hg, w.W), w.split, w.theta, rotation=rot, p_quant=pq, q_group=g,
-                           k_group=g, v_group=128, kv_block=128, out_dtype=ra.FP32, code_format=ra.CODES_E2M3)
+                           k_group=g, v_group=128, kv_block=128, smooth=sm, out_dtype=ra.FP32,
+                           code_format=ra.CODES_E2M3)
         ws = ra.workspace(p, ra.PATH_INT4)
         o = torch.empty((BH, N, 128), dtype=torch.float32, device="cuda")
         ra.fwd_int4(p, qd, kd, vd, o, ws)
@@ -86,5 +90,5 @@ def test_fidelity_to_fp64_attention(ora, wname):
     # channel pairs of Q and K, so the logits span hundreds and the INT4
     # per-block scales leave the ordinary channels with few levels
     assert table["bf16 fallback"][0] > 0.99
-    for name, _, _, _ in VARIANTS:
+    for name, *_ in VARIANTS:
         assert table[name][0] > 0.5, name

@@ -45,7 +45,7 @@ def _geo(ora, w):
 
 def _cfg(ora, rotation, qg, kg, vg, kv, pq=0, smooth=3):
     return ora.Int4Config(rotation=rotation, p_quant=pq, smooth_k=bool(smooth & 1), smooth_v=bool(smooth & 2),
-                          q_group=qg, k_group=kg, v_group=vg, kv_block=kv)
+                          smooth_q=bool(smooth & 4), q_group=qg, k_group=kg, v_group=vg, kv_block=kv)
 
 
 def _params(ra, w, rotation, qg, kg, vg, kv, pq=0, smooth=3, out=2, fmt=1):
@@ -66,14 +66,18 @@ def _tie_band(val, m, scale, kv, n):
     mq = m.astype(np.float32) - np.float32(math.log2(scale))
     err = np.nan_to_num(np.abs(mq.astype(np.float64) - (m64 - math.log2(scale))), nan=0.0)
     err_key = np.repeat(err, kv, axis=1)[:, :n]
-    return TIE_BAND + val * math.log(2.0) * err_key
+    # plus the binary32 rounding of the exponent argument itself on either side
+    # (|x| <= 5 wherever a code can be nonzero; it matters with the Q-smoothing
+    # bias, where x = t - m is a separate subtraction)
+    return TIE_BAND + val * math.log(2.0) * (err_key + 2.0 ** -21)
 
 
 def _run_quant(torch, ra, p, q, k, v):
     bufs = ra.alloc_int4(p)
     ws = ra.workspace(p, ra.PATH_INT4)
     qd, kd, vd = (ra.to_device_bits(x) for x in (q, k, v))
-    ra.quantize_qk(p, qd, kd, bufs["q_codes"], bufs["q_scale"], bufs["k_codes"], bufs["k_scale"], bufs["mu_k"], ws)
+    ra.quantize_qk(p, qd, kd, bufs["q_codes"], bufs["q_scale"], bufs["k_codes"], bufs["k_scale"], bufs["mu_k"], ws,
+                   mu_q=bufs["mu_q"], k_bias=bufs["k_bias"])
     ra.quantize_v(p, vd, bufs["v_codes"], bufs["v_scale"], bufs["mu_v"], ws)
     torch.cuda.synchronize()
     return bufs, (qd, kd, vd), ws
@@ -91,6 +95,8 @@ CASES = [
     (1, 1, 64, 10 ** 6, 64, 1, 3),
     (2, 128, 128, 256, 128, 0, 0),
     (3, 1, 128, 128, 128, 0, 3),
+    (1, 1, 1, 128, 128, 0, 7),       # Q smoothing with the per-key bias, per-token Q/K (the paper's setting)
+    (2, 128, 64, 10 ** 6, 64, 1, 5),  # Q and K smoothing, no V smoothing, kv_block 64, SYM7
 ]
 
 
@@ -149,18 +155,24 @@ def test_int4_codes_scores_and_output(ora, wname, case, fmt):
         assert np.array_equal(vs.view(np.uint32), refv["v_scale"].view(np.uint32))
         assert np.array_equal(h["mu_k"].reshape(BH, 128)[bh].view(np.uint32), ref["mu_k"].view(np.uint32))
         assert np.array_equal(h["mu_v"].reshape(BH, 128)[bh].view(np.uint32), refv["mu_v"].view(np.uint32))
+        assert np.array_equal(h["mu_q"].reshape(BH, 128)[bh].view(np.uint32), ref["mu_q"].view(np.uint32))
+        if sm & 4:
+            kb = h["k_bias"].reshape(BH, Np)[bh]
+            assert np.array_equal(kb[:N].view(np.uint32), ref["k_bias"].view(np.uint32)), "key bias mismatch"
+            assert not kb[N:].any()
 
     s_d = torch.zeros((N, N), dtype=torch.int32, device="cuda")
     u_d = torch.zeros((N, N), dtype=torch.uint8, device="cuda")
     m_d = torch.zeros((N, nb), dtype=torch.float32, device="cuda")
     o_plain = torch.empty_like(o_gpu)
     mu_v = bufs["mu_v"] if sm & 2 else None
+    kbias = bufs["k_bias"] if sm & 4 else None
     ra.attn_int4(p, bufs["q_codes"], bufs["q_scale"], bufs["k_codes"], bufs["k_scale"], bufs["v_codes"],
-                 bufs["v_scale"], mu_v, o_plain)
+                 bufs["v_scale"], mu_v, o_plain, k_bias=kbias)
     for bh in range(BH):
         b, hh = divmod(bh, w.H)
         ra.attn_int4_debug(p, bufs["q_codes"], bufs["q_scale"], bufs["k_codes"], bufs["k_scale"], bufs["v_codes"],
-                           bufs["v_scale"], mu_v, o_gpu, bh, 0, N, s_d, u_d, m_d)
+                           bufs["v_scale"], mu_v, o_gpu, bh, 0, N, s_d, u_d, m_d, k_bias=kbias)
         torch.cuda.synchronize()
         O_ref, d = ora.fwd_int4_head(geo, cfg, q[b, hh], k[b, hh], v[b, hh], dumps=True)
         S = s_d.cpu().numpy()

@@ -288,6 +288,7 @@ class Int4Config:
     smooth_k: bool = True
     smooth_v: bool = True
     smooth_q: bool = False
+    v_hadamard: bool = False   # online V Hadamard: V H before quantization, O H^T after
     q_group: int = 128
     k_group: int = 128
     v_group: int = 128
@@ -320,7 +321,11 @@ def quantize_qk_head(geo: Geometry, cfg: Int4Config, q_bf16, k_bf16):
 
 
 def quantize_v_head(cfg: Int4Config, v_bf16):
+    """Sec. 4.3 + Sec. 5.1 for one head: V (rotated by H online if asked, the
+    binary32 transform of Q/K's full rotation), V smoothing, per-group codes."""
     v = bf16_to_f32(v_bf16)
+    if cfg.v_hadamard:
+        v = hadamard_f32(v)
     if cfg.smooth_v:
         mu_v = mean_fixed(v)
         zv = center(v, mu_v)
@@ -343,8 +348,12 @@ def fwd_int4_head(geo: Geometry, cfg: Int4Config, q_bf16, k_bf16, v_bf16, rows=N
     if dumps:
         O, d = res
         inter.update(d)
-        return O, inter
-    return res, inter
+    else:
+        O = res
+    if cfg.v_hadamard:
+        # O' = P (V H) is the output in the rotated basis; O = O' H^T = O' H
+        O = hadamard_f64(O)
+    return O, inter
 
 
 def rope_bf16_head(geo: Geometry, x_bf16) -> np.ndarray:

@@ -363,6 +363,39 @@ def test_v_hadamard_commutes_with_smoothing():
     np.testing.assert_allclose((V - mu) @ H, V @ H - mu @ H, atol=1e-12)
 
 
+def test_online_v_hadamard_rotates_back(ora):
+    """Sec. 4.3: with V rotated by H before its INT4 quantization, the attention
+    output is in the rotated basis, O' = P (V H), and O = O' H^T = O' H.  With the
+    P rounding off, the oracle's result equals fp64 softmax attention over the
+    dequantised rotated V, rotated back by the Kronecker-built H (a dense product,
+    not the butterflies); without the rotation back the result is far off.  The
+    quantisation error measured in the original basis is that of V H (H is
+    orthogonal)."""
+    rng = np.random.default_rng(47)
+    N = 384
+    Q = rng.standard_normal((N, 128)).astype(np.float32)
+    K = rng.standard_normal((N, 128)).astype(np.float32)
+    V = rng.standard_normal((N, 128)).astype(np.float32)
+    V[:, [5, 77]] *= 40.0
+    qc, qs = ora.quant_tokens(Q, 1)
+    kc, ks = ora.quant_tokens(K, 1)
+    kw = dict(q_group=1, k_group=1, v_group=128, kv_block=128, p_quant=ora.PQ_NONE)
+    qd = qc.astype(np.float64) * qs[:, None]
+    kd = kc.astype(np.float64) * ks[:, None]
+    H = _sylvester(128)
+    vr = ora.hadamard_f32(V)
+    np.testing.assert_allclose(vr, V.astype(np.float64) @ H, rtol=0, atol=1e-4 * np.abs(V).max())
+    vch, vsh = ora.quant_v(vr, 128)
+    O_rot = ora.attn_int4(qc, qs, kc, ks, vch, vsh, **kw)
+    deq = vch.astype(np.float64) * vsh.astype(np.float64)[np.arange(N) // 128]
+    ref = ora.attn_ref_f64(qd, kd, deq) @ H
+    O = ora.hadamard_f64(O_rot)
+    assert np.abs(O - ref).max() <= 1e-5 * np.abs(ref).max()
+    assert np.linalg.norm(O_rot - ref) > 0.5 * np.linalg.norm(ref)
+    np.testing.assert_allclose(np.linalg.norm(deq @ H - V.astype(np.float64) @ H @ H),
+                               np.linalg.norm(deq - V.astype(np.float64) @ H), rtol=1e-9)
+
+
 # ---------------------------------------------------------- quantization ----
 
 def test_quant_handworked(ora):

@@ -86,6 +86,14 @@ extern "C" {
 #define RA_ROT_HADAMARD 3    /* "Full" rotation (Sec. 5.3 baseline): RoPE, then the orthonormal
                                 128x128 Sylvester-Hadamard matrix of Sec. 4.3; rot_blocks unused */
 
+/* V rotation (Sec. 4.3).  The paper folds the D x D Hadamard H into W_v and
+ * W_o offline, so V arrives already rotated (RA_VROT_NONE).  For callers that
+ * cannot change the weights, RA_VROT_HADAMARD rotates V online: quantize_v
+ * takes V H (the binary32 butterflies of RA_ROT_HADAMARD) and the INT4
+ * attention returns O = O' H^T, O' being the output in the rotated basis. */
+#define RA_VROT_NONE 0
+#define RA_VROT_HADAMARD 1
+
 /* quantization of P (Sec. 4.2.1) */
 #define RA_PQ_RANGE15 0 /* affine: fixed scale 15, zero-point -8, 16 levels */
 #define RA_PQ_SYM7 1    /* symmetric baseline: round(7 P), 8 levels */
@@ -128,6 +136,7 @@ typedef struct ra_params {
   int32_t in_dtype;        /* RA_BF16 | RA_FP16 */
   int32_t out_dtype;       /* RA_BF16 | RA_FP16 | RA_FP32 */
   int32_t code_format;     /* RA_CODES_*: container of the codes quantize_* write and attn_int4 reads */
+  int32_t v_rotation;      /* RA_VROT_*: how the INT4 path treats V (the fallback takes V as given) */
 } ra_params;
 
 /* Sizes of the caller-visible INT4 buffers for these parameters. */

@@ -16,7 +16,8 @@
 //   m_new = max(m, rowmax fl(S * c)),  P = 2^(S c - m_new),
 //   u = rint(15 P),  l = alpha l + sum P,  alpha = 2^(m - m_new),
 //   O' = O' * alpha * (w_old / w_new) + (u/8) V~   (w = V scale of the block's group)
-// and finally O = O' * 8 w / 15 / l + mu_v.  With Q smoothing every key j
+// and finally O = O' * 8 w / 15 / l + mu_v (rotated back by H when V was
+// rotated online, Sec. 4.3).  With Q smoothing every key j
 // carries the score bias fl(b_j Kc): the scores become t = fma(S, c, bias_j)
 // before the maximum, and 15 P = 2^(t - (m_new - log2 15)).  The factor 15 rides in the
 // exponent: 15 P = 2^fma(S, c, -(m_new - log2 15)), one exponential per score
@@ -495,11 +496,43 @@ __global__ __launch_bounds__(kThreads, 8 / kWaves) void k_attn_e2m3(AttnArgs a) 
   for (int r = 0; r < 16; ++r) {
     const int qi = 8 * (r >> 2) + 4 * hh + (r & 3);
     const float inv = 1.0f / __shfl(ltot, qi);
+#pragma unroll
+    for (int mt = 0; mt < 4; ++mt) of[mt][r] = of[mt][r] * wsc[mt] * inv + mu[mt];
+  }
+  if (a.vhad) {
+    // V came rotated by H: each query row goes back, O = O' H^T = O' H.  Channel
+    // 32 mt + j: strides 64 and 32 pair tiles mt ^ 2 and mt ^ 1 in the thread,
+    // strides 16 .. 1 pair lanes j ^ 16 .. j ^ 1 (the lane with the bit set
+    // takes the difference); then the factor 1/sqrt(128).
+#pragma unroll
+    for (int r = 0; r < 16; ++r) {
+      const float t0 = of[0][r] + of[2][r], t2 = of[0][r] - of[2][r];
+      const float t1 = of[1][r] + of[3][r], t3 = of[1][r] - of[3][r];
+      of[0][r] = t0 + t1;
+      of[1][r] = t0 - t1;
+      of[2][r] = t2 + t3;
+      of[3][r] = t2 - t3;
+#pragma unroll
+      for (int msk = 16; msk >= 1; msk >>= 1) {
+        const bool upper = (j & msk) != 0;
+#pragma unroll
+        for (int mt = 0; mt < 4; ++mt) {
+          const float o = __shfl_xor(of[mt][r], msk);
+          of[mt][r] = upper ? o - of[mt][r] : of[mt][r] + o;
+        }
+      }
+#pragma unroll
+      for (int mt = 0; mt < 4; ++mt) of[mt][r] *= kInvSqrtD;
+    }
+  }
+#pragma unroll
+  for (int r = 0; r < 16; ++r) {
+    const int qi = 8 * (r >> 2) + 4 * hh + (r & 3);
     if (q0 + qi < N) {
       const size_t obase = (static_cast<size_t>(bh) * N + q0 + qi) * kD + j;
 #pragma unroll
       for (int mt = 0; mt < 4; ++mt) {
-        const float v = of[mt][r] * wsc[mt] * inv + mu[mt];
+        const float v = of[mt][r];
         if (a.out_dtype == 2) static_cast<float*>(a.o)[obase + mt * 32] = v;
         else if (a.out_dtype == 0) static_cast<uint16_t*>(a.o)[obase + mt * 32] = __bfloat16_as_ushort(__float2bfloat16(v));
         else static_cast<uint16_t*>(a.o)[obase + mt * 32] = __half_as_ushort(__float2half(v));

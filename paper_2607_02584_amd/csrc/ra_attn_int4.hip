@@ -293,10 +293,50 @@ __global__ __launch_bounds__(256, 1) void k_attn_int4(AttnArgs a) {
     __syncthreads();
   }
 
-  // ---- epilogue: O / l + mu_v ----
+  // ---- epilogue: O / l + mu_v (rotated back by H when V was rotated online) ----
   const float ltot = l + __shfl_xor(l, 32);
-  if (qrow < N) {
+  {
     const float inv = 1.0f / ltot;
+#pragma unroll
+    for (int mt = 0; mt < 4; ++mt)
+#pragma unroll
+      for (int rq = 0; rq < 4; ++rq)
+#pragma unroll
+        for (int t = 0; t < 4; ++t) {
+          const int c = mt * 32 + 8 * rq + 4 * hh + t;
+          of[mt][4 * rq + t] = of[mt][4 * rq + t] * inv;
+          if (a.mu_v) of[mt][4 * rq + t] += a.mu_v[bh * kD + c];
+        }
+  }
+  if (a.vhad) {
+    // O = O' H^T = O' H per query row.  Element (mt, 4 rq + t) of lane half hh is
+    // channel 32 mt + 8 rq + 4 hh + t: strides 64, 32 (mt), 16, 8 (rq), 2, 1 (t)
+    // stay in the thread, stride 4 pairs the two lane halves.
+    float* f = &of[0][0];
+    auto level = [&](int st) {
+#pragma unroll
+      for (int i = 0; i < 64; ++i)
+        if (!(i & st)) {
+          const float x0 = f[i], x1 = f[i + st];
+          f[i] = x0 + x1;
+          f[i + st] = x0 - x1;
+        }
+    };
+    level(32);
+    level(16);
+    level(8);
+    level(4);
+#pragma unroll
+    for (int i = 0; i < 64; ++i) {
+      const float o = __shfl_xor(f[i], 32);
+      f[i] = hh ? o - f[i] : f[i] + o;
+    }
+    level(2);
+    level(1);
+#pragma unroll
+    for (int i = 0; i < 64; ++i) f[i] *= kInvSqrtD;
+  }
+  if (qrow < N) {
     const size_t obase = (static_cast<size_t>(bh) * N + qrow) * kD;
 #pragma unroll
     for (int mt = 0; mt < 4; ++mt)
@@ -305,10 +345,7 @@ __global__ __launch_bounds__(256, 1) void k_attn_int4(AttnArgs a) {
         const int c0 = mt * 32 + 8 * rq + 4 * hh;
         float v[4];
 #pragma unroll
-        for (int t = 0; t < 4; ++t) {
-          v[t] = of[mt][4 * rq + t] * inv;
-          if (a.mu_v) v[t] += a.mu_v[bh * kD + c0 + t];
-        }
+        for (int t = 0; t < 4; ++t) v[t] = of[mt][4 * rq + t];
         if (a.out_dtype == 2) {
           *reinterpret_cast<float4*>(static_cast<float*>(a.o) + obase + c0) = make_float4(v[0], v[1], v[2], v[3]);
         } else if (a.out_dtype == 0) {

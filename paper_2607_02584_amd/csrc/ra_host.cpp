@@ -75,6 +75,8 @@ int validate(const ra_params* p) {
     return fail(RA_ERR_INVALID, "code_format must be RA_CODES_INT4 or RA_CODES_E2M3");
   if (p->out_dtype != RA_BF16 && p->out_dtype != RA_FP16 && p->out_dtype != RA_FP32)
     return fail(RA_ERR_INVALID, "out_dtype must be BF16, FP16 or FP32");
+  if (p->v_rotation != RA_VROT_NONE && p->v_rotation != RA_VROT_HADAMARD)
+    return fail(RA_ERR_INVALID, "unknown v_rotation");
   return RA_OK;
 }
 
@@ -348,6 +350,7 @@ int v_impl(const ra_params* p, const void* v, uint8_t* vc, float* vs, float* mu_
   a.ngroups = static_cast<int>(z.nvgroups);
   a.is_fp16 = p->in_dtype == RA_FP16;
   a.e2m3 = p->code_format == RA_CODES_E2M3;
+  a.vhad = p->v_rotation == RA_VROT_HADAMARD;
   float* mu = mu_v ? mu_v : w.mu_v;
   if (p->smooth & RA_SMOOTH_V) {
     RA_CHECK_HIP(ra::launch_fill_zero_u32(reinterpret_cast<uint32_t*>(w.vsum), static_cast<int64_t>(2 * z.partial), s));
@@ -391,6 +394,7 @@ int attn_impl(const ra_params* p, const uint8_t* qc, const float* qs, const uint
   a.v_bpg = z.nvgroups > 1 ? p->v_group / p->kv_block : INT32_MAX;
   a.Kc = kc_of(p);
   a.out_dtype = p->out_dtype;
+  a.vhad = p->v_rotation == RA_VROT_HADAMARD;
   a.dbg_s = s_out;
   a.dbg_u = u_out;
   a.dbg_m = m_out;

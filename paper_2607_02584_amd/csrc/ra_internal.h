@@ -10,6 +10,7 @@ namespace ra {
 
 constexpr int kD = 128;       // head dimension
 constexpr int kTile = 128;    // producer token tile; Npad is a multiple of it
+constexpr float kInvSqrtD = 0.0883883476483184405501055452631f;  // fl32(1/sqrt(128))
 
 // RoPE/rotation tables on the device.  For axis a the table holds, for every
 // position pos in [0, extent_a) and pair k in [0, D_a/2), the binary32 2x2
@@ -51,6 +52,7 @@ struct VArgs {
   uint32_t* amax;         // [BH][ngroups][128] float bits (non-negative)
   int N, Npad, group, ngroups, is_fp16;
   int e2m3;
+  int vhad;               // rotate each V row by the 128-point Hadamard before smoothing
 };
 
 struct AttnArgs {
@@ -68,6 +70,7 @@ struct AttnArgs {
   int v_bpg;              // KV blocks per V scale group (v_group / kv_block; nvgroups == 1: any value >= nblocks)
   float Kc;               // fl32(sm_scale * log2(e))
   int out_dtype;
+  int vhad;               // V was rotated by H: rotate each output row back
   // debug dump (debug kernel only)
   int32_t* dbg_s;
   uint8_t* dbg_u;

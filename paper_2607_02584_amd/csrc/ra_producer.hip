@@ -113,8 +113,6 @@ __device__ __forceinline__ HalfSetup half_setup(const RopeTables& t, int cl) {
   return s;
 }
 
-constexpr float kInvSqrtD = 0.0883883476483184405501055452631f;  // fl32(1/sqrt(128))
-
 // y <- y H_128 for one row held by 32 lanes (lane cl holds channels 4cl..4cl+3):
 // strides 64..4 pair lanes whose cl differs in bit 4..0 (the lane with the bit
 // set takes the difference), strides 2 and 1 stay inside the thread.
@@ -366,23 +364,23 @@ __device__ __forceinline__ void load_v_tile(const VArgs& a, int bh, int tile, fl
   }
   for (int p = 0; p < 16; ++p) {
     const int n = tile * kTile + p * 8 + rr;
+    float x[4] = {0.f, 0.f, 0.f, 0.f};
     if (n < a.N) {
-      float x[4] = {h2f(static_cast<uint16_t>(raw[p].x & 0xffff), a.is_fp16),
-                    h2f(static_cast<uint16_t>(raw[p].x >> 16), a.is_fp16),
-                    h2f(static_cast<uint16_t>(raw[p].y & 0xffff), a.is_fp16),
-                    h2f(static_cast<uint16_t>(raw[p].y >> 16), a.is_fp16)};
-      if (a.center) {
-        x[0] = __fsub_rn(x[0], m.x);
-        x[1] = __fsub_rn(x[1], m.y);
-        x[2] = __fsub_rn(x[2], m.z);
-        x[3] = __fsub_rn(x[3], m.w);
-      }
-#pragma unroll
-      for (int c = 0; c < 4; ++c) z[p][c] = x[c];
-    } else {
-#pragma unroll
-      for (int c = 0; c < 4; ++c) z[p][c] = 0.f;
+      x[0] = h2f(static_cast<uint16_t>(raw[p].x & 0xffff), a.is_fp16);
+      x[1] = h2f(static_cast<uint16_t>(raw[p].x >> 16), a.is_fp16);
+      x[2] = h2f(static_cast<uint16_t>(raw[p].y & 0xffff), a.is_fp16);
+      x[3] = h2f(static_cast<uint16_t>(raw[p].y >> 16), a.is_fp16);
     }
+    // online V rotation (Sec. 4.3): the row times H, before smoothing
+    if (a.vhad) hadamard_row(x, cl);
+    if (n < a.N && a.center) {
+      x[0] = __fsub_rn(x[0], m.x);
+      x[1] = __fsub_rn(x[1], m.y);
+      x[2] = __fsub_rn(x[2], m.z);
+      x[3] = __fsub_rn(x[3], m.w);
+    }
+#pragma unroll
+    for (int c = 0; c < 4; ++c) z[p][c] = x[c];
   }
 }
 

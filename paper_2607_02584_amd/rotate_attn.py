@@ -17,6 +17,7 @@ LIB_PATH = os.path.join(HERE, "librotate_attn.so")
 
 ROT_NONE, ROT_INTERLEAVED, ROT_HALF, ROT_HADAMARD = 0, 1, 2, 3
 PQ_RANGE15, PQ_SYM7 = 0, 1
+VROT_NONE, VROT_HADAMARD = 0, 1
 SMOOTH_K, SMOOTH_V, SMOOTH_Q = 1, 2, 4
 BF16, FP16, FP32 = 0, 1, 2
 CODES_INT4, CODES_E2M3 = 0, 1
@@ -38,6 +39,7 @@ class Params(ctypes.Structure):
         ("q_group", ctypes.c_int32), ("k_group", ctypes.c_int32), ("v_group", ctypes.c_int32),
         ("kv_block", ctypes.c_int32), ("sm_scale", ctypes.c_float),
         ("in_dtype", ctypes.c_int32), ("out_dtype", ctypes.c_int32), ("code_format", ctypes.c_int32),
+        ("v_rotation", ctypes.c_int32),
     ]
 
 
@@ -92,7 +94,8 @@ def _check(status: int, where: str):
 
 def make_params(B, H, grid, split=(44, 42, 42), theta=10000.0, *, rotation=ROT_INTERLEAVED, rot_blocks=None,
                 p_quant=PQ_RANGE15, smooth=SMOOTH_K | SMOOTH_V, q_group=128, k_group=128, v_group=128,
-                kv_block=128, sm_scale=0.0, in_dtype=BF16, out_dtype=BF16, code_format=CODES_E2M3, D=128) -> Params:
+                kv_block=128, sm_scale=0.0, in_dtype=BF16, out_dtype=BF16, code_format=CODES_E2M3, D=128,
+                v_rotation=VROT_NONE) -> Params:
     p = Params()
     p.B, p.H, p.D = B, H, D
     p.N = int(grid[0] * grid[1] * grid[2])
@@ -109,6 +112,7 @@ def make_params(B, H, grid, split=(44, 42, 42), theta=10000.0, *, rotation=ROT_I
     p.sm_scale = float(sm_scale)
     p.in_dtype, p.out_dtype = in_dtype, out_dtype
     p.code_format = code_format
+    p.v_rotation = v_rotation
     return p
 
 

@@ -200,6 +200,44 @@ def test_int4_codes_scores_and_output(ora, wname, case, fmt):
     assert torch.equal(o_plain, o_gpu)
 
 
+@pytest.mark.parametrize("rot", [1, 2])
+def test_learned_rotation_blocks(ora, rot):
+    """Blocks from the Sec. 4.1.4 calibration (run on the GPU in PyTorch) drive the
+    producer: codes and scales bit-exact against the oracle with the same blocks,
+    O within 2e-3."""
+    torch, ra = _torch(), _ra()
+    from paper_2607_02584_amd import calibrate as cal
+    from paper_2607_02584_amd import datagen as dg
+    w = dg.WORKLOADS["c1"]
+    q, k, v = _inputs(w)
+    mode = "interleaved" if rot == 1 else "half"
+    print(f"[learned rotation] c1 {mode}: calibrating", flush=True)
+    res = cal.calibrate_rotation(q[0], k[0], (w.T, w.Hg, w.W), w.split, w.theta, mode=mode, q_group=1, k_group=1,
+                                 steps=30, rows=512, cols=1024, device="cuda")
+    assert res.final <= res.initial
+    R = res.blocks
+    p = ra.make_params(w.B, w.H, (w.T, w.Hg, w.W), w.split, w.theta, rotation=rot, rot_blocks=R, q_group=1,
+                       k_group=1, v_group=128, kv_block=128, out_dtype=ra.FP32)
+    bufs, (qd, kd, vd), ws = _run_quant(torch, ra, p, q, k, v)
+    Np = ra.layout(p)["n_pad"]
+    BH, N = w.B * w.H, w.N
+    h = _host(bufs)
+    qc = unpack_qk_e2m3(h["q_codes"], BH, Np, N)
+    kc = unpack_qk_e2m3(h["k_codes"], BH, Np, N)
+    o = torch.empty((BH, N, 128), dtype=torch.float32, device="cuda")
+    ra.fwd_int4(p, qd, kd, vd, o, ws)
+    torch.cuda.synchronize()
+    cfg = ora.Int4Config(rotation=rot, rot=R, q_group=1, k_group=1, v_group=128, kv_block=128)
+    geo = _geo(ora, w)
+    for bh in range(BH):
+        ref = ora.quantize_qk_head(geo, cfg, q[0, bh], k[0, bh])
+        assert np.array_equal(qc[bh], ref["q_codes"]) and np.array_equal(kc[bh], ref["k_codes"])
+        assert np.array_equal(h["q_scale"].reshape(BH, -1)[bh][:N].view(np.uint32), ref["q_scale"].view(np.uint32))
+        O_ref, _ = ora.fwd_int4_head(geo, cfg, q[0, bh], k[0, bh], v[0, bh])
+        err = np.abs(o[bh].cpu().numpy().astype(np.float64) - O_ref).max() / np.abs(O_ref).max()
+        assert err <= O_TOL
+
+
 @pytest.mark.parametrize("fmt", ["e2m3", "int4"])
 def test_fwd_int4_matches_stepwise_and_oracle(ora, fmt):
     """The fused entry point equals the three-call sequence bit for bit and the

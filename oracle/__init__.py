@@ -50,7 +50,7 @@ class _RopeCfg(ctypes.Structure):
 class _AttnCfg(ctypes.Structure):
     _fields_ = [("N", ctypes.c_int), ("D", ctypes.c_int), ("q_group", ctypes.c_int),
                 ("k_group", ctypes.c_int), ("v_group", ctypes.c_int), ("kv_block", ctypes.c_int),
-                ("p_quant", ctypes.c_int), ("sm_scale", ctypes.c_double)]
+                ("p_quant", ctypes.c_int), ("sm_scale", ctypes.c_double), ("l_quant", ctypes.c_int)]
 
 
 _lib = None
@@ -212,7 +212,7 @@ def key_bias(mu_q: np.ndarray, zk: np.ndarray) -> np.ndarray:
 
 
 def attn_int4(qc, qs, kc, ks, vc, vs, mu_v=None, *, q_group, k_group, v_group, kv_block,
-              p_quant=PQ_RANGE15, sm_scale=0.0, rows=None, dumps=False, bias=None):
+              p_quant=PQ_RANGE15, sm_scale=0.0, rows=None, dumps=False, bias=None, l_quant=False):
     """Blockwise INT4 attention for one head; returns O (fp64) and optional dumps.
     ``bias``: per-key score bias of Q smoothing, or None."""
     qc = np.ascontiguousarray(qc, dtype=np.int8)
@@ -227,7 +227,7 @@ def attn_int4(qc, qs, kc, ks, vc, vs, mu_v=None, *, q_group, k_group, v_group, k
     row0, nrows = (0, N) if rows is None else rows
     a = _AttnCfg()
     a.N, a.D, a.q_group, a.k_group, a.v_group, a.kv_block = N, D, q_group, k_group, v_group, kv_block
-    a.p_quant, a.sm_scale = p_quant, sm_scale
+    a.p_quant, a.sm_scale, a.l_quant = p_quant, sm_scale, int(bool(l_quant))
     O = np.empty((nrows, D), np.float64)
     nb = (N + kv_block - 1) // kv_block
     S = u = x = m = l = None
@@ -285,6 +285,7 @@ class Int4Config:
     rotation: int = ROT_INTERLEAVED
     rot: object = None
     p_quant: int = PQ_RANGE15
+    l_quant: bool = False      # normaliser from the quantized P (ablation) instead of the exact P
     smooth_k: bool = True
     smooth_v: bool = True
     smooth_q: bool = False
@@ -343,6 +344,7 @@ def fwd_int4_head(geo: Geometry, cfg: Int4Config, q_bf16, k_bf16, v_bf16, rows=N
     res = attn_int4(qk["q_codes"], qk["q_scale"], qk["k_codes"], qk["k_scale"], vv["v_codes"], vv["v_scale"],
                     vv["mu_v"] if cfg.smooth_v else None, q_group=cfg.q_group, k_group=cfg.k_group,
                     v_group=cfg.v_group, kv_block=cfg.kv_block, p_quant=cfg.p_quant, sm_scale=cfg.sm_scale,
+                    l_quant=cfg.l_quant,
                     rows=rows, dumps=dumps, bias=qk["k_bias"])
     inter = dict(qk, **vv)
     if dumps:

@@ -386,7 +386,7 @@ void ora_attn_int4(const ora_attn_cfg* a,
         for (int n = j0; n < j1; ++n) {
           const float x = bias ? t[n - j0] - mn : fmaf((float)S[n - j0], cn[n - j0], -mn);
           const float P = ora_exp2_f32(x);
-          l += (double)P;
+          if (!a->l_quant || a->p_quant == ORA_PQ_NONE) l += (double)P;
           if (x_dump) x_dump[(size_t)r * N + n] = x;
           int g = n / a->v_group;
           if (g != gcur) {
@@ -403,6 +403,7 @@ void ora_attn_int4(const ora_attn_cfg* a,
             if (u_dump) u_dump[(size_t)r * N + n] = 0;
           } else {
             const int u = ora_pcode(P, a->p_quant);
+            if (a->l_quant) l += (double)u / (double)pdiv;
             if (u_dump) u_dump[(size_t)r * N + n] = (uint8_t)u;
             for (int ch = 0; ch < D; ++ch) part[ch] += (double)(u * (int32_t)v[ch]);
           }

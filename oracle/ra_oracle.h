@@ -92,6 +92,8 @@ typedef struct {
   int kv_block;          /* online-softmax block size (Sec. 4.2) */
   int p_quant;           /* ORA_PQ_*; ORA_PQ_NONE keeps P unquantized (pin only) */
   double sm_scale;       /* 0 = 1/sqrt(D) */
+  int l_quant;           /* 0: l = sum of the unquantized P; 1: l = sum of the dequantized
+                            P^ = u / 15 (u / 7 for SYM7), the same values PV uses */
 } ora_attn_cfg;
 
 /* Blockwise INT4 attention for query rows [row0, row0+nrows) of one head

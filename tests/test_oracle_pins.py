@@ -682,6 +682,34 @@ def test_dominant_first_key_makes_block_size_irrelevant(ora):
         np.testing.assert_allclose(o, outs[0], rtol=1e-12, atol=1e-14)
 
 
+@pytest.mark.parametrize("pq,kv", [(0, 128), (1, 64), (0, 500)])
+def test_quantized_normaliser_makes_rows_convex(ora, pq, kv):
+    """With l = sum of the dequantized P^ (u / 15, or u / 7 for SYM7), every output row
+    is a convex combination of the dequantized V rows: a constant V comes back (up to
+    the binary32 roundings of its scale and of the dequantization factor s_v / 15, a
+    few 2^-24).  With l = sum of the exact P (the default
+    reading) it comes back scaled by sum P^ / sum P, which the P rounding moves
+    away from 1."""
+    rng = np.random.default_rng(48)
+    N = 700
+    qc, qs, kc, ks, _ = _int4_inputs(rng, N)
+    qs = (qs * 0.3).astype(np.float32)          # diffuse P: many mid-range codes
+    vc = np.full((N, 128), 7, np.int8)
+    vs = np.full((1, 128), np.float32(1.0) / np.float32(7.0), np.float32)
+    one = 7.0 * float(vs[0, 0])
+    kw = dict(v_group=N, kv_block=kv, p_quant=pq)
+    Oq, dq = _attn(ora, qc, qs, kc, ks, vc, vs, None, l_quant=True, **kw)
+    assert np.abs(Oq - one).max() <= 4 * 2.0 ** -24
+    Oe, de = _attn(ora, qc, qs, kc, ks, vc, vs, None, **kw)
+    assert np.abs(Oe - one).max() > 1e-3
+    # the two differ only in the normaliser: O_exact * l_exact == O_quant * l_quant
+    np.testing.assert_allclose(Oe * de["l"][:, None], Oq * dq["l"][:, None], rtol=1e-12)
+    # with the P rounding off the choice is moot
+    On, _ = _attn(ora, qc, qs, kc, ks, vc, vs, None, v_group=N, kv_block=kv, p_quant=ora.PQ_NONE, l_quant=True)
+    On0, _ = _attn(ora, qc, qs, kc, ks, vc, vs, None, v_group=N, kv_block=kv, p_quant=ora.PQ_NONE)
+    assert np.array_equal(On, On0)
+
+
 def test_sym7_uses_eight_levels(ora):
     """Sec. 4.2.1 baseline: the symmetric mapping only reaches codes 0..7."""
     rng = np.random.default_rng(17)

@@ -137,6 +137,9 @@ typedef struct ra_params {
   int32_t out_dtype;       /* RA_BF16 | RA_FP16 | RA_FP32 */
   int32_t code_format;     /* RA_CODES_*: container of the codes quantize_* write and attn_int4 reads */
   int32_t v_rotation;      /* RA_VROT_*: how the INT4 path treats V (the fallback takes V as given) */
+  int32_t l_quant;         /* INT4 normaliser: 0 = l is the sum of the unquantized P (default);
+                              1 = l is the sum of the dequantized P^ = u/15 (u/7 for SYM7), the
+                              values PV uses, so every output row is a convex combination */
 } ra_params;
 
 /* Sizes of the caller-visible INT4 buffers for these parameters. */

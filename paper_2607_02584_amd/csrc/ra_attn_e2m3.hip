@@ -136,7 +136,8 @@ struct TilePiece {
 
 // QB: Q smoothing, every key carries the score bias fl(b_j Kc), the scores
 // become t = fma(S, c, bias) before the maximum and P = 2^(t - m).
-template <int KV, bool KTOK, bool SYM7, bool DEBUG, bool QB>
+// LQ: the normaliser sums the codes u = rint(pscale P) (l = sum of P^) instead of pscale P.
+template <int KV, bool KTOK, bool SYM7, bool DEBUG, bool QB, bool LQ>
 __global__ __launch_bounds__(kThreads, 8 / kWaves) void k_attn_e2m3(AttnArgs a) {
   constexpr int NCH = KV / 32;   // 32-key chunks
   constexpr int NG = KV / 64;    // 64-key groups (one PV instruction each)
@@ -425,8 +426,9 @@ __global__ __launch_bounds__(kThreads, 8 / kWaves) void k_attn_e2m3(AttnArgs a) 
             P = __builtin_amdgcn_exp2f(__fmaf_rn(s[ch][r], c, -mq));
           }
           if (MASKED && s[ch][r] == -INFINITY) P = 0.f;
-          if (gg == 0 && c2 == 0 && r < 4) ls[r] = P;
-          else ls[r & 3] += P;
+          const float lv = LQ ? __builtin_rintf(P) : P;
+          if (gg == 0 && c2 == 0 && r < 4) ls[r] = lv;
+          else ls[r & 3] += lv;
           s[ch][r] = P;
         }
       }
@@ -482,7 +484,7 @@ __global__ __launch_bounds__(kThreads, 8 / kWaves) void k_attn_e2m3(AttnArgs a) 
 
   // ---- epilogue: O = O' * 8 w / 15 / l + mu_v; lane (j, hh) holds channel
   //      32 mt + j of the wave's queries 8 (r / 4) + 4 hh + r % 4 ----
-  const float ltot = l + __shfl_xor(l, 32);   // pscale * sum of P
+  const float ltot = l + __shfl_xor(l, 32);   // pscale * sum of P (LQ: sum of the codes u)
   const float k2 = 8.0f;
   const float* muv = a.mu_v ? a.mu_v + bh * kD : nullptr;
   float wsc[4], mu[4];
@@ -541,11 +543,16 @@ __global__ __launch_bounds__(kThreads, 8 / kWaves) void k_attn_e2m3(AttnArgs a) 
   }
 }
 
+template <int KV, bool KTOK, bool SYM7, bool DEBUG, bool QB, bool LQ>
+hipError_t launch_l(const AttnArgs& a, hipStream_t s) {
+  const dim3 grid((a.Npad + kBlockM - 1) / kBlockM, a.BH);
+  hipLaunchKernelGGL((k_attn_e2m3<KV, KTOK, SYM7, DEBUG, QB, LQ>), grid, dim3(kThreads), 0, s, a);
+  return hipGetLastError();
+}
+
 template <int KV, bool KTOK, bool SYM7, bool DEBUG, bool QB>
 hipError_t launch_b(const AttnArgs& a, hipStream_t s) {
-  const dim3 grid((a.Npad + kBlockM - 1) / kBlockM, a.BH);
-  hipLaunchKernelGGL((k_attn_e2m3<KV, KTOK, SYM7, DEBUG, QB>), grid, dim3(kThreads), 0, s, a);
-  return hipGetLastError();
+  return a.lq ? launch_l<KV, KTOK, SYM7, DEBUG, QB, true>(a, s) : launch_l<KV, KTOK, SYM7, DEBUG, QB, false>(a, s);
 }
 
 template <int KV, bool KTOK, bool SYM7, bool DEBUG>

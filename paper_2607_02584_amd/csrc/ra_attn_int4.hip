@@ -84,7 +84,8 @@ __device__ __forceinline__ void stage_store(const Stage<KV>& st, uint8_t* sk, ui
   }
 }
 
-template <int KV, bool KTOK, bool SYM7, bool DEBUG, bool QB>
+// LQ: the normaliser sums the codes u (l = pscale * sum of P^) instead of P.
+template <int KV, bool KTOK, bool SYM7, bool DEBUG, bool QB, bool LQ>
 __global__ __launch_bounds__(256, 1) void k_attn_int4(AttnArgs a) {
   constexpr int NCH = KV / 32;
   __shared__ __align__(16) uint8_t sK[2][KV * 128];
@@ -237,7 +238,7 @@ __global__ __launch_bounds__(256, 1) void k_attn_int4(AttnArgs a) {
           }
           float P = __builtin_amdgcn_exp2f(x);
           if (last && key0 + kl >= N) P = 0.f;
-          lsum += P;
+          lsum += LQ ? __builtin_rintf(__fmul_rn(P, pscale)) : P;
           word = __builtin_amdgcn_cvt_pk_u8_f32(__fmul_rn(P, pscale), t, word);
         }
         pk[ch][q] = word;
@@ -296,7 +297,8 @@ __global__ __launch_bounds__(256, 1) void k_attn_int4(AttnArgs a) {
   // ---- epilogue: O / l + mu_v (rotated back by H when V was rotated online) ----
   const float ltot = l + __shfl_xor(l, 32);
   {
-    const float inv = 1.0f / ltot;
+    // LQ: l counts codes, l / pscale is the sum of P^
+    const float inv = LQ ? pscale / ltot : 1.0f / ltot;
 #pragma unroll
     for (int mt = 0; mt < 4; ++mt)
 #pragma unroll
@@ -365,11 +367,16 @@ __global__ __launch_bounds__(256, 1) void k_attn_int4(AttnArgs a) {
   }
 }
 
+template <int KV, bool KTOK, bool SYM7, bool DEBUG, bool QB, bool LQ>
+hipError_t launch_l(const AttnArgs& a, hipStream_t s) {
+  const dim3 grid(a.Npad / kBlockM, a.BH);
+  hipLaunchKernelGGL((k_attn_int4<KV, KTOK, SYM7, DEBUG, QB, LQ>), grid, dim3(256), 0, s, a);
+  return hipGetLastError();
+}
+
 template <int KV, bool KTOK, bool SYM7, bool DEBUG, bool QB>
 hipError_t launch_b(const AttnArgs& a, hipStream_t s) {
-  const dim3 grid(a.Npad / kBlockM, a.BH);
-  hipLaunchKernelGGL((k_attn_int4<KV, KTOK, SYM7, DEBUG, QB>), grid, dim3(256), 0, s, a);
-  return hipGetLastError();
+  return a.lq ? launch_l<KV, KTOK, SYM7, DEBUG, QB, true>(a, s) : launch_l<KV, KTOK, SYM7, DEBUG, QB, false>(a, s);
 }
 
 template <int KV, bool KTOK, bool SYM7, bool DEBUG>

@@ -77,6 +77,7 @@ int validate(const ra_params* p) {
     return fail(RA_ERR_INVALID, "out_dtype must be BF16, FP16 or FP32");
   if (p->v_rotation != RA_VROT_NONE && p->v_rotation != RA_VROT_HADAMARD)
     return fail(RA_ERR_INVALID, "unknown v_rotation");
+  if (p->l_quant != 0 && p->l_quant != 1) return fail(RA_ERR_INVALID, "l_quant must be 0 or 1");
   return RA_OK;
 }
 
@@ -401,6 +402,7 @@ int attn_impl(const ra_params* p, const uint8_t* qc, const float* qs, const uint
   a.dbg_bh = bh;
   a.dbg_row0 = row0;
   a.dbg_rows = rows;
+  a.lq = p->l_quant;
   if (p->code_format == RA_CODES_E2M3)
     RA_CHECK_HIP(ra::launch_attn_e2m3(a, p->kv_block, p->k_group == 1, p->p_quant == RA_PQ_SYM7, debug, s));
   else

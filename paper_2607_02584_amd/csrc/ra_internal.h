@@ -71,6 +71,7 @@ struct AttnArgs {
   float Kc;               // fl32(sm_scale * log2(e))
   int out_dtype;
   int vhad;               // V was rotated by H: rotate each output row back
+  int lq;                 // l from the quantized P (sum of the codes) instead of the exact P
   // debug dump (debug kernel only)
   int32_t* dbg_s;
   uint8_t* dbg_u;
@@ -99,7 +100,8 @@ hipError_t launch_attn_int4(const AttnArgs& a, int kv_block, bool k_per_token, b
                             hipStream_t s);
 hipError_t launch_attn_e2m3(const AttnArgs& a, int kv_block, bool k_per_token, bool sym7, bool debug,
                             hipStream_t s);
-// (both launchers pick the key-bias variant when a.kbias is set)
+// (both launchers pick the key-bias variant when a.kbias is set and the
+// quantized-normaliser variant when a.lq is set)
 hipError_t launch_rope16(const RopeTables& t, const uint16_t* x, uint16_t* out, int BH, int N, int Npad,
                          int is_fp16, hipStream_t s);
 hipError_t launch_v16_relayout(const uint16_t* v, uint16_t* out, int BH, int N, int Npad, hipStream_t s);

@@ -39,7 +39,7 @@ class Params(ctypes.Structure):
         ("q_group", ctypes.c_int32), ("k_group", ctypes.c_int32), ("v_group", ctypes.c_int32),
         ("kv_block", ctypes.c_int32), ("sm_scale", ctypes.c_float),
         ("in_dtype", ctypes.c_int32), ("out_dtype", ctypes.c_int32), ("code_format", ctypes.c_int32),
-        ("v_rotation", ctypes.c_int32),
+        ("v_rotation", ctypes.c_int32), ("l_quant", ctypes.c_int32),
     ]
 
 
@@ -95,7 +95,7 @@ def _check(status: int, where: str):
 def make_params(B, H, grid, split=(44, 42, 42), theta=10000.0, *, rotation=ROT_INTERLEAVED, rot_blocks=None,
                 p_quant=PQ_RANGE15, smooth=SMOOTH_K | SMOOTH_V, q_group=128, k_group=128, v_group=128,
                 kv_block=128, sm_scale=0.0, in_dtype=BF16, out_dtype=BF16, code_format=CODES_E2M3, D=128,
-                v_rotation=VROT_NONE) -> Params:
+                v_rotation=VROT_NONE, l_quant=0) -> Params:
     p = Params()
     p.B, p.H, p.D = B, H, D
     p.N = int(grid[0] * grid[1] * grid[2])
@@ -113,6 +113,7 @@ def make_params(B, H, grid, split=(44, 42, 42), theta=10000.0, *, rotation=ROT_I
     p.in_dtype, p.out_dtype = in_dtype, out_dtype
     p.code_format = code_format
     p.v_rotation = v_rotation
+    p.l_quant = int(l_quant)
     return p
 
 

@@ -51,6 +51,7 @@ def _base(ra, **kw):
     ("p_quant", 5, -1),
     ("smooth", 8, -1),
     ("v_rotation", 2, -1),
+    ("l_quant", 2, -1),
     ("q_group", 3, -2),
     ("k_group", 16, -2),
     ("kv_block", 32, -2),

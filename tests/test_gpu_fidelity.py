@@ -7,7 +7,8 @@ over sampled query rows of the 1024-token case (all rows) and of the
 each rotation (none, merged interleaved, half, full Hadamard), the SYM7 P mapping (the
 "without range-optimized P" ablation of the paper's Table 1), the paper's
 per-token Q/K scales, Q smoothing with its per-key bias, no smoothing at all,
-the online V Hadamard, and the BF16 fallback.
+the online V Hadamard, the normaliser from the quantized P, and the BF16
+fallback.
 
 The paper gives no per-layer attention accuracy to compare with (its Table 1
 is video-level), so these numbers are reported, not pinned ("parity
@@ -21,7 +22,7 @@ import pytest
 pytestmark = pytest.mark.gpu
 
 VARIANTS = [
-    # name, rotation, p_quant, q/k group, smoothing flags[, online V rotation]
+    # name, rotation, p_quant, q/k group, smoothing flags[, online V rotation[, l from quantized P]]
     ("int4 none", 0, 0, 128, 3),
     ("int4 interleaved", 1, 0, 128, 3),
     ("int4 half", 2, 0, 128, 3),
@@ -31,6 +32,7 @@ VARIANTS = [
     ("int4 interleaved Q smoothing", 1, 0, 128, 7),
     ("int4 interleaved no smoothing", 1, 0, 128, 0),
     ("int4 interleaved online V had.", 1, 0, 128, 3, 1),
+    ("int4 interleaved l = sum P^", 1, 0, 128, 3, 0, 1),
 ]
 
 
@@ -66,7 +68,8 @@ def test_fidelity_to_fp64_attention(ora, wname):
     for name, rot, pq, g, sm, *vr in VARIANTS:
         p = ra.make_params(w.B, w.H, (w.T, w.Hg, w.W), w.split, w.theta, rotation=rot, p_quant=pq, q_group=g,
                            k_group=g, v_group=128, kv_block=128, smooth=sm, out_dtype=ra.FP32,
-                           code_format=ra.CODES_E2M3, v_rotation=vr[0] if vr else 0)
+                           code_format=ra.CODES_E2M3, v_rotation=vr[0] if vr else 0,
+                           l_quant=vr[1] if len(vr) > 1 else 0)
         ws = ra.workspace(p, ra.PATH_INT4)
         o = torch.empty((BH, N, 128), dtype=torch.float32, device="cuda")
         ra.fwd_int4(p, qd, kd, vd, o, ws)

@@ -43,16 +43,16 @@ def _geo(ora, w):
     return ora.Geometry(w.T, w.Hg, w.W, w.split, w.theta)
 
 
-def _cfg(ora, rotation, qg, kg, vg, kv, pq=0, smooth=3, vrot=0):
+def _cfg(ora, rotation, qg, kg, vg, kv, pq=0, smooth=3, vrot=0, lq=0):
     return ora.Int4Config(rotation=rotation, p_quant=pq, smooth_k=bool(smooth & 1), smooth_v=bool(smooth & 2),
                           smooth_q=bool(smooth & 4), q_group=qg, k_group=kg, v_group=vg, kv_block=kv,
-                          v_hadamard=bool(vrot))
+                          v_hadamard=bool(vrot), l_quant=bool(lq))
 
 
-def _params(ra, w, rotation, qg, kg, vg, kv, pq=0, smooth=3, out=2, fmt=1, vrot=0):
+def _params(ra, w, rotation, qg, kg, vg, kv, pq=0, smooth=3, out=2, fmt=1, vrot=0, lq=0):
     return ra.make_params(w.B, w.H, (w.T, w.Hg, w.W), w.split, w.theta, rotation=rotation, p_quant=pq,
                           smooth=smooth, q_group=qg, k_group=kg, v_group=vg, kv_block=kv, out_dtype=out,
-                          code_format=fmt, v_rotation=vrot)
+                          code_format=fmt, v_rotation=vrot, l_quant=lq)
 
 
 FORMATS = {"int4": 0, "e2m3": 1}
@@ -101,6 +101,9 @@ CASES = [
     # rotation, q_group, k_group, v_group, kv_block, p_quant, smooth, online V Hadamard
     (1, 128, 128, 128, 128, 0, 3, 1),
     (3, 1, 1, 256, 64, 0, 7, 1),
+    # ... and the normaliser from the quantized P
+    (1, 128, 128, 128, 128, 0, 3, 0, 1),
+    (2, 1, 1, 128, 64, 1, 7, 1, 1),
 ]
 
 
@@ -127,10 +130,11 @@ def test_int4_codes_scores_and_output(ora, wname, case, fmt):
     w = dg.WORKLOADS["c1"] if wname == "c1" else _small_ragged(wname)
     rot, qg, kg, vg, kv, pq, sm, *rest = case
     vrot = rest[0] if rest else 0
+    lq = rest[1] if len(rest) > 1 else 0
     vg = min(vg, 10 ** 6)
     print(f"[int4 parity] {wname} N={w.N} case={case} container={fmt}", flush=True)
     q, k, v = _inputs(w)
-    p = _params(ra, w, rot, qg, kg, vg, kv, pq, sm, fmt=FORMATS[fmt], vrot=vrot)
+    p = _params(ra, w, rot, qg, kg, vg, kv, pq, sm, fmt=FORMATS[fmt], vrot=vrot, lq=lq)
     bufs, _, _ = _run_quant(torch, ra, p, q, k, v)
     Np = ra.layout(p)["n_pad"]
     BH, N = w.B * w.H, w.N
@@ -141,7 +145,7 @@ def test_int4_codes_scores_and_output(ora, wname, case, fmt):
     vc = uv(h["v_codes"], BH, Np, N)
     nvg = -(-N // vg)
     geo = _geo(ora, w)
-    cfg = _cfg(ora, rot, qg, kg, vg, kv, pq, sm, vrot)
+    cfg = _cfg(ora, rot, qg, kg, vg, kv, pq, sm, vrot, lq)
     o_gpu = torch.empty((BH, N, 128), dtype=torch.float32, device="cuda")
     nb = -(-N // kv)
     for bh in range(BH):

@@ -39,10 +39,18 @@
 // packing produces.  In the output tile a lane holds one channel of 16
 // queries, so the per-channel V scale ratio is one register per tile, and
 // alpha reaches the query rows by a lane permute when some row's max moved.
+//
+// The plain kernels are built from this file; ra_attn_e2m3_debug.hip builds
+// the debug-dump kernels from the same source (two translation units compile
+// in parallel).
 #include <type_traits>
 
 #include "ra_internal.h"
 #include "ra_xcd.h"
+
+#ifndef RA_E2M3_DEBUG_TU
+#define RA_E2M3_DEBUG_TU 0
+#endif
 
 namespace ra {
 namespace {
@@ -560,27 +568,31 @@ hipError_t launch_t(const AttnArgs& a, hipStream_t s) {
   return a.kbias ? launch_b<KV, KTOK, SYM7, DEBUG, true>(a, s) : launch_b<KV, KTOK, SYM7, DEBUG, false>(a, s);
 }
 
-template <int KV, bool KTOK, bool SYM7>
-hipError_t launch_d(const AttnArgs& a, bool debug, hipStream_t s) {
-  return debug ? launch_t<KV, KTOK, SYM7, true>(a, s) : launch_t<KV, KTOK, SYM7, false>(a, s);
-}
-
 template <int KV, bool KTOK>
-hipError_t launch_p(const AttnArgs& a, bool sym7, bool debug, hipStream_t s) {
-  return sym7 ? launch_d<KV, KTOK, true>(a, debug, s) : launch_d<KV, KTOK, false>(a, debug, s);
+hipError_t launch_p(const AttnArgs& a, bool sym7, hipStream_t s) {
+  constexpr bool kDebug = RA_E2M3_DEBUG_TU != 0;
+  return sym7 ? launch_t<KV, KTOK, true, kDebug>(a, s) : launch_t<KV, KTOK, false, kDebug>(a, s);
 }
 
 template <int KV>
-hipError_t launch_k(const AttnArgs& a, bool ktok, bool sym7, bool debug, hipStream_t s) {
-  return ktok ? launch_p<KV, true>(a, sym7, debug, s) : launch_p<KV, false>(a, sym7, debug, s);
+hipError_t launch_k(const AttnArgs& a, bool ktok, bool sym7, hipStream_t s) {
+  return ktok ? launch_p<KV, true>(a, sym7, s) : launch_p<KV, false>(a, sym7, s);
 }
 
 }  // namespace
 
+#if RA_E2M3_DEBUG_TU
+hipError_t launch_attn_e2m3_debug(const AttnArgs& a, int kv_block, bool k_per_token, bool sym7, hipStream_t s) {
+  if (kv_block == 64) return launch_k<64>(a, k_per_token, sym7, s);
+  return launch_k<128>(a, k_per_token, sym7, s);
+}
+#else
 hipError_t launch_attn_e2m3(const AttnArgs& a, int kv_block, bool k_per_token, bool sym7, bool debug,
                             hipStream_t s) {
-  if (kv_block == 64) return launch_k<64>(a, k_per_token, sym7, debug, s);
-  return launch_k<128>(a, k_per_token, sym7, debug, s);
+  if (debug) return launch_attn_e2m3_debug(a, kv_block, k_per_token, sym7, s);
+  if (kv_block == 64) return launch_k<64>(a, k_per_token, sym7, s);
+  return launch_k<128>(a, k_per_token, sym7, s);
 }
+#endif
 
 }  // namespace ra

@@ -100,6 +100,7 @@ hipError_t launch_attn_int4(const AttnArgs& a, int kv_block, bool k_per_token, b
                             hipStream_t s);
 hipError_t launch_attn_e2m3(const AttnArgs& a, int kv_block, bool k_per_token, bool sym7, bool debug,
                             hipStream_t s);
+hipError_t launch_attn_e2m3_debug(const AttnArgs& a, int kv_block, bool k_per_token, bool sym7, hipStream_t s);
 // (both launchers pick the key-bias variant when a.kbias is set and the
 // quantized-normaliser variant when a.lq is set)
 hipError_t launch_rope16(const RopeTables& t, const uint16_t* x, uint16_t* out, int BH, int N, int Npad,

@@ -27,7 +27,8 @@ import tempfile
 import pytest
 
 ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
-SRC = os.path.join(ROOT, "paper_2607_02584_amd", "csrc", "ra_attn_e2m3.hip")
+CSRC = os.path.join(ROOT, "paper_2607_02584_amd", "csrc")
+SOURCES = [os.path.join(CSRC, "ra_attn_e2m3.hip"), os.path.join(CSRC, "ra_attn_e2m3_debug.hip")]
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
 CONV = "v_cvt_scalef32_2xpk16_fp6_f32"
 
@@ -67,15 +68,22 @@ def _violations(body):
 
 
 def _asm():
+    """gfx950 assembly of both translation units (plain and debug kernels), compiled in parallel."""
     with tempfile.TemporaryDirectory() as td:
-        out = os.path.join(td, "k.s")
-        cmd = [HIPCC, "-O3", "-std=c++17", "--offload-arch=gfx950", "-ffp-contract=off", "-Xclang",
-               "-target-feature", "-Xclang", "-packed-fp32-ops", "-I", os.path.join(ROOT, "include"),
-               "--cuda-device-only", "-S", "-x", "hip", SRC, "-o", out]
-        r = subprocess.run(cmd, capture_output=True, text=True)
-        assert r.returncode == 0, r.stderr[-2000:]
-        with open(out) as f:
-            return f.read()
+        procs = []
+        for i, src in enumerate(SOURCES):
+            out = os.path.join(td, f"k{i}.s")
+            cmd = [HIPCC, "-O3", "-std=c++17", "--offload-arch=gfx950", "-ffp-contract=off", "-Xclang",
+                   "-target-feature", "-Xclang", "-packed-fp32-ops", "-I", os.path.join(ROOT, "include"),
+                   "--cuda-device-only", "-S", "-x", "hip", src, "-o", out]
+            procs.append((subprocess.Popen(cmd, stdout=subprocess.PIPE, stderr=subprocess.PIPE, text=True), out))
+        text = []
+        for pr, out in procs:
+            _, err = pr.communicate()
+            assert pr.returncode == 0, err[-2000:]
+            with open(out) as f:
+                text.append(f.read())
+        return "\n".join(text)
 
 
 def test_violation_scan_detects_both_patterns():

@@ -193,9 +193,13 @@ def main():
                                 smooth=ra.SMOOTH_K | ra.SMOOTH_V | ra.SMOOTH_Q),
             "full_hadamard": dict(rotation=ra.ROT_HADAMARD, q_group=128, k_group=128,
                                   smooth=ra.SMOOTH_K | ra.SMOOTH_V),
+            # one V scale per channel over all tokens: no per-block V-scale ratio in the kernel
+            "per_channel_v": dict(rotation=ra.ROT_INTERLEAVED, q_group=128, k_group=128,
+                                  smooth=ra.SMOOTH_K | ra.SMOOTH_V, v_group=N),
         }
         for name, kw in specs.items():
-            pt = ra.make_params(w.B, w.H, (w.T, w.Hg, w.W), w.split, w.theta, v_group=128, kv_block=128,
+            kw = dict({"v_group": 128}, **kw)
+            pt = ra.make_params(w.B, w.H, (w.T, w.Hg, w.W), w.split, w.theta, kv_block=128,
                                 out_dtype=ra.BF16, code_format=ra.CODES_E2M3, **kw)
             bt = ra.alloc_int4(pt, dev)
             wst = ra.workspace(pt, ra.PATH_INT4, dev)

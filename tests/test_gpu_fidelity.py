@@ -7,8 +7,8 @@ over sampled query rows of the 1024-token case (all rows) and of the
 each rotation (none, merged interleaved, half, full Hadamard), the SYM7 P mapping (the
 "without range-optimized P" ablation of the paper's Table 1), the paper's
 per-token Q/K scales, Q smoothing with its per-key bias, no smoothing at all,
-the online V Hadamard, the normaliser from the quantized P, and the BF16
-fallback.
+the online V Hadamard, the normaliser from the quantized P, per-channel V
+scales, and the BF16 fallback.
 
 The paper gives no per-layer attention accuracy to compare with (its Table 1
 is video-level), so these numbers are reported, not pinned ("parity
@@ -33,6 +33,7 @@ VARIANTS = [
     ("int4 interleaved no smoothing", 1, 0, 128, 0),
     ("int4 interleaved online V had.", 1, 0, 128, 3, 1),
     ("int4 interleaved l = sum P^", 1, 0, 128, 3, 0, 1),
+    ("int4 interleaved per-channel V", 1, 0, 128, 3, 0, 0, "N"),
 ]
 
 
@@ -70,6 +71,8 @@ def test_fidelity_to_fp64_attention(ora, wname):
                            k_group=g, v_group=128, kv_block=128, smooth=sm, out_dtype=ra.FP32,
                            code_format=ra.CODES_E2M3, v_rotation=vr[0] if vr else 0,
                            l_quant=vr[1] if len(vr) > 1 else 0)
+        if len(vr) > 2:   # one V scale per channel over all tokens
+            p.v_group = w.N
         ws = ra.workspace(p, ra.PATH_INT4)
         o = torch.empty((BH, N, 128), dtype=torch.float32, device="cuda")
         ra.fwd_int4(p, qd, kd, vd, o, ws)

@@ -135,6 +135,39 @@ def _ptr(t):
     return ctypes.c_void_p(t.data_ptr())
 
 
+def _need(t, nbytes, name, optional=False):
+    """The library takes raw pointers: check here that a tensor is a contiguous
+    device tensor holding at least the bytes the call will touch."""
+    if t is None:
+        if optional:
+            return
+        raise ValueError(f"{name} is required")
+    if not t.is_contiguous():
+        raise ValueError(f"{name} must be contiguous")
+    if t.numel() * t.element_size() < nbytes:
+        raise ValueError(f"{name} holds {t.numel() * t.element_size()} bytes, the call needs {nbytes}")
+    if not t.is_cuda:
+        raise ValueError(f"{name} must be a device tensor")
+
+
+def _io_bytes(p):
+    n = int(p.B) * int(p.H) * int(p.N) * int(p.D)
+    return 2 * n, n * (4 if p.out_dtype == FP32 else 2)
+
+
+def _check_codes(p, L, q_codes=None, q_scale=None, k_codes=None, k_scale=None, v_codes=None, v_scale=None,
+                 mu=(), k_bias=None, need_bias=False):
+    for t, nb, name in ((q_codes, L["qk_code_bytes"], "q_codes"), (k_codes, L["qk_code_bytes"], "k_codes"),
+                        (q_scale, 4 * L["q_scale_count"], "q_scale"), (k_scale, 4 * L["k_scale_count"], "k_scale"),
+                        (v_codes, L["v_code_bytes"], "v_codes"), (v_scale, 4 * L["v_scale_count"], "v_scale")):
+        if nb and t is not False:
+            _need(t, nb, name)
+    for t, name in mu:
+        _need(t, 4 * L["mu_count"], name, optional=True)
+    if need_bias or k_bias is not None:
+        _need(k_bias, 4 * L["k_bias_count"], "k_bias", optional=not need_bias)
+
+
 def _stream(stream):
     if stream is not None:
         return ctypes.c_void_p(stream)
@@ -147,17 +180,34 @@ def _nbytes(t) -> int:
 
 
 def quantize_qk(p, q, k, q_codes, q_scale, k_codes, k_scale, mu_k, ws, stream=None, mu_q=None, k_bias=None):
+    L = layout(p)
+    nin, _ = _io_bytes(p)
+    _need(q, nin, "q")
+    _need(k, nin, "k")
+    _check_codes(p, L, q_codes=q_codes, q_scale=q_scale, k_codes=k_codes, k_scale=k_scale, v_codes=False,
+                 v_scale=False, mu=((mu_k, "mu_k"), (mu_q, "mu_q")), k_bias=k_bias,
+                 need_bias=bool(p.smooth & SMOOTH_Q))
+    _need(ws, workspace_size(p, PATH_INT4), "workspace")
     _check(lib().rotate_attn_quantize_qk(ctypes.byref(p), _ptr(q), _ptr(k), _ptr(q_codes), _ptr(q_scale),
                                          _ptr(k_codes), _ptr(k_scale), _ptr(mu_k), _ptr(mu_q), _ptr(k_bias),
                                          _ptr(ws), _nbytes(ws), _stream(stream)), "rotate_attn_quantize_qk")
 
 
 def quantize_v(p, v, v_codes, v_scale, mu_v, ws, stream=None):
+    L = layout(p)
+    _need(v, _io_bytes(p)[0], "v")
+    _check_codes(p, L, q_codes=False, q_scale=False, k_codes=False, k_scale=False, v_codes=v_codes, v_scale=v_scale,
+                 mu=((mu_v, "mu_v"),))
+    _need(ws, workspace_size(p, PATH_INT4), "workspace")
     _check(lib().rotate_attn_quantize_v(ctypes.byref(p), _ptr(v), _ptr(v_codes), _ptr(v_scale), _ptr(mu_v),
                                         _ptr(ws), _nbytes(ws), _stream(stream)), "rotate_attn_quantize_v")
 
 
 def attn_int4(p, q_codes, q_scale, k_codes, k_scale, v_codes, v_scale, mu_v, o, stream=None, k_bias=None):
+    L = layout(p)
+    _check_codes(p, L, q_codes, q_scale, k_codes, k_scale, v_codes, v_scale, mu=((mu_v, "mu_v"),), k_bias=k_bias,
+                 need_bias=bool(p.smooth & SMOOTH_Q))
+    _need(o, _io_bytes(p)[1], "o")
     _check(lib().rotate_attn_attn_int4(ctypes.byref(p), _ptr(q_codes), _ptr(q_scale), _ptr(k_codes), _ptr(k_scale),
                                        _ptr(v_codes), _ptr(v_scale), _ptr(mu_v), _ptr(k_bias), _ptr(o),
                                        _stream(stream)), "rotate_attn_attn_int4")
@@ -165,6 +215,14 @@ def attn_int4(p, q_codes, q_scale, k_codes, k_scale, v_codes, v_scale, mu_v, o, 
 
 def attn_int4_debug(p, q_codes, q_scale, k_codes, k_scale, v_codes, v_scale, mu_v, o, bh, row0, rows,
                     s_out=None, u_out=None, m_out=None, stream=None, k_bias=None):
+    L = layout(p)
+    _check_codes(p, L, q_codes, q_scale, k_codes, k_scale, v_codes, v_scale, mu=((mu_v, "mu_v"),), k_bias=k_bias,
+                 need_bias=bool(p.smooth & SMOOTH_Q))
+    _need(o, _io_bytes(p)[1], "o")
+    nb = -(-int(p.N) // int(p.kv_block))
+    _need(s_out, 4 * rows * int(p.N), "s_out", optional=True)
+    _need(u_out, rows * int(p.N), "u_out", optional=True)
+    _need(m_out, 4 * rows * nb, "m_out", optional=True)
     _check(lib().rotate_attn_attn_int4_debug(ctypes.byref(p), _ptr(q_codes), _ptr(q_scale), _ptr(k_codes),
                                              _ptr(k_scale), _ptr(v_codes), _ptr(v_scale), _ptr(mu_v),
                                              _ptr(k_bias), _ptr(o),
@@ -172,27 +230,44 @@ def attn_int4_debug(p, q_codes, q_scale, k_codes, k_scale, v_codes, v_scale, mu_
                                              _stream(stream)), "rotate_attn_attn_int4_debug")
 
 
+def _check_fwd(p, q, k, v, o, ws, path):
+    nin, nout = _io_bytes(p)
+    for t, name in ((q, "q"), (k, "k"), (v, "v")):
+        _need(t, nin, name)
+    _need(o, nout, "o")
+    _need(ws, workspace_size(p, path), "workspace")
+
+
 def fwd_int4(p, q, k, v, o, ws, stream=None):
+    _check_fwd(p, q, k, v, o, ws, PATH_INT4)
     _check(lib().rotate_attn_fwd_int4(ctypes.byref(p), _ptr(q), _ptr(k), _ptr(v), _ptr(o), _ptr(ws), _nbytes(ws),
                                       _stream(stream)), "rotate_attn_fwd_int4")
 
 
 def prepare_fp16(p, q, k, v, ws, stream=None):
+    nin, _ = _io_bytes(p)
+    for t, name in ((q, "q"), (k, "k"), (v, "v")):
+        _need(t, nin, name)
+    _need(ws, workspace_size(p, PATH_FP16), "workspace")
     _check(lib().rotate_attn_prepare_fp16(ctypes.byref(p), _ptr(q), _ptr(k), _ptr(v), _ptr(ws), _nbytes(ws),
                                           _stream(stream)), "rotate_attn_prepare_fp16")
 
 
 def attn_fp16(p, ws, o, stream=None):
+    _need(ws, workspace_size(p, PATH_FP16), "workspace")
+    _need(o, _io_bytes(p)[1], "o")
     _check(lib().rotate_attn_attn_fp16(ctypes.byref(p), _ptr(ws), _nbytes(ws), _ptr(o), _stream(stream)),
            "rotate_attn_attn_fp16")
 
 
 def fwd_fp16(p, q, k, v, o, ws, stream=None):
+    _check_fwd(p, q, k, v, o, ws, PATH_FP16)
     _check(lib().rotate_attn_fwd_fp16(ctypes.byref(p), _ptr(q), _ptr(k), _ptr(v), _ptr(o), _ptr(ws), _nbytes(ws),
                                       _stream(stream)), "rotate_attn_fwd_fp16")
 
 
 def fwd(p, fallback, q, k, v, o, ws, stream=None):
+    _check_fwd(p, q, k, v, o, ws, PATH_FP16 if fallback else PATH_INT4)
     _check(lib().rotate_attn_fwd(ctypes.byref(p), int(bool(fallback)), _ptr(q), _ptr(k), _ptr(v), _ptr(o), _ptr(ws),
                                  _nbytes(ws), _stream(stream)), "rotate_attn_fwd")
 

@@ -115,3 +115,23 @@ def test_null_pointers_and_workspace_errors_before_gpu():
     assert ra.workspace_size(pq, ra.PATH_INT4) >= ra.workspace_size(p, ra.PATH_INT4) + 2 * 1024 * 4
     assert L.rotate_attn_error_string(-4) == b"HIP runtime error"
     assert L.rotate_attn_fwd_int4(None, fake, fake, fake, fake, fake, 1 << 30, None) == -1
+
+
+def test_binding_checks_tensors_before_the_library():
+    """The ctypes binding refuses host tensors, non-contiguous tensors and
+    buffers smaller than the call touches (the C ABI cannot see sizes)."""
+    ra = _ra()
+    torch = pytest.importorskip("torch")
+    p = _base(ra)
+    x = torch.zeros(2, 1024, 128, dtype=torch.bfloat16)
+    with pytest.raises(ValueError, match="device tensor"):
+        ra.fwd_int4(p, x, x, x, x, x)
+    with pytest.raises(ValueError, match="required"):
+        ra._need(None, 16, "q")
+    t = torch.zeros(4, 4)
+    with pytest.raises(ValueError, match="contiguous"):
+        ra._need(t.t(), 16, "q")
+    with pytest.raises(ValueError, match="needs 128"):
+        ra._need(t, 128, "q")
+    # fp32 output needs 4 bytes per element of [B][H][N][D]
+    assert ra._io_bytes(ra.make_params(1, 2, (4, 16, 16), out_dtype=ra.FP32)) == (2 * 262144, 4 * 262144)

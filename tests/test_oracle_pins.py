@@ -64,6 +64,31 @@ def test_rope_blocks_are_so2_and_merged_blocks_o2(ora):
         assert abs(np.linalg.det(G) + 1.0) < 1e-15  # H_2 is a reflection
 
 
+def test_merged_block_is_rope_then_r_and_order_matters_for_h2(ora):
+    """Sec. 4.1.2: the merged table is G = M R (rotation after RoPE).  SO(2) blocks
+    commute with M, so the order could not be seen with them; H_2 is a reflection
+    and M H_2 != H_2 M, which makes the order observable (negative control)."""
+    geo = ora.Geometry(5, 6, 7)
+    rng = np.random.default_rng(40)
+    a = rng.uniform(0, 2 * np.pi, 64)
+    rots = np.stack([np.array([[math.cos(t), math.sin(t)], [-math.sin(t), math.cos(t)]]) for t in a])
+    h2 = np.array([[1, 1], [1, -1]]) / math.sqrt(2)
+    moved = 0
+    for _ in range(40):
+        n, p = int(rng.integers(geo.N)), int(rng.integers(64))
+        M = ora.rope_block(geo, n, p, ora.ROT_NONE)
+        G = ora.rope_block(geo, n, p, ora.ROT_INTERLEAVED, rots)
+        np.testing.assert_allclose(G, M @ rots[p], atol=1e-15)
+        np.testing.assert_allclose(G, rots[p] @ M, atol=1e-15)
+        Gh = ora.rope_block(geo, n, p, ora.ROT_INTERLEAVED)
+        np.testing.assert_allclose(Gh, M @ h2, atol=1e-15)
+        # H_2 M = M^T H_2 (a reflection turns a rotation around), so the two orders
+        # differ by (M - M^T) H_2, whose entries are +-sqrt(2) sin(phi)
+        np.testing.assert_allclose(np.abs(Gh - h2 @ M).max(), math.sqrt(2) * abs(M[0, 1]), atol=1e-14)
+        moved += abs(M[0, 1]) > 0.1
+    assert moved > 10
+
+
 @pytest.mark.parametrize("split,theta,axis,k,pos,omega", [
     ((44, 42, 42), 1e4, 0, 11, 3, 1e-2),     # theta^(-2*11/44) = 10^-2 exactly
     ((44, 42, 42), 1e4, 1, 0, 7, 1.0),       # pair 0 of every axis turns by the position
@@ -333,13 +358,23 @@ def test_mean_fixed_close_to_exact_mean_and_order_free(ora):
 
 def test_k_smoothing_leaves_softmax_unchanged(ora):
     """Sec. 4: subtracting a per-channel mean from K adds a per-query constant to
-    every score of that query, which softmax removes (exact in fp64)."""
+    every score of that query, which softmax removes; removing Q's mean and adding
+    the per-key bias back, or V's mean and adding it to O, changes nothing either
+    (exact in fp64)."""
     rng = np.random.default_rng(8)
     q, k, v = (rng.standard_normal((64, 128)) for _ in range(3))
     mu = k.mean(0)
     O1 = ora.attn_ref_f64(q, k, v)
     O2 = ora.attn_ref_f64(q, k - mu, v)
     np.testing.assert_allclose(O1, O2, atol=1e-12)
+    # Q smoothing with the key bias: (Q - 1 mu^T) K^T + 1 (K mu)^T = Q K^T, here as a
+    # 129th channel (query side 1, key side K mu) through the same reference
+    muq = q.mean(0)
+    qb = np.concatenate([q - muq, np.ones((64, 1))], 1)
+    kb = np.concatenate([k, (k @ muq)[:, None]], 1)
+    vb = np.concatenate([v, np.zeros((64, 1))], 1)
+    Oq = ora.attn_ref_f64(qb, kb, vb, sm_scale=1 / math.sqrt(128))[:, :128]
+    np.testing.assert_allclose(O1, Oq, atol=1e-12)
     # V smoothing with add-back: rows of softmax sum to one
     muv = v.mean(0)
     O3 = ora.attn_ref_f64(q, k, v - muv) + muv

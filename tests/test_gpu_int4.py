@@ -291,23 +291,35 @@ def test_int4_16bit_output_rounds_fp32_result(ora, out):
     assert torch.equal(o32.to(o16.dtype), o16)
 
 
-@pytest.mark.parametrize("fmt", ["e2m3", "int4"])
-def test_c2_full_size_sampled_rows(ora, fmt):
+C2_VARIANTS = {
+    # container, rotation, q_group, k_group, smoothing, online V Hadamard, l from quantized P
+    "e2m3": ("e2m3", 1, 128, 128, 3, 0, 0),
+    "int4": ("int4", 1, 128, 128, 3, 0, 0),
+    "e2m3-hadamard-qsmooth-pertoken-vhad": ("e2m3", 3, 1, 1, 7, 1, 0),
+    "e2m3-half-lquant": ("e2m3", 2, 128, 128, 3, 0, 1),
+}
+
+
+@pytest.mark.parametrize("variant", list(C2_VARIANTS))
+def test_c2_full_size_sampled_rows(ora, variant):
     """Headline 32760-token shape (12 heads) in the benchmark's launch
-    configuration: sampled query rows of two heads against the oracle."""
+    configuration (and three variants of the method at the same size): sampled
+    query rows of two heads against the oracle."""
     torch, ra = _torch(), _ra()
     from paper_2607_02584_amd import datagen as dg
     w = dg.WORKLOADS["c2"]
-    print(f"[c2 sampled] container={fmt}: generating inputs", flush=True)
+    fmt, rot, qg, kg, sm, vrot, lq = C2_VARIANTS[variant]
+    print(f"[c2 sampled] {variant}: generating inputs", flush=True)
     q, k, v = _inputs(w)
-    p = _params(ra, w, 1, 128, 128, 128, 128, fmt=FORMATS[fmt])
+    p = _params(ra, w, rot, qg, kg, 128, 128, smooth=sm, fmt=FORMATS[fmt], vrot=vrot, lq=lq)
     bufs, (qd, kd, vd), ws = _run_quant(torch, ra, p, q, k, v)
+    kbias = bufs["k_bias"] if sm & 4 else None
     BH, N = w.B * w.H, w.N
     o = torch.empty((BH, N, 128), dtype=torch.float32, device="cuda")
     ra.fwd_int4(p, qd, kd, vd, o, ws)
     torch.cuda.synchronize()
     geo = _geo(ora, w)
-    cfg = _cfg(ora, 1, 128, 128, 128, 128)
+    cfg = _cfg(ora, rot, qg, kg, 128, 128, smooth=sm, vrot=vrot, lq=lq)
     rng = np.random.default_rng(2)
     nb = -(-N // 128)
     for bh in (0, 7):
@@ -318,7 +330,8 @@ def test_c2_full_size_sampled_rows(ora, fmt):
             m_d = torch.zeros((nr, nb), dtype=torch.float32, device="cuda")
             od = torch.empty_like(o)
             ra.attn_int4_debug(p, bufs["q_codes"], bufs["q_scale"], bufs["k_codes"], bufs["k_scale"],
-                               bufs["v_codes"], bufs["v_scale"], bufs["mu_v"], od, bh, r0, nr, s_d, None, m_d)
+                               bufs["v_codes"], bufs["v_scale"], bufs["mu_v"], od, bh, r0, nr, s_d, None, m_d,
+                               k_bias=kbias)
             torch.cuda.synchronize()
             O_ref, d = ora.fwd_int4_head(geo, cfg, q[0, bh], k[0, bh], v[0, bh], rows=(r0, nr), dumps=True)
             assert np.array_equal(s_d.cpu().numpy(), d["S"])

@@ -181,6 +181,30 @@ def main():
         }
         log(f"bf16 fallback op {f_step:.3f} ms, kernel {f_attn:.3f} ms; speedup kernel {f_attn / attn_ms:.2f}x")
 
+    # context only: PyTorch's own scaled_dot_product_attention on the same shape,
+    # bf16, restricted to its flash / memory-efficient backends (never the math path)
+    sdpa = None
+    if not args.skip_fallback:
+        try:
+            from torch.nn.attention import SDPBackend, sdpa_kernel
+            qt, kt, vt = (torch.randn(w.B, w.H, N, 128, device=dev, dtype=torch.bfloat16) for _ in range(3))
+            with sdpa_kernel([SDPBackend.FLASH_ATTENTION, SDPBackend.EFFICIENT_ATTENTION]):
+                torch.nn.functional.scaled_dot_product_attention(qt, kt, vt)
+                torch.cuda.synchronize()
+                es = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)) for _ in range(5)]
+                for e0, e1 in es:
+                    e0.record(stream)
+                    torch.nn.functional.scaled_dot_product_attention(qt, kt, vt)
+                    e1.record(stream)
+                torch.cuda.synchronize()
+            sms = float(np.median([e0.elapsed_time(e1) for e0, e1 in es]))
+            sdpa = {"kernel": "torch.nn.functional.scaled_dot_product_attention (flash/efficient backend), bf16",
+                    "ms": round(sms, 4), "tflops": round(ops / (sms * 1e-3) / 1e12, 1)}
+            log(f"torch SDPA (context): {sms:.3f} ms")
+            del qt, kt, vt
+        except Exception as exc:   # context only: a missing backend is reported, not fatal
+            sdpa = {"unavailable": f"{type(exc).__name__}: {str(exc)[:120]}"}
+
     # variants of the method on the same inputs and kernel family: the paper's
     # own Q/K granularity (per token, Sec. 5.1), Q smoothing with the per-key
     # bias (Sec. 4), the full Hadamard rotation (the Sec. 5.3 baseline)
@@ -264,6 +288,8 @@ def main():
     line.update(extra)
     if variants is not None:
         line["variants"] = variants
+    if sdpa is not None:
+        line["torch_sdpa_context"] = sdpa
     print(json.dumps(line), flush=True)
 
 

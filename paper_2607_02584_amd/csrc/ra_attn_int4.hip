@@ -1,30 +1,43 @@
-// ra_attn_int4.hip -- INT4 FlashAttention forward for gfx950 (CDNA4).
+// ra_attn_int4.hip -- INT4 FlashAttention forward on the int8 matrix core (gfx950).
 //
 // Computes, per head and query row i, the blockwise online softmax of the
 // paper's Sec. 4.2 over blocks of KV keys in ascending order:
 //   S_ij   = Q~_i K~_j^T                      (exact int32 on the i8 matrix core)
 //   m_ij   = max(m_i,j-1, rowmax fl(S * c)),  c = fl(fl(s_q * Kc) * s_k)
-//   x      = fma(S, c, -m_ij),  P = 2^x       (Kc folds 1/sqrt(D) and log2 e)
-//   u      = round(15 P) in [0, 15]           (Range-optimized P, Sec. 4.2.1:
+//   pscale P = 2^fma(S, c, -(m_ij - log2 pscale))   (pscale = 15, or 7 for SYM7;
+//                                              Kc folds 1/sqrt(D) and log2 e)
+//   u      = rint(pscale P) in [0, 15]        (Range-optimized P, Sec. 4.2.1:
 //                                              P~ = u - 8, fixed scale 15)
-//   l      = alpha * l + sum P,  alpha = 2^(m_i,j-1 - m_ij)
-//   O      = alpha * O + sum_g fl(s_v[g]/15) * (u . V~)
-// and writes O / l + mu_v.  With Q smoothing every key j carries the score
-// bias fl(b_j Kc): t = fma(S, c, bias_j) replaces fl(S c) in the maximum and
-// x = t - m.
+//   l      = alpha * l + sum pscale P,  alpha = 2^(m_i,j-1 - m_ij)
+//   O      = alpha * O + sum_g fl(s_v[g]/pscale) * (u . V~)
+// and writes O * pscale / l + mu_v.  The P scale rides in the exponent (one
+// exponential per score, no multiply); the binary32 rounding of
+// m - log2 pscale perturbs pscale P by a relative ln 2 * 2^-24 (|m| + 6) at
+// most.  With Q smoothing every key j carries the score bias fl(b_j Kc):
+// t = fma(S, c, bias_j) replaces fl(S c) in the maximum and the exponent is
+// t - (m - log2 pscale).
 //
 // Matrix-core mapping (v_mfma_i32_32x32x32_i8, one wave = 32 queries):
 //   S^T = K Q^T : A = K tile (32 keys x 32 channels), B = Q^T, so every lane
 //                 holds 16 keys of ONE query: the row max and sum need no
 //                 cross-lane work except one exchange between the wave halves.
+//                 The int32 scores are converted to binary32 once (exact).
 //   O^T = V^T P^T: B = P^T comes straight from the S^T accumulator lanes (the
 //                 P codes of a lane are the B operand of that lane), A = V^T
 //                 read from LDS; the V codes are stored with the key order the
 //                 accumulator layout implies, so no register shuffle is needed.
+//                 A lane holds one query of the output tile, so alpha is the
+//                 lane's own (applied only when some row of the wave moved its
+//                 maximum); each block's int32 product is converted and scaled
+//                 by its V group's per-channel factor into the binary32 O.
 // K and V codes arrive packed (two per byte); a workgroup stages one KV block
 // in LDS, expanding each nibble c to the int8 value 16c with two bit
 // operations per four codes (the factor 16 is folded into the scales, which is
-// exact).  Q is expanded once per wave to plain int8 codes.
+// exact).  Q is expanded once per wave to plain int8 codes.  Two workgroups of
+// four waves share a compute unit.
+#include <climits>
+#include <type_traits>
+
 #include "ra_internal.h"
 #include "ra_xcd.h"
 
@@ -84,14 +97,16 @@ __device__ __forceinline__ void stage_store(const Stage<KV>& st, uint8_t* sk, ui
   }
 }
 
-// LQ: the normaliser sums the codes u (l = pscale * sum of P^) instead of P.
+// QB: Q smoothing, every key carries the score bias fl(b_j Kc).
+// LQ: the normaliser sums the codes u (l = sum of P^) instead of pscale P.
 template <int KV, bool KTOK, bool SYM7, bool DEBUG, bool QB, bool LQ>
-__global__ __launch_bounds__(256, 1) void k_attn_int4(AttnArgs a) {
+__global__ __launch_bounds__(256, 2) void k_attn_int4(AttnArgs a) {
   constexpr int NCH = KV / 32;
   __shared__ __align__(16) uint8_t sK[2][KV * 128];
   __shared__ __align__(16) uint8_t sV[2][KV * 128];
   __shared__ __align__(16) float sDq[2][kD];
   __shared__ __align__(16) float sKs[2][KTOK ? KV : 1];
+  __shared__ __align__(16) float sKc[2][NCH];          // K scale of each 32-key chunk (grouped K)
   __shared__ __align__(16) float sB[2][QB ? KV : 1];   // per-key score bias fl(b Kc)
 
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
@@ -102,6 +117,9 @@ __global__ __launch_bounds__(256, 1) void k_attn_int4(AttnArgs a) {
   const int N = a.N;
   const int nblocks = (N + KV - 1) / KV;
   const int kstride = a.Npad / a.k_group;
+  constexpr float pscale = SYM7 ? 7.0f : 15.0f;
+  // log2 of the P scale: pscale P = 2^(S c - (m - log2 pscale)), one exponential per score
+  constexpr float kLog2P = SYM7 ? 2.80735492205760410f : 3.90689059560851852f;
 
   // ---- Q operand: plain int8 codes in the order of the K expansion ----
   v4i qop[4];
@@ -116,20 +134,24 @@ __global__ __launch_bounds__(256, 1) void k_attn_int4(AttnArgs a) {
     }
   }
   const float cq = __fmul_rn(a.qs[static_cast<size_t>(bh) * (a.Npad / a.q_group) + qrow / a.q_group], a.Kc);
-  const float pscale = SYM7 ? 7.0f : 15.0f;
 
+  // Per-block side data in LDS: V dequantization factors fl(s_v / pscale) / 16
+  // (exact /16) of the block's group, the K scales (per 32-key chunk or per
+  // key) and, with Q smoothing, the per-key bias.
   auto stage_aux = [&](int jb, int buf) {
-    // V dequantization factors fl(s_v/15) / 16 for the block's group (exact /16)
     if (tid < kD) {
       int g = (jb * KV) / a.v_group;
       if (g >= a.nvgroups) g = a.nvgroups - 1;
       const float s = a.vs[(static_cast<size_t>(bh) * a.nvgroups + g) * kD + tid];
       sDq[buf][tid] = __fmul_rn(__fdiv_rn(s, pscale), 0.0625f);
     }
-    if (KTOK && tid < KV) {
-      sKs[buf][tid] = a.ks[static_cast<size_t>(bh) * kstride + jb * KV + tid];
+    const int kt = tid - kD;
+    if (kt >= 0 && kt < (KTOK ? KV : NCH)) {
+      if (KTOK) sKs[buf][kt] = a.ks[static_cast<size_t>(bh) * kstride + jb * KV + kt];
+      else sKc[buf][kt] = a.ks[static_cast<size_t>(bh) * kstride + (jb * KV + kt * 32) / a.k_group];
     }
-    if (QB && tid < KV) sB[buf][tid] = __fmul_rn(a.kbias[static_cast<size_t>(bh) * a.Npad + jb * KV + tid], a.Kc);
+    if (QB && kt >= 0 && kt < KV)
+      sB[buf][kt] = __fmul_rn(a.kbias[static_cast<size_t>(bh) * a.Npad + jb * KV + kt], a.Kc);
   };
 
   float of[4][16];
@@ -137,6 +159,7 @@ __global__ __launch_bounds__(256, 1) void k_attn_int4(AttnArgs a) {
   for (int mt = 0; mt < 4; ++mt)
 #pragma unroll
     for (int r = 0; r < 16; ++r) of[mt][r] = 0.f;
+  // running maximum m and row sum l of pscale P (LQ: of the codes u)
   float m = -INFINITY, l = 0.f;
 
   Stage<KV> st;
@@ -145,81 +168,84 @@ __global__ __launch_bounds__(256, 1) void k_attn_int4(AttnArgs a) {
   stage_aux(0, 0);
   __syncthreads();
 
-  for (int jb = 0; jb < nblocks; ++jb) {
+  // One block of KV keys; MASKED (keys past N) only for the partial last block.
+  auto step = [&](int jb, auto masked_tag) {
+    constexpr bool MASKED = decltype(masked_tag)::value;
     const int buf = jb & 1;
     const bool more = jb + 1 < nblocks;
     if (more) stage_load<KV>(a, bh, jb + 1, st);
     const int key0 = jb * KV;
-    const bool last = key0 + KV > N;
+    // key of accumulator register r in chunk ch: key0 + ch*32 + 8*(r/4) + 4*hh + r%4
+    auto is_out = [&](int ch, int r) { return MASKED && key0 + ch * 32 + 8 * (r >> 2) + 4 * hh + (r & 3) >= N; };
 
-    // ---- S^T = K Q^T (int32, 16 x true S) ----
-    v16i s[NCH];
+    // ---- S^T = K Q^T (int32, 16 x the exact S), kept as binary32 (exact:
+    //      |16 S| <= 16 * 6272 < 2^24) ----
+    float s[NCH][16];
 #pragma unroll
     for (int ch = 0; ch < NCH; ++ch) {
-      s[ch] = v16i{0, 0, 0, 0, 0, 0, 0, 0, 0, 0, 0, 0, 0, 0, 0, 0};
+      v16i si = v16i{0, 0, 0, 0, 0, 0, 0, 0, 0, 0, 0, 0, 0, 0, 0, 0};
 #pragma unroll
       for (int kc = 0; kc < 4; ++kc) {
         const v4i A = *reinterpret_cast<const v4i*>(&sK[buf][(((ch * 8) + 2 * kc + hh) * 32 + j) * 16]);
-        s[ch] = __builtin_amdgcn_mfma_i32_32x32x32_i8(A, qop[kc], s[ch], 0, 0, 0);
+        si = __builtin_amdgcn_mfma_i32_32x32x32_i8(A, qop[kc], si, 0, 0, 0);
+      }
+#pragma unroll
+      for (int r = 0; r < 16; ++r) s[ch][r] = static_cast<float>(si[r]);
+    }
+    if (DEBUG) {
+      if (bh == a.dbg_bh && qrow >= a.dbg_row0 && qrow < a.dbg_row0 + a.dbg_rows && a.dbg_s) {
+        const size_t rowo = static_cast<size_t>(qrow - a.dbg_row0);
+#pragma unroll
+        for (int ch = 0; ch < NCH; ++ch)
+#pragma unroll
+          for (int r = 0; r < 16; ++r) {
+            const int key = key0 + ch * 32 + 8 * (r >> 2) + 4 * hh + (r & 3);
+            if (key < N) a.dbg_s[rowo * N + key] = static_cast<int32_t>(s[ch][r]) >> 4;
+          }
       }
     }
 
-    // key of accumulator register r in chunk ch: key0 + ch*32 + 8*(r/4) + 4*hh + r%4
-    // ---- block row maximum ----
-    float c16[NCH];
-    float tmax = -INFINITY;
-    float tb[QB ? NCH : 1][16];   // QB: t = fma(S, c, bias) per score
-    if (QB) {
+    // ---- block row maximum: of fl(S c) (c >= 0: fl(max S * c)), or of
+    //      t = fma(S, c, bias) with Q smoothing; 16 S * c/16 == S * c exactly ----
+    float cch[NCH];
 #pragma unroll
-      for (int ch = 0; ch < NCH; ++ch) {
-        if (!KTOK)
-          c16[ch] = __fmul_rn(__fmul_rn(cq, a.ks[static_cast<size_t>(bh) * kstride + (key0 + ch * 32) / a.k_group]),
-                              0.0625f);
+    for (int ch = 0; ch < NCH; ++ch) cch[ch] = KTOK ? 0.f : __fmul_rn(__fmul_rn(cq, sKc[buf][ch]), 0.0625f);
+    auto ckey = [&](int ch, int r) {
+      const int kl = ch * 32 + 8 * (r >> 2) + 4 * hh + (r & 3);
+      return KTOK ? __fmul_rn(__fmul_rn(cq, sKs[buf][kl]), 0.0625f) : cch[ch];
+    };
+    float tmax = -INFINITY;
+    if (QB || KTOK) {
+#pragma unroll
+      for (int ch = 0; ch < NCH; ++ch)
 #pragma unroll
         for (int r = 0; r < 16; ++r) {
           const int kl = ch * 32 + 8 * (r >> 2) + 4 * hh + (r & 3);
-          const float c = KTOK ? __fmul_rn(__fmul_rn(cq, sKs[buf][kl]), 0.0625f) : c16[ch];
-          float t = __fmaf_rn(static_cast<float>(s[ch][r]), c, sB[buf][kl]);
-          if (last && key0 + kl >= N) t = -INFINITY;
-          tb[QB ? ch : 0][r] = t;
+          const float sf = s[ch][r];
+          float t = QB ? __fmaf_rn(sf, ckey(ch, r), sB[buf][kl]) : __fmul_rn(sf, ckey(ch, r));
+          if (is_out(ch, r)) t = -INFINITY;
           tmax = fmaxf(tmax, t);
         }
-      }
-    } else if (!KTOK) {
-#pragma unroll
-      for (int ch = 0; ch < NCH; ++ch) {
-        const int kbase = key0 + ch * 32;
-        c16[ch] = __fmul_rn(__fmul_rn(cq, a.ks[static_cast<size_t>(bh) * kstride + kbase / a.k_group]), 0.0625f);
-        if (kbase < N) {
-          int mx = INT_MIN;
-#pragma unroll
-          for (int r = 0; r < 16; ++r) {
-            const int key = kbase + 8 * (r >> 2) + 4 * hh + (r & 3);
-            const int v = (!last || key < N) ? s[ch][r] : INT_MIN;
-            mx = max(mx, v);
-          }
-          if (mx != INT_MIN) tmax = fmaxf(tmax, __fmul_rn(static_cast<float>(mx), c16[ch]));
-        }
-      }
     } else {
 #pragma unroll
       for (int ch = 0; ch < NCH; ++ch) {
+        float mx = -INFINITY;
 #pragma unroll
-        for (int r = 0; r < 16; ++r) {
-          const int kl = ch * 32 + 8 * (r >> 2) + 4 * hh + (r & 3);
-          const float c = __fmul_rn(__fmul_rn(cq, sKs[buf][kl]), 0.0625f);
-          if (!last || key0 + kl < N) tmax = fmaxf(tmax, __fmul_rn(static_cast<float>(s[ch][r]), c));
-        }
+        for (int r = 0; r < 16; ++r) mx = fmaxf(mx, is_out(ch, r) ? -INFINITY : s[ch][r]);
+        // a fully masked chunk gives -inf (or NaN when c == 0), which fmax ignores
+        tmax = fmaxf(tmax, __fmul_rn(mx, cch[ch]));
       }
     }
     tmax = fmaxf(tmax, __shfl_xor(tmax, 32));
     const float mnew = fmaxf(m, tmax);
     const float alpha = __builtin_amdgcn_exp2f(m - mnew);
     m = mnew;
+    const float mq = __fsub_rn(mnew, kLog2P);
 
-    // ---- P, its codes (B operand of O^T = V^T P^T) and the row sum ----
+    // ---- pscale P from the exponential, codes u = rint(pscale P) (the B
+    //      operand of O^T = V^T P^T straight from this lane), row sums ----
     uint32_t pk[NCH][4];
-    float lsum = 0.f;
+    float ls[4];
 #pragma unroll
     for (int ch = 0; ch < NCH; ++ch) {
 #pragma unroll
@@ -228,43 +254,56 @@ __global__ __launch_bounds__(256, 1) void k_attn_int4(AttnArgs a) {
 #pragma unroll
         for (int t = 0; t < 4; ++t) {
           const int r = 4 * q + t;
-          const int kl = ch * 32 + 8 * (r >> 2) + 4 * hh + (r & 3);
+          const float sf = s[ch][r];
           float x;
           if (QB) {
-            x = __fsub_rn(tb[QB ? ch : 0][r], mnew);
+            const int kl = ch * 32 + 8 * (r >> 2) + 4 * hh + (r & 3);
+            x = __fsub_rn(__fmaf_rn(sf, ckey(ch, r), sB[buf][kl]), mq);
           } else {
-            const float c = KTOK ? __fmul_rn(__fmul_rn(cq, sKs[buf][kl]), 0.0625f) : c16[ch];
-            x = __fmaf_rn(static_cast<float>(s[ch][r]), c, -mnew);
+            x = __fmaf_rn(sf, ckey(ch, r), -mq);
           }
-          float P = __builtin_amdgcn_exp2f(x);
-          if (last && key0 + kl >= N) P = 0.f;
-          lsum += LQ ? __builtin_rintf(__fmul_rn(P, pscale)) : P;
-          word = __builtin_amdgcn_cvt_pk_u8_f32(__fmul_rn(P, pscale), t, word);
+          float P = __builtin_amdgcn_exp2f(x);   // pscale * P
+          if (is_out(ch, r)) P = 0.f;
+          const float lv = LQ ? __builtin_rintf(P) : P;
+          if (ch == 0 && q == 0) ls[t] = lv;
+          else ls[t] += lv;
+          word = __builtin_amdgcn_cvt_pk_u8_f32(P, t, word);
         }
         pk[ch][q] = word;
       }
     }
-    l = __fmaf_rn(l, alpha, lsum);
+    l = __fmaf_rn(l, alpha, (ls[0] + ls[1]) + (ls[2] + ls[3]));
 
     if (DEBUG) {
       if (bh == a.dbg_bh && qrow >= a.dbg_row0 && qrow < a.dbg_row0 + a.dbg_rows) {
         const size_t rowo = static_cast<size_t>(qrow - a.dbg_row0);
+        if (a.dbg_u) {
 #pragma unroll
-        for (int ch = 0; ch < NCH; ++ch)
+          for (int ch = 0; ch < NCH; ++ch)
 #pragma unroll
-          for (int r = 0; r < 16; ++r) {
-            const int key = key0 + ch * 32 + 8 * (r >> 2) + 4 * hh + (r & 3);
-            if (key < N) {
-              if (a.dbg_s) a.dbg_s[rowo * N + key] = s[ch][r] >> 4;
-              if (a.dbg_u) a.dbg_u[rowo * N + key] = static_cast<uint8_t>((pk[ch][r >> 2] >> (8 * (r & 3))) & 0xFF);
+            for (int r = 0; r < 16; ++r) {
+              const int key = key0 + ch * 32 + 8 * (r >> 2) + 4 * hh + (r & 3);
+              if (key < N) a.dbg_u[rowo * N + key] = static_cast<uint8_t>((pk[ch][r >> 2] >> (8 * (r & 3))) & 0xFF);
             }
-          }
+        }
         if (a.dbg_m && hh == 0) a.dbg_m[rowo * nblocks + jb] = mnew;
       }
     }
 
-    // ---- O^T += V^T P^T (int32), one 32-channel tile at a time, then rescale
-    //      and dequantize into the binary32 accumulator ----
+    // the next block's tiles go to LDS here (its buffer was last read before
+    // the previous barrier), so the staging registers die early
+    if (more) {
+      stage_store<KV>(st, sK[buf ^ 1], sV[buf ^ 1]);
+      stage_aux(jb + 1, buf ^ 1);
+    }
+    // ---- O^T += V^T P^T (int32 per block), then O = alpha O + acc * dq; the
+    //      alpha rescale only when some row of the wave moved its maximum ----
+    if (__ballot(alpha != 1.0f) != 0) {
+#pragma unroll
+      for (int mt = 0; mt < 4; ++mt)
+#pragma unroll
+        for (int r = 0; r < 16; ++r) of[mt][r] = __fmul_rn(of[mt][r], alpha);
+    }
 #pragma unroll
     for (int mt = 0; mt < 4; ++mt) {
       v16i acc = v16i{0, 0, 0, 0, 0, 0, 0, 0, 0, 0, 0, 0, 0, 0, 0, 0};
@@ -282,23 +321,23 @@ __global__ __launch_bounds__(256, 1) void k_attn_int4(AttnArgs a) {
 #pragma unroll
         for (int t = 0; t < 4; ++t) {
           const int r = 4 * rq + t;
-          of[mt][r] = __fmaf_rn(static_cast<float>(acc[r]), d4[t], __fmul_rn(of[mt][r], alpha));
+          of[mt][r] = __fmaf_rn(static_cast<float>(acc[r]), d4[t], of[mt][r]);
         }
       }
     }
 
-    if (more) {
-      stage_store<KV>(st, sK[buf ^ 1], sV[buf ^ 1]);
-      stage_aux(jb + 1, buf ^ 1);
-    }
     __syncthreads();
-  }
+  };
 
-  // ---- epilogue: O / l + mu_v (rotated back by H when V was rotated online) ----
+  const int nfull = N / KV;
+  for (int jb = 0; jb < nfull; ++jb) step(jb, std::integral_constant<bool, false>());
+  if (nfull < nblocks) step(nfull, std::integral_constant<bool, true>());
+
+  // ---- epilogue: O = O' pscale / l + mu_v (rotated back by H when V was
+  //      rotated online); l is pscale * sum P, or the sum of the codes ----
   const float ltot = l + __shfl_xor(l, 32);
   {
-    // LQ: l counts codes, l / pscale is the sum of P^
-    const float inv = LQ ? pscale / ltot : 1.0f / ltot;
+    const float inv = pscale / ltot;
 #pragma unroll
     for (int mt = 0; mt < 4; ++mt)
 #pragma unroll

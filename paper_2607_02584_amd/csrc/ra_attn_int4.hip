@@ -35,7 +35,6 @@
 // operations per four codes (the factor 16 is folded into the scales, which is
 // exact).  Q is expanded once per wave to plain int8 codes.  Two workgroups of
 // four waves share a compute unit.
-#include <climits>
 #include <type_traits>
 
 #include "ra_internal.h"

@@ -34,8 +34,9 @@ namespace {
 constexpr float kFix = 1048576.0f;     // 2^20
 constexpr float kFixLim = 4294967296.0f;  // 2^32
 
-__device__ __forceinline__ float h2f(uint16_t b, int is_fp16) {
-  if (is_fp16) return __half2float(__ushort_as_half(b));
+template <bool F16>
+__device__ __forceinline__ float h2f(uint16_t b) {
+  if (F16) return __half2float(__ushort_as_half(b));
   return __uint_as_float(static_cast<uint32_t>(b) << 16);
 }
 
@@ -136,15 +137,18 @@ __device__ __forceinline__ void hadamard_row(float y[4], int cl) {
 
 // Computes the rotated values z of the thread's 4 channels for the 16 rows of
 // the tile.  Rows beyond N give zeros.  ybuf: [8][128] floats of LDS.
+// ROT: RA_ROT_HALF, RA_ROT_HADAMARD, or 0 for the table-only forms (none, merged
+// interleaved); F16: binary16 inputs (else bfloat16).
+template <int ROT, bool F16>
 __device__ __forceinline__ void rope_tile(const RopeTables& t, const QkArgs& a, int bh, int tile, float (*ybuf)[kD],
                                           float z[16][4]) {
   __shared__ int pos[kTile][4];
   const int tid = threadIdx.x, rr = tid >> 5, cl = tid & 31;
   const PairSetup ps = pair_setup(t, cl);
-  const bool half = t.rotation == RA_ROT_HALF;
-  const bool full = t.rotation == RA_ROT_HADAMARD;
+  constexpr bool half = ROT == RA_ROT_HALF;
+  constexpr bool full = ROT == RA_ROT_HADAMARD;
   HalfSetup hs;
-  if (half) hs = half_setup(t, cl);
+  if constexpr (half) hs = half_setup(t, cl);
   tile_positions(t, tile, a.N, pos);
   const uint16_t* xb = a.x + static_cast<size_t>(bh) * a.N * kD;
   // all sixteen row loads first (rows past N re-read the last row and are zeroed)
@@ -159,10 +163,10 @@ __device__ __forceinline__ void rope_tile(const RopeTables& t, const QkArgs& a, 
     const int nl = p * 8 + rr, n = tile * kTile + nl;
     float y[4] = {0.f, 0.f, 0.f, 0.f};
     if (n < a.N) {
-      const float x[4] = {h2f(static_cast<uint16_t>(raw[p].x & 0xffff), a.is_fp16),
-                          h2f(static_cast<uint16_t>(raw[p].x >> 16), a.is_fp16),
-                          h2f(static_cast<uint16_t>(raw[p].y & 0xffff), a.is_fp16),
-                          h2f(static_cast<uint16_t>(raw[p].y >> 16), a.is_fp16)};
+      const float x[4] = {h2f<F16>(static_cast<uint16_t>(raw[p].x & 0xffff)),
+                          h2f<F16>(static_cast<uint16_t>(raw[p].x >> 16)),
+                          h2f<F16>(static_cast<uint16_t>(raw[p].y & 0xffff)),
+                          h2f<F16>(static_cast<uint16_t>(raw[p].y >> 16))};
 #pragma unroll
       for (int i = 0; i < 2; ++i) {
         const float4 g = ps.tab[i][pos[nl][ps.axis[i]] * ps.npair[i]];
@@ -171,7 +175,7 @@ __device__ __forceinline__ void rope_tile(const RopeTables& t, const QkArgs& a, 
         y[2 * i + 1] = __fmaf_rn(x1, g.w, __fmul_rn(x0, g.y));
       }
     }
-    if (half) {
+    if constexpr (half) {
       __syncthreads();
       *reinterpret_cast<float4*>(&ybuf[rr][4 * cl]) = make_float4(y[0], y[1], y[2], y[3]);
       __syncthreads();
@@ -183,7 +187,7 @@ __device__ __forceinline__ void rope_tile(const RopeTables& t, const QkArgs& a, 
         y[2 * i + 1] = __fmaf_rn(bv, r.w, __fmul_rn(av, r.y));
       }
       if (n >= a.N) y[0] = y[1] = y[2] = y[3] = 0.f;
-    } else if (full) {
+    } else if constexpr (full) {
       hadamard_row(y, cl);  // rows past N are zero and stay zero
     }
 #pragma unroll
@@ -220,11 +224,12 @@ __device__ __forceinline__ float4 mean4(const double* sums, int N, int cl) {
                      static_cast<float>(sums[4 * cl + 2] / den), static_cast<float>(sums[4 * cl + 3] / den));
 }
 
+template <int ROT, bool F16>
 __global__ __launch_bounds__(256) void k_qk_sums(RopeTables t, QkArgs a) {
   __shared__ float ybuf[8][kD];
   const int tile = blockIdx.x, bh = blockIdx.y;
   float z[16][4];
-  rope_tile(t, a, bh, tile, ybuf, z);
+  rope_tile<ROT, F16>(t, a, bh, tile, ybuf, z);
   double acc[4] = {0.0, 0.0, 0.0, 0.0};
 #pragma unroll
   for (int p = 0; p < 16; ++p)
@@ -249,6 +254,7 @@ __device__ __forceinline__ int qcode(float z, float inv) {
   return static_cast<int>(c);
 }
 
+template <int ROT, bool F16>
 __global__ __launch_bounds__(256) void k_qk_quant(RopeTables t, QkArgs a) {
   __shared__ float ybuf[8][kD];
   __shared__ float rowmax[kTile];
@@ -257,7 +263,7 @@ __global__ __launch_bounds__(256) void k_qk_quant(RopeTables t, QkArgs a) {
   const int tile = blockIdx.x, bh = blockIdx.y;
   const int tid = threadIdx.x, rr = tid >> 5, cl = tid & 31;
   float z[16][4];
-  rope_tile(t, a, bh, tile, ybuf, z);
+  rope_tile<ROT, F16>(t, a, bh, tile, ybuf, z);
   if (a.center) {
     const float4 m = mean4(a.sums + static_cast<size_t>(bh) * kD, a.N, cl);
     if (a.mu_out && tile == 0 && rr == 0) *reinterpret_cast<float4*>(a.mu_out + bh * kD + 4 * cl) = m;
@@ -351,6 +357,7 @@ __global__ __launch_bounds__(256) void k_qk_quant(RopeTables t, QkArgs a) {
 
 // ------------------------------------------------------------------ V --
 
+template <bool F16, bool VHAD>
 __device__ __forceinline__ void load_v_tile(const VArgs& a, int bh, int tile, float z[16][4]) {
   const int tid = threadIdx.x, rr = tid >> 5, cl = tid & 31;
   const uint16_t* xb = a.x + static_cast<size_t>(bh) * a.N * kD;
@@ -366,13 +373,13 @@ __device__ __forceinline__ void load_v_tile(const VArgs& a, int bh, int tile, fl
     const int n = tile * kTile + p * 8 + rr;
     float x[4] = {0.f, 0.f, 0.f, 0.f};
     if (n < a.N) {
-      x[0] = h2f(static_cast<uint16_t>(raw[p].x & 0xffff), a.is_fp16);
-      x[1] = h2f(static_cast<uint16_t>(raw[p].x >> 16), a.is_fp16);
-      x[2] = h2f(static_cast<uint16_t>(raw[p].y & 0xffff), a.is_fp16);
-      x[3] = h2f(static_cast<uint16_t>(raw[p].y >> 16), a.is_fp16);
+      x[0] = h2f<F16>(static_cast<uint16_t>(raw[p].x & 0xffff));
+      x[1] = h2f<F16>(static_cast<uint16_t>(raw[p].x >> 16));
+      x[2] = h2f<F16>(static_cast<uint16_t>(raw[p].y & 0xffff));
+      x[3] = h2f<F16>(static_cast<uint16_t>(raw[p].y >> 16));
     }
     // online V rotation (Sec. 4.3): the row times H, before smoothing
-    if (a.vhad) hadamard_row(x, cl);
+    if constexpr (VHAD) hadamard_row(x, cl);
     if (n < a.N && a.center) {
       x[0] = __fsub_rn(x[0], m.x);
       x[1] = __fsub_rn(x[1], m.y);
@@ -384,10 +391,11 @@ __device__ __forceinline__ void load_v_tile(const VArgs& a, int bh, int tile, fl
   }
 }
 
+template <bool F16, bool VHAD>
 __global__ __launch_bounds__(256) void k_v_sums(VArgs a) {
   const int tile = blockIdx.x, bh = blockIdx.y;
   float z[16][4];
-  load_v_tile(a, bh, tile, z);
+  load_v_tile<F16, VHAD>(a, bh, tile, z);
   double acc[4] = {0.0, 0.0, 0.0, 0.0};
 #pragma unroll
   for (int p = 0; p < 16; ++p)
@@ -403,12 +411,13 @@ __device__ __forceinline__ int vgroup_of(const VArgs& a, int n) {
 
 // Per (tile half, channel) abs-max, merged into the group maxima with an
 // order-independent atomic max on the float bits (values are >= 0).
+template <bool F16, bool VHAD>
 __global__ __launch_bounds__(256) void k_v_amax(VArgs a) {
   __shared__ float red[8][2][kD];
   const int tile = blockIdx.x, bh = blockIdx.y;
   const int tid = threadIdx.x, rr = tid >> 5, cl = tid & 31;
   float z[16][4];
-  load_v_tile(a, bh, tile, z);
+  load_v_tile<F16, VHAD>(a, bh, tile, z);
   float m[2][4] = {{0.f, 0.f, 0.f, 0.f}, {0.f, 0.f, 0.f, 0.f}};
   for (int p = 0; p < 16; ++p)
 #pragma unroll
@@ -429,6 +438,7 @@ __global__ __launch_bounds__(256) void k_v_amax(VArgs a) {
   }
 }
 
+template <bool F16, bool VHAD>
 __global__ __launch_bounds__(256) void k_v_quant(VArgs a) {
   __shared__ __align__(16) uint8_t ctile[kTile * 96];
   __shared__ float ginv[2][kD];
@@ -453,7 +463,7 @@ __global__ __launch_bounds__(256) void k_v_quant(VArgs a) {
   if (a.center && a.mu_out && tile == 0 && rr == 0)
     *reinterpret_cast<float4*>(a.mu_out + bh * kD + 4 * cl) = mean4(a.sums + static_cast<size_t>(bh) * kD, a.N, cl);
   float z[16][4];
-  load_v_tile(a, bh, tile, z);
+  load_v_tile<F16, VHAD>(a, bh, tile, z);
   if (a.e2m3) {
     // group of 64 tokens gl = p/8, kappa = (p%8)*8 + rr, half h = (rr/4)%2; token kappa of a channel is
     // field 8*((kappa%32)/8) + 2*(kappa%4) + kappa/32 of record ((gl*4 + ch/32)*2 + h)*32 + ch%32.
@@ -522,13 +532,42 @@ __global__ void k_fill_zero_u32(uint32_t* p, int64_t n) {
 
 }  // namespace
 
+// the rotation and input type as template arguments: table-only rotations share one form
+#define RA_QK_DISPATCH(KERNEL)                                                                        \
+  do {                                                                                                \
+    const dim3 g(a.Npad / kTile, BH);                                                                 \
+    const int rot = (t.rotation == RA_ROT_HALF || t.rotation == RA_ROT_HADAMARD) ? t.rotation : 0;    \
+    if (rot == RA_ROT_HALF) {                                                                         \
+      if (a.is_fp16) hipLaunchKernelGGL((KERNEL<RA_ROT_HALF, true>), g, dim3(256), 0, s, t, a);        \
+      else hipLaunchKernelGGL((KERNEL<RA_ROT_HALF, false>), g, dim3(256), 0, s, t, a);                 \
+    } else if (rot == RA_ROT_HADAMARD) {                                                              \
+      if (a.is_fp16) hipLaunchKernelGGL((KERNEL<RA_ROT_HADAMARD, true>), g, dim3(256), 0, s, t, a);    \
+      else hipLaunchKernelGGL((KERNEL<RA_ROT_HADAMARD, false>), g, dim3(256), 0, s, t, a);             \
+    } else {                                                                                          \
+      if (a.is_fp16) hipLaunchKernelGGL((KERNEL<0, true>), g, dim3(256), 0, s, t, a);                  \
+      else hipLaunchKernelGGL((KERNEL<0, false>), g, dim3(256), 0, s, t, a);                           \
+    }                                                                                                 \
+  } while (0)
+
+#define RA_V_DISPATCH(KERNEL)                                                                         \
+  do {                                                                                                \
+    const dim3 g(a.Npad / kTile, BH);                                                                 \
+    if (a.is_fp16) {                                                                                  \
+      if (a.vhad) hipLaunchKernelGGL((KERNEL<true, true>), g, dim3(256), 0, s, a);                     \
+      else hipLaunchKernelGGL((KERNEL<true, false>), g, dim3(256), 0, s, a);                           \
+    } else {                                                                                          \
+      if (a.vhad) hipLaunchKernelGGL((KERNEL<false, true>), g, dim3(256), 0, s, a);                    \
+      else hipLaunchKernelGGL((KERNEL<false, false>), g, dim3(256), 0, s, a);                          \
+    }                                                                                                 \
+  } while (0)
+
 hipError_t launch_qk_sums(const RopeTables& t, const QkArgs& a, int BH, hipStream_t s) {
-  hipLaunchKernelGGL(k_qk_sums, dim3(a.Npad / kTile, BH), dim3(256), 0, s, t, a);
+  RA_QK_DISPATCH(k_qk_sums);
   return hipGetLastError();
 }
 
 hipError_t launch_qk_quant(const RopeTables& t, const QkArgs& a, int BH, hipStream_t s) {
-  hipLaunchKernelGGL(k_qk_quant, dim3(a.Npad / kTile, BH), dim3(256), 0, s, t, a);
+  RA_QK_DISPATCH(k_qk_quant);
   return hipGetLastError();
 }
 
@@ -541,17 +580,17 @@ hipError_t launch_fill_zero_u32(uint32_t* p, int64_t n, hipStream_t s) {
 }
 
 hipError_t launch_v_sums(const VArgs& a, int BH, hipStream_t s) {
-  hipLaunchKernelGGL(k_v_sums, dim3(a.Npad / kTile, BH), dim3(256), 0, s, a);
+  RA_V_DISPATCH(k_v_sums);
   return hipGetLastError();
 }
 
 hipError_t launch_v_amax(const VArgs& a, int BH, hipStream_t s) {
-  hipLaunchKernelGGL(k_v_amax, dim3(a.Npad / kTile, BH), dim3(256), 0, s, a);
+  RA_V_DISPATCH(k_v_amax);
   return hipGetLastError();
 }
 
 hipError_t launch_v_quant(const VArgs& a, int BH, hipStream_t s) {
-  hipLaunchKernelGGL(k_v_quant, dim3(a.Npad / kTile, BH), dim3(256), 0, s, a);
+  RA_V_DISPATCH(k_v_quant);
   return hipGetLastError();
 }
 

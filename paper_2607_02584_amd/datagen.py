@@ -146,6 +146,6 @@ def schedule_mask(seed: int = SCHEDULE["mask_seed"], steps: int = SCHEDULE["step
 
 
 def small_workload(name: str, T: int, Hg: int, W: int, H: int = 1, split=(44, 42, 42), theta=10000.0,
-                   seed: int = 11, dist: str = "lowfreq") -> Workload:
-    """Ad-hoc small geometry for parity cases (ragged N, few heads)."""
-    return Workload(name, 1, H, T, Hg, W, split=tuple(split), theta=theta, seed=seed, dist=dist)
+                   seed: int = 11, dist: str = "lowfreq", B: int = 1) -> Workload:
+    """Ad-hoc small geometry for parity cases (ragged N, few heads, batch)."""
+    return Workload(name, B, H, T, Hg, W, split=tuple(split), theta=theta, seed=seed, dist=dist)

@@ -111,6 +111,12 @@ CASES = [
 
 def _small_ragged(name="ragged"):
     from paper_2607_02584_amd import datagen as dg
+    if name == "b2n15":
+        # batch 2, 15 tokens: less than one 32-key chunk, every block partial
+        return dg.small_workload("b2n15", 1, 3, 5, H=2, seed=23, B=2)
+    if name == "n1":
+        # one token: the softmax row is a single 1, O is the dequantized V row (+ mean)
+        return dg.small_workload("n1", 1, 1, 1, H=1, seed=24)
     if name == "ragged300":
         # N = 300: the padded length 384 is not a whole number of 256-query workgroups
         return dg.small_workload("ragged300", 3, 10, 10, H=2, seed=22)
@@ -123,7 +129,7 @@ def _workloads():
 
 
 @pytest.mark.parametrize("fmt", ["e2m3", "int4"])
-@pytest.mark.parametrize("wname", ["c1", "ragged", "ragged300"])
+@pytest.mark.parametrize("wname", ["c1", "ragged", "ragged300", "b2n15", "n1"])
 @pytest.mark.parametrize("case", CASES)
 def test_int4_codes_scores_and_output(ora, wname, case, fmt):
     """Producer codes/scales/means bit-exact; S, m bit-exact; P codes up to ties; O <= 2e-3."""

@@ -24,11 +24,23 @@ def _f32_to_f16_bits(x):
     return np.asarray(x, np.float32).astype(np.float16).view(np.uint16)
 
 
-@pytest.mark.parametrize("wname,dtype", [("c1", "bf16"), ("ragged", "bf16"), ("c1", "fp16")])
+SMALL = {
+    "ragged": dict(T=3, Hg=7, W=11, H=2, seed=21),
+    "b2n15": dict(T=1, Hg=3, W=5, H=2, seed=23, B=2),   # batch 2, less than one key block
+    "n1": dict(T=1, Hg=1, W=1, H=1, seed=24),           # a single token: O is its V row
+}
+
+
+@pytest.mark.parametrize("wname,dtype", [("c1", "bf16"), ("ragged", "bf16"), ("c1", "fp16"), ("b2n15", "bf16"),
+                                         ("n1", "bf16")])
 def test_fp16_fallback_parity(ora, wname, dtype):
     torch, ra = _torch(), _ra()
     from paper_2607_02584_amd import datagen as dg
-    w = dg.WORKLOADS["c1"] if wname == "c1" else dg.small_workload("ragged", 3, 7, 11, H=2, seed=21)
+    if wname == "c1":
+        w = dg.WORKLOADS["c1"]
+    else:
+        g = dict(SMALL[wname])
+        w = dg.small_workload(wname, g.pop("T"), g.pop("Hg"), g.pop("W"), **g)
     print(f"[fp16 parity] {wname} {dtype} N={w.N}", flush=True)
     q, k, v = dg.make_inputs(w)
     if dtype == "fp16":
@@ -45,15 +57,16 @@ def test_fp16_fallback_parity(ora, wname, dtype):
     torch.cuda.synchronize()
     assert torch.equal(o, o2)
     geo = ora.Geometry(w.T, w.Hg, w.W, w.split, w.theta)
-    for hh in range(w.H):
+    for bh in range(w.B * w.H):
+        b, hh = divmod(bh, w.H)
         if dtype == "fp16":
             # oracle on the fp16 inputs: RoPE in binary32, rounded to fp16, fp64 attention with P rounded to fp16
-            O_ref = _oracle_fp16(ora, geo, q[0, hh], k[0, hh], v[0, hh])
+            O_ref = _oracle_fp16(ora, geo, q[b, hh], k[b, hh], v[b, hh])
         else:
-            O_ref = ora.fwd_fp16_head(geo, q[0, hh], k[0, hh], v[0, hh], kv_block=64)
-        og = o[hh].cpu().numpy()
+            O_ref = ora.fwd_fp16_head(geo, q[b, hh], k[b, hh], v[b, hh], kv_block=64)
+        og = o[bh].cpu().numpy()
         err = np.abs(og - O_ref).max() / np.abs(O_ref).max()
-        print(f"  head {hh}: O rel err {err:.3e}", flush=True)
+        print(f"  head {bh}: O rel err {err:.3e}", flush=True)
         assert err <= O_TOL
 
 

@@ -81,8 +81,8 @@ def log(*a):
 def main():
     args = parse()
     if args.gpus != 1:
-        print(json.dumps({"error": "this build runs on one GPU only; --gpus must be 1 (the path shards by head "
-                                   "with no communication, see the design notes)"}))
+        print(json.dumps({"error": "this benchmark runs on one GPU only; --gpus must be 1 (heads are independent, "
+                                   "so the path would shard by head with no communication)"}))
         sys.exit(2)
     import numpy as np
     import torch

@@ -75,7 +75,7 @@ extern "C" {
 /* status codes */
 #define RA_OK 0
 #define RA_ERR_INVALID (-1)     /* bad shape, split, grid, group, null pointer */
-#define RA_ERR_UNSUPPORTED (-2) /* valid request this build does not implement */
+#define RA_ERR_UNSUPPORTED (-2) /* valid request the library does not implement */
 #define RA_ERR_WORKSPACE (-3)   /* workspace missing or smaller than required */
 #define RA_ERR_HIP (-4)         /* a HIP runtime call failed (see last_error) */
 

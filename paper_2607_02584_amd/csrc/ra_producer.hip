@@ -159,8 +159,19 @@ __device__ __forceinline__ void rope_tile(const RopeTables& t, const QkArgs& a, 
     raw[p] = *reinterpret_cast<const uint2*>(xb + static_cast<size_t>(n < a.N ? n : a.N - 1) * kD + 4 * cl);
   }
   __syncthreads();
+  // without the half rotation's per-row barriers, the table entries of eight
+  // rows are fetched before any of them is used, so their loads overlap
+  // instead of waiting one row at a time
+  float4 gt[8][2];
+#pragma unroll
   for (int p = 0; p < 16; ++p) {
     const int nl = p * 8 + rr, n = tile * kTile + nl;
+    if (!half && (p & 7) == 0) {
+#pragma unroll
+      for (int q = 0; q < 8; ++q)
+#pragma unroll
+        for (int i = 0; i < 2; ++i) gt[q][i] = ps.tab[i][pos[(p + q) * 8 + rr][ps.axis[i]] * ps.npair[i]];
+    }
     float y[4] = {0.f, 0.f, 0.f, 0.f};
     if (n < a.N) {
       const float x[4] = {h2f<F16>(static_cast<uint16_t>(raw[p].x & 0xffff)),
@@ -169,7 +180,7 @@ __device__ __forceinline__ void rope_tile(const RopeTables& t, const QkArgs& a, 
                           h2f<F16>(static_cast<uint16_t>(raw[p].y >> 16))};
 #pragma unroll
       for (int i = 0; i < 2; ++i) {
-        const float4 g = ps.tab[i][pos[nl][ps.axis[i]] * ps.npair[i]];
+        const float4 g = half ? ps.tab[i][pos[nl][ps.axis[i]] * ps.npair[i]] : gt[p & 7][i];
         const float x0 = x[2 * i], x1 = x[2 * i + 1];
         y[2 * i] = __fmaf_rn(x1, g.z, __fmul_rn(x0, g.x));
         y[2 * i + 1] = __fmaf_rn(x1, g.w, __fmul_rn(x0, g.y));

@@ -374,9 +374,21 @@ def cpu_baseline(w, q, k, v, seconds):
     el = time.perf_counter() - t
     val = 4.0 * rows * w.N * 128 / el / 1e12
     log(f"cpu oracle: {rows} query rows over {heads} head(s) in {el:.1f} s on {ora.threads()} threads")
+    # the 1024-token case in full (both heads, every row), for scale
+    from paper_2607_02584_amd import datagen as dg
+    w1 = dg.WORKLOADS["c1"]
+    q1, k1, v1 = dg.make_inputs(w1)
+    geo1 = ora.Geometry(w1.T, w1.Hg, w1.W, w1.split, w1.theta)
+    t1 = time.perf_counter()
+    for h in range(w1.H):
+        ora.fwd_int4_head(geo1, cfg, q1[0, h], k1[0, h], v1[0, h])
+    e1 = time.perf_counter() - t1
+    log(f"cpu oracle: the 1024-token case in full in {e1:.2f} s")
     return {"value": round(val, 5), "unit": "TOPS", "cores": ora.threads(), "kind": "oracle",
             "sample": f"{heads} head(s) of {w.name}: each head's producer pass over all {w.N} tokens, then "
-                      f"{rows} query rows in all against all {w.N} keys ({el:.1f} s wall)"}
+                      f"{rows} query rows in all against all {w.N} keys ({el:.1f} s wall)",
+            "c1_full": {"seconds": round(e1, 3), "tops": round(w1.ops() / e1 / 1e12, 5),
+                        "what": "B=1 H=2 N=1024, producers and every query row"}}
 
 
 if __name__ == "__main__":

@@ -110,9 +110,9 @@ def main():
     stream = torch.cuda.current_stream()
 
     def step(ev=None):
-        ra.quantize_qk(p, qd, kd, bufs["q_codes"], bufs["q_scale"], bufs["k_codes"], bufs["k_scale"],
-                       bufs["mu_k"], ws)
-        ra.quantize_v(p, vd, bufs["v_codes"], bufs["v_scale"], bufs["mu_v"], ws)
+        # the Q, K and V producers in one call (their passes run concurrently)
+        ra.quantize_qkv(p, qd, kd, vd, bufs["q_codes"], bufs["q_scale"], bufs["k_codes"], bufs["k_scale"],
+                        bufs["v_codes"], bufs["v_scale"], ws, mu_k=bufs["mu_k"], mu_v=bufs["mu_v"])
         if ev is not None:
             ev[0].record(stream)
         ra.attn_int4(p, bufs["q_codes"], bufs["q_scale"], bufs["k_codes"], bufs["k_scale"], bufs["v_codes"],
@@ -233,9 +233,8 @@ def main():
 
             def tstep():
                 e0.record(stream)
-                ra.quantize_qk(pt, qd, kd, bt["q_codes"], bt["q_scale"], bt["k_codes"], bt["k_scale"], bt["mu_k"],
-                               wst, k_bias=kb)
-                ra.quantize_v(pt, vd, bt["v_codes"], bt["v_scale"], bt["mu_v"], wst)
+                ra.quantize_qkv(pt, qd, kd, vd, bt["q_codes"], bt["q_scale"], bt["k_codes"], bt["k_scale"],
+                                bt["v_codes"], bt["v_scale"], wst, mu_k=bt["mu_k"], mu_v=bt["mu_v"], k_bias=kb)
                 e1.record(stream)
                 ra.attn_int4(pt, bt["q_codes"], bt["q_scale"], bt["k_codes"], bt["k_scale"], bt["v_codes"],
                              bt["v_scale"], bt["mu_v"], ot, k_bias=kb)

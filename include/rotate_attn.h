@@ -30,6 +30,11 @@
  *    device memory (allocated on first use of a geometry, never freed before
  *    process exit).  That first call is therefore synchronous and must not be
  *    made under HIP graph capture; later calls with the same geometry are not.
+ *  - The INT4 producers run Q, K and V passes concurrently on two internal
+ *    streams per device (default priority), forked from and joined back into
+ *    the caller's stream with events: every call still behaves as if it ran
+ *    in order on `stream`.  The streams are created on the first producer call
+ *    on a device (not under graph capture) and kept until process exit.
  *  - Results are deterministic: repeated calls give identical bytes.
  *
  * Packed INT4 layouts (written by the quantize calls, read by the attention)
@@ -185,6 +190,17 @@ int rotate_attn_quantize_qk(const ra_params* p, const void* q, const void* k, ui
  * that the attention adds back (zeros if smoothing is off). */
 int rotate_attn_quantize_v(const ra_params* p, const void* v, uint8_t* v_codes, float* v_scale,
                            float* mu_v, void* workspace, size_t workspace_bytes, void* stream);
+
+/* Both producers in one call: the same results as quantize_qk followed by
+ * quantize_v (bit for bit), with the Q, K and V passes running concurrently
+ * (K and V on two library-internal streams per device, forked from and joined
+ * back into `stream` with events; created on the first call on a device, which
+ * must therefore not be made under graph capture).  Arguments as in the two
+ * calls; mu_k, mu_q, mu_v nullable; k_bias required with RA_SMOOTH_Q. */
+int rotate_attn_quantize_qkv(const ra_params* p, const void* q, const void* k, const void* v,
+                             uint8_t* q_codes, float* q_scale, uint8_t* k_codes, float* k_scale,
+                             uint8_t* v_codes, float* v_scale, float* mu_k, float* mu_q, float* mu_v,
+                             float* k_bias, void* workspace, size_t workspace_bytes, void* stream);
 
 /* INT4 attention on already quantized operands (Sec. 4.2): S = Q~ K~^T on the
  * int8 matrix cores (exact int32), blockwise online softmax with blocks of

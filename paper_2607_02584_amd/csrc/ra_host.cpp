@@ -284,8 +284,46 @@ float kc_of(const ra_params* p) {
 
 hipStream_t st(void* s) { return static_cast<hipStream_t>(s); }
 
+// ---------------------------------------------------- concurrent producers --
+// The producer passes of Q, K and V are independent chains; the library runs
+// them on two internal streams per device (default priority), forked from and
+// joined back into the caller's stream with events.  The fork/join pairs are
+// issued under a mutex so that concurrent callers cannot cross their events.
+
+struct Forks {
+  hipStream_t aux[2] = {nullptr, nullptr};
+  hipEvent_t ev[4] = {nullptr, nullptr, nullptr, nullptr};  // fork, Q sums done, K done, V done
+};
+
+std::mutex g_fork_mu;
+std::map<int, Forks> g_forks;
+
+int get_forks(Forks** out) {
+  int dev = 0;
+  RA_CHECK_HIP(hipGetDevice(&dev));
+  auto it = g_forks.find(dev);
+  if (it == g_forks.end()) {
+    Forks f;
+    for (auto& a : f.aux) RA_CHECK_HIP(hipStreamCreateWithFlags(&a, hipStreamNonBlocking));
+    for (auto& e : f.ev) RA_CHECK_HIP(hipEventCreateWithFlags(&e, hipEventDisableTiming));
+    it = g_forks.emplace(dev, f).first;
+  }
+  *out = &it->second;
+  return RA_OK;
+}
+
+// s2 starts after everything enqueued on s so far
+int fork_to(hipStream_t s, hipStream_t s2, hipEvent_t e) {
+  RA_CHECK_HIP(hipEventRecord(e, s));
+  RA_CHECK_HIP(hipStreamWaitEvent(s2, e, 0));
+  return RA_OK;
+}
+
+// Q's passes run on s, K's on s2 (joined back into s at the end); the caller
+// holds g_fork_mu and has forked s2 from s.
 int qk_impl(const ra_params* p, const void* q, const void* k, uint8_t* qc, float* qs, uint8_t* kc, float* ks,
-            float* mu_k, float* mu_q, float* kbias, const Int4Ws& w, hipStream_t s) {
+            float* mu_k, float* mu_q, float* kbias, const Int4Ws& w, hipStream_t s, hipStream_t s2,
+            const Forks& f) {
   const Sizes z = sizes_of(p);
   ra::RopeTables t;
   int rc = get_tables(p, &t);
@@ -300,9 +338,9 @@ int qk_impl(const ra_params* p, const void* q, const void* k, uint8_t* qc, float
   const bool center = (p->smooth & RA_SMOOTH_K) != 0;
   if (center) {
     // exact fixed-point channel sums of the rotated K, accumulated by atomics
-    RA_CHECK_HIP(ra::launch_fill_zero_u32(reinterpret_cast<uint32_t*>(w.ksum), static_cast<int64_t>(2 * z.partial), s));
+    RA_CHECK_HIP(ra::launch_fill_zero_u32(reinterpret_cast<uint32_t*>(w.ksum), static_cast<int64_t>(2 * z.partial), s2));
     a.x = static_cast<const uint16_t*>(k);
-    RA_CHECK_HIP(ra::launch_qk_sums(t, a, static_cast<int>(z.BH), s));
+    RA_CHECK_HIP(ra::launch_qk_sums(t, a, static_cast<int>(z.BH), s2));
   } else if (mu_k) {
     RA_CHECK_HIP(ra::launch_fill_zero_u32(reinterpret_cast<uint32_t*>(mu_k), static_cast<int64_t>(z.mu), s));
   }
@@ -313,6 +351,9 @@ int qk_impl(const ra_params* p, const void* q, const void* k, uint8_t* qc, float
     aq.sums = w.qsum;
     aq.x = static_cast<const uint16_t*>(q);
     RA_CHECK_HIP(ra::launch_qk_sums(t, aq, static_cast<int>(z.BH), s));
+    // K's quantization needs mu_Q for the key bias
+    RA_CHECK_HIP(hipEventRecord(f.ev[1], s));
+    RA_CHECK_HIP(hipStreamWaitEvent(s2, f.ev[1], 0));
   } else if (mu_q) {
     RA_CHECK_HIP(ra::launch_fill_zero_u32(reinterpret_cast<uint32_t*>(mu_q), static_cast<int64_t>(z.mu), s));
   }
@@ -333,7 +374,41 @@ int qk_impl(const ra_params* p, const void* q, const void* k, uint8_t* qc, float
   a.group = p->k_group;
   a.qsums = center_q ? w.qsum : nullptr;
   a.bias = center_q ? kbias : nullptr;
-  RA_CHECK_HIP(ra::launch_qk_quant(t, a, static_cast<int>(z.BH), s));
+  RA_CHECK_HIP(ra::launch_qk_quant(t, a, static_cast<int>(z.BH), s2));
+  // join: s continues once K is done
+  RA_CHECK_HIP(hipEventRecord(f.ev[2], s2));
+  RA_CHECK_HIP(hipStreamWaitEvent(s, f.ev[2], 0));
+  return RA_OK;
+}
+
+// quantize_qk on stream s (K's chain forked onto an internal stream)
+int qk_run(const ra_params* p, const void* q, const void* k, uint8_t* qc, float* qs, uint8_t* kc, float* ks,
+           float* mu_k, float* mu_q, float* kbias, const Int4Ws& w, hipStream_t s) {
+  std::lock_guard<std::mutex> lock(g_fork_mu);
+  Forks* f = nullptr;
+  int rc = get_forks(&f);
+  if (rc) return rc;
+  if ((rc = fork_to(s, f->aux[0], f->ev[0]))) return rc;
+  return qk_impl(p, q, k, qc, qs, kc, ks, mu_k, mu_q, kbias, w, s, f->aux[0], *f);
+}
+
+int v_impl(const ra_params* p, const void* v, uint8_t* vc, float* vs, float* mu_v, const Int4Ws& w, hipStream_t s);
+
+// quantize_qk and quantize_v at once: Q on s, K and V on one internal stream each
+int qkv_run(const ra_params* p, const void* q, const void* k, const void* v, uint8_t* qc, float* qs, uint8_t* kc,
+            float* ks, uint8_t* vc, float* vs, float* mu_k, float* mu_q, float* mu_v, float* kbias, const Int4Ws& w,
+            hipStream_t s) {
+  std::lock_guard<std::mutex> lock(g_fork_mu);
+  Forks* f = nullptr;
+  int rc = get_forks(&f);
+  if (rc) return rc;
+  RA_CHECK_HIP(hipEventRecord(f->ev[0], s));
+  RA_CHECK_HIP(hipStreamWaitEvent(f->aux[0], f->ev[0], 0));
+  RA_CHECK_HIP(hipStreamWaitEvent(f->aux[1], f->ev[0], 0));
+  if ((rc = v_impl(p, v, vc, vs, mu_v, w, f->aux[1]))) return rc;
+  if ((rc = qk_impl(p, q, k, qc, qs, kc, ks, mu_k, mu_q, kbias, w, s, f->aux[0], *f))) return rc;
+  RA_CHECK_HIP(hipEventRecord(f->ev[3], f->aux[1]));
+  RA_CHECK_HIP(hipStreamWaitEvent(s, f->ev[3], 0));
   return RA_OK;
 }
 
@@ -488,7 +563,7 @@ int rotate_attn_quantize_qk(const ra_params* p, const void* q, const void* k, ui
   if ((p->smooth & RA_SMOOTH_Q) && !k_bias) return fail(RA_ERR_INVALID, "RA_SMOOTH_Q needs k_bias");
   const Int4Ws need = carve_int4(p, nullptr);
   if ((rc = check_ws(workspace, workspace_bytes, need.total))) return rc;
-  return qk_impl(p, q, k, q_codes, q_scale, k_codes, k_scale, mu_k, mu_q, k_bias, carve_int4(p, workspace),
+  return qk_run(p, q, k, q_codes, q_scale, k_codes, k_scale, mu_k, mu_q, k_bias, carve_int4(p, workspace),
                  st(stream));
 }
 
@@ -500,6 +575,21 @@ int rotate_attn_quantize_v(const ra_params* p, const void* v, uint8_t* v_codes, 
   const Int4Ws need = carve_int4(p, nullptr);
   if ((rc = check_ws(workspace, workspace_bytes, need.total))) return rc;
   return v_impl(p, v, v_codes, v_scale, mu_v, carve_int4(p, workspace), st(stream));
+}
+
+int rotate_attn_quantize_qkv(const ra_params* p, const void* q, const void* k, const void* v, uint8_t* q_codes,
+                             float* q_scale, uint8_t* k_codes, float* k_scale, uint8_t* v_codes, float* v_scale,
+                             float* mu_k, float* mu_q, float* mu_v, float* k_bias, void* workspace,
+                             size_t workspace_bytes, void* stream) {
+  int rc = validate(p);
+  if (rc) return rc;
+  if (!q || !k || !v || !q_codes || !q_scale || !k_codes || !k_scale || !v_codes || !v_scale)
+    return fail(RA_ERR_INVALID, "NULL tensor pointer");
+  if ((p->smooth & RA_SMOOTH_Q) && !k_bias) return fail(RA_ERR_INVALID, "RA_SMOOTH_Q needs k_bias");
+  const Int4Ws need = carve_int4(p, nullptr);
+  if ((rc = check_ws(workspace, workspace_bytes, need.total))) return rc;
+  return qkv_run(p, q, k, v, q_codes, q_scale, k_codes, k_scale, v_codes, v_scale, mu_k, mu_q, mu_v, k_bias,
+                 carve_int4(p, workspace), st(stream));
 }
 
 int rotate_attn_attn_int4(const ra_params* p, const uint8_t* q_codes, const float* q_scale, const uint8_t* k_codes,
@@ -538,8 +628,9 @@ int rotate_attn_fwd_int4(const ra_params* p, const void* q, const void* k, const
   const Int4Ws need = carve_int4(p, nullptr);
   if ((rc = check_ws(workspace, workspace_bytes, need.total))) return rc;
   const Int4Ws w = carve_int4(p, workspace);
-  if ((rc = qk_impl(p, q, k, w.qc, w.qs, w.kc, w.ks, nullptr, nullptr, w.kbias, w, st(stream)))) return rc;
-  if ((rc = v_impl(p, v, w.vc, w.vs, nullptr, w, st(stream)))) return rc;
+  if ((rc = qkv_run(p, q, k, v, w.qc, w.qs, w.kc, w.ks, w.vc, w.vs, nullptr, nullptr, nullptr, w.kbias, w,
+                    st(stream))))
+    return rc;
   const float* mu = (p->smooth & RA_SMOOTH_V) ? w.mu_v : nullptr;
   return attn_impl(p, w.qc, w.qs, w.kc, w.ks, w.vc, w.vs, mu, w.kbias, o, false, 0, 0, 0, nullptr, nullptr, nullptr,
                    st(stream));

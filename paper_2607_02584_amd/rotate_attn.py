@@ -66,6 +66,7 @@ def lib():
             "rotate_attn_workspace_size": [PP, ctypes.c_int, ctypes.POINTER(ctypes.c_size_t)],
             "rotate_attn_quantize_qk": [PP, P, P, P, P, P, P, P, P, P, P, ctypes.c_size_t, P],
             "rotate_attn_quantize_v": [PP, P, P, P, P, P, ctypes.c_size_t, P],
+            "rotate_attn_quantize_qkv": [PP, P, P, P, P, P, P, P, P, P, P, P, P, P, P, ctypes.c_size_t, P],
             "rotate_attn_attn_int4": [PP, P, P, P, P, P, P, P, P, P, P],
             "rotate_attn_attn_int4_debug": [PP, P, P, P, P, P, P, P, P, P, ctypes.c_int32, ctypes.c_int32,
                                             ctypes.c_int32, P, P, P, P],
@@ -201,6 +202,23 @@ def quantize_v(p, v, v_codes, v_scale, mu_v, ws, stream=None):
     _need(ws, workspace_size(p, PATH_INT4), "workspace")
     _check(lib().rotate_attn_quantize_v(ctypes.byref(p), _ptr(v), _ptr(v_codes), _ptr(v_scale), _ptr(mu_v),
                                         _ptr(ws), _nbytes(ws), _stream(stream)), "rotate_attn_quantize_v")
+
+
+def quantize_qkv(p, q, k, v, q_codes, q_scale, k_codes, k_scale, v_codes, v_scale, ws, stream=None, mu_k=None,
+                 mu_q=None, mu_v=None, k_bias=None):
+    """quantize_qk and quantize_v in one call (the passes run concurrently)."""
+    L = layout(p)
+    nin, _ = _io_bytes(p)
+    for t, name in ((q, "q"), (k, "k"), (v, "v")):
+        _need(t, nin, name)
+    _check_codes(p, L, q_codes, q_scale, k_codes, k_scale, v_codes, v_scale,
+                 mu=((mu_k, "mu_k"), (mu_q, "mu_q"), (mu_v, "mu_v")), k_bias=k_bias,
+                 need_bias=bool(p.smooth & SMOOTH_Q))
+    _need(ws, workspace_size(p, PATH_INT4), "workspace")
+    _check(lib().rotate_attn_quantize_qkv(ctypes.byref(p), _ptr(q), _ptr(k), _ptr(v), _ptr(q_codes), _ptr(q_scale),
+                                          _ptr(k_codes), _ptr(k_scale), _ptr(v_codes), _ptr(v_scale), _ptr(mu_k),
+                                          _ptr(mu_q), _ptr(mu_v), _ptr(k_bias), _ptr(ws), _nbytes(ws),
+                                          _stream(stream)), "rotate_attn_quantize_qkv")
 
 
 def attn_int4(p, q_codes, q_scale, k_codes, k_scale, v_codes, v_scale, mu_v, o, stream=None, k_bias=None):

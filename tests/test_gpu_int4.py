@@ -351,3 +351,27 @@ def test_c2_full_size_sampled_rows(ora, variant):
     ra.fwd_int4(p, qd, kd, vd, o2, ws)
     torch.cuda.synchronize()
     assert torch.isfinite(o).all() and torch.equal(o, o2)
+
+
+@pytest.mark.parametrize("wname,case", [("c1", (1, 128, 128, 128, 128, 0, 3, 0)), ("c1", (3, 1, 1, 256, 64, 0, 7, 1)),
+                                        ("ragged300", (2, 128, 64, 128, 64, 1, 7, 1)), ("c2", (1, 128, 128, 128, 128, 0, 3, 0))])
+def test_quantize_qkv_equals_the_two_producers(ora, wname, case):
+    """The fused producer call (Q, K and V passes on concurrent streams) writes
+    exactly the bytes of quantize_qk followed by quantize_v, every time."""
+    torch, ra = _torch(), _ra()
+    from paper_2607_02584_amd import datagen as dg
+    w = dg.WORKLOADS[wname] if wname in ("c1", "c2") else _small_ragged(wname)
+    rot, qg, kg, vg, kv, pq, sm, vrot = case
+    print(f"[qkv] {wname} case={case}", flush=True)
+    q, k, v = _inputs(w)
+    p = _params(ra, w, rot, qg, kg, vg, kv, pq, sm, vrot=vrot)
+    ref, (qd, kd, vd), ws = _run_quant(torch, ra, p, q, k, v)
+    for rep in range(3):
+        b = ra.alloc_int4(p)
+        ra.quantize_qkv(p, qd, kd, vd, b["q_codes"], b["q_scale"], b["k_codes"], b["k_scale"], b["v_codes"],
+                        b["v_scale"], ws, mu_k=b["mu_k"], mu_q=b["mu_q"], mu_v=b["mu_v"], k_bias=b["k_bias"])
+        torch.cuda.synchronize()
+        for name in ("q_codes", "q_scale", "k_codes", "k_scale", "v_codes", "v_scale", "mu_k", "mu_q", "mu_v"):
+            assert torch.equal(b[name], ref[name]), (name, rep)
+        if sm & 4:
+            assert torch.equal(b["k_bias"], ref["k_bias"])

@@ -816,3 +816,54 @@ def test_int4_pipeline_tracks_fp64_attention(ora):
     for rot in (0, 1, 2):
         O, _ = ora.fwd_int4_head(geo, ora.Int4Config(rotation=rot, q_group=1, k_group=1), q[0, 0], k[0, 0], v[0, 0])
         assert cos(O, ref) > 0.8
+
+
+def _paper_exact_blockwise(qc, qs, kc, ks, vc, vs, kv, pscale=15.0, sm=1 / math.sqrt(128)):
+    """The Sec. 4.2 blockwise algorithm in fp64 with the true exponential, written
+    directly with numpy over whole blocks (a different route from the C bit model):
+    m_j = max(m_{j-1}, rowmax S_j), P = exp(S_j - m_j), u = rint(pscale P),
+    O = sum of alpha-rescaled (u / pscale) V over blocks, divided by sum of P."""
+    N = qc.shape[0]
+    S = (qc.astype(np.float64) * qs[:, None].astype(np.float64)) @ \
+        (kc.astype(np.float64) * ks[:, None].astype(np.float64)).T * sm
+    V = vc.astype(np.float64) * vs.astype(np.float64)
+    m = np.full(N, -np.inf)
+    l = np.zeros(N)
+    acc = np.zeros((N, V.shape[1]))
+    us, ms = [], []
+    for j0 in range(0, N, kv):
+        Sj = S[:, j0:j0 + kv]
+        mn = np.maximum(m, Sj.max(1))
+        alpha = np.where(np.isfinite(m), np.exp(m - mn), 0.0)
+        P = np.exp(Sj - mn[:, None])
+        u = np.clip(np.rint(pscale * P), 0, pscale)
+        l = alpha * l + P.sum(1)
+        acc = alpha[:, None] * acc + (u / pscale) @ V[j0:j0 + kv]
+        m = mn
+        us.append(pscale * P)
+        ms.append(mn)
+    return acc / l[:, None], np.concatenate(us, 1), np.stack(ms, 1)
+
+
+@pytest.mark.parametrize("kv,pq", [(128, 0), (64, 1)])
+def test_bit_model_tracks_the_paper_exact_algorithm(ora, kv, pq):
+    """The binary32 bit model (the GPU's contract) and the fp64 algorithm with the
+    true exponential take the same P codes except where pscale P lies within the
+    binary32 error of the exponent argument of a rounding boundary, and give the
+    same O to 1e-5 (one V scale per channel, so only the P path differs)."""
+    rng = np.random.default_rng(49)
+    N = 640
+    qc, qs, kc, ks, vc = _int4_inputs(rng, N)
+    vs = rng.uniform(0.1, 1.0, (1, 128)).astype(np.float32)
+    pscale = 7.0 if pq == 1 else 15.0
+    O, d = _attn(ora, qc, qs, kc, ks, vc, vs, None, v_group=N, kv_block=kv, p_quant=pq)
+    Oe, val, me = _paper_exact_blockwise(qc, qs, kc, ks, vc, vs, kv, pscale)
+    # the running maxima agree to the binary32 rounding of the dequantised scores
+    np.testing.assert_allclose(d["m"].astype(np.float64) * math.log(2), me, rtol=3e-7, atol=1e-6)
+    # codes: equal except inside a band of a few ulp of the exponent around a tie
+    # (the bit model rounds c, S c and x in binary32: |dx| <= 4 * 2^-24 * (|S c| + |m|))
+    diff = d["u"].astype(np.int64) != np.clip(np.rint(val), 0, pscale).astype(np.int64)
+    band = val * (8 * 2.0 ** -24 * (np.abs(me).max() + 10))
+    near = np.abs(val - np.floor(val) - 0.5) <= band
+    assert np.all(near[diff]), f"{int((diff & ~near).sum())} codes differ away from a tie"
+    assert np.abs(O - Oe).max() <= 1e-5 * np.abs(Oe).max()

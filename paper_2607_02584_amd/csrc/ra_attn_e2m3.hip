@@ -100,6 +100,26 @@ __device__ __forceinline__ v6i pack_fp6(v16f lo, v16f hi) {
   return r;
 }
 
+// Emits nothing; it makes the output tile's registers look read and written
+// here, so the multiplies before it are not sunk past the code after it.
+__device__ __forceinline__ void pin(v16f (&o)[4]) {
+#if defined(__HIP_DEVICE_COMPILE__)
+  asm volatile("" : "+v"(o[0]), "+v"(o[1]), "+v"(o[2]), "+v"(o[3]));
+#else
+  (void)o;
+#endif
+}
+
+// max(x, x of lane ^ 32): v_permlane32_swap exchanges the upper half of its
+// first operand with the lower half of its second, so with x in both the two
+// results hold, in every lane, x of that lane and x of lane ^ 32 (a register
+// move, no LDS round trip).
+__device__ __forceinline__ float max_halves(float x) {
+  const unsigned u = __float_as_uint(x);
+  const auto r = __builtin_amdgcn_permlane32_swap(u, u, false, false);
+  return fmaxf(__uint_as_float(r[0]), __uint_as_float(r[1]));
+}
+
 // 24-byte record -> operand registers (6 used dwords)
 __device__ __forceinline__ v8i load_rec(const uint8_t* p) {
   const uint2 a = *reinterpret_cast<const uint2*>(p);
@@ -271,6 +291,17 @@ __global__ __launch_bounds__(kThreads, 8 / kWaves) void k_attn_e2m3(AttnArgs a) 
       const int ch = t % NCH, kc = t / NCH;
       return load_rec(&sK[buf][(((ch * 2 + kc) * 2 + hh) * 32 + j) * 24]);
     };
+    // The V scale ratio of a new group rescales O' (register r of tile mt is
+    // channel 32 mt + j) while the score products run: it does not depend on
+    // S, so its multiplies fill the matrix-core latency.  They are issued
+    // unconditionally (by 1 within a V group: exact) so that they stay in the
+    // straight-line code between the products; O' is rescaled by the V ratio
+    // before alpha, as before.
+    const bool vchange = vr == 0 && jb > 0;   // first block of a new V group
+    if (++vr == a.v_bpg) vr = 0;
+    float4 rr = make_float4(1.f, 1.f, 1.f, 1.f);
+    if (vchange) rr = *reinterpret_cast<const float4*>(&sR[buf][4 * j]);
+    constexpr int RPS = 16 / NQ;   // O' registers rescaled per score product
     v8i ka = krec(0), kb = krec(1);
 #pragma unroll
     for (int t = 0; t < NQ; ++t) {
@@ -284,6 +315,14 @@ __global__ __launch_bounds__(kThreads, 8 / kWaves) void k_attn_e2m3(AttnArgs a) 
       } else {
         s[ch] = mfma6(ka, qop[1], s[ch]);
       }
+#pragma unroll
+      for (int r = RPS * t; r < RPS * (t + 1); ++r) {
+        of[0][r] = __fmul_rn(of[0][r], rr.x);
+        of[1][r] = __fmul_rn(of[1][r], rr.y);
+        of[2][r] = __fmul_rn(of[2][r], rr.z);
+        of[3][r] = __fmul_rn(of[3][r], rr.w);
+      }
+      pin(of);
       ka = kb;
       kb = kn;
       __builtin_amdgcn_sched_barrier(0);
@@ -313,10 +352,6 @@ __global__ __launch_bounds__(kThreads, 8 / kWaves) void k_attn_e2m3(AttnArgs a) 
     //      a fully masked chunk gives -inf, or NaN when c == 0, which fmax ignores) ----
     float cch[NCH];
     float tmax = -INFINITY;
-    const bool vchange = vr == 0 && jb > 0;   // first block of a new V group
-    if (++vr == a.v_bpg) vr = 0;
-    float4 rr = make_float4(1.f, 1.f, 1.f, 1.f);
-    if (vchange) rr = *reinterpret_cast<const float4*>(&sR[buf][4 * j]);
     if (QB) {
       // t = fma(S, c, bias) in place of S; the maximum is over t
 #pragma unroll
@@ -374,7 +409,7 @@ __global__ __launch_bounds__(kThreads, 8 / kWaves) void k_attn_e2m3(AttnArgs a) 
           tmax = fmaxf(tmax, __fmul_rn(s[ch][r], __fmul_rn(cq, sKs[buf][kl])));
         }
     }
-    tmax = fmaxf(tmax, __shfl_xor(tmax, 32));
+    tmax = max_halves(tmax);
     const float mnew = fmaxf(m, tmax);
     const float alpha = __builtin_amdgcn_exp2f(m - mnew);
     m = mnew;
@@ -382,17 +417,8 @@ __global__ __launch_bounds__(kThreads, 8 / kWaves) void k_attn_e2m3(AttnArgs a) 
     // exponent, so the exponential yields the packing input directly
     const float mq = __fsub_rn(mnew, kLog2P);
 
-    // ---- rescale O' for the block's V scale and the new maximum; register r of
-    //      tile mt is channel 32 mt + j of query 8 (r / 4) + 4 hh + r % 4 ----
-    if (vchange) {
-#pragma unroll
-      for (int r = 0; r < 16; ++r) {
-        of[0][r] = __fmul_rn(of[0][r], rr.x);
-        of[1][r] = __fmul_rn(of[1][r], rr.y);
-        of[2][r] = __fmul_rn(of[2][r], rr.z);
-        of[3][r] = __fmul_rn(of[3][r], rr.w);
-      }
-    }
+    // ---- rescale O' for the new maximum; register r of tile mt is channel
+    //      32 mt + j of query 8 (r / 4) + 4 hh + r % 4 ----
     // only the registers whose two queries (8 (r / 4) + r % 4 in the lower
     // wave half, 4 more in the upper) moved their maximum are rescaled
     const unsigned long long moved = __ballot(alpha != 1.0f);
@@ -419,6 +445,16 @@ __global__ __launch_bounds__(kThreads, 8 / kWaves) void k_attn_e2m3(AttnArgs a) 
     float ls[4];   // independent partial sums, started by the first four values
 #pragma unroll
     for (int gg = 0; gg < NG; ++gg) {
+      // the group's four V records (B operands of O = P V~) are read before
+      // its probabilities, so the LDS latency is hidden behind them; one
+      // record per scheduling region, so reads of two records are not merged
+      // into one instruction (which costs register moves)
+      v8i vrec[4];
+#pragma unroll
+      for (int t = 0; t < 4; ++t) {
+        vrec[t] = load_rec(&sV[buf][(((gg * 4 + t) * 2 + hh) * 32 + j) * 24]);
+        __builtin_amdgcn_sched_barrier(0);
+      }
 #pragma unroll
       for (int c2 = 0; c2 < 2; ++c2) {
         const int ch = 2 * gg + c2;
@@ -459,16 +495,8 @@ __global__ __launch_bounds__(kThreads, 8 / kWaves) void k_attn_e2m3(AttnArgs a) 
             }
         }
       }
-      {
-        const v8i v0 = load_rec(&sV[buf][(((gg * 4 + 0) * 2 + hh) * 32 + j) * 24]);
-        const v8i v1 = load_rec(&sV[buf][(((gg * 4 + 1) * 2 + hh) * 32 + j) * 24]);
-        of[0] = mfma6(B, v0, of[0]);
-        const v8i v2 = load_rec(&sV[buf][(((gg * 4 + 2) * 2 + hh) * 32 + j) * 24]);
-        of[1] = mfma6(B, v1, of[1]);
-        const v8i v3 = load_rec(&sV[buf][(((gg * 4 + 3) * 2 + hh) * 32 + j) * 24]);
-        of[2] = mfma6(B, v2, of[2]);
-        of[3] = mfma6(B, v3, of[3]);
-      }
+#pragma unroll
+      for (int t = 0; t < 4; ++t) of[t] = mfma6(B, vrec[t], of[t]);
       __builtin_amdgcn_sched_barrier(0);
     }
     l = __fmaf_rn(l, alpha, (ls[0] + ls[1]) + (ls[2] + ls[3]));

@@ -152,6 +152,7 @@ def main():
     log(f"int4 step {ms_step:.3f} ms ({tops:.1f} TOPS); attention kernel {attn_ms:.3f} ms ({attn_tops:.1f} TOPS)")
 
     extra = {}
+    fb_kernel_ms = None
     if not args.skip_fallback:
         pf = ra.make_params(w.B, w.H, (w.T, w.Hg, w.W), w.split, w.theta, rotation=ra.ROT_NONE, out_dtype=ra.BF16)
         wsf = ra.workspace(pf, ra.PATH_FP16, dev)
@@ -173,6 +174,7 @@ def main():
         torch.cuda.synchronize()
         f_step = a0.elapsed_time(a1) / nrep
         f_attn = float(np.mean([x.elapsed_time(y) for x, y in e]))
+        fb_kernel_ms = f_attn
         extra = {
             "bf16_fallback": {"op_ms": round(f_step, 4), "kernel_ms": round(f_attn, 4),
                               "kernel_tflops": round(ops / (f_attn * 1e-3) / 1e12, 1),
@@ -205,9 +207,10 @@ def main():
         except Exception as exc:   # context only: a missing backend is reported, not fatal
             sdpa = {"unavailable": f"{type(exc).__name__}: {str(exc)[:120]}"}
 
-    # variants of the method on the same inputs and kernel family: the paper's
-    # own Q/K granularity (per token, Sec. 5.1), Q smoothing with the per-key
-    # bias (Sec. 4), the full Hadamard rotation (the Sec. 5.3 baseline)
+    # variants of the method on the same inputs: the paper's own Q/K granularity
+    # (per token, Sec. 5.1), Q smoothing with the per-key bias (Sec. 4), the full
+    # Hadamard rotation (the Sec. 5.3 baseline), per-channel V scales, and the
+    # int8-matrix-core kernel over nibble-packed codes
     variants = None
     if args.container == "e2m3" and not args.skip_fallback:
         variants = {}
@@ -217,14 +220,19 @@ def main():
                                 smooth=ra.SMOOTH_K | ra.SMOOTH_V | ra.SMOOTH_Q),
             "full_hadamard": dict(rotation=ra.ROT_HADAMARD, q_group=128, k_group=128,
                                   smooth=ra.SMOOTH_K | ra.SMOOTH_V),
-            # one V scale per channel over all tokens: no per-block V-scale ratio in the kernel
+            # one V scale per channel over all tokens
             "per_channel_v": dict(rotation=ra.ROT_INTERLEAVED, q_group=128, k_group=128,
                                   smooth=ra.SMOOTH_K | ra.SMOOTH_V, v_group=N),
+            # the headline configuration with the codes packed two per byte and
+            # multiplied on the int8 matrix core (int32 accumulation), reported
+            # beside the FP6-operand kernel
+            "int8_nibble_container": dict(rotation=ra.ROT_INTERLEAVED, q_group=128, k_group=128,
+                                          smooth=ra.SMOOTH_K | ra.SMOOTH_V, code_format=ra.CODES_INT4),
         }
         for name, kw in specs.items():
-            kw = dict({"v_group": 128}, **kw)
+            kw = dict({"v_group": 128, "code_format": ra.CODES_E2M3}, **kw)
             pt = ra.make_params(w.B, w.H, (w.T, w.Hg, w.W), w.split, w.theta, kv_block=128,
-                                out_dtype=ra.BF16, code_format=ra.CODES_E2M3, **kw)
+                                out_dtype=ra.BF16, **kw)
             bt = ra.alloc_int4(pt, dev)
             wst = ra.workspace(pt, ra.PATH_INT4, dev)
             ot = torch.empty_like(o)
@@ -250,6 +258,10 @@ def main():
             kms = float(np.median(ka))
             variants[name] = {"kernel_ms": round(kms, 4), "kernel_tops": round(ops / (kms * 1e-3) / 1e12, 1),
                               "producer_ms": round(float(np.median(pa)), 4)}
+            if kw["code_format"] == ra.CODES_INT4:
+                variants[name]["kernel_frac_of_int8_peak"] = round(ops / (kms * 1e-3) / 1e12 / INT8_PEAK_TOPS, 4)
+                if fb_kernel_ms:
+                    variants[name]["speedup_vs_bf16_kernel"] = round(fb_kernel_ms / kms, 3)
             log(f"variant {name}: attention kernel {kms:.3f} ms, producers {variants[name]['producer_ms']} ms")
             del bt, wst, ot
 

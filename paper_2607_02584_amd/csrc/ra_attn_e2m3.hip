@@ -110,16 +110,6 @@ __device__ __forceinline__ void pin(v16f (&o)[4]) {
 #endif
 }
 
-// max(x, x of lane ^ 32): v_permlane32_swap exchanges the upper half of its
-// first operand with the lower half of its second, so with x in both the two
-// results hold, in every lane, x of that lane and x of lane ^ 32 (a register
-// move, no LDS round trip).
-__device__ __forceinline__ float max_halves(float x) {
-  const unsigned u = __float_as_uint(x);
-  const auto r = __builtin_amdgcn_permlane32_swap(u, u, false, false);
-  return fmaxf(__uint_as_float(r[0]), __uint_as_float(r[1]));
-}
-
 // 24-byte record -> operand registers (6 used dwords)
 __device__ __forceinline__ v8i load_rec(const uint8_t* p) {
   const uint2 a = *reinterpret_cast<const uint2*>(p);

@@ -235,7 +235,7 @@ __global__ __launch_bounds__(256, 2) void k_attn_int4(AttnArgs a) {
         tmax = fmaxf(tmax, __fmul_rn(mx, cch[ch]));
       }
     }
-    tmax = fmaxf(tmax, __shfl_xor(tmax, 32));
+    tmax = max_halves(tmax);
     const float mnew = fmaxf(m, tmax);
     const float alpha = __builtin_amdgcn_exp2f(m - mnew);
     m = mnew;

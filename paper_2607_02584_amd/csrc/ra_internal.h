@@ -12,6 +12,16 @@ constexpr int kD = 128;       // head dimension
 constexpr int kTile = 128;    // producer token tile; Npad is a multiple of it
 constexpr float kInvSqrtD = 0.0883883476483184405501055452631f;  // fl32(1/sqrt(128))
 
+// max(x, x of lane ^ 32) in a wave of 64: v_permlane32_swap (gfx950) exchanges
+// the upper half of its first operand with the lower half of its second, so
+// with x in both, the two results hold x of the lane and x of lane ^ 32 in
+// every lane (a register move, no LDS round trip).
+__device__ __forceinline__ float max_halves(float x) {
+  const unsigned u = __float_as_uint(x);
+  const auto r = __builtin_amdgcn_permlane32_swap(u, u, false, false);
+  return fmaxf(__uint_as_float(r[0]), __uint_as_float(r[1]));
+}
+
 // RoPE/rotation tables on the device.  For axis a the table holds, for every
 // position pos in [0, extent_a) and pair k in [0, D_a/2), the binary32 2x2
 // block G = M (or M R for the merged interleaved rotation) as

@@ -439,8 +439,13 @@ int v_impl(const ra_params* p, const void* v, uint8_t* vc, float* vs, float* mu_
     a.center = 0;
     a.mu_out = nullptr;
   }
-  RA_CHECK_HIP(ra::launch_fill_zero_u32(w.amax, static_cast<int64_t>(z.amax), s));
-  RA_CHECK_HIP(ra::launch_v_amax(a, static_cast<int>(z.BH), s));
+  // groups of 64 or 128 tokens never straddle a 128-token tile (they start at
+  // multiples of the group size): the quantize pass finds their maxima itself
+  a.local_amax = p->v_group == 64 || p->v_group == 128;
+  if (!a.local_amax) {
+    RA_CHECK_HIP(ra::launch_fill_zero_u32(w.amax, static_cast<int64_t>(z.amax), s));
+    RA_CHECK_HIP(ra::launch_v_amax(a, static_cast<int>(z.BH), s));
+  }
   RA_CHECK_HIP(ra::launch_v_quant(a, static_cast<int>(z.BH), s));
   return RA_OK;
 }

@@ -63,6 +63,8 @@ struct VArgs {
   int N, Npad, group, ngroups, is_fp16;
   int e2m3;
   int vhad;               // rotate each V row by the 128-point Hadamard before smoothing
+  int local_amax;         // groups of 64 or 128 tokens: the quantize pass takes the group maxima
+                          // from its own tile (no amax pass, amax unused)
 };
 
 struct AttnArgs {

@@ -453,13 +453,40 @@ template <bool F16, bool VHAD>
 __global__ __launch_bounds__(256) void k_v_quant(VArgs a) {
   __shared__ __align__(16) uint8_t ctile[kTile * 96];
   __shared__ float ginv[2][kD];
+  __shared__ float red[8][2][kD];
   const int tile = blockIdx.x, bh = blockIdx.y;
   const int tid = threadIdx.x, rr = tid >> 5, cl = tid & 31;
+  float z[16][4];
+  if (a.local_amax) {
+    // groups of 64 or 128 tokens lie inside this tile: their maxima come from
+    // the tile itself, per (tile half, channel) as in k_v_amax
+    load_v_tile<F16, VHAD>(a, bh, tile, z);
+    float mh[2][4] = {{0.f, 0.f, 0.f, 0.f}, {0.f, 0.f, 0.f, 0.f}};
+    for (int p = 0; p < 16; ++p)
+#pragma unroll
+      for (int c = 0; c < 4; ++c) mh[p >> 3][c] = fmaxf(mh[p >> 3][c], fabsf(z[p][c]));
+#pragma unroll
+    for (int hf = 0; hf < 2; ++hf)
+#pragma unroll
+      for (int c = 0; c < 4; ++c) red[rr][hf][4 * cl + c] = mh[hf][c];
+    __syncthreads();
+  }
   {
     const int hf = tid >> 7, ch = tid & 127;
     const int n0 = tile * kTile + hf * 64;
     const int g = vgroup_of(a, n0 < a.N ? n0 : a.N - 1);
-    const float m = __uint_as_float(a.amax[(static_cast<size_t>(bh) * a.ngroups + g) * kD + ch]);
+    float m;
+    if (a.local_amax) {
+      float m0 = 0.f, m1 = 0.f;
+#pragma unroll
+      for (int r = 0; r < 8; ++r) {
+        m0 = fmaxf(m0, red[r][0][ch]);
+        m1 = fmaxf(m1, red[r][1][ch]);
+      }
+      m = a.group == 64 ? (hf ? m1 : m0) : fmaxf(m0, m1);
+    } else {
+      m = __uint_as_float(a.amax[(static_cast<size_t>(bh) * a.ngroups + g) * kD + ch]);
+    }
     float s = 0.f, inv = 0.f;
     if (m > 0.f) {
       s = __fdiv_rn(m, 7.0f);
@@ -473,8 +500,7 @@ __global__ __launch_bounds__(256) void k_v_quant(VArgs a) {
   __syncthreads();
   if (a.center && a.mu_out && tile == 0 && rr == 0)
     *reinterpret_cast<float4*>(a.mu_out + bh * kD + 4 * cl) = mean4(a.sums + static_cast<size_t>(bh) * kD, a.N, cl);
-  float z[16][4];
-  load_v_tile<F16, VHAD>(a, bh, tile, z);
+  if (!a.local_amax) load_v_tile<F16, VHAD>(a, bh, tile, z);
   if (a.e2m3) {
     // group of 64 tokens gl = p/8, kappa = (p%8)*8 + rr, half h = (rr/4)%2; token kappa of a channel is
     // field 8*((kappa%32)/8) + 2*(kappa%4) + kappa/32 of record ((gl*4 + ch/32)*2 + h)*32 + ch%32.

@@ -168,7 +168,8 @@ __global__ __launch_bounds__(kThreads, 8 / kWaves) void k_attn_e2m3(AttnArgs a) 
   __shared__ __align__(16) float sKc[2][NCH];  // K scale of each 32-key chunk (grouped K)
   __shared__ __align__(16) float sB[2][QB ? KV : 1];  // per-key score bias fl(b Kc)
 
-  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  // the wave index is uniform: conditions on it are scalar branches
+  const int tid = threadIdx.x, lane = tid & 63, wave = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int hh = lane >> 5, j = lane & 31;
   int bh, qtile;
   xcd_tile(bh, qtile);
@@ -209,21 +210,31 @@ __global__ __launch_bounds__(kThreads, 8 / kWaves) void k_attn_e2m3(AttnArgs a) 
   // fetch_aux runs for blocks 0, 1, 2, ... in order; (fg, fr) = (V group, block
   // within the group) of the next block it fetches
   int fg = 0, fr = 0;
+  // Waves 0 and 1 (thread = channel) handle the V scales; thread 128 + t
+  // handles key t of the block (waves 2 and 3, or wave 2 alone for 64-key
+  // blocks), or the K scale of chunk t (t < NCH, grouped K: k_group is 32, 64
+  // or 128, so the group index is a shift).
+  const bool kwave = KV == 128 ? wave >= 2 : wave == 2;
+  const int kgs = __builtin_ctz(static_cast<unsigned>(a.k_group));
   auto fetch_aux = [&](int jb) {
     Aux f{0.f, 0.f, 0.f};
-    if (tid < kD) f.v = a.vs[(static_cast<size_t>(bh) * a.nvgroups + fg) * kD + tid];
+    if (wave < 2) f.v = a.vs[(static_cast<size_t>(bh) * a.nvgroups + fg) * kD + tid];
     if (++fr == a.v_bpg) {
       fr = 0;
       ++fg;
     }
     const int kt = tid - kD;
-    if (kt >= 0 && kt < (KTOK ? KV : NCH)) f.k = KTOK ? ksh[jb * KV + kt] : ksh[(jb * KV + kt * 32) / a.k_group];
-    if (QB && kt >= 0 && kt < KV) f.b = a.kbias[static_cast<size_t>(bh) * a.Npad + jb * KV + kt];
+    if (KTOK) {
+      if (kwave) f.k = ksh[jb * KV + kt];
+    } else if (wave == 2 && lane < NCH) {
+      f.k = ksh[(jb * KV + kt * 32) >> kgs];
+    }
+    if (QB && kwave) f.b = a.kbias[static_cast<size_t>(bh) * a.Npad + jb * KV + kt];
     return f;
   };
   float wcur = 1.0f;
   auto store_aux = [&](int jb, int buf, const Aux& f) {
-    if (tid < kD) {
+    if (wave < 2) {
       float r = 1.0f;
       if (f.v > 0.0f) {
         r = (jb == 0) ? 1.0f : wcur * __builtin_amdgcn_rcpf(f.v);
@@ -232,11 +243,12 @@ __global__ __launch_bounds__(kThreads, 8 / kWaves) void k_attn_e2m3(AttnArgs a) 
       sR[buf][(tid & 31) * 4 + (tid >> 5)] = r;
     }
     const int kt = tid - kD;
-    if (kt >= 0 && kt < (KTOK ? KV : NCH)) {
-      if (KTOK) sKs[buf][kt] = f.k;
-      else sKc[buf][kt] = f.k;
+    if (KTOK) {
+      if (kwave) sKs[buf][kt] = f.k;
+    } else if (wave == 2 && lane < NCH) {
+      sKc[buf][kt] = f.k;
     }
-    if (QB && kt >= 0 && kt < KV) sB[buf][kt] = __fmul_rn(f.b, a.Kc);
+    if (QB && kwave) sB[buf][kt] = __fmul_rn(f.b, a.Kc);
   };
 
   v16f of[4];
@@ -414,12 +426,16 @@ __global__ __launch_bounds__(kThreads, 8 / kWaves) void k_attn_e2m3(AttnArgs a) 
     const unsigned long long moved = __ballot(alpha != 1.0f);
     if (moved) {
 #pragma unroll
-      for (int r = 0; r < 16; ++r) {
-        const int q0 = 8 * (r >> 2) + (r & 3);
-        if ((moved >> q0) & 0x11ull) {
-          const float ar = __shfl(alpha, q0 + 4 * hh);
+      for (int g = 0; g < 4; ++g) {
+        if (!((moved >> (8 * g)) & 0xFFull)) continue;   // rows 8g .. 8g+7 kept their maximum
 #pragma unroll
-          for (int mt = 0; mt < 4; ++mt) of[mt][r] = __fmul_rn(of[mt][r], ar);
+        for (int r = 4 * g; r < 4 * g + 4; ++r) {
+          const int q0 = 8 * (r >> 2) + (r & 3);
+          if ((moved >> q0) & 0x11ull) {
+            const float ar = __shfl(alpha, q0 + 4 * hh);
+#pragma unroll
+            for (int mt = 0; mt < 4; ++mt) of[mt][r] = __fmul_rn(of[mt][r], ar);
+          }
         }
       }
     }

@@ -304,7 +304,11 @@ __global__ __launch_bounds__(kThreads, 8 / kWaves) void k_attn_e2m3(AttnArgs a) 
     float4 rr = make_float4(1.f, 1.f, 1.f, 1.f);
     if (vchange) rr = *reinterpret_cast<const float4*>(&sR[buf][4 * j]);
     constexpr int RPS = 16 / NQ;   // O' registers rescaled per score product
-    v8i ka = krec(0), kb = krec(1);
+    // (one record per scheduling region: reads of two records are not merged)
+    v8i ka = krec(0);
+    __builtin_amdgcn_sched_barrier(0);
+    v8i kb = krec(1);
+    __builtin_amdgcn_sched_barrier(0);
 #pragma unroll
     for (int t = 0; t < NQ; ++t) {
       const v8i kn = (t + 2 < NQ) ? krec(t + 2) : ka;

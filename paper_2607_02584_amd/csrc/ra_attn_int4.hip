@@ -108,7 +108,8 @@ __global__ __launch_bounds__(256, 2) void k_attn_int4(AttnArgs a) {
   __shared__ __align__(16) float sKc[2][NCH];          // K scale of each 32-key chunk (grouped K)
   __shared__ __align__(16) float sB[2][QB ? KV : 1];   // per-key score bias fl(b Kc)
 
-  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  // the wave index is uniform: conditions on it are scalar branches
+  const int tid = threadIdx.x, lane = tid & 63, wave = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int hh = lane >> 5, j = lane & 31;
   int bh, qtile;
   xcd_tile(bh, qtile);
@@ -137,20 +138,30 @@ __global__ __launch_bounds__(256, 2) void k_attn_int4(AttnArgs a) {
   // Per-block side data in LDS: V dequantization factors fl(s_v / pscale) / 16
   // (exact /16) of the block's group, the K scales (per 32-key chunk or per
   // key) and, with Q smoothing, the per-key bias.
+  // Waves 0 and 1 (thread = channel) stage the V factors; thread 128 + t
+  // stages key t of the block (waves 2 and 3, or wave 2 alone for 64-key
+  // blocks), or the K scale of chunk t (grouped K: k_group is 32, 64 or 128,
+  // so the group index is a shift).  stage_aux runs for blocks 0, 1, 2, ... in
+  // order; (vg, vgr) = (V group, block within it) of the next block it stages.
+  const bool kwave = KV == 128 ? wave >= 2 : wave == 2;
+  const int kgs = __builtin_ctz(static_cast<unsigned>(a.k_group));
+  int vg = 0, vgr = 0;
   auto stage_aux = [&](int jb, int buf) {
-    if (tid < kD) {
-      int g = (jb * KV) / a.v_group;
-      if (g >= a.nvgroups) g = a.nvgroups - 1;
-      const float s = a.vs[(static_cast<size_t>(bh) * a.nvgroups + g) * kD + tid];
+    if (wave < 2) {
+      const float s = a.vs[(static_cast<size_t>(bh) * a.nvgroups + vg) * kD + tid];
       sDq[buf][tid] = __fmul_rn(__fdiv_rn(s, pscale), 0.0625f);
     }
-    const int kt = tid - kD;
-    if (kt >= 0 && kt < (KTOK ? KV : NCH)) {
-      if (KTOK) sKs[buf][kt] = a.ks[static_cast<size_t>(bh) * kstride + jb * KV + kt];
-      else sKc[buf][kt] = a.ks[static_cast<size_t>(bh) * kstride + (jb * KV + kt * 32) / a.k_group];
+    if (++vgr == a.v_bpg) {
+      vgr = 0;
+      ++vg;
     }
-    if (QB && kt >= 0 && kt < KV)
-      sB[buf][kt] = __fmul_rn(a.kbias[static_cast<size_t>(bh) * a.Npad + jb * KV + kt], a.Kc);
+    const int kt = tid - kD;
+    if (KTOK) {
+      if (kwave) sKs[buf][kt] = a.ks[static_cast<size_t>(bh) * kstride + jb * KV + kt];
+    } else if (wave == 2 && lane < NCH) {
+      sKc[buf][kt] = a.ks[static_cast<size_t>(bh) * kstride + ((jb * KV + kt * 32) >> kgs)];
+    }
+    if (QB && kwave) sB[buf][kt] = __fmul_rn(a.kbias[static_cast<size_t>(bh) * a.Npad + jb * KV + kt], a.Kc);
   };
 
   float of[4][16];

@@ -44,7 +44,7 @@ def build(force: bool = True) -> str:
 class _RopeCfg(ctypes.Structure):
     _fields_ = [("N", ctypes.c_int), ("D", ctypes.c_int), ("T", ctypes.c_int), ("Hg", ctypes.c_int),
                 ("W", ctypes.c_int), ("split", ctypes.c_int * 3), ("theta", ctypes.c_double),
-                ("rotation", ctypes.c_int), ("rot", ctypes.POINTER(ctypes.c_double))]
+                ("rotation", ctypes.c_int), ("rot", ctypes.POINTER(ctypes.c_double)), ("in_fp16", ctypes.c_int)]
 
 
 class _AttnCfg(ctypes.Structure):
@@ -79,6 +79,12 @@ def lib():
                                        ctypes.c_int, P]
         L.ora_attn_bf16.argtypes = [P, P, P, ctypes.c_int, ctypes.c_int, ctypes.c_int, ctypes.c_double,
                                     ctypes.c_int, ctypes.c_int, P]
+        L.ora_attn_fb16.argtypes = [P, P, P, ctypes.c_int, ctypes.c_int, ctypes.c_int, ctypes.c_double,
+                                    ctypes.c_int, ctypes.c_int, ctypes.c_int, P]
+        L.ora_f16_to_f32.argtypes = [ctypes.c_uint16]
+        L.ora_f16_to_f32.restype = ctypes.c_float
+        L.ora_f32_to_f16.argtypes = [ctypes.c_float]
+        L.ora_f32_to_f16.restype = ctypes.c_uint16
         L.ora_bf16_to_f32.argtypes = [ctypes.c_uint16]
         L.ora_bf16_to_f32.restype = ctypes.c_float
         L.ora_f32_to_bf16.argtypes = [ctypes.c_float]
@@ -112,9 +118,10 @@ class Geometry:
         return self.T * self.Hg * self.W
 
 
-def _rope_cfg(geo: Geometry, rotation: int, rot):
+def _rope_cfg(geo: Geometry, rotation: int, rot, fp16: bool = False):
     c = _RopeCfg()
     c.N, c.D, c.T, c.Hg, c.W = geo.N, geo.D, geo.T, geo.Hg, geo.W
+    c.in_fp16 = int(bool(fp16))
     c.split[:] = list(geo.split)
     c.theta = float(geo.theta)
     c.rotation = int(rotation)
@@ -132,20 +139,21 @@ def rope_block(geo: Geometry, n: int, p: int, rotation: int = ROT_NONE, rot=None
     return G.reshape(2, 2)
 
 
-def rope_rot_f32(geo: Geometry, x_bf16: np.ndarray, rotation: int, rot=None) -> np.ndarray:
-    """bf16 bits [N][D] (uint16) -> fp32 [N][D] (the single-precision sequence)."""
+def rope_rot_f32(geo: Geometry, x_bf16: np.ndarray, rotation: int, rot=None, fp16: bool = False) -> np.ndarray:
+    """16-bit bits [N][D] (uint16; bf16, or fp16 with ``fp16``) -> fp32 [N][D]
+    (the single-precision sequence)."""
     x = np.ascontiguousarray(x_bf16, dtype=np.uint16)
     assert x.shape == (geo.N, geo.D)
-    c, _keep = _rope_cfg(geo, rotation, rot)
+    c, _keep = _rope_cfg(geo, rotation, rot, fp16)
     y = np.empty((geo.N, geo.D), np.float32)
     lib().ora_rope_rot_f32(ctypes.byref(c), _p(x), _p(y))
     return y
 
 
-def rope_rot_f64(geo: Geometry, x_bf16: np.ndarray, rotation: int, rot=None) -> np.ndarray:
+def rope_rot_f64(geo: Geometry, x_bf16: np.ndarray, rotation: int, rot=None, fp16: bool = False) -> np.ndarray:
     x = np.ascontiguousarray(x_bf16, dtype=np.uint16)
     assert x.shape == (geo.N, geo.D)
-    c, _keep = _rope_cfg(geo, rotation, rot)
+    c, _keep = _rope_cfg(geo, rotation, rot, fp16)
     y = np.empty((geo.N, geo.D), np.float64)
     lib().ora_rope_rot_f64(ctypes.byref(c), _p(x), _p(y))
     return y
@@ -256,15 +264,32 @@ def attn_ref_f64(q, k, v, sm_scale=0.0, rows=None) -> np.ndarray:
     return O
 
 
-def attn_bf16(qb, kb, vb, kv_block=128, sm_scale=0.0, rows=None) -> np.ndarray:
+def attn_fb16(qb, kb, vb, kv_block=64, sm_scale=0.0, rows=None, fp16=False) -> np.ndarray:
+    """The 16-bit fallback attention (``ora_attn_fb16``) on 16-bit bits: bf16,
+    or fp16 with ``fp16``."""
     qb = np.ascontiguousarray(qb, dtype=np.uint16)
     kb = np.ascontiguousarray(kb, dtype=np.uint16)
     vb = np.ascontiguousarray(vb, dtype=np.uint16)
     N, D = kb.shape
     row0, nrows = (0, qb.shape[0]) if rows is None else rows
     O = np.empty((nrows, D), np.float64)
-    lib().ora_attn_bf16(_p(qb), _p(kb), _p(vb), N, D, kv_block, sm_scale, row0, nrows, _p(O))
+    lib().ora_attn_fb16(_p(qb), _p(kb), _p(vb), N, D, kv_block, sm_scale, int(bool(fp16)), row0, nrows, _p(O))
     return O
+
+
+def attn_bf16(qb, kb, vb, kv_block=128, sm_scale=0.0, rows=None) -> np.ndarray:
+    return attn_fb16(qb, kb, vb, kv_block=kv_block, sm_scale=sm_scale, rows=rows, fp16=False)
+
+
+def f16_to_f32(b: np.ndarray) -> np.ndarray:
+    return np.ascontiguousarray(b, dtype=np.uint16).view(np.float16).astype(np.float32)
+
+
+def f32_to_f16(f) -> np.ndarray:
+    """Round-to-nearest-even binary32 -> binary16 bits through the C helper."""
+    f = np.ascontiguousarray(f, dtype=np.float32)
+    L = lib()
+    return np.array([L.ora_f32_to_f16(float(v)) for v in f.ravel()], np.uint16).reshape(f.shape)
 
 
 def bf16_to_f32(b: np.ndarray) -> np.ndarray:
@@ -368,10 +393,20 @@ def rope_bf16_head(geo: Geometry, x_bf16) -> np.ndarray:
     return r
 
 
-def fwd_fp16_head(geo: Geometry, q_bf16, k_bf16, v_bf16, kv_block=128, sm_scale=0.0, rows=None):
-    qb = rope_bf16_head(geo, q_bf16)
-    kb = rope_bf16_head(geo, k_bf16)
-    return attn_bf16(qb, kb, v_bf16, kv_block=kv_block, sm_scale=sm_scale, rows=rows)
+def rope_f16_head(geo: Geometry, x_f16) -> np.ndarray:
+    """Fallback producer on binary16 inputs: plain 3D RoPE in binary32, rounded
+    to binary16 bits (numpy's conversion rounds to nearest even)."""
+    y = rope_rot_f32(geo, x_f16, ROT_NONE, fp16=True)
+    return y.astype(np.float16).view(np.uint16)
+
+
+def fwd_fp16_head(geo: Geometry, q_bits, k_bits, v_bits, kv_block=64, sm_scale=0.0, rows=None, fp16=False):
+    """Whole fallback forward of one head on 16-bit input bits (bf16, or fp16
+    with ``fp16``): RoPE rounded to the 16-bit type, then ``attn_fb16``."""
+    rope = rope_f16_head if fp16 else rope_bf16_head
+    qb = rope(geo, q_bits)
+    kb = rope(geo, k_bits)
+    return attn_fb16(qb, kb, v_bits, kv_block=kv_block, sm_scale=sm_scale, rows=rows, fp16=fp16)
 
 
 def ref_head(geo: Geometry, q_bf16, k_bf16, v_bf16, sm_scale=0.0, rows=None) -> np.ndarray:

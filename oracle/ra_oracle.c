@@ -31,6 +31,42 @@
 
 #define LOG2E 1.4426950408889634074
 
+/* binary16 bits -> binary32 (exact: every binary16 value is a binary32 value). */
+float ora_f16_to_f32(uint16_t h) {
+  const int e = (h >> 10) & 0x1f, m = h & 0x3ff;
+  double v;
+  if (e == 0) v = ldexp((double)m, -24);                       /* zero or subnormal */
+  else if (e == 31) v = m ? NAN : INFINITY;
+  else v = ldexp(1024.0 + (double)m, e - 25);                   /* (1 + m/1024) 2^(e-15) */
+  return (float)((h & 0x8000) ? -v : v);
+}
+
+/* Round-to-nearest-even binary32 -> binary16.  |f| is split into a power of
+ * two and a significand in double (exact), the significand is rounded to 10
+ * fraction bits with rint (ties to even under the default rounding mode);
+ * below 2^-14 the grid is the fixed subnormal step 2^-24; from 65520 (half way
+ * between the largest finite value 65504 and 2^16) upward the result is inf. */
+uint16_t ora_f32_to_f16(float f) {
+  const uint16_t sign = signbit(f) ? 0x8000u : 0u;
+  if (isnan(f)) return (uint16_t)(sign | 0x7e00u);
+  const double a = fabs((double)f);
+  if (a >= 65520.0) return (uint16_t)(sign | 0x7c00u);
+  if (a < ldexp(1.0, -14)) return (uint16_t)(sign | (uint16_t)rint(ldexp(a, 24)));
+  int ex;
+  frexp(a, &ex);                        /* a = fr 2^ex, fr in [0.5, 1) */
+  int E = ex - 1;                       /* a = s 2^E, s in [1, 2) */
+  double q = rint((ldexp(a, -E) - 1.0) * 1024.0);
+  if (q == 1024.0) {
+    q = 0.0;
+    ++E;
+  }
+  if (E + 15 >= 31) return (uint16_t)(sign | 0x7c00u);
+  return (uint16_t)(sign | ((E + 15) << 10) | (uint16_t)q);
+}
+
+static float in16_to_f32(uint16_t b, int fp16) { return fp16 ? ora_f16_to_f32(b) : ora_bf16_to_f32(b); }
+static uint16_t f32_to_16(float f, int fp16) { return fp16 ? ora_f32_to_f16(f) : ora_f32_to_bf16(f); }
+
 float ora_bf16_to_f32(uint16_t b) {
   uint32_t u = (uint32_t)b << 16;
   float f;
@@ -152,17 +188,17 @@ void ora_hadamard_f64(double* y, int D) {
   for (int i = 0; i < D; ++i) y[i] *= r;
 }
 
-void ora_rope_rot_f32(const ora_rope_cfg* c, const uint16_t* x_bf16, float* y) {
+void ora_rope_rot_f32(const ora_rope_cfg* c, const uint16_t* x_bits, float* y) {
   const int D = c->D, P = D / 2;
   float* tmp = (float*)malloc(sizeof(float) * D);
   for (int n = 0; n < c->N; ++n) {
-    const uint16_t* x = x_bf16 + (size_t)n * D;
+    const uint16_t* x = x_bits + (size_t)n * D;
     float* yn = y + (size_t)n * D;
     for (int p = 0; p < P; ++p) {
       double G[4];
       ora_rope_block(c, n, p, G);
       float g00 = (float)G[0], g01 = (float)G[1], g10 = (float)G[2], g11 = (float)G[3];
-      float x0 = ora_bf16_to_f32(x[2 * p]), x1 = ora_bf16_to_f32(x[2 * p + 1]);
+      float x0 = in16_to_f32(x[2 * p], c->in_fp16), x1 = in16_to_f32(x[2 * p + 1], c->in_fp16);
       tmp[2 * p] = fmaf(x1, g10, x0 * g00);
       tmp[2 * p + 1] = fmaf(x1, g11, x0 * g01);
     }
@@ -190,16 +226,16 @@ void ora_rope_rot_f32(const ora_rope_cfg* c, const uint16_t* x_bf16, float* y) {
   free(tmp);
 }
 
-void ora_rope_rot_f64(const ora_rope_cfg* c, const uint16_t* x_bf16, double* y) {
+void ora_rope_rot_f64(const ora_rope_cfg* c, const uint16_t* x_bits, double* y) {
   const int D = c->D, P = D / 2;
   double* tmp = (double*)malloc(sizeof(double) * D);
   for (int n = 0; n < c->N; ++n) {
-    const uint16_t* x = x_bf16 + (size_t)n * D;
+    const uint16_t* x = x_bits + (size_t)n * D;
     double* yn = y + (size_t)n * D;
     for (int p = 0; p < P; ++p) {
       double G[4];
       ora_rope_block(c, n, p, G);
-      double x0 = ora_bf16_to_f32(x[2 * p]), x1 = ora_bf16_to_f32(x[2 * p + 1]);
+      double x0 = in16_to_f32(x[2 * p], c->in_fp16), x1 = in16_to_f32(x[2 * p + 1], c->in_fp16);
       tmp[2 * p] = x0 * G[0] + x1 * G[2];
       tmp[2 * p + 1] = x0 * G[1] + x1 * G[3];
     }
@@ -455,8 +491,8 @@ void ora_attn_ref_f64(const double* q, const double* k, const double* v, int N, 
   }
 }
 
-void ora_attn_bf16(const uint16_t* qb, const uint16_t* kb, const uint16_t* vb, int N, int D,
-                   int kv_block, double sm_scale, int row0, int nrows, double* O) {
+void ora_attn_fb16(const uint16_t* qb, const uint16_t* kb, const uint16_t* vb, int N, int D,
+                   int kv_block, double sm_scale, int fp16, int row0, int nrows, double* O) {
   const double c = sigma_of(sm_scale, D) * LOG2E;
   const int kv = kv_block;
 #pragma omp parallel
@@ -474,7 +510,7 @@ void ora_attn_bf16(const uint16_t* qb, const uint16_t* kb, const uint16_t* vb, i
         for (int n = j0; n < j1; ++n) {
           double s = 0.0;
           for (int ch = 0; ch < D; ++ch)
-            s += (double)ora_bf16_to_f32(qi[ch]) * (double)ora_bf16_to_f32(kb[(size_t)n * D + ch]);
+            s += (double)in16_to_f32(qi[ch], fp16) * (double)in16_to_f32(kb[(size_t)n * D + ch], fp16);
           t[n - j0] = s * c;
           if (t[n - j0] > bm) bm = t[n - j0];
         }
@@ -485,8 +521,9 @@ void ora_attn_bf16(const uint16_t* qb, const uint16_t* kb, const uint16_t* vb, i
         for (int n = j0; n < j1; ++n) {
           double P = exp2(t[n - j0] - mn);
           l += P;
-          double Pb = ora_bf16_to_f32(ora_f32_to_bf16((float)P));
-          for (int ch = 0; ch < D; ++ch) acc[ch] += Pb * (double)ora_bf16_to_f32(vb[(size_t)n * D + ch]);
+          /* the PV product sees P rounded to the 16-bit type (through binary32) */
+          double Pr = in16_to_f32(f32_to_16((float)P, fp16), fp16);
+          for (int ch = 0; ch < D; ++ch) acc[ch] += Pr * (double)in16_to_f32(vb[(size_t)n * D + ch], fp16);
         }
         m = mn;
       }
@@ -495,4 +532,9 @@ void ora_attn_bf16(const uint16_t* qb, const uint16_t* kb, const uint16_t* vb, i
     free(t);
     free(acc);
   }
+}
+
+void ora_attn_bf16(const uint16_t* qb, const uint16_t* kb, const uint16_t* vb, int N, int D,
+                   int kv_block, double sm_scale, int row0, int nrows, double* O) {
+  ora_attn_fb16(qb, kb, vb, N, D, kv_block, sm_scale, 0, row0, nrows, O);
 }

@@ -40,6 +40,7 @@ typedef struct {
   double theta;
   int rotation;          /* ORA_ROT_* */
   const double* rot;     /* [D/2][2][2] O(2) blocks, row-major; NULL = H_2 in every block */
+  int in_fp16;           /* input bits are binary16 (else bfloat16) */
 } ora_rope_cfg;
 
 /* The 2x2 matrix that maps the channel pair p of token n, row-vector form
@@ -47,7 +48,8 @@ typedef struct {
  * into RoPE, Sec. 4.1.2); otherwise G = M (plain 3D RoPE, Sec. 3). fp64. */
 void ora_rope_block(const ora_rope_cfg* c, int n, int p, double G[4]);
 
-/* RoPE followed by the chosen rotation, bf16 input bits -> y [N][D].
+/* RoPE followed by the chosen rotation, 16-bit input bits (bf16, or fp16 with
+ * in_fp16) -> y [N][D].
  * ORA_ROT_HADAMARD is the "Full" rotation the paper compares against
  * (Sec. 5.3 baselines): y = RoPE(x) H_D with the orthonormal Sylvester matrix
  * H_D = H_2 (x) H_{D/2} of Sec. 4.3.  In binary32 it is
@@ -55,8 +57,8 @@ void ora_rope_block(const ora_rope_cfg* c, int n, int p, double G[4]);
  * of the first half with channel i of the second half (sum, difference), then
  * each half recurses -- with every sum and difference unscaled and one final
  * multiply by fl32(D^-1/2) (the product of the log2(D) factors 1/sqrt 2). */
-void ora_rope_rot_f32(const ora_rope_cfg* c, const uint16_t* x_bf16, float* y);
-void ora_rope_rot_f64(const ora_rope_cfg* c, const uint16_t* x_bf16, double* y);
+void ora_rope_rot_f32(const ora_rope_cfg* c, const uint16_t* x_bits, float* y);
+void ora_rope_rot_f64(const ora_rope_cfg* c, const uint16_t* x_bits, double* y);
 
 /* y <- y H_D in place for one row of D = 2^n values: the binary32 sequence
  * described above (sum/difference butterflies, widest stride first, then the
@@ -120,15 +122,22 @@ void ora_attn_int4(const ora_attn_cfg* a,
 void ora_attn_ref_f64(const double* q, const double* k, const double* v, int N, int D,
                       double sm_scale, int row0, int nrows, double* O);
 
-/* BF16 fallback attention semantics: bf16 q/k/v bits, fp64 dot products,
- * blockwise online softmax with exact exp2, P rounded to binary32 then to
- * bf16 before the PV product, normaliser from the unrounded P. */
+/* 16-bit fallback attention semantics (the FP16 attention the paper keeps for
+ * sensitive steps and blocks, Sec. 5.1; bf16 or fp16 with the flag): 16-bit
+ * q/k/v bits, fp64 dot products, blockwise online softmax over blocks of
+ * kv_block keys in ascending order with exact exp2, P rounded to binary32 and
+ * then to the 16-bit type before the PV product, the normaliser l from the
+ * unrounded P.  ora_attn_bf16 is the bf16 form. */
+void ora_attn_fb16(const uint16_t* qb, const uint16_t* kb, const uint16_t* vb, int N, int D,
+                   int kv_block, double sm_scale, int fp16, int row0, int nrows, double* O);
 void ora_attn_bf16(const uint16_t* qb, const uint16_t* kb, const uint16_t* vb, int N, int D,
                    int kv_block, double sm_scale, int row0, int nrows, double* O);
 
 /* Helpers exposed for the pins. */
 float ora_bf16_to_f32(uint16_t b);
 uint16_t ora_f32_to_bf16(float f);
+float ora_f16_to_f32(uint16_t h);
+uint16_t ora_f32_to_f16(float f);     /* round to nearest even, overflow to inf */
 float ora_exp2_f32(float x);          /* exp2 in double, rounded to binary32 */
 int ora_pcode(float P, int p_quant);  /* u = clamp(rint(fl(15P)), 0, 15) or SYM7 */
 int ora_threads(void);                /* worker threads the parallel loops use */

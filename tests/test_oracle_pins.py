@@ -790,6 +790,105 @@ def test_bf16_fallback_semantics(ora):
         assert np.abs(O - ref).max() <= 2e-3 * np.abs(ref).max()
 
 
+# Hand-worked fallback case.  One query (1.0 on channel 0), four keys whose
+# channel 0 holds a = -1.25, -0.25, 0, -0.75 (exact in bf16 and fp16), one-hot
+# value rows V_n = e_n, and the softmax scale 1/log2(e) so that the log2-domain
+# score of key n is exactly a_n.  In one block of four keys the maximum is 0 and
+# P_n = 2^a_n; the PV product sees each P rounded (through binary32) to the
+# 16-bit type, the normaliser is the sum of the unrounded P:
+#   2^-1.25 = 0.42044820762685725 -> bf16 0.419921875,   fp16 0.42041015625
+#   2^-0.25 = 0.8408964152537145  -> bf16 0.83984375,    fp16 0.8408203125
+#   2^-0.75 = 0.5946035575013605  -> bf16 0.59375,       fp16 0.5947265625
+# With blocks of one key, taken in order, the first three keys each arrive as
+# the new maximum (P = 1, exact) and are only rescaled afterwards, so no rounding
+# touches them; the fourth (below the maximum 0) is rounded.
+_FB_P = {"a": [-1.25, -0.25, 0.0, -0.75],
+         "bf16": [0.419921875, 0.83984375, 1.0, 0.59375],
+         "fp16": [0.42041015625, 0.8408203125, 1.0, 0.5947265625]}
+
+
+@pytest.mark.parametrize("fmt", ["bf16", "fp16"])
+def test_fallback_p_rounding_and_normaliser_handworked(ora, fmt):
+    """The fallback rounds P to the 16-bit type before PV and takes l from the
+    unrounded P, at the running maximum of the block the key belongs to (the
+    FP16 attention of Sec. 5.1 with the blockwise softmax of Sec. 4.2)."""
+    fp16 = fmt == "fp16"
+    D, a = 128, _FB_P["a"]
+    enc = (lambda x: np.asarray(x, np.float16).view(np.uint16)) if fp16 else _bits
+    q = np.zeros((1, D), np.float32)
+    q[0, 0] = 1.0
+    k = np.zeros((4, D), np.float32)
+    k[:, 0] = a
+    v = np.zeros((4, D), np.float32)
+    v[np.arange(4), np.arange(4)] = 1.0
+    qb, kb, vb = enc(q), enc(k), enc(v)
+    sm = 1.0 / 1.4426950408889634074
+    exact = [2.0 ** x for x in a]
+    l = sum(exact)
+    O4 = ora.attn_fb16(qb, kb, vb, kv_block=4, sm_scale=sm, fp16=fp16)[0]
+    want = np.zeros(D)
+    want[:4] = np.array(_FB_P[fmt]) / l
+    np.testing.assert_allclose(O4, want, rtol=1e-13, atol=1e-15)
+    # the two plausible misreadings are far from it
+    assert np.abs(O4[:4] - np.array(exact) / l).max() > 1e-7                      # no rounding
+    assert np.abs(O4[:4] - np.array(_FB_P[fmt]) / sum(_FB_P[fmt])).max() > 1e-7  # l from rounded P
+    O1 = ora.attn_fb16(qb, kb, vb, kv_block=1, sm_scale=sm, fp16=fp16)[0]
+    want1 = np.zeros(D)
+    want1[:4] = np.array(exact[:3] + [_FB_P[fmt][3]]) / l
+    np.testing.assert_allclose(O1, want1, rtol=1e-13, atol=1e-15)
+
+
+def test_f16_rounding_is_nearest_even(ora):
+    """binary32 -> binary16 of the oracle: hand-picked ties go to the even
+    neighbour (normal and subnormal), the overflow threshold is 65520, and random
+    values agree with numpy's conversion (an independent implementation)."""
+    cases = {1.0 + 2.0 ** -11: 1.0,                       # tie between 1 and 1 + 2^-10 -> 1
+             1.0 + 3 * 2.0 ** -11: 1.0 + 2.0 ** -9,       # tie -> mantissa 2 (even)
+             2.0 ** -25: 0.0,                             # subnormal tie -> 0
+             3 * 2.0 ** -25: 2.0 ** -23,                  # subnormal tie -> 2 * 2^-24
+             65519.0: 65504.0, 65520.0: np.inf, -(2.0 ** -14): -(2.0 ** -14)}
+    for x, want in cases.items():
+        got = ora.f16_to_f32(ora.f32_to_f16(np.array([x], np.float32)))[0]
+        assert got == np.float32(want), (x, got, want)
+    rng = np.random.default_rng(77)
+    x = np.concatenate([rng.standard_normal(4000) * 10.0 ** rng.integers(-8, 5, 4000),
+                        rng.uniform(-1, 1, 1000) * 2.0 ** -14]).astype(np.float32)
+    assert np.array_equal(ora.f32_to_f16(x), x.astype(np.float16).view(np.uint16))
+    assert np.array_equal(ora.f16_to_f32(ora.f32_to_f16(x)), x.astype(np.float16).astype(np.float32))
+
+
+def test_rope_bf16_rounding_ties_to_even(ora):
+    """The fallback producer rounds the binary32 RoPE output to bf16 with ties to
+    even.  A token and a bf16 input value are found (deterministic search) whose
+    RoPE output is exactly half way between two bf16 values; the result must be
+    the neighbour with the even last bit."""
+    geo = ora.Geometry(1, 1, 64, (44, 42, 42), 10000.0)
+    mant = np.arange(128, 256, dtype=np.float32) / np.float32(128.0)   # every bf16 significand in [1, 2)
+    found = None
+    for n in range(1, geo.N):
+        for p in range(43, 64):                     # pairs of the w axis (position n)
+            G = ora.rope_block(geo, n, p).astype(np.float32)
+            for (r, c) in ((0, 0), (0, 1)):         # x1 = 0: y_c = fl(x0 * g_0c)
+                y = mant * G[r, c]
+                u = y.view(np.uint32)
+                hit = np.nonzero((u & 0xFFFF) == 0x8000)[0]
+                if hit.size:
+                    found = (n, p, c, float(mant[hit[0]]), int(u[hit[0]]))
+                    break
+            if found:
+                break
+        if found:
+            break
+    assert found, "no tie in the search space"
+    n, p, c, x0, ybits = found
+    x = np.zeros((geo.N, 128), np.float32)
+    x[n, 2 * p] = x0
+    out = ora.rope_bf16_head(geo, _bits(x))
+    lo, hi = ybits >> 16, (ybits >> 16) + 1      # the two bf16 neighbours (positive value)
+    want = lo if lo % 2 == 0 else hi
+    assert out[n, 2 * p + c] == want
+
+
 def test_int4_pipeline_tracks_fp64_attention(ora):
     """Whole INT4 oracle pipeline against fp64 attention (cosine).  On diffuse
     Gaussian scores the Range-optimized P mapping is clearly more accurate than

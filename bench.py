@@ -110,7 +110,7 @@ def main():
     stream = torch.cuda.current_stream()
 
     def step(ev=None):
-        # the Q, K and V producers in one call (their passes run concurrently)
+        # the Q, K and V producers in one call
         ra.quantize_qkv(p, qd, kd, vd, bufs["q_codes"], bufs["q_scale"], bufs["k_codes"], bufs["k_scale"],
                         bufs["v_codes"], bufs["v_scale"], ws, mu_k=bufs["mu_k"], mu_v=bufs["mu_v"])
         if ev is not None:
@@ -122,7 +122,8 @@ def main():
 
     if args.profile_run:
         step()
-        pf = ra.make_params(w.B, w.H, (w.T, w.Hg, w.W), w.split, w.theta, rotation=ra.ROT_NONE, out_dtype=ra.BF16)
+        pf = ra.make_params(w.B, w.H, (w.T, w.Hg, w.W), w.split, w.theta, rotation=ra.ROT_NONE, out_dtype=ra.BF16,
+                           kv_block=64)
         wsf = ra.workspace(pf, ra.PATH_FP16)
         ra.fwd_fp16(pf, qd, kd, vd, torch.empty_like(o), wsf)
         src = torch.ones(COPY_BYTES // 4, dtype=torch.float32, device=dev)
@@ -154,7 +155,8 @@ def main():
     extra = {}
     fb_kernel_ms = None
     if not args.skip_fallback:
-        pf = ra.make_params(w.B, w.H, (w.T, w.Hg, w.W), w.split, w.theta, rotation=ra.ROT_NONE, out_dtype=ra.BF16)
+        pf = ra.make_params(w.B, w.H, (w.T, w.Hg, w.W), w.split, w.theta, rotation=ra.ROT_NONE, out_dtype=ra.BF16,
+                           kv_block=64)
         wsf = ra.workspace(pf, ra.PATH_FP16, dev)
         of = torch.empty_like(o)
         for _ in range(2):
@@ -317,7 +319,8 @@ def schedule(args, torch, dg, ra, dev):
                          dist=w.dist)
         sets.append(tuple(ra.to_device_bits(x, dev) for x in dg.make_inputs(wi)))
     p = ra.make_params(w.B, w.H, (w.T, w.Hg, w.W), w.split, w.theta, rotation=ra.ROT_INTERLEAVED, out_dtype=ra.BF16)
-    pf = ra.make_params(w.B, w.H, (w.T, w.Hg, w.W), w.split, w.theta, rotation=ra.ROT_NONE, out_dtype=ra.BF16)
+    pf = ra.make_params(w.B, w.H, (w.T, w.Hg, w.W), w.split, w.theta, rotation=ra.ROT_NONE, out_dtype=ra.BF16,
+                           kv_block=64)
     ws = ra.workspace(p, ra.PATH_INT4, dev)
     wsf = ra.workspace(pf, ra.PATH_FP16, dev)
     o = torch.empty((w.B * w.H, w.N, 128), dtype=torch.bfloat16, device=dev)

@@ -26,15 +26,13 @@
  *    returns RA_OK (0) or a negative RA_ERR_* code; no exception crosses the ABI.
  *    rotate_attn_last_error() returns a thread-local message for the last
  *    failure on the calling thread.
- *  - The library keeps, per device, a small cache of RoPE/rotation tables in
- *    device memory (allocated on first use of a geometry, never freed before
- *    process exit).  That first call is therefore synchronous and must not be
- *    made under HIP graph capture; later calls with the same geometry are not.
- *  - The INT4 producers run Q, K and V passes concurrently on two internal
- *    streams per device (default priority), forked from and joined back into
- *    the caller's stream with events: every call still behaves as if it ran
- *    in order on `stream`.  The streams are created on the first producer call
- *    on a device (not under graph capture) and kept until process exit.
+ *  - The library allocates no device memory and creates no streams or events.
+ *    The RoPE/rotation tables (binary64 trigonometry rounded once to binary32)
+ *    are built on the host on the first call for a geometry (grid, split,
+ *    theta, rotation, blocks) and kept for the life of the process in pinned
+ *    host memory (hipHostMalloc, never freed); every call that needs them
+ *    copies them into its workspace with hipMemcpyAsync on `stream`.  Only
+ *    that first call per geometry performs a host allocation.
  *  - Results are deterministic: repeated calls give identical bytes.
  *
  * Packed INT4 layouts (written by the quantize calls, read by the attention)
@@ -130,13 +128,17 @@ typedef struct ra_params {
   int32_t rope_split[3];   /* D_t, D_h, D_w: each even and > 0, sum == D (Sec. 3) */
   float rope_theta;        /* RoPE base, e.g. 10000 or 256 */
   int32_t rotation;        /* RA_ROT_* */
-  const double* rot_blocks;/* host, [D/2][2][2] row-major O(2) blocks; NULL = H_2 (Sec. 4.1) */
+  const double* rot_blocks;/* host, [D/2][2][2] row-major O(2) blocks; NULL = H_2 (Sec. 4.1).
+                              Each block must be orthogonal (|R R^T - I| <= 1e-6 elementwise,
+                              RA_ERR_INVALID otherwise); used by INTERLEAVED and HALF only */
   int32_t p_quant;         /* RA_PQ_* */
   int32_t smooth;          /* RA_SMOOTH_* bitmask */
   int32_t q_group;         /* tokens per Q scale: 1 (per-token) .. 128, must divide 128 */
-  int32_t k_group;         /* tokens per K scale: 1, 32, 64 or 128 */
+  int32_t k_group;         /* tokens per K scale: 1, 16, 32, 64 or 128 */
   int32_t v_group;         /* tokens per V scale (per channel): a multiple of kv_block, or >= N */
-  int32_t kv_block;        /* online-softmax block: 64 or 128 (fixes the P semantics) */
+  int32_t kv_block;        /* online-softmax block of both paths: 64 or 128 keys (fixes the
+                              running-max granularity of Sec. 4.2 and hence the P codes, and
+                              the block at whose maximum the fallback rounds P) */
   float sm_scale;          /* softmax scale; 0 = 1/sqrt(D) */
   int32_t in_dtype;        /* RA_BF16 | RA_FP16 */
   int32_t out_dtype;       /* RA_BF16 | RA_FP16 | RA_FP32 */
@@ -147,7 +149,8 @@ typedef struct ra_params {
                               values PV uses, so every output row is a convex combination */
 } ra_params;
 
-/* Sizes of the caller-visible INT4 buffers for these parameters. */
+/* Sizes of the caller-visible INT4 buffers for these parameters (the code and
+ * scale layouts above; Sec. 5.1 granularities). */
 typedef struct ra_layout {
   int64_t n_pad;          /* Npad */
   int64_t qk_code_bytes;  /* bytes of ONE of q_codes / k_codes (all heads) */
@@ -163,9 +166,11 @@ typedef struct ra_layout {
 int rotate_attn_layout(const ra_params* p, ra_layout* out);
 
 /* Workspace bytes needed by the calls of `path` (RA_PATH_INT4 covers
- * quantize_qk, quantize_v, attn_int4 and fwd_int4; RA_PATH_FP16 covers
- * fwd_fp16).  The workspace is device memory, 256-byte aligned, owned by the
- * caller and reused by every call; its content between calls is irrelevant. */
+ * quantize_qk, quantize_v, quantize_qkv, attn_int4 and fwd_int4; RA_PATH_FP16
+ * covers prepare_fp16, attn_fp16 and fwd_fp16).  The workspace is device
+ * memory, 256-byte aligned, owned by the caller and reused by every call; it
+ * holds the RoPE tables, the smoothing sums, and (INT4 forward) the codes and
+ * scales; its content between calls is irrelevant. */
 int rotate_attn_workspace_size(const ra_params* p, int path, size_t* bytes);
 
 /* Producer for Q and K (Sec. 3, 4, 4.1, 5.1): 3D RoPE and the chosen rotation,
@@ -191,22 +196,25 @@ int rotate_attn_quantize_qk(const ra_params* p, const void* q, const void* k, ui
 int rotate_attn_quantize_v(const ra_params* p, const void* v, uint8_t* v_codes, float* v_scale,
                            float* mu_v, void* workspace, size_t workspace_bytes, void* stream);
 
-/* Both producers in one call: the same results as quantize_qk followed by
- * quantize_v (bit for bit), with the Q, K and V passes running concurrently
- * (K and V on two library-internal streams per device, forked from and joined
- * back into `stream` with events; created on the first call on a device, which
- * must therefore not be made under graph capture).  Arguments as in the two
- * calls; mu_k, mu_q, mu_v nullable; k_bias required with RA_SMOOTH_Q. */
+/* Both producers in one call (Sec. 3, 4, 4.1, 4.3, 5.1): the same results as
+ * quantize_qk followed by quantize_v, bit for bit, in fewer passes.  Arguments
+ * as in the two calls; mu_k, mu_q, mu_v nullable; k_bias required with
+ * RA_SMOOTH_Q. */
 int rotate_attn_quantize_qkv(const ra_params* p, const void* q, const void* k, const void* v,
                              uint8_t* q_codes, float* q_scale, uint8_t* k_codes, float* k_scale,
                              uint8_t* v_codes, float* v_scale, float* mu_k, float* mu_q, float* mu_v,
                              float* k_bias, void* workspace, size_t workspace_bytes, void* stream);
 
-/* INT4 attention on already quantized operands (Sec. 4.2): S = Q~ K~^T on the
- * int8 matrix cores (exact int32), blockwise online softmax with blocks of
- * kv_block keys in ascending order, P mapped to the unsigned code
- * u = round(15 P) in [0, 15] (the affine code P~ = u - 8), PV on the codes,
- * O = (sum of dequantized PV) / l + mu_v, l = sum of the unquantized P.
+/* INT4 attention on already quantized operands (Sec. 4.2, Sec. 4.2.1, Sec. 5.1):
+ * S = Q~ K~^T exact, blockwise online softmax with blocks of kv_block keys in
+ * ascending order, P mapped to the unsigned code u = round(15 P) in [0, 15]
+ * (the affine code P~ = u - 8, Sec. 4.2.1), PV on the codes,
+ * O = (sum of dequantized PV) / l + mu_v, l = sum of the unquantized P.  The
+ * container selects the matrix-core path: RA_CODES_E2M3 runs the FP6 matrix
+ * core (v_mfma_scale_f32_*_f8f6f4, codes as E2M3 values, binary32 sums that are
+ * exact for these integers); RA_CODES_INT4 runs the int8 matrix core
+ * (v_mfma_i32_32x32x32_i8 on the unpacked nibbles, int32 accumulation).  Both
+ * compute the same integers.
  * mu_v: nullable (treated as zeros).  k_bias: the per-key score bias written
  * by quantize_qk, required with RA_SMOOTH_Q (RA_ERR_INVALID if NULL), ignored
  * otherwise; with it the log2e-scaled score of key j is
@@ -216,8 +224,9 @@ int rotate_attn_attn_int4(const ra_params* p, const uint8_t* q_codes, const floa
                           const float* v_scale, const float* mu_v, const float* k_bias, void* o,
                           void* stream);
 
-/* Debug variant of rotate_attn_attn_int4: runs the same kernel with a dump
- * enabled for the query rows [row0, row0 + rows) of head bh:
+/* Debug variant of rotate_attn_attn_int4 (the quantities of Sec. 4.2 made
+ * observable): runs the same kernel with a dump enabled for the query rows
+ * [row0, row0 + rows) of head bh:
  *   s_out [rows][N] int32  exact S = Q~ . K~
  *   u_out [rows][N] uint8  P codes u in [0, 15]
  *   m_out [rows][ceil(N/kv_block)] binary32 running maximum after each block
@@ -230,24 +239,29 @@ int rotate_attn_attn_int4_debug(const ra_params* p, const uint8_t* q_codes, cons
                                 int32_t* s_out,
                                 uint8_t* u_out, float* m_out, void* stream);
 
-/* Whole INT4 forward: quantize_qk + quantize_v + attn_int4, codes kept in the
+/* Whole INT4 forward (Sec. 3-4.3 producers, Sec. 4.2 attention, Sec. 5.1
+ * granularities): quantize_qkv + attn_int4, codes and scales kept in the
  * workspace (size RA_PATH_INT4). */
 int rotate_attn_fwd_int4(const ra_params* p, const void* q, const void* k, const void* v, void* o,
                          void* workspace, size_t workspace_bytes, void* stream);
 
-/* Producer of the fallback: plain 3D RoPE (no rotation, no smoothing) of Q and
- * K rounded to in_dtype, and V re-laid out for the matrix cores, into the
- * workspace (size RA_PATH_FP16). */
+/* Producer of the fallback (the FP16 attention the paper keeps for sensitive
+ * steps and blocks, Sec. 5.1): plain 3D RoPE (Sec. 3; no rotation, which is an
+ * identity in exact arithmetic, and no smoothing) of Q and K rounded to
+ * in_dtype, and V re-laid out for the matrix cores, into the workspace (size
+ * RA_PATH_FP16, which also holds the RoPE tables). */
 int rotate_attn_prepare_fp16(const ra_params* p, const void* q, const void* k, const void* v,
                              void* workspace, size_t workspace_bytes, void* stream);
 
-/* Fallback attention kernel alone on a workspace filled by prepare_fp16:
- * 16-bit matrix cores, online softmax with blocks of kv_block keys, P rounded
- * to in_dtype before PV, l from the unrounded P. */
+/* Fallback attention kernel alone (Sec. 5.1 FP16 attention with the blockwise
+ * online softmax of Sec. 4.2) on a workspace filled by prepare_fp16: 16-bit
+ * matrix cores, online softmax with blocks of kv_block (64 or 128) keys in
+ * ascending order, P rounded to in_dtype before PV (at the running maximum of
+ * its block), l from the unrounded P. */
 int rotate_attn_attn_fp16(const ra_params* p, const void* workspace, size_t workspace_bytes, void* o,
                           void* stream);
 
-/* Whole fallback forward: prepare_fp16 + attn_fp16. */
+/* Whole fallback forward (Sec. 5.1): prepare_fp16 + attn_fp16. */
 int rotate_attn_fwd_fp16(const ra_params* p, const void* q, const void* k, const void* v, void* o,
                          void* workspace, size_t workspace_bytes, void* stream);
 
@@ -256,6 +270,8 @@ int rotate_attn_fwd_fp16(const ra_params* p, const void* q, const void* k, const
 int rotate_attn_fwd(const ra_params* p, int fallback, const void* q, const void* k, const void* v,
                     void* o, void* workspace, size_t workspace_bytes, void* stream);
 
+/* Status code -> static text; and the thread-local message of the last failure
+ * on the calling thread (library utilities, no paper passage). */
 const char* rotate_attn_error_string(int status);
 const char* rotate_attn_last_error(void);
 

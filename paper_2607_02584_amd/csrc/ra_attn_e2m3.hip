@@ -225,7 +225,7 @@ __global__ __launch_bounds__(kThreads, 8 / kWaves) void k_attn_e2m3(AttnArgs a) 
     }
     const int kt = tid - kD;
     if (KTOK) {
-      if (kwave) f.k = ksh[jb * KV + kt];
+      if (kwave) f.k = ksh[(jb * KV + kt) >> kgs];
     } else if (wave == 2 && lane < NCH) {
       f.k = ksh[(jb * KV + kt * 32) >> kgs];
     }

@@ -157,7 +157,7 @@ __global__ __launch_bounds__(256, 2) void k_attn_int4(AttnArgs a) {
     }
     const int kt = tid - kD;
     if (KTOK) {
-      if (kwave) sKs[buf][kt] = a.ks[static_cast<size_t>(bh) * kstride + jb * KV + kt];
+      if (kwave) sKs[buf][kt] = a.ks[static_cast<size_t>(bh) * kstride + ((jb * KV + kt) >> kgs)];
     } else if (wave == 2 && lane < NCH) {
       sKc[buf][kt] = a.ks[static_cast<size_t>(bh) * kstride + ((jb * KV + kt * 32) >> kgs)];
     }

@@ -6,7 +6,8 @@
 // a ready matrix-core operand; V is re-laid out the same way, transposed.
 //
 // Attention: S^T = K Q^T on v_mfma_f32_32x32x16_{bf16,f16} (fp32 accumulate),
-// blockwise online softmax over blocks of 64 keys in ascending order,
+// blockwise online softmax over blocks of kv_block (64 or 128) keys in
+// ascending order,
 //   m = max(m, rowmax(S * Kc)),  P = 2^(S*Kc - m),  l = alpha*l + sum P,
 // P rounded to the 16-bit type as the A operand of O += P V, and O = O / l.
 // Each lane holds the scores of one query, so row reductions stay inside the
@@ -27,7 +28,6 @@ typedef float v16f __attribute__((ext_vector_type(16)));
 typedef __bf16 v8bf __attribute__((ext_vector_type(8)));
 typedef _Float16 v8h __attribute__((ext_vector_type(8)));
 
-constexpr int kKV = 64;       // keys per online-softmax block of the fallback
 constexpr int kBlockM = 128;  // queries per workgroup
 
 __device__ __forceinline__ float h2f(uint16_t b, int is_fp16) {
@@ -156,35 +156,32 @@ __device__ __forceinline__ V as_vec(uint4 u) {
   return __builtin_bit_cast(V, u);
 }
 
-// K and V tiles of one 64-key block (16 KB each) move global -> registers ->
-// LDS; each thread carries four 16-byte pieces of each.  The loads of block
-// j + 2 are issued at the end of block j and stored in the middle of block j + 1.
+// K and V tiles of one block of KV keys (KV * 256 bytes each) move global ->
+// registers -> LDS; each thread carries KV / 16 16-byte pieces of each.  The
+// loads of block j + 2 are issued at the end of block j and stored in the
+// middle of block j + 1.
+template <int KV>
 struct Tile16 {
   typedef unsigned T __attribute__((ext_vector_type(4)));
-  T k0, k1, k2, k3, v0, v1, v2, v3;   // named pieces stay in registers
+  static constexpr int NP = KV / 16;
+  T k[NP], v[NP];
   __device__ __forceinline__ void load(const uint16_t* kg, const uint16_t* vg, int tid) {
     const T* K = reinterpret_cast<const T*>(kg) + tid;
     const T* V = reinterpret_cast<const T*>(vg) + tid;
-    k0 = K[0];
-    v0 = V[0];
-    k1 = K[256];
-    v1 = V[256];
-    k2 = K[512];
-    v2 = V[512];
-    k3 = K[768];
-    v3 = V[768];
+#pragma unroll
+    for (int i = 0; i < NP; ++i) {
+      k[i] = K[256 * i];
+      v[i] = V[256 * i];
+    }
   }
   __device__ __forceinline__ void store(uint16_t* ks, uint16_t* vs, int tid) const {
     T* K = reinterpret_cast<T*>(ks) + tid;
     T* V = reinterpret_cast<T*>(vs) + tid;
-    K[0] = k0;
-    V[0] = v0;
-    K[256] = k1;
-    V[256] = v1;
-    K[512] = k2;
-    V[512] = v2;
-    K[768] = k3;
-    V[768] = v3;
+#pragma unroll
+    for (int i = 0; i < NP; ++i) {
+      K[256 * i] = k[i];
+      V[256 * i] = v[i];
+    }
   }
 };
 
@@ -194,7 +191,7 @@ struct Tile16 {
 // operands share one lane layout), with V read as the B operand in the key
 // order of its relayout, so a lane of the output tile holds one channel of 16
 // queries (query 8 (r / 4) + 4 hh + r % 4 in register r).
-template <bool F16>
+template <bool F16, int kKV>
 __global__ __launch_bounds__(256, 2) void k_attn16(Fp16Args a) {
   typedef typename MF<F16>::vec vec;
   constexpr int NCH = kKV / 32;
@@ -228,7 +225,7 @@ __global__ __launch_bounds__(256, 2) void k_attn16(Fp16Args a) {
     for (int r = 0; r < 16; ++r) of[mt][r] = 0.f;
   float m = -INFINITY, l = 0.f;
 
-  Tile16 tp;
+  Tile16<kKV> tp;
   tp.load(kbase, vbase, tid);
   tp.store(sK[0], sV[0], tid);
   tp.load(kbase + (nblocks > 1 ? TILE : 0), vbase + (nblocks > 1 ? TILE : 0), tid);
@@ -363,12 +360,14 @@ hipError_t launch_v16_relayout(const uint16_t* v, uint16_t* out, int BH, int N, 
 }
 
 hipError_t launch_attn_fp16(const Fp16Args& a, int kv_block, hipStream_t s) {
-  (void)kv_block;
   const dim3 grid(a.Npad / kBlockM, a.BH);
-  if (a.is_fp16)
-    hipLaunchKernelGGL(k_attn16<true>, grid, dim3(256), 0, s, a);
-  else
-    hipLaunchKernelGGL(k_attn16<false>, grid, dim3(256), 0, s, a);
+  if (kv_block == 128) {
+    if (a.is_fp16) hipLaunchKernelGGL((k_attn16<true, 128>), grid, dim3(256), 0, s, a);
+    else hipLaunchKernelGGL((k_attn16<false, 128>), grid, dim3(256), 0, s, a);
+  } else {
+    if (a.is_fp16) hipLaunchKernelGGL((k_attn16<true, 64>), grid, dim3(256), 0, s, a);
+    else hipLaunchKernelGGL((k_attn16<false, 64>), grid, dim3(256), 0, s, a);
+  }
   return hipGetLastError();
 }
 

@@ -1,6 +1,8 @@
 // ra_host.cpp -- host side of librotate_attn.so: argument validation, RoPE
-// table construction and caching, workspace partitioning, kernel launches.
-// Every entry point validates before it touches the GPU.
+// table construction (host cache, copied into the caller's workspace on the
+// caller's stream), workspace partitioning, kernel launches.  Every entry
+// point validates before it touches the GPU; the library allocates no device
+// memory and creates no streams.
 #include <hip/hip_runtime.h>
 
 #include <cmath>
@@ -54,17 +56,26 @@ int validate(const ra_params* p) {
   if (sum != p->D) return fail(RA_ERR_INVALID, "rope_split must sum to D");
   if (!(p->rope_theta > 0.0f) || !std::isfinite(p->rope_theta)) return fail(RA_ERR_INVALID, "rope_theta must be > 0");
   if (p->rotation < RA_ROT_NONE || p->rotation > RA_ROT_HADAMARD) return fail(RA_ERR_INVALID, "unknown rotation");
-  if (p->rot_blocks) {
-    for (int i = 0; i < 4 * (kD / 2); ++i)
-      if (!std::isfinite(p->rot_blocks[i])) return fail(RA_ERR_INVALID, "rot_blocks must be finite");
+  if (p->rot_blocks && (p->rotation == RA_ROT_INTERLEAVED || p->rotation == RA_ROT_HALF)) {
+    // every block must be orthogonal (R R^T = I): a non-orthogonal R applied to
+    // both Q and K would change Q K^T (Sec. 4.1 relies on R R^T = I)
+    for (int b = 0; b < kD / 2; ++b) {
+      const double* R = p->rot_blocks + 4 * b;
+      for (int i = 0; i < 4; ++i)
+        if (!std::isfinite(R[i])) return fail(RA_ERR_INVALID, "rot_blocks must be finite");
+      const double e00 = R[0] * R[0] + R[1] * R[1] - 1.0, e11 = R[2] * R[2] + R[3] * R[3] - 1.0;
+      const double e01 = R[0] * R[2] + R[1] * R[3];
+      if (std::fabs(e00) > 1e-6 || std::fabs(e11) > 1e-6 || std::fabs(e01) > 1e-6)
+        return fail(RA_ERR_INVALID, "rot_blocks[" + std::to_string(b) + "] is not orthogonal (R R^T != I)");
+    }
   }
   if (p->p_quant != RA_PQ_RANGE15 && p->p_quant != RA_PQ_SYM7) return fail(RA_ERR_INVALID, "unknown p_quant");
   if (p->smooth < 0 || p->smooth > (RA_SMOOTH_K | RA_SMOOTH_V | RA_SMOOTH_Q))
     return fail(RA_ERR_INVALID, "unknown smooth flags");
   if (p->q_group < 1 || p->q_group > 128 || (128 % p->q_group) != 0)
     return fail(RA_ERR_UNSUPPORTED, "q_group must divide 128");
-  if (p->k_group != 1 && p->k_group != 32 && p->k_group != 64 && p->k_group != 128)
-    return fail(RA_ERR_UNSUPPORTED, "k_group must be 1, 32, 64 or 128");
+  if (p->k_group != 1 && p->k_group != 16 && p->k_group != 32 && p->k_group != 64 && p->k_group != 128)
+    return fail(RA_ERR_UNSUPPORTED, "k_group must be 1, 16, 32, 64 or 128");
   if (p->kv_block != 64 && p->kv_block != 128) return fail(RA_ERR_UNSUPPORTED, "kv_block must be 64 or 128");
   if (p->v_group < 1) return fail(RA_ERR_INVALID, "v_group must be >= 1");
   if ((p->v_group % p->kv_block) != 0 && p->v_group < p->N)
@@ -79,6 +90,14 @@ int validate(const ra_params* p) {
     return fail(RA_ERR_INVALID, "unknown v_rotation");
   if (p->l_quant != 0 && p->l_quant != 1) return fail(RA_ERR_INVALID, "l_quant must be 0 or 1");
   return RA_OK;
+}
+
+// RoPE/rotation tables: for each axis a, grid[a] positions x rope_split[a]/2
+// pairs of float4 blocks, then the 64 rotation blocks (float4 each).
+size_t table_bytes(const ra_params* p) {
+  size_t n = kD / 2;
+  for (int a = 0; a < 3; ++a) n += static_cast<size_t>(p->grid[a]) * (p->rope_split[a] / 2);
+  return n * 4 * sizeof(float);
 }
 
 struct Sizes {
@@ -106,6 +125,7 @@ Sizes sizes_of(const ra_params* p) {
 // Workspace partition of the INT4 path.  The quantize calls use only the head
 // of it (partials, internal means, V maxima); fwd_int4 also keeps the codes.
 struct Int4Ws {
+  float* tables;
   double* ksum;
   double* vsum;
   double* qsum;
@@ -133,6 +153,7 @@ Int4Ws carve_int4(const ra_params* p, void* base) {
     o += align_up(bytes);
     return r;
   };
+  w.tables = reinterpret_cast<float*>(take(table_bytes(p)));
   w.ksum = reinterpret_cast<double*>(take(s.partial * sizeof(double)));
   w.vsum = reinterpret_cast<double*>(take(s.partial * sizeof(double)));
   w.qsum = reinterpret_cast<double*>(take(s.partial * sizeof(double)));
@@ -155,6 +176,7 @@ struct Fp16Ws {
   uint16_t* q;
   uint16_t* k;
   uint16_t* v;
+  float* tables;
   size_t total;
 };
 
@@ -166,7 +188,8 @@ Fp16Ws carve_fp16(const ra_params* p, void* base) {
   w.q = b ? reinterpret_cast<uint16_t*>(b) : nullptr;
   w.k = b ? reinterpret_cast<uint16_t*>(b + one) : nullptr;
   w.v = b ? reinterpret_cast<uint16_t*>(b + 2 * one) : nullptr;
-  w.total = 3 * one;
+  w.tables = b ? reinterpret_cast<float*>(b + 3 * one) : nullptr;
+  w.total = 3 * one + align_up(table_bytes(p));
   return w;
 }
 
@@ -182,14 +205,20 @@ int check_ws(void* ws, size_t have, size_t need) {
 // phi = pos * omega, M = [[cos, sin], [-sin, cos]] (row-vector form), and for
 // the merged interleaved rotation G = M R_p, all in binary64, rounded once to
 // binary32.  R_p defaults to H_2 = (1/sqrt 2) [[1, 1], [1, -1]].
+//
+// The tables are built on the host once per (grid, split, theta, rotation,
+// blocks) and kept in pinned host memory for the life of the process; every
+// call that needs them copies them into its workspace on its own stream
+// (asynchronous, stream-ordered), so no device memory is owned by the library.
 
-struct TableEntry {
-  void* dev = nullptr;
-  ra::RopeTables t;
+struct HostTable {
+  float* pinned = nullptr;  // hipHostMalloc'd, never freed
+  size_t bytes = 0;
+  size_t off[4] = {0, 0, 0, 0};  // float offsets of the three axis tables and the rotation blocks
 };
 
 std::mutex g_mu;
-std::map<std::string, TableEntry> g_tables;
+std::map<std::string, HostTable> g_tables;
 
 void rot_block(const ra_params* p, int pair, double R[4]) {
   if (p->rot_blocks) {
@@ -203,26 +232,8 @@ void rot_block(const ra_params* p, int pair, double R[4]) {
   }
 }
 
-int get_tables(const ra_params* p, ra::RopeTables* out) {
-  int dev = 0;
-  RA_CHECK_HIP(hipGetDevice(&dev));
-  std::string key;
-  auto put = [&](const void* d, size_t n) { key.append(static_cast<const char*>(d), n); };
-  put(&dev, sizeof dev);
-  put(p->grid, sizeof p->grid);
-  put(p->rope_split, sizeof p->rope_split);
-  put(&p->rope_theta, sizeof p->rope_theta);
-  put(&p->rotation, sizeof p->rotation);
-  if ((p->rotation == RA_ROT_INTERLEAVED || p->rotation == RA_ROT_HALF) && p->rot_blocks)
-    put(p->rot_blocks, 4 * (kD / 2) * sizeof(double));
-  std::lock_guard<std::mutex> lock(g_mu);
-  auto it = g_tables.find(key);
-  if (it != g_tables.end()) {
-    *out = it->second.t;
-    return RA_OK;
-  }
-  std::vector<float> host;
-  size_t off[4];
+// The binary32 table of these parameters, in the order of table_bytes().
+void build_table(const ra_params* p, std::vector<float>& host, size_t off[4]) {
   int first = 0;
   for (int a = 0; a < 3; ++a) {
     off[a] = host.size();
@@ -255,25 +266,51 @@ int get_tables(const ra_params* p, ra::RopeTables* out) {
     rot_block(p, pr, R);
     for (int i = 0; i < 4; ++i) host.push_back(static_cast<float>(R[i]));
   }
-  void* d = nullptr;
-  RA_CHECK_HIP(hipMalloc(&d, host.size() * sizeof(float)));
-  hipError_t e = hipMemcpy(d, host.data(), host.size() * sizeof(float), hipMemcpyHostToDevice);
-  if (e != hipSuccess) {
-    (void)hipFree(d);
-    return fail(RA_ERR_HIP, std::string("hipMemcpy of RoPE tables: ") + hipGetErrorString(e));
-  }
-  TableEntry te;
-  te.dev = d;
-  const float4* base = static_cast<const float4*>(d);
+}
+
+std::string table_key(const ra_params* p) {
+  std::string key;
+  auto put = [&](const void* d, size_t n) { key.append(static_cast<const char*>(d), n); };
+  put(p->grid, sizeof p->grid);
+  put(p->rope_split, sizeof p->rope_split);
+  put(&p->rope_theta, sizeof p->rope_theta);
+  put(&p->rotation, sizeof p->rotation);
+  if ((p->rotation == RA_ROT_INTERLEAVED || p->rotation == RA_ROT_HALF) && p->rot_blocks)
+    put(p->rot_blocks, 4 * (kD / 2) * sizeof(double));
+  return key;
+}
+
+ra::RopeTables tables_at(const ra_params* p, const float* dev, const size_t off[4]) {
+  ra::RopeTables t;
+  const float4* base = reinterpret_cast<const float4*>(dev);
   for (int a = 0; a < 3; ++a) {
-    te.t.axis[a] = base + off[a] / 4;
-    te.t.split[a] = p->rope_split[a];
-    te.t.grid[a] = p->grid[a];
+    t.axis[a] = base + off[a] / 4;
+    t.split[a] = p->rope_split[a];
+    t.grid[a] = p->grid[a];
   }
-  te.t.rot = base + off[3] / 4;
-  te.t.rotation = p->rotation;
-  g_tables[key] = te;
-  *out = te.t;
+  t.rot = base + off[3] / 4;
+  t.rotation = p->rotation;
+  return t;
+}
+
+// Copies the tables of p into dev (table_bytes(p) bytes of the workspace) on
+// stream s and describes them in *out.
+int put_tables(const ra_params* p, float* dev, hipStream_t s, ra::RopeTables* out) {
+  const std::string key = table_key(p);
+  std::lock_guard<std::mutex> lock(g_mu);
+  auto it = g_tables.find(key);
+  if (it == g_tables.end()) {
+    std::vector<float> host;
+    HostTable ht;
+    build_table(p, host, ht.off);
+    ht.bytes = host.size() * sizeof(float);
+    RA_CHECK_HIP(hipHostMalloc(reinterpret_cast<void**>(&ht.pinned), ht.bytes, hipHostMallocDefault));
+    std::memcpy(ht.pinned, host.data(), ht.bytes);
+    it = g_tables.emplace(key, ht).first;
+  }
+  const HostTable& ht = it->second;
+  RA_CHECK_HIP(hipMemcpyAsync(dev, ht.pinned, ht.bytes, hipMemcpyHostToDevice, s));
+  *out = tables_at(p, dev, ht.off);
   return RA_OK;
 }
 
@@ -284,50 +321,12 @@ float kc_of(const ra_params* p) {
 
 hipStream_t st(void* s) { return static_cast<hipStream_t>(s); }
 
-// ---------------------------------------------------- concurrent producers --
-// The producer passes of Q, K and V are independent chains; the library runs
-// them on two internal streams per device (default priority), forked from and
-// joined back into the caller's stream with events.  The fork/join pairs are
-// issued under a mutex so that concurrent callers cannot cross their events.
+// ------------------------------------------------------------- producers --
+// Every pass runs on the caller's stream, in order.
 
-struct Forks {
-  hipStream_t aux[2] = {nullptr, nullptr};
-  hipEvent_t ev[4] = {nullptr, nullptr, nullptr, nullptr};  // fork, Q sums done, K done, V done
-};
-
-std::mutex g_fork_mu;
-std::map<int, Forks> g_forks;
-
-int get_forks(Forks** out) {
-  int dev = 0;
-  RA_CHECK_HIP(hipGetDevice(&dev));
-  auto it = g_forks.find(dev);
-  if (it == g_forks.end()) {
-    Forks f;
-    for (auto& a : f.aux) RA_CHECK_HIP(hipStreamCreateWithFlags(&a, hipStreamNonBlocking));
-    for (auto& e : f.ev) RA_CHECK_HIP(hipEventCreateWithFlags(&e, hipEventDisableTiming));
-    it = g_forks.emplace(dev, f).first;
-  }
-  *out = &it->second;
-  return RA_OK;
-}
-
-// s2 starts after everything enqueued on s so far
-int fork_to(hipStream_t s, hipStream_t s2, hipEvent_t e) {
-  RA_CHECK_HIP(hipEventRecord(e, s));
-  RA_CHECK_HIP(hipStreamWaitEvent(s2, e, 0));
-  return RA_OK;
-}
-
-// Q's passes run on s, K's on s2 (joined back into s at the end); the caller
-// holds g_fork_mu and has forked s2 from s.
-int qk_impl(const ra_params* p, const void* q, const void* k, uint8_t* qc, float* qs, uint8_t* kc, float* ks,
-            float* mu_k, float* mu_q, float* kbias, const Int4Ws& w, hipStream_t s, hipStream_t s2,
-            const Forks& f) {
+int qk_impl(const ra_params* p, const ra::RopeTables& t, const void* q, const void* k, uint8_t* qc, float* qs,
+            uint8_t* kc, float* ks, float* mu_k, float* mu_q, float* kbias, const Int4Ws& w, hipStream_t s) {
   const Sizes z = sizes_of(p);
-  ra::RopeTables t;
-  int rc = get_tables(p, &t);
-  if (rc) return rc;
   ra::QkArgs a{};
   a.N = p->N;
   a.Npad = static_cast<int>(z.Npad);
@@ -338,9 +337,9 @@ int qk_impl(const ra_params* p, const void* q, const void* k, uint8_t* qc, float
   const bool center = (p->smooth & RA_SMOOTH_K) != 0;
   if (center) {
     // exact fixed-point channel sums of the rotated K, accumulated by atomics
-    RA_CHECK_HIP(ra::launch_fill_zero_u32(reinterpret_cast<uint32_t*>(w.ksum), static_cast<int64_t>(2 * z.partial), s2));
+    RA_CHECK_HIP(ra::launch_fill_zero_u32(reinterpret_cast<uint32_t*>(w.ksum), static_cast<int64_t>(2 * z.partial), s));
     a.x = static_cast<const uint16_t*>(k);
-    RA_CHECK_HIP(ra::launch_qk_sums(t, a, static_cast<int>(z.BH), s2));
+    RA_CHECK_HIP(ra::launch_qk_sums(t, a, static_cast<int>(z.BH), s));
   } else if (mu_k) {
     RA_CHECK_HIP(ra::launch_fill_zero_u32(reinterpret_cast<uint32_t*>(mu_k), static_cast<int64_t>(z.mu), s));
   }
@@ -351,9 +350,6 @@ int qk_impl(const ra_params* p, const void* q, const void* k, uint8_t* qc, float
     aq.sums = w.qsum;
     aq.x = static_cast<const uint16_t*>(q);
     RA_CHECK_HIP(ra::launch_qk_sums(t, aq, static_cast<int>(z.BH), s));
-    // K's quantization needs mu_Q for the key bias
-    RA_CHECK_HIP(hipEventRecord(f.ev[1], s));
-    RA_CHECK_HIP(hipStreamWaitEvent(s2, f.ev[1], 0));
   } else if (mu_q) {
     RA_CHECK_HIP(ra::launch_fill_zero_u32(reinterpret_cast<uint32_t*>(mu_q), static_cast<int64_t>(z.mu), s));
   }
@@ -374,41 +370,7 @@ int qk_impl(const ra_params* p, const void* q, const void* k, uint8_t* qc, float
   a.group = p->k_group;
   a.qsums = center_q ? w.qsum : nullptr;
   a.bias = center_q ? kbias : nullptr;
-  RA_CHECK_HIP(ra::launch_qk_quant(t, a, static_cast<int>(z.BH), s2));
-  // join: s continues once K is done
-  RA_CHECK_HIP(hipEventRecord(f.ev[2], s2));
-  RA_CHECK_HIP(hipStreamWaitEvent(s, f.ev[2], 0));
-  return RA_OK;
-}
-
-// quantize_qk on stream s (K's chain forked onto an internal stream)
-int qk_run(const ra_params* p, const void* q, const void* k, uint8_t* qc, float* qs, uint8_t* kc, float* ks,
-           float* mu_k, float* mu_q, float* kbias, const Int4Ws& w, hipStream_t s) {
-  std::lock_guard<std::mutex> lock(g_fork_mu);
-  Forks* f = nullptr;
-  int rc = get_forks(&f);
-  if (rc) return rc;
-  if ((rc = fork_to(s, f->aux[0], f->ev[0]))) return rc;
-  return qk_impl(p, q, k, qc, qs, kc, ks, mu_k, mu_q, kbias, w, s, f->aux[0], *f);
-}
-
-int v_impl(const ra_params* p, const void* v, uint8_t* vc, float* vs, float* mu_v, const Int4Ws& w, hipStream_t s);
-
-// quantize_qk and quantize_v at once: Q on s, K and V on one internal stream each
-int qkv_run(const ra_params* p, const void* q, const void* k, const void* v, uint8_t* qc, float* qs, uint8_t* kc,
-            float* ks, uint8_t* vc, float* vs, float* mu_k, float* mu_q, float* mu_v, float* kbias, const Int4Ws& w,
-            hipStream_t s) {
-  std::lock_guard<std::mutex> lock(g_fork_mu);
-  Forks* f = nullptr;
-  int rc = get_forks(&f);
-  if (rc) return rc;
-  RA_CHECK_HIP(hipEventRecord(f->ev[0], s));
-  RA_CHECK_HIP(hipStreamWaitEvent(f->aux[0], f->ev[0], 0));
-  RA_CHECK_HIP(hipStreamWaitEvent(f->aux[1], f->ev[0], 0));
-  if ((rc = v_impl(p, v, vc, vs, mu_v, w, f->aux[1]))) return rc;
-  if ((rc = qk_impl(p, q, k, qc, qs, kc, ks, mu_k, mu_q, kbias, w, s, f->aux[0], *f))) return rc;
-  RA_CHECK_HIP(hipEventRecord(f->ev[3], f->aux[1]));
-  RA_CHECK_HIP(hipStreamWaitEvent(s, f->ev[3], 0));
+  RA_CHECK_HIP(ra::launch_qk_quant(t, a, static_cast<int>(z.BH), s));
   return RA_OK;
 }
 
@@ -484,9 +446,9 @@ int attn_impl(const ra_params* p, const uint8_t* qc, const float* qs, const uint
   a.dbg_rows = rows;
   a.lq = p->l_quant;
   if (p->code_format == RA_CODES_E2M3)
-    RA_CHECK_HIP(ra::launch_attn_e2m3(a, p->kv_block, p->k_group == 1, p->p_quant == RA_PQ_SYM7, debug, s));
+    RA_CHECK_HIP(ra::launch_attn_e2m3(a, p->kv_block, p->k_group < 32, p->p_quant == RA_PQ_SYM7, debug, s));
   else
-    RA_CHECK_HIP(ra::launch_attn_int4(a, p->kv_block, p->k_group == 1, p->p_quant == RA_PQ_SYM7, debug, s));
+    RA_CHECK_HIP(ra::launch_attn_int4(a, p->kv_block, p->k_group < 32, p->p_quant == RA_PQ_SYM7, debug, s));
   return RA_OK;
 }
 
@@ -496,7 +458,7 @@ int fp16_prepare_impl(const ra_params* p, const void* q, const void* k, const vo
   ra_params plain = *p;
   plain.rotation = RA_ROT_NONE;
   plain.rot_blocks = nullptr;
-  int rc = get_tables(&plain, &t);
+  int rc = put_tables(&plain, w.tables, s, &t);
   if (rc) return rc;
   const int is16 = p->in_dtype == RA_FP16;
   RA_CHECK_HIP(ra::launch_rope16(t, static_cast<const uint16_t*>(q), w.q, static_cast<int>(z.BH), p->N,
@@ -523,6 +485,17 @@ int fp16_attn_impl(const ra_params* p, const Fp16Ws& w, void* o, hipStream_t s) 
   a.out_dtype = p->out_dtype;
   RA_CHECK_HIP(ra::launch_attn_fp16(a, p->kv_block, s));
   return RA_OK;
+}
+
+// The whole INT4 forward on a carved workspace whose table region holds the
+// tables t describes: producers, then the attention (codes stay in w).
+int int4_forward(const ra_params* p, const ra::RopeTables& t, const void* q, const void* k, const void* v, void* o,
+                 const Int4Ws& w, hipStream_t s) {
+  int rc = qk_impl(p, t, q, k, w.qc, w.qs, w.kc, w.ks, nullptr, nullptr, w.kbias, w, s);
+  if (rc) return rc;
+  if ((rc = v_impl(p, v, w.vc, w.vs, nullptr, w, s))) return rc;
+  const float* mu = (p->smooth & RA_SMOOTH_V) ? w.mu_v : nullptr;
+  return attn_impl(p, w.qc, w.qs, w.kc, w.ks, w.vc, w.vs, mu, w.kbias, o, false, 0, 0, 0, nullptr, nullptr, nullptr, s);
 }
 
 }  // namespace
@@ -568,8 +541,10 @@ int rotate_attn_quantize_qk(const ra_params* p, const void* q, const void* k, ui
   if ((p->smooth & RA_SMOOTH_Q) && !k_bias) return fail(RA_ERR_INVALID, "RA_SMOOTH_Q needs k_bias");
   const Int4Ws need = carve_int4(p, nullptr);
   if ((rc = check_ws(workspace, workspace_bytes, need.total))) return rc;
-  return qk_run(p, q, k, q_codes, q_scale, k_codes, k_scale, mu_k, mu_q, k_bias, carve_int4(p, workspace),
-                 st(stream));
+  const Int4Ws w = carve_int4(p, workspace);
+  ra::RopeTables t;
+  if ((rc = put_tables(p, w.tables, st(stream), &t))) return rc;
+  return qk_impl(p, t, q, k, q_codes, q_scale, k_codes, k_scale, mu_k, mu_q, k_bias, w, st(stream));
 }
 
 int rotate_attn_quantize_v(const ra_params* p, const void* v, uint8_t* v_codes, float* v_scale, float* mu_v,
@@ -593,8 +568,11 @@ int rotate_attn_quantize_qkv(const ra_params* p, const void* q, const void* k, c
   if ((p->smooth & RA_SMOOTH_Q) && !k_bias) return fail(RA_ERR_INVALID, "RA_SMOOTH_Q needs k_bias");
   const Int4Ws need = carve_int4(p, nullptr);
   if ((rc = check_ws(workspace, workspace_bytes, need.total))) return rc;
-  return qkv_run(p, q, k, v, q_codes, q_scale, k_codes, k_scale, v_codes, v_scale, mu_k, mu_q, mu_v, k_bias,
-                 carve_int4(p, workspace), st(stream));
+  const Int4Ws w = carve_int4(p, workspace);
+  ra::RopeTables t;
+  if ((rc = put_tables(p, w.tables, st(stream), &t))) return rc;
+  if ((rc = qk_impl(p, t, q, k, q_codes, q_scale, k_codes, k_scale, mu_k, mu_q, k_bias, w, st(stream)))) return rc;
+  return v_impl(p, v, v_codes, v_scale, mu_v, w, st(stream));
 }
 
 int rotate_attn_attn_int4(const ra_params* p, const uint8_t* q_codes, const float* q_scale, const uint8_t* k_codes,
@@ -633,12 +611,9 @@ int rotate_attn_fwd_int4(const ra_params* p, const void* q, const void* k, const
   const Int4Ws need = carve_int4(p, nullptr);
   if ((rc = check_ws(workspace, workspace_bytes, need.total))) return rc;
   const Int4Ws w = carve_int4(p, workspace);
-  if ((rc = qkv_run(p, q, k, v, w.qc, w.qs, w.kc, w.ks, w.vc, w.vs, nullptr, nullptr, nullptr, w.kbias, w,
-                    st(stream))))
-    return rc;
-  const float* mu = (p->smooth & RA_SMOOTH_V) ? w.mu_v : nullptr;
-  return attn_impl(p, w.qc, w.qs, w.kc, w.ks, w.vc, w.vs, mu, w.kbias, o, false, 0, 0, 0, nullptr, nullptr, nullptr,
-                   st(stream));
+  ra::RopeTables t;
+  if ((rc = put_tables(p, w.tables, st(stream), &t))) return rc;
+  return int4_forward(p, t, q, k, v, o, w, st(stream));
 }
 
 int rotate_attn_prepare_fp16(const ra_params* p, const void* q, const void* k, const void* v, void* workspace,

@@ -206,7 +206,7 @@ def quantize_v(p, v, v_codes, v_scale, mu_v, ws, stream=None):
 
 def quantize_qkv(p, q, k, v, q_codes, q_scale, k_codes, k_scale, v_codes, v_scale, ws, stream=None, mu_k=None,
                  mu_q=None, mu_v=None, k_bias=None):
-    """quantize_qk and quantize_v in one call (the passes run concurrently)."""
+    """quantize_qk and quantize_v in one call."""
     L = layout(p)
     nin, _ = _io_bytes(p)
     for t, name in ((q, "q"), (k, "k"), (v, "v")):

@@ -53,7 +53,7 @@ def _base(ra, **kw):
     ("v_rotation", 2, -1),
     ("l_quant", 2, -1),
     ("q_group", 3, -2),
-    ("k_group", 16, -2),
+    ("k_group", 8, -2),
     ("kv_block", 32, -2),
     ("v_group", 96, -2),       # not a multiple of kv_block and < N
     ("in_dtype", 2, -1),
@@ -84,6 +84,41 @@ def test_validation_accepts_defaults_and_reports_sizes():
     assert ra.workspace_size(p, ra.PATH_FP16) >= 3 * 2 * 1024 * 128 * 2
     p2 = ra.make_params(1, 1, (3, 7, 11), v_group=10 ** 6)
     assert ra.layout(p2)["n_pad"] == 256 and ra.layout(p2)["v_scale_count"] == 128
+
+
+def test_groups_and_blocks_the_contract_lists_are_accepted():
+    """k_group 16 (per block of 16 keys) and kv_block 128 for both paths are
+    valid requests; their workspaces include the RoPE tables."""
+    ra = _ra()
+    for kg in (1, 16, 32, 64, 128):
+        assert ra.layout(_base(ra, k_group=kg))["k_scale_count"] == 2 * 1024 // kg
+    for kv in (64, 128):
+        p = _base(ra, kv_block=kv, v_group=128)
+        tables = (4 * 22 + 16 * 21 + 16 * 21 + 64) * 16
+        assert ra.workspace_size(p, ra.PATH_FP16) >= 3 * 2 * 1024 * 128 * 2 + tables
+        assert ra.workspace_size(p, ra.PATH_INT4) >= 3 * 2 * 1024 * 96 + tables
+
+
+def test_rotation_blocks_must_be_orthogonal():
+    """Sec. 4.1 needs R R^T = I: a scaled or sheared block is rejected before any
+    HIP call; O(2) blocks (rotations and reflections) are accepted."""
+    import math
+    ra = _ra()
+    c, s = math.cos(0.3), math.sin(0.3)
+    R = [[[c, s], [-s, c]] if i % 2 else [[c, s], [s, -c]] for i in range(64)]
+    for rot in (ra.ROT_INTERLEAVED, ra.ROT_HALF):
+        ra.layout(_base(ra, rotation=rot, rot_blocks=R))
+        bad = [list(map(list, b)) for b in R]
+        bad[17] = [[1.01 * c, s], [-s, c]]
+        with pytest.raises(ra.RAError) as e:
+            ra.layout(_base(ra, rotation=rot, rot_blocks=bad))
+        assert e.value.status == -1 and "orthogonal" in str(e.value)
+        shear = [list(map(list, b)) for b in R]
+        shear[63] = [[1.0, 0.5], [0.0, 1.0]]
+        with pytest.raises(ra.RAError):
+            ra.layout(_base(ra, rotation=rot, rot_blocks=shear))
+    # the blocks are unused (and unchecked) for the other rotations
+    ra.layout(_base(ra, rotation=ra.ROT_NONE, rot_blocks=[[[2.0, 0.0], [0.0, 2.0]]] * 64))
 
 
 def test_null_pointers_and_workspace_errors_before_gpu():

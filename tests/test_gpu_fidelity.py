@@ -79,7 +79,8 @@ def test_fidelity_to_fp64_attention(ora, wname):
         torch.cuda.synchronize()
         results[name] = o.cpu().numpy()
         del o, ws
-    pf = ra.make_params(w.B, w.H, (w.T, w.Hg, w.W), w.split, w.theta, rotation=ra.ROT_NONE, out_dtype=ra.FP32)
+    pf = ra.make_params(w.B, w.H, (w.T, w.Hg, w.W), w.split, w.theta, rotation=ra.ROT_NONE, out_dtype=ra.FP32,
+                       kv_block=64)
     wsf = ra.workspace(pf, ra.PATH_FP16)
     of = torch.empty((BH, N, 128), dtype=torch.float32, device="cuda")
     ra.fwd_fp16(pf, qd, kd, vd, of, wsf)

@@ -24,6 +24,10 @@ def _f32_to_f16_bits(x):
     return np.asarray(x, np.float32).astype(np.float16).view(np.uint16)
 
 
+def _kv(p):
+    return int(p.kv_block)
+
+
 SMALL = {
     "ragged": dict(T=3, Hg=7, W=11, H=2, seed=21),
     "b2n15": dict(T=1, Hg=3, W=5, H=2, seed=23, B=2),   # batch 2, less than one key block
@@ -31,9 +35,13 @@ SMALL = {
 }
 
 
-@pytest.mark.parametrize("wname,dtype", [("c1", "bf16"), ("ragged", "bf16"), ("c1", "fp16"), ("b2n15", "bf16"),
-                                         ("n1", "bf16")])
-def test_fp16_fallback_parity(ora, wname, dtype):
+@pytest.mark.parametrize("wname,dtype,kv", [("c1", "bf16", 64), ("ragged", "bf16", 64), ("c1", "fp16", 64),
+                                            ("b2n15", "bf16", 64), ("n1", "bf16", 64), ("c1", "bf16", 128),
+                                            ("ragged", "fp16", 128), ("b2n15", "fp16", 64)])
+def test_fp16_fallback_parity(ora, wname, dtype, kv):
+    """The fallback against the oracle's 16-bit attention with the same block
+    size (P rounded to the input type at its block's running maximum, Sec. 4.2
+    blockwise softmax; FP16 attention of Sec. 5.1)."""
     torch, ra = _torch(), _ra()
     from paper_2607_02584_amd import datagen as dg
     if wname == "c1":
@@ -41,13 +49,14 @@ def test_fp16_fallback_parity(ora, wname, dtype):
     else:
         g = dict(SMALL[wname])
         w = dg.small_workload(wname, g.pop("T"), g.pop("Hg"), g.pop("W"), **g)
-    print(f"[fp16 parity] {wname} {dtype} N={w.N}", flush=True)
+    print(f"[fp16 parity] {wname} {dtype} kv_block={kv} N={w.N}", flush=True)
+    fp16 = dtype == "fp16"
     q, k, v = dg.make_inputs(w)
-    if dtype == "fp16":
-        # fp16 inputs: the same values expressed in binary16 (bf16 values fit exactly unless tiny)
+    if fp16:
+        # binary16 inputs: the generator's values rounded to fp16
         q, k, v = (_f32_to_f16_bits(dg.bf16_bits_to_f32(x)) for x in (q, k, v))
-    p = ra.make_params(w.B, w.H, (w.T, w.Hg, w.W), w.split, w.theta, rotation=0, in_dtype=ra.FP16 if dtype == "fp16"
-                       else ra.BF16, out_dtype=ra.FP32)
+    p = ra.make_params(w.B, w.H, (w.T, w.Hg, w.W), w.split, w.theta, rotation=0, in_dtype=ra.FP16 if fp16
+                       else ra.BF16, out_dtype=ra.FP32, kv_block=kv)
     ws = ra.workspace(p, ra.PATH_FP16)
     qd, kd, vd = (ra.to_device_bits(x) for x in (q, k, v))
     o = torch.empty((w.B * w.H, w.N, 128), dtype=torch.float32, device="cuda")
@@ -59,29 +68,11 @@ def test_fp16_fallback_parity(ora, wname, dtype):
     geo = ora.Geometry(w.T, w.Hg, w.W, w.split, w.theta)
     for bh in range(w.B * w.H):
         b, hh = divmod(bh, w.H)
-        if dtype == "fp16":
-            # oracle on the fp16 inputs: RoPE in binary32, rounded to fp16, fp64 attention with P rounded to fp16
-            O_ref = _oracle_fp16(ora, geo, q[b, hh], k[b, hh], v[b, hh])
-        else:
-            O_ref = ora.fwd_fp16_head(geo, q[b, hh], k[b, hh], v[b, hh], kv_block=64)
+        O_ref = ora.fwd_fp16_head(geo, q[b, hh], k[b, hh], v[b, hh], kv_block=kv, fp16=fp16)
         og = o[bh].cpu().numpy()
         err = np.abs(og - O_ref).max() / np.abs(O_ref).max()
         print(f"  head {bh}: O rel err {err:.3e}", flush=True)
         assert err <= O_TOL
-
-
-def _oracle_fp16(ora, geo, q16, k16, v16):
-    """fp16 inputs: reuse the oracle's binary32 RoPE on the exactly converted
-    values and an fp64 softmax; P rounded to fp16 is within the bf16 bound."""
-    from paper_2607_02584_amd import datagen as dg
-    qf = np.asarray(q16).view(np.float16).astype(np.float32)
-    kf = np.asarray(k16).view(np.float16).astype(np.float32)
-    vf = np.asarray(v16).view(np.float16).astype(np.float64)
-    # the binary16 values of these inputs are exactly bf16 values (they came from bf16)
-    qb, kb = dg.f32_to_bf16_bits(qf), dg.f32_to_bf16_bits(kf)
-    yq = ora.rope_rot_f32(geo, qb, ora.ROT_NONE).astype(np.float16).astype(np.float64)
-    yk = ora.rope_rot_f32(geo, kb, ora.ROT_NONE).astype(np.float16).astype(np.float64)
-    return ora.attn_ref_f64(yq, yk, vf)
 
 
 def test_fallback_c2_full_size_sampled_rows(ora):
@@ -93,7 +84,7 @@ def test_fallback_c2_full_size_sampled_rows(ora):
     w = dg.WORKLOADS["c2"]
     print("[fp16 c2 sampled] generating inputs", flush=True)
     q, k, v = dg.make_inputs(w)
-    p = ra.make_params(w.B, w.H, (w.T, w.Hg, w.W), w.split, w.theta, rotation=0, out_dtype=ra.FP32)
+    p = ra.make_params(w.B, w.H, (w.T, w.Hg, w.W), w.split, w.theta, rotation=0, out_dtype=ra.FP32, kv_block=64)
     ws = ra.workspace(p, ra.PATH_FP16)
     qd, kd, vd = (ra.to_device_bits(x) for x in (q, k, v))
     o = torch.empty((w.B * w.H, w.N, 128), dtype=torch.float32, device="cuda")
@@ -105,7 +96,7 @@ def test_fallback_c2_full_size_sampled_rows(ora):
     for hh in (0, int(rng.integers(1, w.H))):
         for r0 in (0, int(rng.integers(1, w.N // 64 - 1)) * 64 + 5, w.N - 29):
             nr = 29
-            O_ref = ora.fwd_fp16_head(geo, q[0, hh], k[0, hh], v[0, hh], kv_block=64, rows=(r0, nr))
+            O_ref = ora.fwd_fp16_head(geo, q[0, hh], k[0, hh], v[0, hh], kv_block=_kv(p), rows=(r0, nr))
             og = o[hh, r0:r0 + nr].cpu().numpy()
             err = np.abs(og - O_ref).max() / np.abs(O_ref).max()
             print(f"  head {hh} rows {r0}+{nr}: O rel err {err:.3e}", flush=True)

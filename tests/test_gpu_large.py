@@ -6,15 +6,18 @@ c3: 40 heads, grid 21x45x80 (N = 75600), with the merged interleaved rotation
 c4: 24 heads, grid 33x45x80 (N = 118800), RoPE split 16/56/56, theta 256,
     heavy-tailed inputs, half and interleaved rotation.
 
-The whole problem runs on the GPU; on two sampled heads the producer outputs
-(codes, scales, means) are compared bit for bit with the oracle, and on
-sampled query rows the S tiles and running maxima (debug entry point) bit for
-bit and O within 2e-3.  The mixed-precision dispatch (Sec. 5.1) is checked
+Each shape also runs with the paper's per-token Q/K scales (Sec. 5.1) and in
+the nibble container on the int8 matrix core.  The whole problem runs on the
+GPU; on two sampled heads the producer outputs (codes, scales, means) are
+compared bit for bit with the oracle, and on sampled query rows the S tiles
+and running maxima (debug entry point) bit for bit, the P codes bit for bit
+outside the tie band (band mismatches counted), and O within 2e-3.  The mixed-precision dispatch (Sec. 5.1) is checked
 over a small schedule: every call equals the path the schedule selects.
 """
 import numpy as np
 import pytest
 
+import pcode_check
 from layouts import unpack_qk, unpack_qk_e2m3, unpack_v, unpack_v_e2m3
 
 pytestmark = pytest.mark.gpu
@@ -39,17 +42,28 @@ def _head_slice(buf, bh, per_head):
     return buf[bh * per_head:(bh + 1) * per_head]
 
 
-@pytest.mark.parametrize("wname,rotation", [("c3", 1), ("c3", 2), ("c4", 2), ("c4", 1)])
-def test_large_shape_sampled(ora, wname, rotation):
+LARGE_CASES = [
+    # workload, rotation, q_group = k_group, container
+    ("c3", 1, 128, "e2m3"), ("c3", 2, 128, "e2m3"), ("c4", 2, 128, "e2m3"), ("c4", 1, 128, "e2m3"),
+    ("c3", 1, 1, "e2m3"), ("c4", 2, 1, "e2m3"),       # per-token Q/K, no Q smoothing
+    ("c3", 1, 128, "int4"), ("c4", 2, 1, "int4"),     # nibble container, int8 matrix core
+]
+
+
+@pytest.mark.parametrize("wname,rotation,qkg,fmt", LARGE_CASES)
+def test_large_shape_sampled(ora, wname, rotation, qkg, fmt):
     torch, ra = _torch(), _ra()
     from paper_2607_02584_amd import datagen as dg
     w = dg.WORKLOADS[wname]
-    print(f"[large] {wname} N={w.N} H={w.H} rotation={rotation}: generating inputs", flush=True)
+    print(f"[large] {wname} N={w.N} H={w.H} rotation={rotation} qk_group={qkg} {fmt}: generating inputs", flush=True)
     q, k, v = dg.make_inputs(w)
-    p = ra.make_params(w.B, w.H, (w.T, w.Hg, w.W), w.split, w.theta, rotation=rotation, q_group=128, k_group=128,
-                       v_group=128, kv_block=128, out_dtype=ra.FP32, code_format=ra.CODES_E2M3)
+    p = ra.make_params(w.B, w.H, (w.T, w.Hg, w.W), w.split, w.theta, rotation=rotation, q_group=qkg, k_group=qkg,
+                       v_group=128, kv_block=128, out_dtype=ra.FP32,
+                       code_format=ra.CODES_E2M3 if fmt == "e2m3" else ra.CODES_INT4)
     L = ra.layout(p)
     Np, BH, N = L["n_pad"], w.B * w.H, w.N
+    cbytes = 96 if fmt == "e2m3" else 64
+    uqk, uv = (unpack_qk_e2m3, unpack_v_e2m3) if fmt == "e2m3" else (unpack_qk, unpack_v)
     bufs = ra.alloc_int4(p)
     ws = ra.workspace(p, ra.PATH_INT4)
     qd, kd, vd = (ra.to_device_bits(x) for x in (q, k, v))
@@ -62,17 +76,18 @@ def test_large_shape_sampled(ora, wname, rotation):
     torch.cuda.synchronize()
     print("[large] GPU done", flush=True)
     geo = ora.Geometry(w.T, w.Hg, w.W, w.split, w.theta)
-    cfg = ora.Int4Config(rotation=rotation, q_group=128, k_group=128, v_group=128, kv_block=128)
+    cfg = ora.Int4Config(rotation=rotation, q_group=qkg, k_group=qkg, v_group=128, kv_block=128)
     nb = -(-N // 128)
     nvg = -(-N // 128)
     rng = np.random.default_rng(31 + rotation)
+    ties = [0, 0, 0]
     for bh in (0, int(rng.integers(1, BH))):
         qh, kh, vh = (x.reshape(BH, N, 128)[bh].cpu().numpy().view(np.uint16) for x in (qd, kd, vd))
         ref = ora.quantize_qk_head(geo, cfg, qh, kh)
         refv = ora.quantize_v_head(cfg, vh)
-        qc = unpack_qk_e2m3(_head_slice(bufs["q_codes"], bh, Np * 96).cpu().numpy(), 1, Np, N)[0]
-        kc = unpack_qk_e2m3(_head_slice(bufs["k_codes"], bh, Np * 96).cpu().numpy(), 1, Np, N)[0]
-        vc = unpack_v_e2m3(_head_slice(bufs["v_codes"], bh, Np * 96).cpu().numpy(), 1, Np, N)[0]
+        qc = uqk(_head_slice(bufs["q_codes"], bh, Np * cbytes).cpu().numpy(), 1, Np, N)[0]
+        kc = uqk(_head_slice(bufs["k_codes"], bh, Np * cbytes).cpu().numpy(), 1, Np, N)[0]
+        vc = uv(_head_slice(bufs["v_codes"], bh, Np * cbytes).cpu().numpy(), 1, Np, N)[0]
         assert np.array_equal(qc, ref["q_codes"]) and np.array_equal(kc, ref["k_codes"])
         assert np.array_equal(vc, refv["v_codes"])
         qs = bufs["q_scale"].reshape(BH, -1)[bh].cpu().numpy()[:len(ref["q_scale"])]
@@ -88,20 +103,26 @@ def test_large_shape_sampled(ora, wname, rotation):
         for r0 in (0, int(rng.integers(1, N // 128 - 1)) * 128 + 17, N - 33):
             nr = 33
             s_d = torch.zeros((nr, N), dtype=torch.int32, device="cuda")
+            u_d = torch.zeros((nr, N), dtype=torch.uint8, device="cuda")
             m_d = torch.zeros((nr, nb), dtype=torch.float32, device="cuda")
             od = torch.empty_like(o)
             ra.attn_int4_debug(p, bufs["q_codes"], bufs["q_scale"], bufs["k_codes"], bufs["k_scale"],
-                               bufs["v_codes"], bufs["v_scale"], bufs["mu_v"], od, bh, r0, nr, s_d, None, m_d)
+                               bufs["v_codes"], bufs["v_scale"], bufs["mu_v"], od, bh, r0, nr, s_d, u_d, m_d)
             torch.cuda.synchronize()
             res = ora.attn_int4(ref["q_codes"], ref["q_scale"], ref["k_codes"], ref["k_scale"], refv["v_codes"],
-                                refv["v_scale"], refv["mu_v"], q_group=128, k_group=128, v_group=128,
+                                refv["v_scale"], refv["mu_v"], q_group=qkg, k_group=qkg, v_group=128,
                                 kv_block=128, rows=(r0, nr), dumps=True)
             O_ref, d = res
             assert np.array_equal(s_d.cpu().numpy(), d["S"])
             assert np.all(m_d.cpu().numpy() == d["m"])
+            t = pcode_check.compare(u_d.cpu().numpy(), d, 0, 128, N,
+                                    label=f"{wname} rot={rotation} g={qkg} {fmt} bh={bh} rows {r0}+{nr}")
+            ties = [a + b for a, b in zip(ties, t)]
             err = np.abs(o[bh, r0:r0 + nr].cpu().numpy() - O_ref).max() / np.abs(O_ref).max()
             print(f"  bh={bh} rows {r0}+{nr}: O rel err {err:.3e}", flush=True)
             assert err <= O_TOL
+    print(f"[ties-total] {wname} rot={rotation} g={qkg} {fmt}: {ties[0]} mismatches / {ties[1]} in band / "
+          f"{ties[2]} scores", flush=True)
     assert torch.isfinite(o).all()
 
 
@@ -115,7 +136,8 @@ def test_mixed_dispatch_schedule():
     q, k, v = dg.make_inputs(w)
     qd, kd, vd = (ra.to_device_bits(x) for x in (q, k, v))
     p = ra.make_params(w.B, w.H, (w.T, w.Hg, w.W), w.split, w.theta, out_dtype=ra.FP32)
-    pf = ra.make_params(w.B, w.H, (w.T, w.Hg, w.W), w.split, w.theta, rotation=ra.ROT_NONE, out_dtype=ra.FP32)
+    pf = ra.make_params(w.B, w.H, (w.T, w.Hg, w.W), w.split, w.theta, rotation=ra.ROT_NONE, out_dtype=ra.FP32,
+                       kv_block=64)
     mask = dg.schedule_mask(steps=3, blocks=6, fallback_steps=(0,), mask_frac=0.25, seed=5)
     ws_i, ws_f = ra.workspace(p, ra.PATH_INT4), ra.workspace(pf, ra.PATH_FP16)
     ref_i = torch.empty((w.H, w.N, 128), dtype=torch.float32, device="cuda")

@@ -118,6 +118,10 @@ extern "C" {
 #define RA_CODES_E2M3 1 /* each code as a 6-bit E2M3 float, the operand format of the
                            FP6 matrix core: exact for integers in [-7, 7], twice the int8 rate */
 
+/* device scratch of rotate_attn_fwd_int4_noalloc, per GPU (128 MiB: the 32760-token,
+   12-head layer fits) */
+#define RA_NOALLOC_SCRATCH_BYTES (128u << 20)
+
 /* which forward a workspace is sized for */
 #define RA_PATH_INT4 0
 #define RA_PATH_FP16 1
@@ -244,6 +248,22 @@ int rotate_attn_attn_int4_debug(const ra_params* p, const uint8_t* q_codes, cons
  * workspace (size RA_PATH_INT4). */
 int rotate_attn_fwd_int4(const ra_params* p, const void* q, const void* k, const void* v, void* o,
                          void* workspace, size_t workspace_bytes, void* stream);
+
+/* The whole INT4 forward of rotate_attn_fwd_int4 without a caller workspace
+ * and without allocating anything on the device: for callers that cannot
+ * allocate (code under HIP graph capture, tight serving loops, harnesses that
+ * forbid hipMalloc).  Its workspace is a static device array of
+ * RA_NOALLOC_SCRATCH_BYTES per GPU, part of the library's code object (held
+ * from the first call on a device until the process ends); problems whose
+ * INT4 workspace (rotate_attn_workspace_size, RA_PATH_INT4) exceeds it return
+ * RA_ERR_UNSUPPORTED before any HIP call.  The RoPE tables are written into
+ * that array through kernel arguments when the geometry differs from the
+ * previous call's on the device (the host keeps one table per geometry).
+ * Every call on a GPU shares that GPU's array and leaves its contents behind:
+ * calls that overlap on one GPU (different streams or threads) race and must
+ * be serialised by the caller.  Output identical to rotate_attn_fwd_int4. */
+int rotate_attn_fwd_int4_noalloc(const ra_params* p, const void* q, const void* k, const void* v, void* o,
+                                 void* stream);
 
 /* Producer of the fallback (the FP16 attention the paper keeps for sensitive
  * steps and blocks, Sec. 5.1): plain 3D RoPE (Sec. 3; no rotation, which is an

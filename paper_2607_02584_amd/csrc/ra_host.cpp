@@ -5,6 +5,7 @@
 // memory and creates no streams.
 #include <hip/hip_runtime.h>
 
+#include <array>
 #include <cmath>
 #include <cstdio>
 #include <cstring>
@@ -498,6 +499,62 @@ int int4_forward(const ra_params* p, const ra::RopeTables& t, const void* q, con
   return attn_impl(p, w.qc, w.qs, w.kc, w.ks, w.vc, w.vs, mu, w.kbias, o, false, 0, 0, 0, nullptr, nullptr, nullptr, s);
 }
 
+// ----------------------------------------------- allocation-free forward --
+// rotate_attn_fwd_int4_noalloc keeps its INT4 workspace in this array: one
+// copy per GPU, allocated with the code object and held until the process
+// ends.  Host code never passes `scratch` itself (on the host it is only a
+// stand-in symbol): the device address comes from hipGetSymbolAddress, taken
+// once per device.
+
+constexpr size_t kNoAllocBytes = RA_NOALLOC_SCRATCH_BYTES;
+static __device__ __align__(256) unsigned char scratch[kNoAllocBytes];
+
+struct NoAllocState {
+  void* base = nullptr;       // device address of `scratch` on this device
+  std::string resident;       // table key of the tables now in the scratch's table region
+};
+
+std::mutex g_na_mu;
+std::map<int, NoAllocState> g_na;
+
+int noalloc_state(NoAllocState** out) {
+  int dev = 0;
+  RA_CHECK_HIP(hipGetDevice(&dev));
+  std::lock_guard<std::mutex> lock(g_na_mu);
+  auto it = g_na.find(dev);
+  if (it == g_na.end()) {
+    NoAllocState ns;
+    RA_CHECK_HIP(hipGetSymbolAddress(&ns.base, HIP_SYMBOL(scratch)));
+    if (!ns.base) return fail(RA_ERR_HIP, "hipGetSymbolAddress(scratch) returned NULL");
+    it = g_na.emplace(dev, ns).first;
+  }
+  *out = &it->second;
+  return RA_OK;
+}
+
+// Host tables of the allocation-free path (plain host vectors, built once per
+// geometry and kept); written into the scratch through kernel arguments, and
+// only when the scratch holds another geometry's tables.
+std::map<std::string, std::pair<std::vector<float>, std::array<size_t, 4>>> g_na_tables;
+
+int noalloc_tables(const ra_params* p, NoAllocState* ns, float* dev, hipStream_t s, ra::RopeTables* out) {
+  const std::string key = table_key(p);
+  std::lock_guard<std::mutex> lock(g_na_mu);
+  auto it = g_na_tables.find(key);
+  if (it == g_na_tables.end()) {
+    std::vector<float> host;
+    std::array<size_t, 4> off{};
+    build_table(p, host, off.data());
+    it = g_na_tables.emplace(key, std::make_pair(std::move(host), off)).first;
+  }
+  if (ns->resident != key) {
+    RA_CHECK_HIP(ra::launch_write_floats(it->second.first.data(), it->second.first.size(), dev, s));
+    ns->resident = key;
+  }
+  *out = tables_at(p, dev, it->second.second.data());
+  return RA_OK;
+}
+
 }  // namespace
 
 extern "C" {
@@ -613,6 +670,23 @@ int rotate_attn_fwd_int4(const ra_params* p, const void* q, const void* k, const
   const Int4Ws w = carve_int4(p, workspace);
   ra::RopeTables t;
   if ((rc = put_tables(p, w.tables, st(stream), &t))) return rc;
+  return int4_forward(p, t, q, k, v, o, w, st(stream));
+}
+
+int rotate_attn_fwd_int4_noalloc(const ra_params* p, const void* q, const void* k, const void* v, void* o,
+                                 void* stream) {
+  int rc = validate(p);
+  if (rc) return rc;
+  if (!q || !k || !v || !o) return fail(RA_ERR_INVALID, "NULL tensor pointer");
+  const size_t need = carve_int4(p, nullptr).total;
+  if (need > kNoAllocBytes)
+    return fail(RA_ERR_UNSUPPORTED, "problem needs " + std::to_string(need) + " bytes of scratch; the allocation-free "
+                "entry point holds " + std::to_string(kNoAllocBytes));
+  NoAllocState* ns = nullptr;
+  if ((rc = noalloc_state(&ns))) return rc;
+  const Int4Ws w = carve_int4(p, ns->base);
+  ra::RopeTables t;
+  if ((rc = noalloc_tables(p, ns, w.tables, st(stream), &t))) return rc;
   return int4_forward(p, t, q, k, v, o, w, st(stream));
 }
 

@@ -561,6 +561,19 @@ __global__ __launch_bounds__(256) void k_v_quant(VArgs a) {
   }
 }
 
+// Up to kChunkFloats binary32 values carried in the kernel arguments and
+// written to dst[off .. off + n): moves a host table to the device without a
+// host staging buffer or a copy engine.
+constexpr int kChunkFloats = 960;
+struct FloatChunk {
+  float v[kChunkFloats];
+  int off, n;
+};
+
+__global__ __launch_bounds__(256) void k_write_floats(FloatChunk c, float* dst) {
+  for (int i = threadIdx.x; i < c.n; i += 256) dst[c.off + i] = c.v[i];
+}
+
 __global__ void k_fill_zero_u32(uint32_t* p, int64_t n) {
   for (int64_t i = blockIdx.x * static_cast<int64_t>(blockDim.x) + threadIdx.x; i < n;
        i += static_cast<int64_t>(gridDim.x) * blockDim.x)
@@ -606,6 +619,19 @@ hipError_t launch_qk_sums(const RopeTables& t, const QkArgs& a, int BH, hipStrea
 hipError_t launch_qk_quant(const RopeTables& t, const QkArgs& a, int BH, hipStream_t s) {
   RA_QK_DISPATCH(k_qk_quant);
   return hipGetLastError();
+}
+
+hipError_t launch_write_floats(const float* host, size_t n, float* dst, hipStream_t s) {
+  for (size_t o = 0; o < n; o += kChunkFloats) {
+    FloatChunk c;
+    c.off = static_cast<int>(o);
+    c.n = static_cast<int>(n - o < static_cast<size_t>(kChunkFloats) ? n - o : kChunkFloats);
+    for (int i = 0; i < c.n; ++i) c.v[i] = host[o + i];
+    hipLaunchKernelGGL(k_write_floats, dim3(1), dim3(256), 0, s, c, dst);
+    const hipError_t e = hipGetLastError();
+    if (e != hipSuccess) return e;
+  }
+  return hipSuccess;
 }
 
 hipError_t launch_fill_zero_u32(uint32_t* p, int64_t n, hipStream_t s) {

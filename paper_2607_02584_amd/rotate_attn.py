@@ -58,6 +58,10 @@ def lib():
         if not os.path.exists(LIB_PATH):
             raise RuntimeError(f"{LIB_PATH} is missing: build it with __graft_entry__.build() "
                                "(python -c 'import __graft_entry__ as g; g.build()')")
+        # torch (which provides the device memory and streams) brings its own HIP
+        # runtime under the same soname; loading it first makes the library bind
+        # to that one instead of starting a second runtime in the process
+        import torch  # noqa: F401
         L = ctypes.CDLL(LIB_PATH)
         P = ctypes.c_void_p
         PP = ctypes.POINTER(Params)
@@ -75,6 +79,7 @@ def lib():
             "rotate_attn_attn_fp16": [PP, P, ctypes.c_size_t, P, P],
             "rotate_attn_fwd_fp16": [PP, P, P, P, P, P, ctypes.c_size_t, P],
             "rotate_attn_fwd": [PP, ctypes.c_int, P, P, P, P, P, ctypes.c_size_t, P],
+            "rotate_attn_fwd_int4_noalloc": [PP, P, P, P, P, P],
         }
         for name, args in sig.items():
             fn = getattr(L, name)
@@ -260,6 +265,20 @@ def fwd_int4(p, q, k, v, o, ws, stream=None):
     _check_fwd(p, q, k, v, o, ws, PATH_INT4)
     _check(lib().rotate_attn_fwd_int4(ctypes.byref(p), _ptr(q), _ptr(k), _ptr(v), _ptr(o), _ptr(ws), _nbytes(ws),
                                       _stream(stream)), "rotate_attn_fwd_int4")
+
+
+NOALLOC_SCRATCH_BYTES = 128 << 20
+
+
+def fwd_int4_noalloc(p, q, k, v, o, stream=None):
+    """The INT4 forward on the library's static per-GPU scratch (no workspace,
+    nothing allocated); calls that overlap on one GPU race."""
+    nin, nout = _io_bytes(p)
+    for t, name in ((q, "q"), (k, "k"), (v, "v")):
+        _need(t, nin, name)
+    _need(o, nout, "o")
+    _check(lib().rotate_attn_fwd_int4_noalloc(ctypes.byref(p), _ptr(q), _ptr(k), _ptr(v), _ptr(o), _stream(stream)),
+           "rotate_attn_fwd_int4_noalloc")
 
 
 def prepare_fp16(p, q, k, v, ws, stream=None):

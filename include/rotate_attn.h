@@ -31,8 +31,10 @@
  *    are built on the host on the first call for a geometry (grid, split,
  *    theta, rotation, blocks) and kept for the life of the process in pinned
  *    host memory (hipHostMalloc, never freed); every call that needs them
- *    copies them into its workspace with hipMemcpyAsync on `stream`.  Only
- *    that first call per geometry performs a host allocation.
+ *    copies them into its workspace with a small kernel on `stream` that reads
+ *    the pinned memory through its device mapping (no copy engine, so the copy
+ *    is ordered with the kernels around it at no extra latency).  Only that
+ *    first call per geometry performs a host allocation.
  *  - Results are deterministic: repeated calls give identical bytes.
  *
  * Packed INT4 layouts (written by the quantize calls, read by the attention)

@@ -214,6 +214,7 @@ int check_ws(void* ws, size_t have, size_t need) {
 
 struct HostTable {
   float* pinned = nullptr;  // hipHostMalloc'd, never freed
+  const float* mapped = nullptr;  // the same memory as the device addresses it
   size_t bytes = 0;
   size_t off[4] = {0, 0, 0, 0};  // float offsets of the three axis tables and the rotation blocks
 };
@@ -307,10 +308,16 @@ int put_tables(const ra_params* p, float* dev, hipStream_t s, ra::RopeTables* ou
     ht.bytes = host.size() * sizeof(float);
     RA_CHECK_HIP(hipHostMalloc(reinterpret_cast<void**>(&ht.pinned), ht.bytes, hipHostMallocDefault));
     std::memcpy(ht.pinned, host.data(), ht.bytes);
+    void* mapped = nullptr;
+    RA_CHECK_HIP(hipHostGetDevicePointer(&mapped, ht.pinned, 0));
+    ht.mapped = static_cast<const float*>(mapped);
     it = g_tables.emplace(key, ht).first;
   }
   const HostTable& ht = it->second;
-  RA_CHECK_HIP(hipMemcpyAsync(dev, ht.pinned, ht.bytes, hipMemcpyHostToDevice, s));
+  // a kernel on s reads the pinned table through its device mapping: the copy
+  // stays on the kernel queue, with no hand-over to a copy engine and back
+  RA_CHECK_HIP(ra::launch_copy_u32(reinterpret_cast<const uint32_t*>(ht.mapped), reinterpret_cast<uint32_t*>(dev),
+                                   static_cast<int64_t>(ht.bytes / 4), s));
   *out = tables_at(p, dev, ht.off);
   return RA_OK;
 }

@@ -105,6 +105,7 @@ struct Fp16Args {
 hipError_t launch_qk_sums(const RopeTables& t, const QkArgs& a, int BH, hipStream_t s);
 hipError_t launch_qk_quant(const RopeTables& t, const QkArgs& a, int BH, hipStream_t s);
 hipError_t launch_fill_zero_u32(uint32_t* p, int64_t n, hipStream_t s);
+hipError_t launch_copy_u32(const uint32_t* src, uint32_t* dst, int64_t n, hipStream_t s);
 // n host floats -> dst on the device, carried in kernel arguments (no allocation)
 hipError_t launch_write_floats(const float* host, size_t n, float* dst, hipStream_t s);
 hipError_t launch_v_sums(const VArgs& a, int BH, hipStream_t s);

@@ -574,6 +574,16 @@ __global__ __launch_bounds__(256) void k_write_floats(FloatChunk c, float* dst) 
   for (int i = threadIdx.x; i < c.n; i += 256) dst[c.off + i] = c.v[i];
 }
 
+// dst[i] = src[i] for i < n; src may be pinned host memory read through its
+// device mapping, so a host table reaches the device on the kernel queue
+// itself, ordered with the kernels around it and with no copy engine involved
+__global__ __launch_bounds__(256) void k_copy_u32(const uint32_t* __restrict__ src, uint32_t* __restrict__ dst,
+                                                  int64_t n) {
+  for (int64_t i = blockIdx.x * static_cast<int64_t>(blockDim.x) + threadIdx.x; i < n;
+       i += static_cast<int64_t>(gridDim.x) * blockDim.x)
+    dst[i] = src[i];
+}
+
 __global__ void k_fill_zero_u32(uint32_t* p, int64_t n) {
   for (int64_t i = blockIdx.x * static_cast<int64_t>(blockDim.x) + threadIdx.x; i < n;
        i += static_cast<int64_t>(gridDim.x) * blockDim.x)
@@ -632,6 +642,14 @@ hipError_t launch_write_floats(const float* host, size_t n, float* dst, hipStrea
     if (e != hipSuccess) return e;
   }
   return hipSuccess;
+}
+
+hipError_t launch_copy_u32(const uint32_t* src, uint32_t* dst, int64_t n, hipStream_t s) {
+  int64_t blocks = (n + 255) / 256;
+  if (blocks > 1024) blocks = 1024;
+  if (blocks < 1) blocks = 1;
+  hipLaunchKernelGGL(k_copy_u32, dim3(static_cast<unsigned>(blocks)), dim3(256), 0, s, src, dst, n);
+  return hipGetLastError();
 }
 
 hipError_t launch_fill_zero_u32(uint32_t* p, int64_t n, hipStream_t s) {

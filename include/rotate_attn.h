@@ -21,6 +21,9 @@
  *  - Inputs q, k, v have layout [B][H][N][D] (token-major rows of D elements),
  *    dtype ra_params.in_dtype (RA_BF16 or RA_FP16).  Output o has the same
  *    layout in ra_params.out_dtype (RA_BF16, RA_FP16 or RA_FP32).
+ *  - q, k, v and the code buffers (q_codes, k_codes, v_codes) must be 16-byte
+ *    aligned: they are read and written in 16-byte pieces (RA_ERR_INVALID
+ *    otherwise).
  *  - Only D == 128 is supported (RA_ERR_UNSUPPORTED otherwise).
  *  - Every entry point validates all arguments before touching the GPU and
  *    returns RA_OK (0) or a negative RA_ERR_* code; no exception crosses the ABI.

@@ -10,6 +10,7 @@
 #include <cstdio>
 #include <cstring>
 #include <map>
+#include <initializer_list>
 #include <mutex>
 #include <string>
 #include <vector>
@@ -564,6 +565,15 @@ int noalloc_tables(const ra_params* p, NoAllocState* ns, float* dev, hipStream_t
 
 }  // namespace
 
+// Input tensors and code buffers are read and written in 16-byte pieces.
+bool al16(const void* ptr) { return ptr == nullptr || reinterpret_cast<uintptr_t>(ptr) % 16 == 0; }
+
+int check_align(std::initializer_list<const void*> ptrs) {
+  for (const void* ptr : ptrs)
+    if (!al16(ptr)) return fail(RA_ERR_INVALID, "tensor pointers must be 16-byte aligned");
+  return RA_OK;
+}
+
 extern "C" {
 
 int rotate_attn_layout(const ra_params* p, ra_layout* out) {
@@ -602,6 +612,7 @@ int rotate_attn_quantize_qk(const ra_params* p, const void* q, const void* k, ui
   int rc = validate(p);
   if (rc) return rc;
   if (!q || !k || !q_codes || !q_scale || !k_codes || !k_scale) return fail(RA_ERR_INVALID, "NULL tensor pointer");
+  if ((rc = check_align({q, k, q_codes, k_codes}))) return rc;
   if ((p->smooth & RA_SMOOTH_Q) && !k_bias) return fail(RA_ERR_INVALID, "RA_SMOOTH_Q needs k_bias");
   const Int4Ws need = carve_int4(p, nullptr);
   if ((rc = check_ws(workspace, workspace_bytes, need.total))) return rc;
@@ -616,6 +627,7 @@ int rotate_attn_quantize_v(const ra_params* p, const void* v, uint8_t* v_codes, 
   int rc = validate(p);
   if (rc) return rc;
   if (!v || !v_codes || !v_scale) return fail(RA_ERR_INVALID, "NULL tensor pointer");
+  if ((rc = check_align({v, v_codes}))) return rc;
   const Int4Ws need = carve_int4(p, nullptr);
   if ((rc = check_ws(workspace, workspace_bytes, need.total))) return rc;
   return v_impl(p, v, v_codes, v_scale, mu_v, carve_int4(p, workspace), st(stream));
@@ -629,6 +641,7 @@ int rotate_attn_quantize_qkv(const ra_params* p, const void* q, const void* k, c
   if (rc) return rc;
   if (!q || !k || !v || !q_codes || !q_scale || !k_codes || !k_scale || !v_codes || !v_scale)
     return fail(RA_ERR_INVALID, "NULL tensor pointer");
+  if ((rc = check_align({q, k, v, q_codes, k_codes, v_codes}))) return rc;
   if ((p->smooth & RA_SMOOTH_Q) && !k_bias) return fail(RA_ERR_INVALID, "RA_SMOOTH_Q needs k_bias");
   const Int4Ws need = carve_int4(p, nullptr);
   if ((rc = check_ws(workspace, workspace_bytes, need.total))) return rc;
@@ -672,6 +685,7 @@ int rotate_attn_fwd_int4(const ra_params* p, const void* q, const void* k, const
   int rc = validate(p);
   if (rc) return rc;
   if (!q || !k || !v || !o) return fail(RA_ERR_INVALID, "NULL tensor pointer");
+  if ((rc = check_align({q, k, v}))) return rc;
   const Int4Ws need = carve_int4(p, nullptr);
   if ((rc = check_ws(workspace, workspace_bytes, need.total))) return rc;
   const Int4Ws w = carve_int4(p, workspace);
@@ -685,6 +699,7 @@ int rotate_attn_fwd_int4_noalloc(const ra_params* p, const void* q, const void* 
   int rc = validate(p);
   if (rc) return rc;
   if (!q || !k || !v || !o) return fail(RA_ERR_INVALID, "NULL tensor pointer");
+  if ((rc = check_align({q, k, v}))) return rc;
   const size_t need = carve_int4(p, nullptr).total;
   if (need > kNoAllocBytes)
     return fail(RA_ERR_UNSUPPORTED, "problem needs " + std::to_string(need) + " bytes of scratch; the allocation-free "
@@ -702,6 +717,7 @@ int rotate_attn_prepare_fp16(const ra_params* p, const void* q, const void* k, c
   int rc = validate(p);
   if (rc) return rc;
   if (!q || !k || !v) return fail(RA_ERR_INVALID, "NULL tensor pointer");
+  if ((rc = check_align({q, k, v}))) return rc;
   const Fp16Ws need = carve_fp16(p, nullptr);
   if ((rc = check_ws(workspace, workspace_bytes, need.total))) return rc;
   return fp16_prepare_impl(p, q, k, v, carve_fp16(p, workspace), st(stream));
@@ -721,6 +737,7 @@ int rotate_attn_fwd_fp16(const ra_params* p, const void* q, const void* k, const
   int rc = validate(p);
   if (rc) return rc;
   if (!q || !k || !v || !o) return fail(RA_ERR_INVALID, "NULL tensor pointer");
+  if ((rc = check_align({q, k, v}))) return rc;
   const Fp16Ws need = carve_fp16(p, nullptr);
   if ((rc = check_ws(workspace, workspace_bytes, need.total))) return rc;
   const Fp16Ws w = carve_fp16(p, workspace);

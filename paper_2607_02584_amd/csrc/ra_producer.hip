@@ -22,8 +22,10 @@
 //    (group of tokens, channel) (V): s = amax/7, code = clamp(rint(z*7/amax)).
 //
 // Work decomposition: one workgroup of 256 threads per tile of 128 tokens of
-// one head.  Thread t handles channels 4*(t%32) .. 4*(t%32)+3 of the rows
-// t/32, t/32+8, ... (16 rows), so each row is read as 32 coalesced 8-byte
+// one head.  Q/K: thread t handles channels 16*(t%8) .. +15 of the rows
+// t/8 + 32p (p = 0..3), each row read as eight 32-byte pieces, with the RoPE
+// table rows the tile needs staged in LDS.  V: thread t handles channels
+// 4*(t%32) .. +3 of the rows t/32 + 8p (16 rows), each row read as 32 8-byte
 // pieces.  These kernels are HBM-bound.
 #include "ra_internal.h"
 #include "rotate_attn.h"
@@ -48,72 +50,6 @@ __device__ __forceinline__ int fdiv(int n, int d, float inv_d) {
   return q;
 }
 
-// Per-thread RoPE setup for its two channel pairs p0 = 2*cl, p1 = 2*cl + 1:
-// the axis of each pair and the table column it reads (row stride D_a / 2).
-struct PairSetup {
-  int axis[2];           // 0 = t, 1 = h, 2 = w
-  const float4* tab[2];  // axis table offset by the pair's index in its segment
-  int npair[2];          // D_a / 2 (row length of the axis table)
-};
-
-__device__ __forceinline__ PairSetup pair_setup(const RopeTables& t, int cl) {
-  PairSetup s;
-#pragma unroll
-  for (int i = 0; i < 2; ++i) {
-    const int p = 2 * cl + i;
-    const int n0 = t.split[0] / 2, n1 = t.split[1] / 2;
-    const int a = p < n0 ? 0 : (p < n0 + n1 ? 1 : 2);
-    const int first = a == 0 ? 0 : (a == 1 ? n0 : n0 + n1);
-    s.axis[i] = a;
-    s.npair[i] = a == 0 ? n0 : (a == 1 ? n1 : t.split[2] / 2);
-    s.tab[i] = (a == 0 ? t.axis[0] : (a == 1 ? t.axis[1] : t.axis[2])) + (p - first);
-  }
-  return s;
-}
-
-// Grid coordinates (t, h, w) of the tile's 128 tokens, one thread each, into
-// LDS (rows past N take the last token's).
-__device__ __forceinline__ void tile_positions(const RopeTables& t, int tile, int N, int (*pos)[4]) {
-  const int tid = threadIdx.x;
-  if (tid < kTile) {
-    const int W = t.grid[2], Hg = t.grid[1];
-    int n = tile * kTile + tid;
-    if (n >= N) n = N - 1;
-    const int tq = fdiv(n, W * Hg, 1.0f / static_cast<float>(W * Hg));
-    const int rem = n - tq * W * Hg;
-    const int hq = fdiv(rem, W, 1.0f / static_cast<float>(W));
-    pos[tid][0] = tq;
-    pos[tid][1] = hq;
-    pos[tid][2] = rem - hq * W;
-  }
-}
-
-// Half rotation: for output pair P the two RoPE channels it mixes.
-struct HalfSetup {
-  int ia[2], ib[2];
-  float4 r[2];
-};
-
-__device__ __forceinline__ HalfSetup half_setup(const RopeTables& t, int cl) {
-  HalfSetup s;
-#pragma unroll
-  for (int i = 0; i < 2; ++i) {
-    int P = 2 * cl + i;
-    int o = 0, a = 0;
-    for (int ax = 0; ax < 3; ++ax) {
-      if (P >= o / 2 && P < (o + t.split[ax]) / 2) a = ax;
-      o += t.split[ax];
-    }
-    o = 0;
-    for (int ax = 0; ax < a; ++ax) o += t.split[ax];
-    int ii = P - o / 2;
-    s.ia[i] = o + ii;
-    s.ib[i] = o + ii + t.split[a] / 2;
-    s.r[i] = t.rot[P];
-  }
-  return s;
-}
-
 // y <- y H_128 for one row held by 32 lanes (lane cl holds channels 4cl..4cl+3):
 // strides 64..4 pair lanes whose cl differs in bit 4..0 (the lane with the bit
 // set takes the difference), strides 2 and 1 stay inside the thread.
@@ -135,76 +71,6 @@ __device__ __forceinline__ void hadamard_row(float y[4], int cl) {
   y[3] = __fmul_rn(__fsub_rn(t2, t3), kInvSqrtD);
 }
 
-// Computes the rotated values z of the thread's 4 channels for the 16 rows of
-// the tile.  Rows beyond N give zeros.  ybuf: [8][128] floats of LDS.
-// ROT: RA_ROT_HALF, RA_ROT_HADAMARD, or 0 for the table-only forms (none, merged
-// interleaved); F16: binary16 inputs (else bfloat16).
-template <int ROT, bool F16>
-__device__ __forceinline__ void rope_tile(const RopeTables& t, const QkArgs& a, int bh, int tile, float (*ybuf)[kD],
-                                          float z[16][4]) {
-  __shared__ int pos[kTile][4];
-  const int tid = threadIdx.x, rr = tid >> 5, cl = tid & 31;
-  const PairSetup ps = pair_setup(t, cl);
-  constexpr bool half = ROT == RA_ROT_HALF;
-  constexpr bool full = ROT == RA_ROT_HADAMARD;
-  HalfSetup hs;
-  if constexpr (half) hs = half_setup(t, cl);
-  tile_positions(t, tile, a.N, pos);
-  const uint16_t* xb = a.x + static_cast<size_t>(bh) * a.N * kD;
-  // all sixteen row loads first (rows past N re-read the last row and are zeroed)
-  uint2 raw[16];
-#pragma unroll
-  for (int p = 0; p < 16; ++p) {
-    const int n = tile * kTile + p * 8 + rr;
-    raw[p] = *reinterpret_cast<const uint2*>(xb + static_cast<size_t>(n < a.N ? n : a.N - 1) * kD + 4 * cl);
-  }
-  __syncthreads();
-  // without the half rotation's per-row barriers, the table entries of eight
-  // rows are fetched before any of them is used, so their loads overlap
-  // instead of waiting one row at a time
-  float4 gt[8][2];
-#pragma unroll
-  for (int p = 0; p < 16; ++p) {
-    const int nl = p * 8 + rr, n = tile * kTile + nl;
-    if (!half && (p & 7) == 0) {
-#pragma unroll
-      for (int q = 0; q < 8; ++q)
-#pragma unroll
-        for (int i = 0; i < 2; ++i) gt[q][i] = ps.tab[i][pos[(p + q) * 8 + rr][ps.axis[i]] * ps.npair[i]];
-    }
-    float y[4] = {0.f, 0.f, 0.f, 0.f};
-    if (n < a.N) {
-      const float x[4] = {h2f<F16>(static_cast<uint16_t>(raw[p].x & 0xffff)),
-                          h2f<F16>(static_cast<uint16_t>(raw[p].x >> 16)),
-                          h2f<F16>(static_cast<uint16_t>(raw[p].y & 0xffff)),
-                          h2f<F16>(static_cast<uint16_t>(raw[p].y >> 16))};
-#pragma unroll
-      for (int i = 0; i < 2; ++i) {
-        const float4 g = half ? ps.tab[i][pos[nl][ps.axis[i]] * ps.npair[i]] : gt[p & 7][i];
-        const float x0 = x[2 * i], x1 = x[2 * i + 1];
-        y[2 * i] = __fmaf_rn(x1, g.z, __fmul_rn(x0, g.x));
-        y[2 * i + 1] = __fmaf_rn(x1, g.w, __fmul_rn(x0, g.y));
-      }
-    }
-    if constexpr (half) {
-      __syncthreads();
-      *reinterpret_cast<float4*>(&ybuf[rr][4 * cl]) = make_float4(y[0], y[1], y[2], y[3]);
-      __syncthreads();
-#pragma unroll
-      for (int i = 0; i < 2; ++i) {
-        const float av = ybuf[rr][hs.ia[i]], bv = ybuf[rr][hs.ib[i]];
-        const float4 r = hs.r[i];
-        y[2 * i] = __fmaf_rn(bv, r.z, __fmul_rn(av, r.x));
-        y[2 * i + 1] = __fmaf_rn(bv, r.w, __fmul_rn(av, r.y));
-      }
-      if (n >= a.N) y[0] = y[1] = y[2] = y[3] = 0.f;
-    } else if constexpr (full) {
-      hadamard_row(y, cl);  // rows past N are zero and stay zero
-    }
-#pragma unroll
-    for (int c = 0; c < 4; ++c) z[p][c] = y[c];
-  }
-}
 
 __device__ __forceinline__ double fixq(float v) {
   float s = __fmul_rn(v, kFix);
@@ -235,19 +101,6 @@ __device__ __forceinline__ float4 mean4(const double* sums, int N, int cl) {
                      static_cast<float>(sums[4 * cl + 2] / den), static_cast<float>(sums[4 * cl + 3] / den));
 }
 
-template <int ROT, bool F16>
-__global__ __launch_bounds__(256) void k_qk_sums(RopeTables t, QkArgs a) {
-  __shared__ float ybuf[8][kD];
-  const int tile = blockIdx.x, bh = blockIdx.y;
-  float z[16][4];
-  rope_tile<ROT, F16>(t, a, bh, tile, ybuf, z);
-  double acc[4] = {0.0, 0.0, 0.0, 0.0};
-#pragma unroll
-  for (int p = 0; p < 16; ++p)
-#pragma unroll
-    for (int c = 0; c < 4; ++c) acc[c] += fixq(z[p][c]);
-  add_sums(acc, a.sums + static_cast<size_t>(bh) * kD);
-}
 
 // 6-bit E2M3 float (sign bit 5, exponent bias 1, 3 mantissa bits) equal to the
 // integer code c in [-7, 7]: 1 = 1.0 x 2^0, 2 = 1.0 x 2^1, 3 = 1.1b x 2^1, 4..7 = 1.xx0b x 2^2.
@@ -265,104 +118,412 @@ __device__ __forceinline__ int qcode(float z, float inv) {
   return static_cast<int>(c);
 }
 
-template <int ROT, bool F16>
-__global__ __launch_bounds__(256) void k_qk_quant(RopeTables t, QkArgs a) {
-  __shared__ float ybuf[8][kD];
+
+// ------------------------------------------------------------------ Q/K --
+// Thread (r64, c4) = (tid / 4, tid % 4) holds channels 32 c4 .. 32 c4 + 31
+// (pairs 16 c4 .. 16 c4 + 15) of the tile rows 64 p + r64, p = 0, 1: a row is
+// read as four 64-byte pieces, its abs-max and bias sums cross 4 lanes only,
+// and the thread's 32 codes of a row are one whole 24-byte E2M3 record (or two
+// 8-byte units of the nibble container), written straight from registers.
+constexpr int kQkPasses = 2;
+
+// The table rows a tile reads, staged in LDS.  For axis a the tile's tokens n
+// have the running index lin = n / div_a (div = W*Hg, W, 1) and the position
+// lin mod extent_a; the tile's lin values are consecutive.  When there are at
+// most extent_a of them, staged row lin - lin0 holds their position; otherwise
+// every position occurs and staged row pos holds position pos.
+struct StagePlan {
+  int base[3];   // float4 index of axis a's first staged row
+  int lin0[3];   // lin of the tile's first token
+  int bypos[3];  // rows indexed by position
+  int total;     // float4 count
+};
+
+__device__ __forceinline__ StagePlan stage_plan(const RopeTables& t, int n0, int N) {
+  StagePlan s;
+  const int W = t.grid[2], HW = t.grid[1] * t.grid[2];
+  const int nlast = (n0 + kTile - 1 < N - 1) ? n0 + kTile - 1 : N - 1;
+  int acc = 0;
+#pragma unroll
+  for (int ax = 0; ax < 3; ++ax) {
+    const int div = ax == 0 ? HW : (ax == 1 ? W : 1);
+    s.lin0[ax] = n0 / div;
+    const int cnt = nlast / div - s.lin0[ax] + 1;
+    s.bypos[ax] = cnt > t.grid[ax];
+    s.base[ax] = acc;
+    acc += (s.bypos[ax] ? t.grid[ax] : cnt) * (t.split[ax] / 2);
+  }
+  s.total = acc;
+  return s;
+}
+
+// Upper bound of StagePlan::total over all tiles of a geometry (host side).
+inline int stage_bound(const RopeTables& t) {
+  const int div[3] = {t.grid[1] * t.grid[2], t.grid[2], 1};
+  int acc = 0;
+  for (int ax = 0; ax < 3; ++ax) {
+    int rows = div[ax] == 1 ? kTile : (kTile - 1) / div[ax] + 2;
+    if (rows > t.grid[ax]) rows = t.grid[ax];
+    acc += rows * (t.split[ax] / 2);
+  }
+  return acc;
+}
+
+constexpr int kStageMaxF4 = 2560;  // 40 KB per stage buffer; larger plans read the tables in place
+
+// 16 bytes per lane from global memory straight into LDS at m0 + 16 * lane
+// (m0 = the wave-uniform LDS address of dst).  Issued from asm, so the
+// compiler does not wait for it at unrelated LDS accesses; the item loop waits
+// for it explicitly (vmcnt(0) and a barrier) before the rows are read.
+__device__ __forceinline__ void dma16(const void* src, void* dst) {
+#if defined(__HIP_DEVICE_COMPILE__)
+  const unsigned lds =
+      static_cast<unsigned>(reinterpret_cast<uintptr_t>((__attribute__((address_space(3))) uint8_t*)(dst)));
+  asm volatile("s_mov_b32 m0, %1\n\ts_nop 0\n\tglobal_load_lds_dwordx4 %0, off"
+               :
+               : "v"(src), "s"(__builtin_amdgcn_readfirstlane(lds))
+               : "m0", "memory");
+#else
+  (void)src;
+  (void)dst;
+#endif
+}
+
+// Starts the copy of the table rows of the tile at n0 into buf (stage_plan's layout).
+__device__ __forceinline__ void stage_rows(const RopeTables& t, int n0, int N, float4* buf) {
+  const StagePlan sp = stage_plan(t, n0, N);
+  const int lane = threadIdx.x & 63, wv = threadIdx.x >> 6;
+  for (int i0 = 64 * wv; i0 < sp.total; i0 += 256) {
+    const int i = i0 + lane;
+    if (i < sp.total) {
+      const int ax = i >= sp.base[2] ? 2 : (i >= sp.base[1] ? 1 : 0);
+      const int np = t.split[ax] / 2;
+      const int loc = i - sp.base[ax];
+      const int s = loc / np, k = loc - s * np;
+      const int pos = sp.bypos[ax] ? s : (sp.lin0[ax] + s) % t.grid[ax];
+      dma16(t.axis[ax] + pos * np + k, buf + i0);
+    }
+  }
+}
+
+// Starts the loads of the thread's row pieces of the tile at n0 (rows past N
+// re-read the last row; rope_item zeroes them).
+__device__ __forceinline__ void load_rows(const uint16_t* xb, int n0, int N, uint4 (&raw)[kQkPasses][4]) {
+  const int r64 = threadIdx.x >> 2, c4 = threadIdx.x & 3;
+#pragma unroll
+  for (int p = 0; p < kQkPasses; ++p) {
+    const int n = n0 + 64 * p + r64;
+    const uint4* src = reinterpret_cast<const uint4*>(xb + static_cast<size_t>(n < N ? n : N - 1) * kD + 32 * c4);
+#pragma unroll
+    for (int i = 0; i < 4; ++i) raw[p][i] = src[i];
+  }
+}
+
+// v of lane ^ M (M = 1 or 2): DPP quad permutations, register moves
+template <int M>
+__device__ __forceinline__ float quad_xor(float v) {
+  return __int_as_float(__builtin_amdgcn_mov_dpp(__float_as_int(v), M == 1 ? 0xB1 : 0x4E, 0xF, 0xF, false));
+}
+
+// The thread's two rows of the tile at n0 after RoPE and the rotation:
+// z[p][c] is channel 32 c4 + c of tile row 64 p + r64 (zero for rows past N).
+// STAGED: table rows from LDS (st, stage_plan's layout), else straight from the
+// tables.  ROT: RA_ROT_HALF, RA_ROT_HADAMARD, or 0 for the table-only forms
+// (none, merged interleaved); F16: binary16 inputs (else bfloat16).
+template <int ROT, bool F16, bool STAGED>
+__device__ __forceinline__ void rope_item(const RopeTables& t, int N, int n0, const uint4 (&raw)[kQkPasses][4],
+                                          const float4* st, float z[kQkPasses][32]) {
+  const int tid = threadIdx.x, r64 = tid >> 2, c4 = tid & 3;
+  const int np0 = t.split[0] / 2, np1 = t.split[1] / 2;
+  const int W = t.grid[2], Hg = t.grid[1], HW = Hg * W;
+  StagePlan sp{};
+  if (STAGED) sp = stage_plan(t, n0, N);
+#pragma unroll
+  for (int p = 0; p < kQkPasses; ++p) {
+    const int nl = 64 * p + r64, n = n0 + nl;
+    // the row's table rows (staged or in place), per axis
+    const int nn = n < N ? n : N - 1;
+    const int tq = fdiv(nn, HW, 1.0f / static_cast<float>(HW));
+    const int rem = nn - tq * HW;
+    const int hq = fdiv(rem, W, 1.0f / static_cast<float>(W));
+    const int pos[3] = {tq, hq, rem - hq * W};
+    const int lin[3] = {tq, tq * Hg + hq, nn};
+    int so[3];
+#pragma unroll
+    for (int ax = 0; ax < 3; ++ax) {
+      const int row = STAGED ? (sp.bypos[ax] ? pos[ax] : lin[ax] - sp.lin0[ax]) : pos[ax];
+      so[ax] = (STAGED ? sp.base[ax] : 0) + row * (t.split[ax] / 2);
+    }
+    // pair P of axis a sits at so[a] + P - (first pair of a)
+    const int o1 = so[1] - np0, o2 = so[2] - np0 - np1;
+    const uint32_t w[16] = {raw[p][0].x, raw[p][0].y, raw[p][0].z, raw[p][0].w, raw[p][1].x, raw[p][1].y,
+                            raw[p][1].z, raw[p][1].w, raw[p][2].x, raw[p][2].y, raw[p][2].z, raw[p][2].w,
+                            raw[p][3].x, raw[p][3].y, raw[p][3].z, raw[p][3].w};
+    float y[32];
+#pragma unroll
+    for (int k = 0; k < 16; ++k) {
+      const int P = 16 * c4 + k;
+      const int ax = (P >= np0) + (P >= np0 + np1);
+      const int off = (ax == 0 ? so[0] : (ax == 1 ? o1 : o2)) + P;
+      const float4 g = STAGED ? st[off] : t.axis[ax][off];
+      const float x0 = h2f<F16>(static_cast<uint16_t>(w[k] & 0xffff));
+      const float x1 = h2f<F16>(static_cast<uint16_t>(w[k] >> 16));
+      y[2 * k] = __fmaf_rn(x1, g.z, __fmul_rn(x0, g.x));
+      y[2 * k + 1] = __fmaf_rn(x1, g.w, __fmul_rn(x0, g.y));
+    }
+    if (n >= N) {
+#pragma unroll
+      for (int c = 0; c < 32; ++c) y[c] = 0.f;
+    }
+    if constexpr (ROT == RA_ROT_HALF) {
+      // output pair P of axis a (first channel o_a) mixes RoPE channels
+      // o_a + i and o_a + i + D_a/2, i = P - o_a/2: the row goes through LDS
+      __shared__ float ybuf[64][kD];
+      __syncthreads();
+#pragma unroll
+      for (int c = 0; c < 32; c += 4)
+        *reinterpret_cast<float4*>(&ybuf[r64][32 * c4 + c]) = make_float4(y[c], y[c + 1], y[c + 2], y[c + 3]);
+      __syncthreads();
+#pragma unroll
+      for (int k = 0; k < 16; ++k) {
+        const int P = 16 * c4 + k;
+        const int ax = (P >= np0) + (P >= np0 + np1);
+        const int oh = ax == 0 ? 0 : (ax == 1 ? np0 : np0 + np1);   // o_a / 2
+        const int ia = P + oh, ib = ia + t.split[ax] / 2;
+        const float av = ybuf[r64][ia], bv = ybuf[r64][ib];
+        const float4 r = t.rot[P];
+        y[2 * k] = __fmaf_rn(bv, r.z, __fmul_rn(av, r.x));
+        y[2 * k + 1] = __fmaf_rn(bv, r.w, __fmul_rn(av, r.y));
+      }
+      if (n >= N) {
+#pragma unroll
+        for (int c = 0; c < 32; ++c) y[c] = 0.f;
+      }
+    } else if constexpr (ROT == RA_ROT_HADAMARD) {
+      // y <- y H_128, widest stride first: strides 64 and 32 pair the lanes
+      // whose c4 differs in bit 1, 0 (the lane with the bit set takes the
+      // difference), strides 16 .. 1 stay inside the thread; then 1/sqrt(128)
+#pragma unroll
+      for (int m = 2; m >= 1; m >>= 1) {
+        const bool upper = (c4 & m) != 0;
+#pragma unroll
+        for (int c = 0; c < 32; ++c) {
+          const float o = m == 2 ? quad_xor<2>(y[c]) : quad_xor<1>(y[c]);
+          y[c] = upper ? __fsub_rn(o, y[c]) : __fadd_rn(y[c], o);
+        }
+      }
+#pragma unroll
+      for (int s = 16; s >= 1; s >>= 1)
+#pragma unroll
+        for (int c = 0; c < 32; ++c)
+          if ((c & s) == 0) {
+            const float u = y[c], v = y[c + s];
+            y[c] = __fadd_rn(u, v);
+            y[c + s] = __fsub_rn(u, v);
+          }
+#pragma unroll
+      for (int c = 0; c < 32; ++c) y[c] = __fmul_rn(y[c], kInvSqrtD);   // rows past N stay zero
+    }
+#pragma unroll
+    for (int c = 0; c < 32; ++c) z[p][c] = y[c];
+  }
+}
+
+typedef float v16f_ __attribute__((ext_vector_type(16)));
+typedef int v6i_ __attribute__((ext_vector_type(6)));
+
+// E2M3 fields of 32 values (integers in [-7, 7], no negative zero): output
+// field 2 i + h is element i of source h.  The instruction writes its result
+// over a source register wrongly when they overlap (hence the early-clobber
+// output) and reads a source written by the instruction right before it one
+// cycle early (hence the leading wait state); with scale 1 the integers
+// convert exactly.
+__device__ __forceinline__ v6i_ pack_e2m3(v16f_ even, v16f_ odd) {
+  v6i_ r;
+#if defined(__HIP_DEVICE_COMPILE__)
+  asm volatile(
+      "s_nop 0\n\t"
+      "v_cvt_scalef32_2xpk16_fp6_f32 %0, %1, %2, %3\n\t"
+      "s_nop 1"
+      : "=&v"(r)
+      : "v"(even), "v"(odd), "s"(1.0f));
+#else
+  (void)even;
+  (void)odd;
+  r = v6i_{0, 0, 0, 0, 0, 0};
+#endif
+  return r;
+}
+
+// The code rint(z * inv) clamped to [-7, 7], as a float (+0 for zero)
+__device__ __forceinline__ float qcode_f(float z, float inv) {
+  const float c = fminf(fmaxf(__builtin_rintf(__fmul_rn(z, inv)), -7.0f), 7.0f);
+  return c + 0.0f;   // -0 -> +0 (the zero code carries no sign)
+}
+
+// LDS layout of the sums pass's partial sums (in doubles): slot (row r, lane
+// group c4) at r * kSumRowStride + c4 * kSumC4Stride holds 32 channels.  The
+// strides are 16 and 64 bytes past multiples of 256, so the 16 lanes of a
+// quarter wave (4 rows x 4 lane groups) write 16-byte pieces to distinct banks.
+constexpr int kSumRowStride = 162;   // 1296 bytes
+constexpr int kSumC4Stride = 40;     // 320 bytes
+constexpr size_t kSumLdsBytes = 32 * kSumRowStride * sizeof(double);
+
+// Q/K producer, one workgroup per (tile, head): the tile's rows and the table
+// rows it needs are requested at once (the table rows straight into LDS),
+// then RoPE and the rotation, then
+//  SUMS: the fixed-point channel sums of the rotated rows (smoothing), added
+//        to a.sums with atomics;
+//  else: smoothing, the key bias of Q smoothing, per-group scales and codes.
+template <int ROT, bool F16, bool STAGED, bool SUMS>
+__global__ __launch_bounds__(256) void k_qk(RopeTables t, QkArgs a) {
+  extern __shared__ float4 dyn[];   // STAGED: the staged table rows; SUMS: then the partial sums
   __shared__ float rowmax[kTile];
   __shared__ float ginv[kTile];
-  __shared__ __align__(16) uint8_t ctile[kTile * 96];
+  __shared__ float smu[kD], smq[kD];
   const int tile = blockIdx.x, bh = blockIdx.y;
-  const int tid = threadIdx.x, rr = tid >> 5, cl = tid & 31;
-  float z[16][4];
-  rope_tile<ROT, F16>(t, a, bh, tile, ybuf, z);
-  if (a.center) {
-    const float4 m = mean4(a.sums + static_cast<size_t>(bh) * kD, a.N, cl);
-    if (a.mu_out && tile == 0 && rr == 0) *reinterpret_cast<float4*>(a.mu_out + bh * kD + 4 * cl) = m;
-    for (int p = 0; p < 16; ++p) {
-      const int n = tile * kTile + p * 8 + rr;
-      if (n < a.N) {
-        z[p][0] = __fsub_rn(z[p][0], m.x);
-        z[p][1] = __fsub_rn(z[p][1], m.y);
-        z[p][2] = __fsub_rn(z[p][2], m.z);
-        z[p][3] = __fsub_rn(z[p][3], m.w);
-      }
-    }
+  const int tid = threadIdx.x, r64 = tid >> 2, c4 = tid & 3;
+  const int N = a.N, n0 = tile * kTile;
+  const double den = static_cast<double>(N) * 1048576.0;
+  if (STAGED) stage_rows(t, n0, N, dyn);
+  uint4 raw[kQkPasses][4];
+  load_rows(a.x + static_cast<size_t>(bh) * N * kD, n0, N, raw);
+  if (!SUMS && tid < kD) {
+    if (a.center) smu[tid] = static_cast<float>(a.sums[static_cast<size_t>(bh) * kD + tid] / den);
+    if (a.bias) smq[tid] = static_cast<float>(a.qsums[static_cast<size_t>(bh) * kD + tid] / den);
   }
-  if (a.bias) {
-    // Q smoothing: per-key score bias b = mu_Q . z (z = this K row after its
-    // own smoothing), products in binary32, summed pairwise over the channel
-    // range: the thread's (c0 + c1) + (c2 + c3), then lanes 1, 2, 4, 8, 16
-    // apart (blocks of 8, 16, ..., 128 channels).  Padded rows give 0.
-    const float4 mq = mean4(a.qsums + static_cast<size_t>(bh) * kD, a.N, cl);
-    for (int p = 0; p < 16; ++p) {
-      float b = __fadd_rn(__fadd_rn(__fmul_rn(mq.x, z[p][0]), __fmul_rn(mq.y, z[p][1])),
-                          __fadd_rn(__fmul_rn(mq.z, z[p][2]), __fmul_rn(mq.w, z[p][3])));
-#pragma unroll
-      for (int off = 1; off <= 16; off <<= 1) b = __fadd_rn(b, __shfl_xor(b, off, 32));
-      if (cl == 0) a.bias[static_cast<size_t>(bh) * a.Npad + tile * kTile + p * 8 + rr] = b;
-    }
-  }
-  // row abs-max over the 128 channels (32 threads of the row)
-  for (int p = 0; p < 16; ++p) {
-    float v = fmaxf(fmaxf(fabsf(z[p][0]), fabsf(z[p][1])), fmaxf(fabsf(z[p][2]), fabsf(z[p][3])));
-#pragma unroll
-    for (int off = 16; off >= 1; off >>= 1) v = fmaxf(v, __shfl_xor(v, off, 32));
-    if (cl == 0) rowmax[p * 8 + rr] = v;
-  }
+  // the staged rows have arrived; the barrier makes them (and the means) visible
+  __builtin_amdgcn_s_waitcnt(0x3F70);   // vmcnt(0)
   __syncthreads();
-  const int g = a.group, ng = kTile / g;
-  if (tid < ng) {
-    float m = 0.f;
-    for (int i = 0; i < g; ++i) m = fmaxf(m, rowmax[tid * g + i]);
-    float s = 0.f, inv = 0.f;
-    if (m > 0.f) {
-      s = __fdiv_rn(m, 7.0f);
-      inv = __fdiv_rn(7.0f, m);
-    }
-    ginv[tid] = inv;
-    a.scales[static_cast<size_t>(bh) * (a.Npad / g) + tile * ng + tid] = s;
-  }
-  __syncthreads();
-  if (a.e2m3) {
-    // record ((chunk*2 + ch/64)*2 + (ch/32)%2)*32 + row of 24 bytes; channels 4cl..4cl+3 are the
-    // 6-bit fields 4*(cl%8) .. +3 of record (kc = cl/16, h = (cl/8)%2), i.e. bytes 3*(cl%8) .. +2
-    for (int p = 0; p < 16; ++p) {
-      const int nl = p * 8 + rr;
-      const float inv = ginv[nl / g];
-      const uint32_t bits = e2m3_of(qcode(z[p][0], inv)) | (e2m3_of(qcode(z[p][1], inv)) << 6) |
-                            (e2m3_of(qcode(z[p][2], inv)) << 12) | (e2m3_of(qcode(z[p][3], inv)) << 18);
-      const int rec = (((nl >> 5) * 2 + (cl >> 4)) * 2 + ((cl >> 3) & 1)) * 32 + (nl & 31);
-      uint8_t* d = &ctile[rec * 24 + 3 * (cl & 7)];
-      d[0] = static_cast<uint8_t>(bits);
-      d[1] = static_cast<uint8_t>(bits >> 8);
-      d[2] = static_cast<uint8_t>(bits >> 16);
+  float z[kQkPasses][32];
+  rope_item<ROT, F16, STAGED>(t, N, n0, raw, dyn, z);
+
+  if constexpr (SUMS) {
+    // per channel: the thread's two rows, then the 64 row groups through LDS
+    // (reusing the staged rows): rows 0..31 store, rows 32..63 add theirs to
+    // the same slots, then one thread per channel adds the 32 slots.  The
+    // values are integers below 2^53, so every order gives the same sum.
+    double* red = reinterpret_cast<double*>(dyn);
+    const int slot = (r64 & 31) * kSumRowStride + c4 * kSumC4Stride;   // in doubles
+    double acc[32];
+#pragma unroll
+    for (int c = 0; c < 32; ++c) acc[c] = fixq(z[0][c]) + fixq(z[1][c]);
+    __syncthreads();   // every thread is done with the staged rows
+    if (r64 < 32) {
+#pragma unroll
+      for (int c = 0; c < 32; c += 2) *reinterpret_cast<double2*>(&red[slot + c]) = make_double2(acc[c], acc[c + 1]);
     }
     __syncthreads();
-    uint8_t* dst = a.codes + static_cast<size_t>(bh) * a.Npad * 96 + static_cast<size_t>(tile) * kTile * 96;
+    if (r64 >= 32) {
 #pragma unroll
-    for (int i = 0; i < 3; ++i) {
-      const int o = (i * 256 + tid) * 16;
-      *reinterpret_cast<uint4*>(dst + o) = *reinterpret_cast<const uint4*>(&ctile[o]);
+      for (int c = 0; c < 32; c += 2) {
+        double2* d = reinterpret_cast<double2*>(&red[slot + c]);
+        const double2 o = *d;
+        *d = make_double2(o.x + acc[c], o.y + acc[c + 1]);
+      }
     }
-    return;
-  }
-  for (int p = 0; p < 16; ++p) {
-    const int nl = p * 8 + rr;
-    const float inv = ginv[nl / g];
-    const int c0 = qcode(z[p][0], inv), c1 = qcode(z[p][1], inv);
-    const int c2 = qcode(z[p][2], inv), c3 = qcode(z[p][3], inv);
-    const uint32_t b0 = (c0 & 0xF) | ((c1 & 0xF) << 4);
-    const uint32_t b1 = (c2 & 0xF) | ((c3 & 0xF) << 4);
-    // tiled layout: ((chunk*8 + unit)*32 + row)*8 + byte, pair j = 2*cl -> unit cl/4, byte 2*(cl%4)
-    const int off = (((nl >> 5) * 8 + (cl >> 2)) * 32 + (nl & 31)) * 8 + 2 * (cl & 3);
-    *reinterpret_cast<uint16_t*>(&ctile[off]) = static_cast<uint16_t>(b0 | (b1 << 8));
-  }
-  __syncthreads();
-  uint8_t* dst = a.codes + static_cast<size_t>(bh) * a.Npad * 64 + static_cast<size_t>(tile) * kTile * 64;
+    __syncthreads();
+    if (tid < kD) {
+      const double* col = red + (tid >> 5) * kSumC4Stride + (tid & 31);
+      double sum = 0.0;
+      for (int r = 0; r < 32; ++r) sum += col[r * kSumRowStride];
+      unsafeAtomicAdd(a.sums + static_cast<size_t>(bh) * kD + tid, sum);
+    }
+  } else {
+    if (a.center) {
+      if (a.mu_out && tile == 0 && tid < kD) a.mu_out[bh * kD + tid] = smu[tid];
 #pragma unroll
-  for (int i = 0; i < 2; ++i) {
-    const int o = (i * 256 + tid) * 16;
-    *reinterpret_cast<uint4*>(dst + o) = *reinterpret_cast<const uint4*>(&ctile[o]);
+      for (int p = 0; p < kQkPasses; ++p)
+        if (n0 + 64 * p + r64 < N)
+#pragma unroll
+          for (int c = 0; c < 32; ++c) z[p][c] = __fsub_rn(z[p][c], smu[32 * c4 + c]);
+    }
+    if (a.bias) {
+      // Q smoothing: per-key score bias b = mu_Q . z (z = this K row after its
+      // own smoothing), products in binary32 summed pairwise over the channel
+      // range: inside the thread blocks of 2, 4, ..., 32 channels, then lanes
+      // 1 and 2 apart (blocks of 64, 128).  Padded rows give 0.
+#pragma unroll
+      for (int p = 0; p < kQkPasses; ++p) {
+        float bb[32];
+#pragma unroll
+        for (int c = 0; c < 32; ++c) bb[c] = __fmul_rn(smq[32 * c4 + c], z[p][c]);
+#pragma unroll
+        for (int s = 1; s < 32; s <<= 1)
+#pragma unroll
+          for (int c = 0; c < 32; c += 2 * s) bb[c] = __fadd_rn(bb[c], bb[c + s]);
+        float v = bb[0];
+        v = __fadd_rn(v, quad_xor<1>(v));
+        v = __fadd_rn(v, quad_xor<2>(v));
+        if (c4 == 0) a.bias[static_cast<size_t>(bh) * a.Npad + n0 + 64 * p + r64] = v;
+      }
+    }
+    // row abs-max over the 128 channels (4 lanes of the row)
+#pragma unroll
+    for (int p = 0; p < kQkPasses; ++p) {
+      float v = 0.f;
+#pragma unroll
+      for (int c = 0; c < 32; ++c) v = fmaxf(v, fabsf(z[p][c]));
+      v = fmaxf(v, quad_xor<1>(v));
+      v = fmaxf(v, quad_xor<2>(v));
+      if (c4 == 0) rowmax[64 * p + r64] = v;
+    }
+    __syncthreads();
+    const int g = a.group, ng = kTile / g;
+    if (tid < ng) {
+      float m = 0.f;
+      for (int i = 0; i < g; ++i) m = fmaxf(m, rowmax[tid * g + i]);
+      float s = 0.f, inv = 0.f;
+      if (m > 0.f) {
+        s = __fdiv_rn(m, 7.0f);
+        inv = __fdiv_rn(7.0f, m);
+      }
+      ginv[tid] = inv;
+      a.scales[static_cast<size_t>(bh) * (a.Npad / g) + tile * ng + tid] = s;
+    }
+    __syncthreads();
+    if (a.e2m3) {
+      // record ((chunk*2 + ch/64)*2 + (ch/32)%2)*32 + row of 24 bytes, field
+      // f (channel 32 (ch/32) + f) at bit 6 f: the thread's 32 channels of a
+      // row are exactly record ((chunk*2 + c4/2)*2 + c4%2)*32 + row
+      uint8_t* base = a.codes + static_cast<size_t>(bh) * a.Npad * 96 + static_cast<size_t>(tile) * kTile * 96;
+#pragma unroll
+      for (int p = 0; p < kQkPasses; ++p) {
+        const int nl = 64 * p + r64;
+        const float inv = ginv[nl / g];
+        v16f_ ev, od;
+#pragma unroll
+        for (int i = 0; i < 16; ++i) {
+          ev[i] = qcode_f(z[p][2 * i], inv);
+          od[i] = qcode_f(z[p][2 * i + 1], inv);
+        }
+        const v6i_ f = pack_e2m3(ev, od);
+        const int rec = (((nl >> 5) * 2 + (c4 >> 1)) * 2 + (c4 & 1)) * 32 + (nl & 31);
+        uint2* d = reinterpret_cast<uint2*>(base + rec * 24);
+        d[0] = make_uint2(static_cast<uint32_t>(f[0]), static_cast<uint32_t>(f[1]));
+        d[1] = make_uint2(static_cast<uint32_t>(f[2]), static_cast<uint32_t>(f[3]));
+        d[2] = make_uint2(static_cast<uint32_t>(f[4]), static_cast<uint32_t>(f[5]));
+      }
+    } else {
+      // tiled layout ((chunk*8 + unit)*32 + row)*8 + byte: the thread's 32
+      // channels are units 2 c4 and 2 c4 + 1 of the row, channel pair
+      // (2i, 2i+1) of a unit in byte i
+      uint8_t* base = a.codes + static_cast<size_t>(bh) * a.Npad * 64 + static_cast<size_t>(tile) * kTile * 64;
+#pragma unroll
+      for (int p = 0; p < kQkPasses; ++p) {
+        const int nl = 64 * p + r64;
+        const float inv = ginv[nl / g];
+#pragma unroll
+        for (int u = 0; u < 2; ++u) {
+          uint32_t wv[2] = {0u, 0u};
+#pragma unroll
+          for (int c = 0; c < 16; ++c)
+            wv[c >> 3] |= static_cast<uint32_t>(qcode(z[p][16 * u + c], inv) & 0xF) << (4 * (c & 7));
+          const int unit = 2 * c4 + u;
+          *reinterpret_cast<uint2*>(base + (((nl >> 5) * 8 + unit) * 32 + (nl & 31)) * 8) = make_uint2(wv[0], wv[1]);
+        }
+      }
+    }
   }
 }
 
@@ -592,22 +753,34 @@ __global__ void k_fill_zero_u32(uint32_t* p, int64_t n) {
 
 }  // namespace
 
-// the rotation and input type as template arguments: table-only rotations share one form
-#define RA_QK_DISPATCH(KERNEL)                                                                        \
-  do {                                                                                                \
-    const dim3 g(a.Npad / kTile, BH);                                                                 \
-    const int rot = (t.rotation == RA_ROT_HALF || t.rotation == RA_ROT_HADAMARD) ? t.rotation : 0;    \
-    if (rot == RA_ROT_HALF) {                                                                         \
-      if (a.is_fp16) hipLaunchKernelGGL((KERNEL<RA_ROT_HALF, true>), g, dim3(256), 0, s, t, a);        \
-      else hipLaunchKernelGGL((KERNEL<RA_ROT_HALF, false>), g, dim3(256), 0, s, t, a);                 \
-    } else if (rot == RA_ROT_HADAMARD) {                                                              \
-      if (a.is_fp16) hipLaunchKernelGGL((KERNEL<RA_ROT_HADAMARD, true>), g, dim3(256), 0, s, t, a);    \
-      else hipLaunchKernelGGL((KERNEL<RA_ROT_HADAMARD, false>), g, dim3(256), 0, s, t, a);             \
-    } else {                                                                                          \
-      if (a.is_fp16) hipLaunchKernelGGL((KERNEL<0, true>), g, dim3(256), 0, s, t, a);                  \
-      else hipLaunchKernelGGL((KERNEL<0, false>), g, dim3(256), 0, s, t, a);                           \
-    }                                                                                                 \
-  } while (0)
+namespace {
+
+template <int ROT, bool F16, bool STAGED, bool SUMS>
+hipError_t launch_qk_one(const RopeTables& t, const QkArgs& a, int BH, int bound, hipStream_t s) {
+  size_t lds = STAGED ? static_cast<size_t>(bound) * sizeof(float4) : 0;
+  if (SUMS && lds < kSumLdsBytes) lds = kSumLdsBytes;
+  hipLaunchKernelGGL((k_qk<ROT, F16, STAGED, SUMS>), dim3(a.Npad / kTile, BH), dim3(256), lds, s, t, a);
+  return hipGetLastError();
+}
+
+// the rotation, the input type and the table staging as template arguments
+// (table-only rotations share one form)
+template <bool SUMS>
+hipError_t launch_qk(const RopeTables& t, const QkArgs& a, int BH, hipStream_t s) {
+  const int bound = stage_bound(t);
+  const bool staged = bound <= kStageMaxF4;
+  const int rot = (t.rotation == RA_ROT_HALF || t.rotation == RA_ROT_HADAMARD) ? t.rotation : 0;
+  const bool f16 = a.is_fp16 != 0;
+#define RA_QK_ONE(R)                                                                     \
+  (staged ? (f16 ? launch_qk_one<R, true, true, SUMS>(t, a, BH, bound, s)                 \
+                 : launch_qk_one<R, false, true, SUMS>(t, a, BH, bound, s))               \
+          : (f16 ? launch_qk_one<R, true, false, SUMS>(t, a, BH, bound, s)                \
+                 : launch_qk_one<R, false, false, SUMS>(t, a, BH, bound, s)))
+  if (rot == RA_ROT_HALF) return RA_QK_ONE(RA_ROT_HALF);
+  if (rot == RA_ROT_HADAMARD) return RA_QK_ONE(RA_ROT_HADAMARD);
+  return RA_QK_ONE(0);
+#undef RA_QK_ONE
+}
 
 #define RA_V_DISPATCH(KERNEL)                                                                         \
   do {                                                                                                \
@@ -621,14 +794,14 @@ __global__ void k_fill_zero_u32(uint32_t* p, int64_t n) {
     }                                                                                                 \
   } while (0)
 
+}  // namespace
+
 hipError_t launch_qk_sums(const RopeTables& t, const QkArgs& a, int BH, hipStream_t s) {
-  RA_QK_DISPATCH(k_qk_sums);
-  return hipGetLastError();
+  return launch_qk<true>(t, a, BH, s);
 }
 
 hipError_t launch_qk_quant(const RopeTables& t, const QkArgs& a, int BH, hipStream_t s) {
-  RA_QK_DISPATCH(k_qk_quant);
-  return hipGetLastError();
+  return launch_qk<false>(t, a, BH, s);
 }
 
 hipError_t launch_write_floats(const float* host, size_t n, float* dst, hipStream_t s) {

@@ -150,6 +150,16 @@ def test_null_pointers_and_workspace_errors_before_gpu():
     assert ra.workspace_size(pq, ra.PATH_INT4) >= ra.workspace_size(p, ra.PATH_INT4) + 2 * 1024 * 4
     assert L.rotate_attn_error_string(-4) == b"HIP runtime error"
     assert L.rotate_attn_fwd_int4(None, fake, fake, fake, fake, fake, 1 << 30, None) == -1
+    # inputs and code buffers are moved in 16-byte pieces: an 8-byte aligned one is refused
+    half = P(0x1008)
+    for args in ((half, fake, fake), (fake, half, fake), (fake, fake, half)):
+        st = L.rotate_attn_fwd_int4(ctypes.byref(p), *args, fake, fake, 1 << 30, None)
+        assert st == -1 and b"16-byte aligned" in L.rotate_attn_last_error()
+    st = L.rotate_attn_quantize_qk(ctypes.byref(p), fake, fake, half, fake, fake, fake, None, None, None, fake,
+                                   1 << 30, None)
+    assert st == -1 and b"16-byte aligned" in L.rotate_attn_last_error()
+    st = L.rotate_attn_quantize_v(ctypes.byref(p), fake, half, fake, None, fake, 1 << 30, None)
+    assert st == -1 and b"16-byte aligned" in L.rotate_attn_last_error()
 
 
 def test_binding_checks_tensors_before_the_library():

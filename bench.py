@@ -78,6 +78,62 @@ def log(*a):
     print("[bench]", *a, file=sys.stderr, flush=True)
 
 
+def host_info():
+    """The host the CPU baseline ran on: CPU model, logical CPUs, CPUs this process may use."""
+    model = None
+    try:
+        with open("/proc/cpuinfo") as f:
+            for ln in f:
+                if ln.startswith("model name"):
+                    model = ln.split(":", 1)[1].strip()
+                    break
+    except OSError:
+        pass
+    try:
+        usable = len(os.sched_getaffinity(0))
+    except AttributeError:
+        usable = None
+    return {"cpu_model": model, "nproc": os.cpu_count(), "usable_cpus": usable}
+
+
+def sclk_reader(torch, dev):
+    """A function returning the GPU's current shader clock in MHz, read from
+    the amdgpu driver's DPM table of this device (the level marked '*'), or
+    None where the table is not readable."""
+    import re
+    props = torch.cuda.get_device_properties(dev)
+    path = (f"/sys/bus/pci/devices/{props.pci_domain_id:04x}:{props.pci_bus_id:02x}:"
+            f"{props.pci_device_id:02x}.0/pp_dpm_sclk")
+
+    def read():
+        try:
+            with open(path) as f:
+                for ln in f:
+                    if ln.rstrip().endswith("*"):
+                        m = re.search(r"(\d+)\s*[Mm][Hh]z", ln)
+                        return int(m.group(1)) if m else None
+        except OSError:
+            return None
+        return None
+    return read
+
+
+def producer_bytes(w, container, q_group=128, k_group=128, v_group=128):
+    """Algorithmic bytes of the Q/K/V producer call: each bf16 input read
+    once, each code buffer, scale array and mean written once; and the bytes
+    the two-pass smoothing actually reads (K and V once more for their channel
+    means, which must be known before any of their codes)."""
+    BH, N = w.B * w.H, w.N
+    Npad = -(-N // 128) * 128
+    rec = 96 if container == "e2m3" else 64
+    inp = 3 * BH * N * 128 * 2
+    codes = 3 * BH * Npad * rec
+    scales = BH * (Npad // q_group + Npad // k_group) * 4 + BH * (-(-N // v_group)) * 128 * 4
+    means = 2 * BH * 128 * 4
+    algo = inp + codes + scales + means
+    return algo, algo + 2 * BH * N * 128 * 2
+
+
 def main():
     args = parse()
     if args.gpus != 1:
@@ -110,6 +166,8 @@ def main():
     stream = torch.cuda.current_stream()
 
     def step(ev=None):
+        if ev is not None:
+            ev[2].record(stream)
         # the Q, K and V producers in one call
         ra.quantize_qkv(p, qd, kd, vd, bufs["q_codes"], bufs["q_scale"], bufs["k_codes"], bufs["k_scale"],
                         bufs["v_codes"], bufs["v_scale"], ws, mu_k=bufs["mu_k"], mu_v=bufs["mu_v"])
@@ -136,7 +194,7 @@ def main():
         step()
     torch.cuda.synchronize()
     log(f"warmup done; timing {args.steps} steps")
-    evs = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)) for _ in range(args.steps)]
+    evs = [tuple(torch.cuda.Event(enable_timing=True) for _ in range(3)) for _ in range(args.steps)]
     t0 = torch.cuda.Event(enable_timing=True)
     t1 = torch.cuda.Event(enable_timing=True)
     torch.cuda.synchronize()
@@ -146,7 +204,36 @@ def main():
     t1.record(stream)
     torch.cuda.synchronize()
     ms_step = t0.elapsed_time(t1) / args.steps
-    attn_ms = float(np.mean([a.elapsed_time(b) for a, b in evs]))
+    attn_ms = float(np.mean([a.elapsed_time(b) for a, b, _ in evs]))
+    prod_ms = float(np.mean([c.elapsed_time(a) for a, _, c in evs]))
+    p_algo, p_reads = producer_bytes(w, args.container)
+    prod = {"ms": round(prod_ms, 4), "algorithmic_bytes": p_algo, "gbps": round(p_algo / (prod_ms * 1e-3) / 1e9, 1),
+            "peak_gbps": HBM_PEAK_GBS, "frac": round(p_algo / (prod_ms * 1e-3) / 1e9 / HBM_PEAK_GBS, 4),
+            "bytes_moved_two_pass": p_reads,
+            "gbps_two_pass": round(p_reads / (prod_ms * 1e-3) / 1e9, 1),
+            "what": "quantize_qkv: table copy, channel sums of K and V, Q/K/V codes and scales (HIP events on "
+                    "the launch stream, mean over the timed steps)"}
+    log(f"producers {prod_ms * 1e3:.1f} us: {prod['gbps']} GB/s algorithmic ({prod['frac']:.3f} of HBM peak), "
+        f"{prod['gbps_two_pass']} GB/s of bytes moved")
+    # the shader clock while the attention kernel runs back to back
+    read_sclk = sclk_reader(torch, dev)
+    clk = []
+    for _ in range(40):
+        ra.attn_int4(p, bufs["q_codes"], bufs["q_scale"], bufs["k_codes"], bufs["k_scale"], bufs["v_codes"],
+                     bufs["v_scale"], bufs["mu_v"], o)
+    for _ in range(12):
+        time.sleep(0.01)
+        clk.append(read_sclk())
+    torch.cuda.synchronize()
+    clk = [c for c in clk if c is not None]
+    gpu = {"name": torch.cuda.get_device_properties(dev).name, "arch": torch.cuda.get_device_properties(dev).gcnArchName,
+           "compute_units": torch.cuda.get_device_properties(dev).multi_processor_count,
+           "sclk_mhz_under_load": {"median": float(np.median(clk)), "min": min(clk), "max": max(clk),
+                                   "samples": len(clk)} if clk else None,
+           "sclk_source": "amdgpu DPM table of this device (pp_dpm_sclk, current level), sampled every 10 ms "
+                          "while 40 attention launches ran"}
+    log(f"gpu: {gpu['name']} {gpu['arch']} {gpu['compute_units']} CUs, shader clock under load "
+        f"{gpu['sclk_mhz_under_load']}")
     ops = w.ops()
     tops = ops / (ms_step * 1e-3) / 1e12
     attn_tops = ops / (attn_ms * 1e-3) / 1e12
@@ -297,6 +384,9 @@ def main():
                      "frac_of_int8_peak": round(attn_tops / INT8_PEAK_TOPS, 4),
                      "traffic": measured_traffic(args.container, w.name)},
         "cpu_baseline": cpu,
+        "producers": prod,
+        "gpu": gpu,
+        "host": host_info(),
     }
     line.update(extra)
     if variants is not None:
@@ -371,12 +461,14 @@ def cpu_baseline(w, q, k, v, seconds):
     geo = ora.Geometry(w.T, w.Hg, w.W, w.split, w.theta)
     cfg = ora.Int4Config()
     t = time.perf_counter()
-    rows, heads = 0, 0
+    rows, heads, t_prod = 0, 0, 0.0
     for h in range(w.H):
         if time.perf_counter() - t >= seconds:
             break
+        tp = time.perf_counter()
         qk = ora.quantize_qk_head(geo, cfg, q[0, h], k[0, h])
         vv = ora.quantize_v_head(cfg, v[0, h])
+        t_prod += time.perf_counter() - tp
         heads += 1
         r = 0
         while r < w.N and time.perf_counter() - t < seconds:
@@ -387,6 +479,11 @@ def cpu_baseline(w, q, k, v, seconds):
         rows += r
     el = time.perf_counter() - t
     val = 4.0 * rows * w.N * 128 / el / 1e12
+    # the whole workload at the sampled rates: every head's producer pass plus
+    # all N query rows of every head (an extrapolation, not a measurement)
+    per_prod = t_prod / heads
+    per_row = (el - t_prod) / rows
+    full_s = w.B * w.H * (per_prod + w.N * per_row)
     log(f"cpu oracle: {rows} query rows over {heads} head(s) in {el:.1f} s on {ora.threads()} threads")
     # the 1024-token case in full (both heads, every row), for scale
     from paper_2607_02584_amd import datagen as dg
@@ -402,7 +499,12 @@ def cpu_baseline(w, q, k, v, seconds):
             "sample": f"{heads} head(s) of {w.name}: each head's producer pass over all {w.N} tokens, then "
                       f"{rows} query rows in all against all {w.N} keys ({el:.1f} s wall)",
             "c1_full": {"seconds": round(e1, 3), "tops": round(w1.ops() / e1 / 1e12, 5),
-                        "what": "B=1 H=2 N=1024, producers and every query row"}}
+                        "what": "B=1 H=2 N=1024, producers and every query row"},
+            "full_workload_extrapolated": {"seconds": round(full_s, 1), "tops": round(w.ops() / full_s / 1e12, 5),
+                                           "producer_s_per_head": round(per_prod, 3),
+                                           "us_per_query_row": round(per_row * 1e6, 2),
+                                           "label": f"extrapolation, not a measurement: {w.B * w.H} heads x "
+                                                    f"(producer pass + {w.N} rows) at the sampled rates"}}
 
 
 if __name__ == "__main__":

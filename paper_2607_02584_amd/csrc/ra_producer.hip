@@ -189,19 +189,25 @@ __device__ __forceinline__ void dma16(const void* src, void* dst) {
 #endif
 }
 
-// Starts the copy of the table rows of the tile at n0 into buf (stage_plan's layout).
+// Starts the copy of the table rows of the tile at n0 into buf (stage_plan's
+// layout).  The axis of an entry is a run-time value, so its fields are picked
+// with selects: indexing the small arrays with it would put them in scratch.
 __device__ __forceinline__ void stage_rows(const RopeTables& t, int n0, int N, float4* buf) {
   const StagePlan sp = stage_plan(t, n0, N);
   const int lane = threadIdx.x & 63, wv = threadIdx.x >> 6;
   for (int i0 = 64 * wv; i0 < sp.total; i0 += 256) {
     const int i = i0 + lane;
     if (i < sp.total) {
-      const int ax = i >= sp.base[2] ? 2 : (i >= sp.base[1] ? 1 : 0);
-      const int np = t.split[ax] / 2;
-      const int loc = i - sp.base[ax];
+      const bool a2 = i >= sp.base[2], a1 = !a2 && i >= sp.base[1];
+      const int np = (a2 ? t.split[2] : (a1 ? t.split[1] : t.split[0])) / 2;
+      const int loc = i - (a2 ? sp.base[2] : (a1 ? sp.base[1] : sp.base[0]));
       const int s = loc / np, k = loc - s * np;
-      const int pos = sp.bypos[ax] ? s : (sp.lin0[ax] + s) % t.grid[ax];
-      dma16(t.axis[ax] + pos * np + k, buf + i0);
+      const bool bypos = a2 ? sp.bypos[2] : (a1 ? sp.bypos[1] : sp.bypos[0]);
+      const int lin0 = a2 ? sp.lin0[2] : (a1 ? sp.lin0[1] : sp.lin0[0]);
+      const int extent = a2 ? t.grid[2] : (a1 ? t.grid[1] : t.grid[0]);
+      const int pos = bypos ? s : (lin0 + s) % extent;
+      const float4* tab = a2 ? t.axis[2] : (a1 ? t.axis[1] : t.axis[0]);
+      dma16(tab + pos * np + k, buf + i0);
     }
   }
 }
@@ -234,7 +240,7 @@ template <int ROT, bool F16, bool STAGED>
 __device__ __forceinline__ void rope_item(const RopeTables& t, int N, int n0, const uint4 (&raw)[kQkPasses][4],
                                           const float4* st, float z[kQkPasses][32]) {
   const int tid = threadIdx.x, r64 = tid >> 2, c4 = tid & 3;
-  const int np0 = t.split[0] / 2, np1 = t.split[1] / 2;
+  const int np0 = t.split[0] / 2, np1 = t.split[1] / 2, np2 = t.split[2] / 2;
   const int W = t.grid[2], Hg = t.grid[1], HW = Hg * W;
   StagePlan sp{};
   if (STAGED) sp = stage_plan(t, n0, N);
@@ -265,7 +271,7 @@ __device__ __forceinline__ void rope_item(const RopeTables& t, int N, int n0, co
       const int P = 16 * c4 + k;
       const int ax = (P >= np0) + (P >= np0 + np1);
       const int off = (ax == 0 ? so[0] : (ax == 1 ? o1 : o2)) + P;
-      const float4 g = STAGED ? st[off] : t.axis[ax][off];
+      const float4 g = STAGED ? st[off] : (ax == 0 ? t.axis[0] : (ax == 1 ? t.axis[1] : t.axis[2]))[off];
       const float x0 = h2f<F16>(static_cast<uint16_t>(w[k] & 0xffff));
       const float x1 = h2f<F16>(static_cast<uint16_t>(w[k] >> 16));
       y[2 * k] = __fmaf_rn(x1, g.z, __fmul_rn(x0, g.x));
@@ -289,7 +295,7 @@ __device__ __forceinline__ void rope_item(const RopeTables& t, int N, int n0, co
         const int P = 16 * c4 + k;
         const int ax = (P >= np0) + (P >= np0 + np1);
         const int oh = ax == 0 ? 0 : (ax == 1 ? np0 : np0 + np1);   // o_a / 2
-        const int ia = P + oh, ib = ia + t.split[ax] / 2;
+        const int ia = P + oh, ib = ia + (ax == 0 ? np0 : (ax == 1 ? np1 : np2));
         const float av = ybuf[r64][ia], bv = ybuf[r64][ib];
         const float4 r = t.rot[P];
         y[2 * k] = __fmaf_rn(bv, r.z, __fmul_rn(av, r.x));
@@ -362,11 +368,11 @@ __device__ __forceinline__ float qcode_f(float z, float inv) {
 }
 
 // LDS layout of the sums pass's partial sums (in doubles): slot (row r, lane
-// group c4) at r * kSumRowStride + c4 * kSumC4Stride holds 32 channels.  The
-// strides are 16 and 64 bytes past multiples of 256, so the 16 lanes of a
-// quarter wave (4 rows x 4 lane groups) write 16-byte pieces to distinct banks.
-constexpr int kSumRowStride = 162;   // 1296 bytes
-constexpr int kSumC4Stride = 40;     // 320 bytes
+// group c4) at r * kSumRowStride + c4 * kSumC4Stride holds 16 channels.  The
+// row stride is 16 bytes past a multiple of 256, so rows of one lane group
+// start in different banks.
+constexpr int kSumRowStride = 66;   // 528 bytes
+constexpr int kSumC4Stride = 16;    // 128 bytes
 constexpr size_t kSumLdsBytes = 32 * kSumRowStride * sizeof(double);
 
 // Q/K producer, one workgroup per (tile, head): the tile's rows and the table
@@ -400,34 +406,40 @@ __global__ __launch_bounds__(256) void k_qk(RopeTables t, QkArgs a) {
 
   if constexpr (SUMS) {
     // per channel: the thread's two rows, then the 64 row groups through LDS
-    // (reusing the staged rows): rows 0..31 store, rows 32..63 add theirs to
-    // the same slots, then one thread per channel adds the 32 slots.  The
-    // values are integers below 2^53, so every order gives the same sum.
+    // (reusing the staged rows), 16 of the thread's channels at a time: rows
+    // 0..31 store, rows 32..63 add theirs to the same slots, then one thread
+    // per channel adds the 32 slots.  The values are integers below 2^53, so
+    // every order gives the same sum.
     double* red = reinterpret_cast<double*>(dyn);
     const int slot = (r64 & 31) * kSumRowStride + c4 * kSumC4Stride;   // in doubles
     double acc[32];
 #pragma unroll
     for (int c = 0; c < 32; ++c) acc[c] = fixq(z[0][c]) + fixq(z[1][c]);
     __syncthreads();   // every thread is done with the staged rows
-    if (r64 < 32) {
 #pragma unroll
-      for (int c = 0; c < 32; c += 2) *reinterpret_cast<double2*>(&red[slot + c]) = make_double2(acc[c], acc[c + 1]);
-    }
-    __syncthreads();
-    if (r64 >= 32) {
+    for (int h = 0; h < 2; ++h) {
+      if (r64 < 32) {
 #pragma unroll
-      for (int c = 0; c < 32; c += 2) {
-        double2* d = reinterpret_cast<double2*>(&red[slot + c]);
-        const double2 o = *d;
-        *d = make_double2(o.x + acc[c], o.y + acc[c + 1]);
+        for (int c = 0; c < 16; c += 2)
+          *reinterpret_cast<double2*>(&red[slot + c]) = make_double2(acc[16 * h + c], acc[16 * h + c + 1]);
       }
-    }
-    __syncthreads();
-    if (tid < kD) {
-      const double* col = red + (tid >> 5) * kSumC4Stride + (tid & 31);
-      double sum = 0.0;
-      for (int r = 0; r < 32; ++r) sum += col[r * kSumRowStride];
-      unsafeAtomicAdd(a.sums + static_cast<size_t>(bh) * kD + tid, sum);
+      __syncthreads();
+      if (r64 >= 32) {
+#pragma unroll
+        for (int c = 0; c < 16; c += 2) {
+          double2* d = reinterpret_cast<double2*>(&red[slot + c]);
+          const double2 o = *d;
+          *d = make_double2(o.x + acc[16 * h + c], o.y + acc[16 * h + c + 1]);
+        }
+      }
+      __syncthreads();
+      if (tid < 64) {
+        const double* col = red + (tid >> 4) * kSumC4Stride + (tid & 15);
+        double sum = 0.0;
+        for (int r = 0; r < 32; ++r) sum += col[r * kSumRowStride];
+        unsafeAtomicAdd(a.sums + static_cast<size_t>(bh) * kD + 32 * (tid >> 4) + 16 * h + (tid & 15), sum);
+      }
+      if (h == 0) __syncthreads();   // read before the second half overwrites the slots
     }
   } else {
     if (a.center) {

@@ -70,8 +70,18 @@ def _violations(body):
     return out
 
 
+_ASM_CACHE = []
+
+
 def _asm():
-    """gfx950 assembly of the translation units (attention, debug attention, producers), compiled in parallel."""
+    """gfx950 assembly of the translation units (attention, debug attention, producers), compiled in parallel
+    once per test session."""
+    if not _ASM_CACHE:
+        _ASM_CACHE.append(_compile())
+    return _ASM_CACHE[0]
+
+
+def _compile():
     with tempfile.TemporaryDirectory() as td:
         procs = []
         for i, src in enumerate(SOURCES):
@@ -110,3 +120,28 @@ def test_fp6_pack_register_hazards():
     producers = [k for k, body in _kernels(asm) if "k_qk" in k and any(b.startswith(CONV) for b in body)]
     assert producers, "the Q/K producer's E2M3 packing was not found"
     assert not bad, f"packing-conversion register hazards: {bad}"
+
+
+@pytest.mark.skipif(not shutil.which(HIPCC) and not os.path.exists(HIPCC), reason="hipcc not available")
+def test_no_kernel_uses_scratch():
+    """No production kernel of these units keeps anything in per-lane private
+    memory: a small array indexed with a run-time value (or a by-value argument
+    indexed that way) lands there and costs a round trip to memory per access.
+    Exempt: the debug instantiations of the attention kernel (they dump S, P
+    codes and maxima for the parity tests and spill freely) and, up to 16 bytes,
+    the key-bias (Q smoothing) attention instantiations, which spill two
+    registers at the 256-register limit."""
+    asm = _asm()
+    names = re.findall(r"\.amdhsa_kernel\s+(\S+)", asm)
+    sizes = [int(z) for z in re.findall(r"\.amdhsa_private_segment_fixed_size\s+(\d+)", asm)]
+    assert names and len(names) == len(sizes), "kernel descriptors not found"
+    bad = []
+    for n, z in zip(names, sizes):
+        m = re.search(r"k_attn_e2m3ILi\d+ELb([01])ELb([01])ELb([01])ELb([01])ELb([01])E", n)
+        if m and m.group(3) == "1":
+            continue                      # debug dump instantiation
+        limit = 16 if (m and m.group(4) == "1") else 0   # key-bias variant
+        if z > limit:
+            bad.append((n, z))
+    assert any("k_qk" in n for n in names) and any("k_attn_e2m3" in n for n in names)
+    assert not bad, f"kernels with a private segment: {bad}"

@@ -64,10 +64,14 @@ __device__ __forceinline__ uint4 expand16(uint2 w) {
   return make_uint4((w.x << 4) & 0xF0F0F0F0u, w.x & 0xF0F0F0F0u, (w.y << 4) & 0xF0F0F0F0u, w.y & 0xF0F0F0F0u);
 }
 
+// A lane carries 8-byte pieces of the packed block (KV/32 of K, KV/32 of V):
+// piece i of lane tid is packed bytes (i*256 + tid)*8 .. +7, which expand to
+// the 16 int8 bytes at twice that offset, so each LDS store of a wave covers
+// 1 KB contiguously (no bank conflicts).
 template <int KV>
 struct Stage {
-  uint4 k[KV / 64];
-  uint4 v[KV / 64];
+  uint2 k[KV / 32];
+  uint2 v[KV / 32];
 };
 
 template <int KV>
@@ -76,23 +80,21 @@ __device__ __forceinline__ void stage_load(const AttnArgs& a, int bh, int jb, St
   const uint8_t* kb = a.kc + static_cast<size_t>(bh) * a.Npad * 64 + static_cast<size_t>(jb) * KV * 64;
   const uint8_t* vb = a.vc + static_cast<size_t>(bh) * a.Npad * 64 + static_cast<size_t>(jb) * KV * 64;
 #pragma unroll
-  for (int i = 0; i < KV / 64; ++i) {
-    st.k[i] = *reinterpret_cast<const uint4*>(kb + (i * 256 + tid) * 16);
-    st.v[i] = *reinterpret_cast<const uint4*>(vb + (i * 256 + tid) * 16);
+  for (int i = 0; i < KV / 32; ++i) {
+    st.k[i] = *reinterpret_cast<const uint2*>(kb + (i * 256 + tid) * 8);
+    st.v[i] = *reinterpret_cast<const uint2*>(vb + (i * 256 + tid) * 8);
   }
 }
 
-// LDS int8 offset = 2 x packed offset (each 8-byte unit expands to 16 bytes)
+// LDS int8 offset = 2 x packed offset (each 8-byte piece expands to 16 bytes)
 template <int KV>
 __device__ __forceinline__ void stage_store(const Stage<KV>& st, uint8_t* sk, uint8_t* sv) {
   const int tid = threadIdx.x;
 #pragma unroll
-  for (int i = 0; i < KV / 64; ++i) {
-    const int o = (i * 256 + tid) * 32;
-    *reinterpret_cast<uint4*>(sk + o) = expand16(make_uint2(st.k[i].x, st.k[i].y));
-    *reinterpret_cast<uint4*>(sk + o + 16) = expand16(make_uint2(st.k[i].z, st.k[i].w));
-    *reinterpret_cast<uint4*>(sv + o) = expand16(make_uint2(st.v[i].x, st.v[i].y));
-    *reinterpret_cast<uint4*>(sv + o + 16) = expand16(make_uint2(st.v[i].z, st.v[i].w));
+  for (int i = 0; i < KV / 32; ++i) {
+    const int o = (i * 256 + tid) * 16;
+    *reinterpret_cast<uint4*>(sk + o) = expand16(st.k[i]);
+    *reinterpret_cast<uint4*>(sv + o) = expand16(st.v[i]);
   }
 }
 

@@ -11,8 +11,12 @@ the online V Hadamard, the normaliser from the quantized P, per-channel V
 scales, and the BF16 fallback.
 
 The paper gives no per-layer attention accuracy to compare with (its Table 1
-is video-level), so these numbers are reported, not pinned ("parity
-unpinned"): the asserts are sanity floors only.  Qualitative expectations from the paper (Sec. 5.4):
+is video-level), so these numbers are not pinned to the paper ("parity
+unpinned").  They are pinned to themselves: the inputs are seeded and every
+kernel is deterministic, so each variant must stay within a small margin of
+the value measured when the test was written (cosine no more than 0.02
+below, relative L2 no more than 0.03 above); a regression in any variant's
+accuracy fails here.  Qualitative expectations from the paper (Sec. 5.4):
 rotation helps on RoPE-structured outliers, the range-optimized P mapping
 beats the symmetric 7-level one.
 """
@@ -35,6 +39,25 @@ VARIANTS = [
     ("int4 interleaved l = sum P^", 1, 0, 128, 3, 0, 1),
     ("int4 interleaved per-channel V", 1, 0, 128, 3, 0, 0, "N"),
 ]
+
+
+# (cosine, relative L2) measured per workload and variant; the test allows
+# cosine down to measured - 0.02 and relative L2 up to measured + 0.03
+MEASURED = {
+    "c1": {"int4 none": (0.679, 0.803), "int4 interleaved": (0.714, 0.759), "int4 half": (0.740, 0.723),
+           "int4 full hadamard": (0.919, 0.404), "int4 interleaved SYM7": (0.714, 0.759),
+           "int4 interleaved per-token": (0.826, 0.594), "int4 interleaved Q smoothing": (0.705, 0.772),
+           "int4 interleaved no smoothing": (0.703, 0.773), "int4 interleaved online V had.": (0.714, 0.759),
+           "int4 interleaved l = sum P^": (0.714, 0.759), "int4 interleaved per-channel V": (0.711, 0.762),
+           "bf16 fallback": (0.9996, 0.030)},
+    "c2": {"int4 none": (0.551, 0.951), "int4 interleaved": (0.571, 0.929), "int4 half": (0.618, 0.876),
+           "int4 full hadamard": (0.855, 0.541), "int4 interleaved SYM7": (0.571, 0.930),
+           "int4 interleaved per-token": (0.724, 0.745), "int4 interleaved Q smoothing": (0.576, 0.924),
+           "int4 interleaved no smoothing": (0.573, 0.927), "int4 interleaved online V had.": (0.571, 0.930),
+           "int4 interleaved l = sum P^": (0.571, 0.930), "int4 interleaved per-channel V": (0.566, 0.940),
+           "bf16 fallback": (0.9985, 0.054)},
+}
+COS_MARGIN, RL2_MARGIN = 0.02, 0.03
 
 
 def _metrics(o, r):
@@ -94,9 +117,17 @@ def test_fidelity_to_fp64_attention(ora, wname):
         cos, rl2 = _metrics(og, rg)
         table[name] = (cos, rl2)
         print(f"  {name:28s} cosine {cos:.6f}   rel L2 {rl2:.4e}", flush=True)
-    # sanity floors only: these workloads put x10..x30 outliers on a few
-    # channel pairs of Q and K, so the logits span hundreds and the INT4
-    # per-block scales leave the ordinary channels with few levels
-    assert table["bf16 fallback"][0] > 0.99
-    for name, *_ in VARIANTS:
-        assert table[name][0] > 0.5, name
+    # these workloads put x10..x30 outliers on a few channel pairs of Q and K,
+    # so the logits span hundreds and the INT4 per-block scales leave the
+    # ordinary channels few levels: the INT4 numbers are low, and each is held
+    # to what it measured
+    assert set(table) == set(MEASURED[wname])
+    for name, (cos, rl2) in table.items():
+        c0, r0 = MEASURED[wname][name]
+        assert cos >= c0 - COS_MARGIN, (name, cos, c0)
+        assert rl2 <= r0 + RL2_MARGIN, (name, rl2, r0)
+    # the paper's qualitative orderings on these inputs: a rotation helps, and
+    # the fallback is far closer than any INT4 variant
+    assert table["int4 full hadamard"][0] > table["int4 none"][0]
+    assert table["int4 half"][0] > table["int4 none"][0]
+    assert table["bf16 fallback"][0] > max(v[0] for k, v in table.items() if k != "bf16 fallback")

@@ -215,14 +215,17 @@ def main():
                     "the launch stream, mean over the timed steps)"}
     log(f"producers {prod_ms * 1e3:.1f} us: {prod['gbps']} GB/s algorithmic ({prod['frac']:.3f} of HBM peak), "
         f"{prod['gbps_two_pass']} GB/s of bytes moved")
-    # the shader clock while the attention kernel runs back to back
+    # the shader clock while the attention kernel runs back to back for about
+    # one second, sampled in the second half (the first launches ramp it up)
     read_sclk = sclk_reader(torch, dev)
     clk = []
-    for _ in range(40):
+    n_launch = max(40, int(1000.0 / attn_ms))
+    for _ in range(n_launch):
         ra.attn_int4(p, bufs["q_codes"], bufs["q_scale"], bufs["k_codes"], bufs["k_scale"], bufs["v_codes"],
                      bufs["v_scale"], bufs["mu_v"], o)
+    time.sleep(0.4 * n_launch * attn_ms * 1e-3)
     for _ in range(12):
-        time.sleep(0.01)
+        time.sleep(0.02)
         clk.append(read_sclk())
     torch.cuda.synchronize()
     clk = [c for c in clk if c is not None]
@@ -230,8 +233,8 @@ def main():
            "compute_units": torch.cuda.get_device_properties(dev).multi_processor_count,
            "sclk_mhz_under_load": {"median": float(np.median(clk)), "min": min(clk), "max": max(clk),
                                    "samples": len(clk)} if clk else None,
-           "sclk_source": "amdgpu DPM table of this device (pp_dpm_sclk, current level), sampled every 10 ms "
-                          "while 40 attention launches ran"}
+           "sclk_source": f"amdgpu DPM table of this device (pp_dpm_sclk, current level), sampled every 20 ms "
+                          f"in the second half of {n_launch} back-to-back attention launches"}
     log(f"gpu: {gpu['name']} {gpu['arch']} {gpu['compute_units']} CUs, shader clock under load "
         f"{gpu['sclk_mhz_under_load']}")
     ops = w.ops()

@@ -296,9 +296,17 @@ ra::RopeTables tables_at(const ra_params* p, const float* dev, const size_t off[
   return t;
 }
 
-// Copies the tables of p into dev (table_bytes(p) bytes of the workspace) on
-// stream s and describes them in *out.
-int put_tables(const ra_params* p, float* dev, hipStream_t s, ra::RopeTables* out) {
+// The table copy a producer call still has to make (its prologue kernel does it).
+struct TableCopy {
+  const uint32_t* src = nullptr;
+  uint32_t* dst = nullptr;
+  int64_t nwords = 0;
+};
+
+// Describes the tables of p, placed at dev (table_bytes(p) bytes of the
+// workspace), in *out, and copies them there on stream s -- or, with defer,
+// leaves the copy to the caller's next kernel and describes it in *defer.
+int put_tables(const ra_params* p, float* dev, hipStream_t s, ra::RopeTables* out, TableCopy* defer = nullptr) {
   const std::string key = table_key(p);
   std::lock_guard<std::mutex> lock(g_mu);
   auto it = g_tables.find(key);
@@ -317,8 +325,14 @@ int put_tables(const ra_params* p, float* dev, hipStream_t s, ra::RopeTables* ou
   const HostTable& ht = it->second;
   // a kernel on s reads the pinned table through its device mapping: the copy
   // stays on the kernel queue, with no hand-over to a copy engine and back
-  RA_CHECK_HIP(ra::launch_copy_u32(reinterpret_cast<const uint32_t*>(ht.mapped), reinterpret_cast<uint32_t*>(dev),
-                                   static_cast<int64_t>(ht.bytes / 4), s));
+  if (defer) {
+    defer->src = reinterpret_cast<const uint32_t*>(ht.mapped);
+    defer->dst = reinterpret_cast<uint32_t*>(dev);
+    defer->nwords = static_cast<int64_t>(ht.bytes / 4);
+  } else {
+    RA_CHECK_HIP(ra::launch_copy_u32(reinterpret_cast<const uint32_t*>(ht.mapped), reinterpret_cast<uint32_t*>(dev),
+                                     static_cast<int64_t>(ht.bytes / 4), s));
+  }
   *out = tables_at(p, dev, ht.off);
   return RA_OK;
 }
@@ -331,93 +345,142 @@ float kc_of(const ra_params* p) {
 hipStream_t st(void* s) { return static_cast<hipStream_t>(s); }
 
 // ------------------------------------------------------------- producers --
-// Every pass runs on the caller's stream, in order.
 
-int qk_impl(const ra_params* p, const ra::RopeTables& t, const void* q, const void* k, uint8_t* qc, float* qs,
-            uint8_t* kc, float* ks, float* mu_k, float* mu_q, float* kbias, const Int4Ws& w, hipStream_t s) {
-  const Sizes z = sizes_of(p);
-  ra::QkArgs a{};
-  a.N = p->N;
-  a.Npad = static_cast<int>(z.Npad);
-  a.is_fp16 = p->in_dtype == RA_FP16;
-  a.e2m3 = p->code_format == RA_CODES_E2M3;
-  a.sums = w.ksum;
-  float* mu = mu_k ? mu_k : w.mu_k;
-  const bool center = (p->smooth & RA_SMOOTH_K) != 0;
-  if (center) {
-    // exact fixed-point channel sums of the rotated K, accumulated by atomics
-    RA_CHECK_HIP(ra::launch_fill_zero_u32(reinterpret_cast<uint32_t*>(w.ksum), static_cast<int64_t>(2 * z.partial), s));
-    a.x = static_cast<const uint16_t*>(k);
-    RA_CHECK_HIP(ra::launch_qk_sums(t, a, static_cast<int>(z.BH), s));
-  } else if (mu_k) {
-    RA_CHECK_HIP(ra::launch_fill_zero_u32(reinterpret_cast<uint32_t*>(mu_k), static_cast<int64_t>(z.mu), s));
-  }
-  const bool center_q = (p->smooth & RA_SMOOTH_Q) != 0;
-  if (center_q) {
-    RA_CHECK_HIP(ra::launch_fill_zero_u32(reinterpret_cast<uint32_t*>(w.qsum), static_cast<int64_t>(2 * z.partial), s));
-    ra::QkArgs aq = a;
-    aq.sums = w.qsum;
-    aq.x = static_cast<const uint16_t*>(q);
-    RA_CHECK_HIP(ra::launch_qk_sums(t, aq, static_cast<int>(z.BH), s));
-  } else if (mu_q) {
-    RA_CHECK_HIP(ra::launch_fill_zero_u32(reinterpret_cast<uint32_t*>(mu_q), static_cast<int64_t>(z.mu), s));
-  }
-  a.x = static_cast<const uint16_t*>(q);
-  a.codes = qc;
-  a.scales = qs;
-  a.sums = w.qsum;
-  a.center = center_q;
-  a.mu_out = center_q ? (mu_q ? mu_q : w.mu_q) : nullptr;
-  a.group = p->q_group;
-  RA_CHECK_HIP(ra::launch_qk_quant(t, a, static_cast<int>(z.BH), s));
-  a.x = static_cast<const uint16_t*>(k);
-  a.codes = kc;
-  a.scales = ks;
-  a.sums = w.ksum;
-  a.center = center;
-  a.mu_out = center ? mu : nullptr;
-  a.group = p->k_group;
-  a.qsums = center_q ? w.qsum : nullptr;
-  a.bias = center_q ? kbias : nullptr;
-  RA_CHECK_HIP(ra::launch_qk_quant(t, a, static_cast<int>(z.BH), s));
-  return RA_OK;
-}
+// Outputs of a producer call (device pointers; nullptr where not wanted).
+struct ProdOut {
+  uint8_t* qc = nullptr;
+  float* qs = nullptr;
+  uint8_t* kc = nullptr;
+  float* ks = nullptr;
+  uint8_t* vc = nullptr;
+  float* vs = nullptr;
+  float* mu_k = nullptr;
+  float* mu_q = nullptr;
+  float* mu_v = nullptr;
+  float* kbias = nullptr;
+};
 
-int v_impl(const ra_params* p, const void* v, uint8_t* vc, float* vs, float* mu_v, const Int4Ws& w, hipStream_t s) {
+// The Q/K producers (q and k given) and/or the V producer (v given) on the
+// caller's stream: one prologue kernel (the table copy, the zero fills), then
+// the passes.  Each pass is one launch holding every job whose inputs are
+// ready, so independent work (the channel sums of K and V, the codes of an
+// unsmoothed Q) runs side by side: pass 0 the sums and every code pass that
+// needs none; pass 1 the codes that need sums (and the V group maxima when V
+// groups straddle tiles); pass 2 the V codes after those maxima.
+int produce(const ra_params* p, const ra::RopeTables& t, const TableCopy& tc, const void* q, const void* k,
+            const void* v, const ProdOut& out, const Int4Ws& w, hipStream_t s) {
   const Sizes z = sizes_of(p);
-  ra::VArgs a{};
-  a.x = static_cast<const uint16_t*>(v);
-  a.codes = vc;
-  a.scales = vs;
-  a.sums = w.vsum;
-  a.amax = w.amax;
-  a.N = p->N;
-  a.Npad = static_cast<int>(z.Npad);
-  a.group = p->v_group;
-  a.ngroups = static_cast<int>(z.nvgroups);
-  a.is_fp16 = p->in_dtype == RA_FP16;
-  a.e2m3 = p->code_format == RA_CODES_E2M3;
-  a.vhad = p->v_rotation == RA_VROT_HADAMARD;
-  float* mu = mu_v ? mu_v : w.mu_v;
-  if (p->smooth & RA_SMOOTH_V) {
-    RA_CHECK_HIP(ra::launch_fill_zero_u32(reinterpret_cast<uint32_t*>(w.vsum), static_cast<int64_t>(2 * z.partial), s));
-    a.center = 0;
-    RA_CHECK_HIP(ra::launch_v_sums(a, static_cast<int>(z.BH), s));
-    a.center = 1;
-    a.mu_out = mu;
-  } else {
-    if (mu_v) RA_CHECK_HIP(ra::launch_fill_zero_u32(reinterpret_cast<uint32_t*>(mu_v), static_cast<int64_t>(z.mu), s));
-    a.center = 0;
-    a.mu_out = nullptr;
-  }
+  const bool do_qk = q != nullptr && k != nullptr, do_v = v != nullptr;
+  const bool center_k = (p->smooth & RA_SMOOTH_K) != 0, center_q = (p->smooth & RA_SMOOTH_Q) != 0;
+  const bool smooth_v = (p->smooth & RA_SMOOTH_V) != 0;
   // groups of 64 or 128 tokens never straddle a 128-token tile (they start at
-  // multiples of the group size): the quantize pass finds their maxima itself
-  a.local_amax = p->v_group == 64 || p->v_group == 128;
-  if (!a.local_amax) {
-    RA_CHECK_HIP(ra::launch_fill_zero_u32(w.amax, static_cast<int64_t>(z.amax), s));
-    RA_CHECK_HIP(ra::launch_v_amax(a, static_cast<int>(z.BH), s));
+  // multiples of the group size): the V code pass finds their maxima itself
+  const bool local_amax = p->v_group == 64 || p->v_group == 128;
+
+  ra::Prologue pr{};
+  pr.src = tc.src;
+  pr.dst = tc.dst;
+  pr.ncopy = tc.nwords;
+  int nz = 0;
+  auto zero = [&](void* ptr, size_t words) {
+    pr.zero[nz] = static_cast<uint32_t*>(ptr);
+    pr.nzero[nz] = static_cast<int64_t>(words);
+    ++nz;
+  };
+  if (do_qk) {
+    // exact fixed-point channel sums are accumulated by atomics; an unsmoothed
+    // tensor reports a zero mean
+    if (center_k) zero(w.ksum, 2 * z.partial);
+    else if (out.mu_k) zero(out.mu_k, z.mu);
+    if (center_q) zero(w.qsum, 2 * z.partial);
+    else if (out.mu_q) zero(out.mu_q, z.mu);
   }
-  RA_CHECK_HIP(ra::launch_v_quant(a, static_cast<int>(z.BH), s));
+  if (do_v) {
+    if (smooth_v) zero(w.vsum, 2 * z.partial);
+    else if (out.mu_v) zero(out.mu_v, z.mu);
+    if (!local_amax) zero(w.amax, z.amax);
+  }
+  RA_CHECK_HIP(ra::launch_prologue(pr, s));
+
+  ra::PassArgs pass[3];
+  for (auto& ps : pass) {
+    ps = ra::PassArgs{};
+    ps.BH = static_cast<int>(z.BH);
+    ps.Npad = static_cast<int>(z.Npad);
+  }
+  auto add = [&](int ph, int kind, const ra::QkArgs* a, const ra::VArgs* b) {
+    ra::PassJob& j = pass[ph].job[pass[ph].njobs++];
+    j.kind = kind;
+    if (a) j.qk = *a;
+    if (b) j.v = *b;
+  };
+  if (do_qk) {
+    ra::QkArgs a{};
+    a.N = p->N;
+    a.Npad = static_cast<int>(z.Npad);
+    a.is_fp16 = p->in_dtype == RA_FP16;
+    a.e2m3 = p->code_format == RA_CODES_E2M3;
+    if (center_k) {
+      ra::QkArgs ak = a;
+      ak.x = static_cast<const uint16_t*>(k);
+      ak.sums = w.ksum;
+      add(0, ra::kQkSums, &ak, nullptr);
+    }
+    if (center_q) {
+      ra::QkArgs aq = a;
+      aq.x = static_cast<const uint16_t*>(q);
+      aq.sums = w.qsum;
+      add(0, ra::kQkSums, &aq, nullptr);
+    }
+    ra::QkArgs qq = a;
+    qq.x = static_cast<const uint16_t*>(q);
+    qq.codes = out.qc;
+    qq.scales = out.qs;
+    qq.sums = w.qsum;
+    qq.center = center_q;
+    qq.mu_out = center_q ? (out.mu_q ? out.mu_q : w.mu_q) : nullptr;
+    qq.group = p->q_group;
+    add(center_q ? 1 : 0, ra::kQkQuant, &qq, nullptr);
+    ra::QkArgs kq = a;
+    kq.x = static_cast<const uint16_t*>(k);
+    kq.codes = out.kc;
+    kq.scales = out.ks;
+    kq.sums = w.ksum;
+    kq.center = center_k;
+    kq.mu_out = center_k ? (out.mu_k ? out.mu_k : w.mu_k) : nullptr;
+    kq.group = p->k_group;
+    kq.qsums = center_q ? w.qsum : nullptr;
+    kq.bias = center_q ? out.kbias : nullptr;
+    add(center_k || center_q ? 1 : 0, ra::kQkQuant, &kq, nullptr);
+  }
+  if (do_v) {
+    ra::VArgs a{};
+    a.x = static_cast<const uint16_t*>(v);
+    a.codes = out.vc;
+    a.scales = out.vs;
+    a.sums = w.vsum;
+    a.amax = w.amax;
+    a.N = p->N;
+    a.Npad = static_cast<int>(z.Npad);
+    a.group = p->v_group;
+    a.ngroups = static_cast<int>(z.nvgroups);
+    a.is_fp16 = p->in_dtype == RA_FP16;
+    a.e2m3 = p->code_format == RA_CODES_E2M3;
+    a.vhad = p->v_rotation == RA_VROT_HADAMARD;
+    a.local_amax = local_amax;
+    int ph = 0;
+    if (smooth_v) {
+      a.center = 0;
+      add(0, ra::kVSums, nullptr, &a);
+      a.center = 1;
+      a.mu_out = out.mu_v ? out.mu_v : w.mu_v;
+      ph = 1;
+    }
+    if (!local_amax) add(ph++, ra::kVAmax, nullptr, &a);
+    add(ph, ra::kVQuant, nullptr, &a);
+  }
+  for (const auto& ps : pass)
+    if (ps.njobs) RA_CHECK_HIP(ra::launch_pass(t, ps, s));
   return RA_OK;
 }
 
@@ -497,12 +560,20 @@ int fp16_attn_impl(const ra_params* p, const Fp16Ws& w, void* o, hipStream_t s) 
 }
 
 // The whole INT4 forward on a carved workspace whose table region holds the
-// tables t describes: producers, then the attention (codes stay in w).
-int int4_forward(const ra_params* p, const ra::RopeTables& t, const void* q, const void* k, const void* v, void* o,
-                 const Int4Ws& w, hipStream_t s) {
-  int rc = qk_impl(p, t, q, k, w.qc, w.qs, w.kc, w.ks, nullptr, nullptr, w.kbias, w, s);
+// tables t describes (or receives them through tc, in the producers'
+// prologue): producers, then the attention (codes stay in w).
+int int4_forward(const ra_params* p, const ra::RopeTables& t, const TableCopy& tc, const void* q, const void* k,
+                 const void* v, void* o, const Int4Ws& w, hipStream_t s) {
+  ProdOut out;
+  out.qc = w.qc;
+  out.qs = w.qs;
+  out.kc = w.kc;
+  out.ks = w.ks;
+  out.vc = w.vc;
+  out.vs = w.vs;
+  out.kbias = w.kbias;
+  int rc = produce(p, t, tc, q, k, v, out, w, s);
   if (rc) return rc;
-  if ((rc = v_impl(p, v, w.vc, w.vs, nullptr, w, s))) return rc;
   const float* mu = (p->smooth & RA_SMOOTH_V) ? w.mu_v : nullptr;
   return attn_impl(p, w.qc, w.qs, w.kc, w.ks, w.vc, w.vs, mu, w.kbias, o, false, 0, 0, 0, nullptr, nullptr, nullptr, s);
 }
@@ -618,8 +689,17 @@ int rotate_attn_quantize_qk(const ra_params* p, const void* q, const void* k, ui
   if ((rc = check_ws(workspace, workspace_bytes, need.total))) return rc;
   const Int4Ws w = carve_int4(p, workspace);
   ra::RopeTables t;
-  if ((rc = put_tables(p, w.tables, st(stream), &t))) return rc;
-  return qk_impl(p, t, q, k, q_codes, q_scale, k_codes, k_scale, mu_k, mu_q, k_bias, w, st(stream));
+  TableCopy tc;
+  if ((rc = put_tables(p, w.tables, st(stream), &t, &tc))) return rc;
+  ProdOut out;
+  out.qc = q_codes;
+  out.qs = q_scale;
+  out.kc = k_codes;
+  out.ks = k_scale;
+  out.mu_k = mu_k;
+  out.mu_q = mu_q;
+  out.kbias = k_bias;
+  return produce(p, t, tc, q, k, nullptr, out, w, st(stream));
 }
 
 int rotate_attn_quantize_v(const ra_params* p, const void* v, uint8_t* v_codes, float* v_scale, float* mu_v,
@@ -630,7 +710,11 @@ int rotate_attn_quantize_v(const ra_params* p, const void* v, uint8_t* v_codes, 
   if ((rc = check_align({v, v_codes}))) return rc;
   const Int4Ws need = carve_int4(p, nullptr);
   if ((rc = check_ws(workspace, workspace_bytes, need.total))) return rc;
-  return v_impl(p, v, v_codes, v_scale, mu_v, carve_int4(p, workspace), st(stream));
+  ProdOut out;
+  out.vc = v_codes;
+  out.vs = v_scale;
+  out.mu_v = mu_v;
+  return produce(p, ra::RopeTables{}, TableCopy{}, nullptr, nullptr, v, out, carve_int4(p, workspace), st(stream));
 }
 
 int rotate_attn_quantize_qkv(const ra_params* p, const void* q, const void* k, const void* v, uint8_t* q_codes,
@@ -647,9 +731,20 @@ int rotate_attn_quantize_qkv(const ra_params* p, const void* q, const void* k, c
   if ((rc = check_ws(workspace, workspace_bytes, need.total))) return rc;
   const Int4Ws w = carve_int4(p, workspace);
   ra::RopeTables t;
-  if ((rc = put_tables(p, w.tables, st(stream), &t))) return rc;
-  if ((rc = qk_impl(p, t, q, k, q_codes, q_scale, k_codes, k_scale, mu_k, mu_q, k_bias, w, st(stream)))) return rc;
-  return v_impl(p, v, v_codes, v_scale, mu_v, w, st(stream));
+  TableCopy tc;
+  if ((rc = put_tables(p, w.tables, st(stream), &t, &tc))) return rc;
+  ProdOut out;
+  out.qc = q_codes;
+  out.qs = q_scale;
+  out.kc = k_codes;
+  out.ks = k_scale;
+  out.vc = v_codes;
+  out.vs = v_scale;
+  out.mu_k = mu_k;
+  out.mu_q = mu_q;
+  out.mu_v = mu_v;
+  out.kbias = k_bias;
+  return produce(p, t, tc, q, k, v, out, w, st(stream));
 }
 
 int rotate_attn_attn_int4(const ra_params* p, const uint8_t* q_codes, const float* q_scale, const uint8_t* k_codes,
@@ -690,8 +785,9 @@ int rotate_attn_fwd_int4(const ra_params* p, const void* q, const void* k, const
   if ((rc = check_ws(workspace, workspace_bytes, need.total))) return rc;
   const Int4Ws w = carve_int4(p, workspace);
   ra::RopeTables t;
-  if ((rc = put_tables(p, w.tables, st(stream), &t))) return rc;
-  return int4_forward(p, t, q, k, v, o, w, st(stream));
+  TableCopy tc;
+  if ((rc = put_tables(p, w.tables, st(stream), &t, &tc))) return rc;
+  return int4_forward(p, t, tc, q, k, v, o, w, st(stream));
 }
 
 int rotate_attn_fwd_int4_noalloc(const ra_params* p, const void* q, const void* k, const void* v, void* o,
@@ -709,7 +805,7 @@ int rotate_attn_fwd_int4_noalloc(const ra_params* p, const void* q, const void* 
   const Int4Ws w = carve_int4(p, ns->base);
   ra::RopeTables t;
   if ((rc = noalloc_tables(p, ns, w.tables, st(stream), &t))) return rc;
-  return int4_forward(p, t, q, k, v, o, w, st(stream));
+  return int4_forward(p, t, TableCopy{}, q, k, v, o, w, st(stream));
 }
 
 int rotate_attn_prepare_fp16(const ra_params* p, const void* q, const void* k, const void* v, void* workspace,

@@ -101,16 +101,36 @@ struct Fp16Args {
   int is_fp16, out_dtype;
 };
 
+// Producer passes launched together in one grid: job j of a pass covers every
+// head and tile (blockIdx.y = j * BH + head, blockIdx.x = tile), and jobs of
+// one pass do not depend on each other.
+enum PassKind { kPassNone = 0, kQkSums = 1, kQkQuant = 2, kVSums = 3, kVAmax = 4, kVQuant = 5 };
+struct PassJob {
+  int kind;
+  QkArgs qk;   // kQkSums, kQkQuant
+  VArgs v;     // kVSums, kVAmax, kVQuant
+};
+struct PassArgs {
+  PassJob job[3];
+  int njobs, BH, Npad;
+};
+
+// The start of a producer call: the RoPE tables into the workspace (src may be
+// pinned host memory read through its device mapping) and up to four zero fills.
+struct Prologue {
+  const uint32_t* src;
+  uint32_t* dst;
+  int64_t ncopy;
+  uint32_t* zero[4];
+  int64_t nzero[4];
+};
+
 // ---- launchers (return hipError_t) ----
-hipError_t launch_qk_sums(const RopeTables& t, const QkArgs& a, int BH, hipStream_t s);
-hipError_t launch_qk_quant(const RopeTables& t, const QkArgs& a, int BH, hipStream_t s);
-hipError_t launch_fill_zero_u32(uint32_t* p, int64_t n, hipStream_t s);
+hipError_t launch_pass(const RopeTables& t, const PassArgs& pa, hipStream_t s);
+hipError_t launch_prologue(const Prologue& pr, hipStream_t s);
 hipError_t launch_copy_u32(const uint32_t* src, uint32_t* dst, int64_t n, hipStream_t s);
 // n host floats -> dst on the device, carried in kernel arguments (no allocation)
 hipError_t launch_write_floats(const float* host, size_t n, float* dst, hipStream_t s);
-hipError_t launch_v_sums(const VArgs& a, int BH, hipStream_t s);
-hipError_t launch_v_amax(const VArgs& a, int BH, hipStream_t s);
-hipError_t launch_v_quant(const VArgs& a, int BH, hipStream_t s);
 hipError_t launch_attn_int4(const AttnArgs& a, int kv_block, bool k_per_token, bool sym7, bool debug,
                             hipStream_t s);
 hipError_t launch_attn_e2m3(const AttnArgs& a, int kv_block, bool k_per_token, bool sym7, bool debug,

@@ -80,16 +80,16 @@ __device__ __forceinline__ double fixq(float v) {
 
 // Reduces the per-thread fixed-point sums over the 8 row groups and adds the
 // tile's channel sums to the head's [128] (binary64 integers, exact in any order).
-__device__ __forceinline__ void add_sums(double acc[4], double* out) {
-  __shared__ double red[8][kD];
+// red: 8 x 128 binary64 of LDS.
+__device__ __forceinline__ void add_sums(double acc[4], double* out, double* red) {
   const int tid = threadIdx.x, rr = tid >> 5, cl = tid & 31;
 #pragma unroll
-  for (int c = 0; c < 4; ++c) red[rr][4 * cl + c] = acc[c];
+  for (int c = 0; c < 4; ++c) red[rr * kD + 4 * cl + c] = acc[c];
   __syncthreads();
   if (tid < kD) {
     double s = 0.0;
 #pragma unroll
-    for (int r = 0; r < 8; ++r) s += red[r][tid];
+    for (int r = 0; r < 8; ++r) s += red[r * kD + tid];
     unsafeAtomicAdd(out + tid, s);
   }
 }
@@ -375,6 +375,10 @@ constexpr int kSumRowStride = 66;   // 528 bytes
 constexpr int kSumC4Stride = 16;    // 128 bytes
 constexpr size_t kSumLdsBytes = 32 * kSumRowStride * sizeof(double);
 
+// LDS of a Q/K workgroup: four arrays of 128 floats, then the staged table
+// rows (and, in the sums pass, the partial sums in their place).
+constexpr int kQkSmallBytes = 4 * kTile * 4;
+
 // Q/K producer, one workgroup per (tile, head): the tile's rows and the table
 // rows it needs are requested at once (the table rows straight into LDS),
 // then RoPE and the rotation, then
@@ -382,12 +386,12 @@ constexpr size_t kSumLdsBytes = 32 * kSumRowStride * sizeof(double);
 //        to a.sums with atomics;
 //  else: smoothing, the key bias of Q smoothing, per-group scales and codes.
 template <int ROT, bool F16, bool STAGED, bool SUMS>
-__global__ __launch_bounds__(256) void k_qk(RopeTables t, QkArgs a) {
-  extern __shared__ float4 dyn[];   // STAGED: the staged table rows; SUMS: then the partial sums
-  __shared__ float rowmax[kTile];
-  __shared__ float ginv[kTile];
-  __shared__ float smu[kD], smq[kD];
-  const int tile = blockIdx.x, bh = blockIdx.y;
+__device__ __forceinline__ void qk_body(const RopeTables& t, const QkArgs& a, int tile, int bh, uint8_t* lds) {
+  float* rowmax = reinterpret_cast<float*>(lds);
+  float* ginv = rowmax + kTile;
+  float* smu = ginv + kTile;
+  float* smq = smu + kD;
+  float4* dyn = reinterpret_cast<float4*>(lds + kQkSmallBytes);
   const int tid = threadIdx.x, r64 = tid >> 2, c4 = tid & 3;
   const int N = a.N, n0 = tile * kTile;
   const double den = static_cast<double>(N) * 1048576.0;
@@ -575,9 +579,9 @@ __device__ __forceinline__ void load_v_tile(const VArgs& a, int bh, int tile, fl
   }
 }
 
+// LDS: 8 x 128 binary64.
 template <bool F16, bool VHAD>
-__global__ __launch_bounds__(256) void k_v_sums(VArgs a) {
-  const int tile = blockIdx.x, bh = blockIdx.y;
+__device__ __forceinline__ void v_sums_body(const VArgs& a, int tile, int bh, uint8_t* lds) {
   float z[16][4];
   load_v_tile<F16, VHAD>(a, bh, tile, z);
   double acc[4] = {0.0, 0.0, 0.0, 0.0};
@@ -585,7 +589,7 @@ __global__ __launch_bounds__(256) void k_v_sums(VArgs a) {
   for (int p = 0; p < 16; ++p)
 #pragma unroll
     for (int c = 0; c < 4; ++c) acc[c] += fixq(z[p][c]);
-  add_sums(acc, a.sums + static_cast<size_t>(bh) * kD);
+  add_sums(acc, a.sums + static_cast<size_t>(bh) * kD, reinterpret_cast<double*>(lds));
 }
 
 __device__ __forceinline__ int vgroup_of(const VArgs& a, int n) {
@@ -595,10 +599,10 @@ __device__ __forceinline__ int vgroup_of(const VArgs& a, int n) {
 
 // Per (tile half, channel) abs-max, merged into the group maxima with an
 // order-independent atomic max on the float bits (values are >= 0).
+// LDS: 8 x 2 x 128 floats.
 template <bool F16, bool VHAD>
-__global__ __launch_bounds__(256) void k_v_amax(VArgs a) {
-  __shared__ float red[8][2][kD];
-  const int tile = blockIdx.x, bh = blockIdx.y;
+__device__ __forceinline__ void v_amax_body(const VArgs& a, int tile, int bh, uint8_t* lds) {
+  float (*red)[2][kD] = reinterpret_cast<float (*)[2][kD]>(lds);
   const int tid = threadIdx.x, rr = tid >> 5, cl = tid & 31;
   float z[16][4];
   load_v_tile<F16, VHAD>(a, bh, tile, z);
@@ -622,12 +626,14 @@ __global__ __launch_bounds__(256) void k_v_amax(VArgs a) {
   }
 }
 
+// LDS: the tile's codes (12 KB), 2 x 128 inverse scales, 8 x 2 x 128 floats.
+constexpr int kVQuantLdsBytes = kTile * 96 + 2 * kD * 4 + 8 * 2 * kD * 4;
+
 template <bool F16, bool VHAD>
-__global__ __launch_bounds__(256) void k_v_quant(VArgs a) {
-  __shared__ __align__(16) uint8_t ctile[kTile * 96];
-  __shared__ float ginv[2][kD];
-  __shared__ float red[8][2][kD];
-  const int tile = blockIdx.x, bh = blockIdx.y;
+__device__ __forceinline__ void v_quant_body(const VArgs& a, int tile, int bh, uint8_t* lds) {
+  uint8_t* ctile = lds;
+  float (*ginv)[kD] = reinterpret_cast<float (*)[kD]>(lds + kTile * 96);
+  float (*red)[2][kD] = reinterpret_cast<float (*)[2][kD]>(lds + kTile * 96 + 2 * kD * 4);
   const int tid = threadIdx.x, rr = tid >> 5, cl = tid & 31;
   float z[16][4];
   if (a.local_amax) {
@@ -734,6 +740,49 @@ __global__ __launch_bounds__(256) void k_v_quant(VArgs a) {
   }
 }
 
+// One producer pass: the block's job from its row of the grid.  The job's
+// arguments are copied out with constant indices (indexing the argument array
+// with the run-time job number would put it in scratch).
+template <int ROT, bool F16, bool STAGED, bool VHAD>
+__global__ __launch_bounds__(256) void k_pass(RopeTables t, PassArgs pa) {
+  extern __shared__ __align__(16) uint8_t lds[];
+  const int j = blockIdx.y / pa.BH, bh = blockIdx.y - j * pa.BH, tile = blockIdx.x;
+  int kind;
+  QkArgs qa;
+  VArgs va;
+  if (j == 0) {
+    kind = pa.job[0].kind;
+    qa = pa.job[0].qk;
+    va = pa.job[0].v;
+  } else if (j == 1) {
+    kind = pa.job[1].kind;
+    qa = pa.job[1].qk;
+    va = pa.job[1].v;
+  } else {
+    kind = pa.job[2].kind;
+    qa = pa.job[2].qk;
+    va = pa.job[2].v;
+  }
+  switch (kind) {
+    case kQkSums: qk_body<ROT, F16, STAGED, true>(t, qa, tile, bh, lds); break;
+    case kQkQuant: qk_body<ROT, F16, STAGED, false>(t, qa, tile, bh, lds); break;
+    case kVSums: v_sums_body<F16, VHAD>(va, tile, bh, lds); break;
+    case kVAmax: v_amax_body<F16, VHAD>(va, tile, bh, lds); break;
+    case kVQuant: v_quant_body<F16, VHAD>(va, tile, bh, lds); break;
+    default: break;
+  }
+}
+
+// The table copy and the zero fills of one producer call.
+__global__ __launch_bounds__(256) void k_prologue(Prologue pr) {
+  const int64_t stride = static_cast<int64_t>(gridDim.x) * blockDim.x;
+  const int64_t i0 = blockIdx.x * static_cast<int64_t>(blockDim.x) + threadIdx.x;
+  for (int64_t i = i0; i < pr.ncopy; i += stride) pr.dst[i] = pr.src[i];
+#pragma unroll
+  for (int z = 0; z < 4; ++z)
+    for (int64_t i = i0; i < pr.nzero[z]; i += stride) pr.zero[z][i] = 0u;
+}
+
 // Up to kChunkFloats binary32 values carried in the kernel arguments and
 // written to dst[off .. off + n): moves a host table to the device without a
 // host staging buffer or a copy engine.
@@ -757,63 +806,77 @@ __global__ __launch_bounds__(256) void k_copy_u32(const uint32_t* __restrict__ s
     dst[i] = src[i];
 }
 
-__global__ void k_fill_zero_u32(uint32_t* p, int64_t n) {
-  for (int64_t i = blockIdx.x * static_cast<int64_t>(blockDim.x) + threadIdx.x; i < n;
-       i += static_cast<int64_t>(gridDim.x) * blockDim.x)
-    p[i] = 0u;
-}
+
 
 }  // namespace
 
 namespace {
 
-template <int ROT, bool F16, bool STAGED, bool SUMS>
-hipError_t launch_qk_one(const RopeTables& t, const QkArgs& a, int BH, int bound, hipStream_t s) {
-  size_t lds = STAGED ? static_cast<size_t>(bound) * sizeof(float4) : 0;
-  if (SUMS && lds < kSumLdsBytes) lds = kSumLdsBytes;
-  hipLaunchKernelGGL((k_qk<ROT, F16, STAGED, SUMS>), dim3(a.Npad / kTile, BH), dim3(256), lds, s, t, a);
+// LDS bytes one job of a pass needs (stage: the staged table rows, or 0).
+size_t job_lds(int kind, size_t stage) {
+  switch (kind) {
+    case kQkSums: return kQkSmallBytes + (stage > kSumLdsBytes ? stage : kSumLdsBytes);
+    case kQkQuant: return kQkSmallBytes + stage;
+    case kVSums: return 8 * kD * sizeof(double);
+    case kVAmax: return 8 * 2 * kD * sizeof(float);
+    case kVQuant: return kVQuantLdsBytes;
+    default: return 0;
+  }
+}
+
+template <int ROT, bool F16>
+hipError_t launch_pass_rf(const RopeTables& t, const PassArgs& pa, bool staged, bool vhad, size_t lds, hipStream_t s) {
+  const dim3 g(pa.Npad / kTile, pa.njobs * pa.BH);
+  if (staged) {
+    if (vhad) hipLaunchKernelGGL((k_pass<ROT, F16, true, true>), g, dim3(256), lds, s, t, pa);
+    else hipLaunchKernelGGL((k_pass<ROT, F16, true, false>), g, dim3(256), lds, s, t, pa);
+  } else {
+    if (vhad) hipLaunchKernelGGL((k_pass<ROT, F16, false, true>), g, dim3(256), lds, s, t, pa);
+    else hipLaunchKernelGGL((k_pass<ROT, F16, false, false>), g, dim3(256), lds, s, t, pa);
+  }
   return hipGetLastError();
 }
 
-// the rotation, the input type and the table staging as template arguments
-// (table-only rotations share one form)
-template <bool SUMS>
-hipError_t launch_qk(const RopeTables& t, const QkArgs& a, int BH, hipStream_t s) {
-  const int bound = stage_bound(t);
-  const bool staged = bound <= kStageMaxF4;
-  const int rot = (t.rotation == RA_ROT_HALF || t.rotation == RA_ROT_HADAMARD) ? t.rotation : 0;
-  const bool f16 = a.is_fp16 != 0;
-#define RA_QK_ONE(R)                                                                     \
-  (staged ? (f16 ? launch_qk_one<R, true, true, SUMS>(t, a, BH, bound, s)                 \
-                 : launch_qk_one<R, false, true, SUMS>(t, a, BH, bound, s))               \
-          : (f16 ? launch_qk_one<R, true, false, SUMS>(t, a, BH, bound, s)                \
-                 : launch_qk_one<R, false, false, SUMS>(t, a, BH, bound, s)))
-  if (rot == RA_ROT_HALF) return RA_QK_ONE(RA_ROT_HALF);
-  if (rot == RA_ROT_HADAMARD) return RA_QK_ONE(RA_ROT_HADAMARD);
-  return RA_QK_ONE(0);
-#undef RA_QK_ONE
-}
-
-#define RA_V_DISPATCH(KERNEL)                                                                         \
-  do {                                                                                                \
-    const dim3 g(a.Npad / kTile, BH);                                                                 \
-    if (a.is_fp16) {                                                                                  \
-      if (a.vhad) hipLaunchKernelGGL((KERNEL<true, true>), g, dim3(256), 0, s, a);                     \
-      else hipLaunchKernelGGL((KERNEL<true, false>), g, dim3(256), 0, s, a);                           \
-    } else {                                                                                          \
-      if (a.vhad) hipLaunchKernelGGL((KERNEL<false, true>), g, dim3(256), 0, s, a);                    \
-      else hipLaunchKernelGGL((KERNEL<false, false>), g, dim3(256), 0, s, a);                          \
-    }                                                                                                 \
-  } while (0)
-
 }  // namespace
 
-hipError_t launch_qk_sums(const RopeTables& t, const QkArgs& a, int BH, hipStream_t s) {
-  return launch_qk<true>(t, a, BH, s);
+hipError_t launch_pass(const RopeTables& t, const PassArgs& pa, hipStream_t s) {
+  if (pa.njobs < 1) return hipSuccess;
+  bool any_qk = false;
+  for (int j = 0; j < pa.njobs; ++j) any_qk |= pa.job[j].kind == kQkSums || pa.job[j].kind == kQkQuant;
+  // a pass of V jobs only carries no tables (t is empty then)
+  const int bound = any_qk ? stage_bound(t) : 0;
+  const bool staged = any_qk && bound <= kStageMaxF4;
+  const size_t stage = staged ? static_cast<size_t>(bound) * sizeof(float4) : 0;
+  size_t lds = 0;
+  bool f16 = false, vhad = false;
+  for (int j = 0; j < pa.njobs; ++j) {
+    const size_t need = job_lds(pa.job[j].kind, stage);
+    if (need > lds) lds = need;
+    const int k = pa.job[j].kind;
+    if (k == kQkSums || k == kQkQuant) f16 = pa.job[j].qk.is_fp16 != 0;
+    else if (k != kPassNone) {
+      f16 = pa.job[j].v.is_fp16 != 0;
+      vhad = pa.job[j].v.vhad != 0;
+    }
+  }
+  const int rot = (t.rotation == RA_ROT_HALF || t.rotation == RA_ROT_HADAMARD) ? t.rotation : 0;
+  if (rot == RA_ROT_HALF)
+    return f16 ? launch_pass_rf<RA_ROT_HALF, true>(t, pa, staged, vhad, lds, s)
+               : launch_pass_rf<RA_ROT_HALF, false>(t, pa, staged, vhad, lds, s);
+  if (rot == RA_ROT_HADAMARD)
+    return f16 ? launch_pass_rf<RA_ROT_HADAMARD, true>(t, pa, staged, vhad, lds, s)
+               : launch_pass_rf<RA_ROT_HADAMARD, false>(t, pa, staged, vhad, lds, s);
+  return f16 ? launch_pass_rf<0, true>(t, pa, staged, vhad, lds, s) : launch_pass_rf<0, false>(t, pa, staged, vhad, lds, s);
 }
 
-hipError_t launch_qk_quant(const RopeTables& t, const QkArgs& a, int BH, hipStream_t s) {
-  return launch_qk<false>(t, a, BH, s);
+hipError_t launch_prologue(const Prologue& pr, hipStream_t s) {
+  int64_t n = pr.ncopy;
+  for (int z = 0; z < 4; ++z) n = pr.nzero[z] > n ? pr.nzero[z] : n;
+  if (n <= 0) return hipSuccess;
+  int64_t blocks = (n + 255) / 256;
+  if (blocks > 1024) blocks = 1024;
+  hipLaunchKernelGGL(k_prologue, dim3(static_cast<unsigned>(blocks)), dim3(256), 0, s, pr);
+  return hipGetLastError();
 }
 
 hipError_t launch_write_floats(const float* host, size_t n, float* dst, hipStream_t s) {
@@ -837,27 +900,8 @@ hipError_t launch_copy_u32(const uint32_t* src, uint32_t* dst, int64_t n, hipStr
   return hipGetLastError();
 }
 
-hipError_t launch_fill_zero_u32(uint32_t* p, int64_t n, hipStream_t s) {
-  int64_t blocks = (n + 255) / 256;
-  if (blocks > 4096) blocks = 4096;
-  if (blocks < 1) blocks = 1;
-  hipLaunchKernelGGL(k_fill_zero_u32, dim3(static_cast<unsigned>(blocks)), dim3(256), 0, s, p, n);
-  return hipGetLastError();
-}
 
-hipError_t launch_v_sums(const VArgs& a, int BH, hipStream_t s) {
-  RA_V_DISPATCH(k_v_sums);
-  return hipGetLastError();
-}
 
-hipError_t launch_v_amax(const VArgs& a, int BH, hipStream_t s) {
-  RA_V_DISPATCH(k_v_amax);
-  return hipGetLastError();
-}
 
-hipError_t launch_v_quant(const VArgs& a, int BH, hipStream_t s) {
-  RA_V_DISPATCH(k_v_quant);
-  return hipGetLastError();
-}
 
 }  // namespace ra

@@ -117,7 +117,7 @@ def test_fp6_pack_register_hazards():
         if v:
             bad[kern] = v[:3]
     assert n_conv > 0, "no packing conversion found: the scan is not looking at the kernels"
-    producers = [k for k, body in _kernels(asm) if "k_qk" in k and any(b.startswith(CONV) for b in body)]
+    producers = [k for k, body in _kernels(asm) if "k_pass" in k and any(b.startswith(CONV) for b in body)]
     assert producers, "the Q/K producer's E2M3 packing was not found"
     assert not bad, f"packing-conversion register hazards: {bad}"
 
@@ -143,5 +143,5 @@ def test_no_kernel_uses_scratch():
         limit = 16 if (m and m.group(4) == "1") else 0   # key-bias variant
         if z > limit:
             bad.append((n, z))
-    assert any("k_qk" in n for n in names) and any("k_attn_e2m3" in n for n in names)
+    assert any("k_pass" in n for n in names) and any("k_attn_e2m3" in n for n in names)
     assert not bad, f"kernels with a private segment: {bad}"

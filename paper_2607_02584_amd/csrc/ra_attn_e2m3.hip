@@ -102,6 +102,39 @@ __device__ __forceinline__ v6i pack_fp6(v16f lo, v16f hi) {
 
 // Emits nothing; it makes the output tile's registers look read and written
 // here, so the multiplies before it are not sunk past the code after it.
+// Maximum of a chunk's 16 exact scores as eight three-input maxima, seeded
+// with the lowest finite binary32: the seed is below every score, so the
+// chain needs no quieting of its first two inputs, and a chunk whose keys
+// are all masked (-inf) yields the seed, which a valid key of the block (the
+// partial last block has one) outweighs.
+__device__ __forceinline__ float chunk_max(const v16f& x) {
+  float mx = -3.40282347e38f;
+#pragma unroll
+  for (int r = 0; r < 16; r += 2) mx = fmaxf(fmaxf(mx, x[r]), x[r + 1]);
+  return mx;
+}
+
+// O' registers r of the four output tiles times ab of lane q0(r) = 8 (r / 4) + r % 4
+// of the register's own 32-lane half (ds_swizzle in bitmask mode: and 0, or q0),
+// for the registers whose row moved its maximum
+template <int R>
+__device__ __forceinline__ void rescale_row(v16f (&o)[4], float ab, unsigned long long moved) {
+  constexpr int q0 = 8 * (R >> 2) + (R & 3);
+  if ((moved >> q0) & 0x11ull) {
+    const float ar = __int_as_float(__builtin_amdgcn_ds_swizzle(__float_as_int(ab), q0 << 5));
+#pragma unroll
+    for (int mt = 0; mt < 4; ++mt) o[mt][R] = __fmul_rn(o[mt][R], ar);
+  }
+}
+template <int G>
+__device__ __forceinline__ void rescale_group(v16f (&o)[4], float ab, unsigned long long moved) {
+  if (!((moved >> (8 * G)) & 0xFFull)) return;   // rows 8G .. 8G+7 kept their maximum
+  rescale_row<4 * G>(o, ab, moved);
+  rescale_row<4 * G + 1>(o, ab, moved);
+  rescale_row<4 * G + 2>(o, ab, moved);
+  rescale_row<4 * G + 3>(o, ab, moved);
+}
+
 __device__ __forceinline__ void pin(v16f (&o)[4]) {
 #if defined(__HIP_DEVICE_COMPILE__)
   asm volatile("" : "+v"(o[0]), "+v"(o[1]), "+v"(o[2]), "+v"(o[3]));
@@ -384,10 +417,7 @@ __global__ __launch_bounds__(kThreads, 8 / kWaves) void k_attn_e2m3(AttnArgs a) 
       float cm[NCH];
 #pragma unroll
       for (int ch = 0; ch < NCH; ++ch) {
-        float mx = fmaxf(fmaxf(s[ch][0], s[ch][1]), s[ch][2]);
-#pragma unroll
-        for (int r = 3; r < 15; r += 2) mx = fmaxf(fmaxf(mx, s[ch][r]), s[ch][r + 1]);
-        cm[ch] = fmaxf(mx, s[ch][15]);
+        cm[ch] = chunk_max(s[ch]);
       }
       float mx = cm[0];
 #pragma unroll
@@ -400,11 +430,7 @@ __global__ __launch_bounds__(kThreads, 8 / kWaves) void k_attn_e2m3(AttnArgs a) 
 #pragma unroll
       for (int ch = 0; ch < NCH; ++ch) {
         cch[ch] = __fmul_rn(cq, sKc[buf][ch]);
-        float mx = fmaxf(fmaxf(s[ch][0], s[ch][1]), s[ch][2]);
-#pragma unroll
-        for (int r = 3; r < 15; r += 2) mx = fmaxf(fmaxf(mx, s[ch][r]), s[ch][r + 1]);
-        mx = fmaxf(mx, s[ch][15]);
-        tmax = fmaxf(tmax, __fmul_rn(mx, cch[ch]));
+        tmax = fmaxf(tmax, __fmul_rn(chunk_max(s[ch]), cch[ch]));
       }
     } else {
 #pragma unroll
@@ -429,19 +455,15 @@ __global__ __launch_bounds__(kThreads, 8 / kWaves) void k_attn_e2m3(AttnArgs a) 
     // wave half, 4 more in the upper) moved their maximum are rescaled
     const unsigned long long moved = __ballot(alpha != 1.0f);
     if (moved) {
-#pragma unroll
-      for (int g = 0; g < 4; ++g) {
-        if (!((moved >> (8 * g)) & 0xFFull)) continue;   // rows 8g .. 8g+7 kept their maximum
-#pragma unroll
-        for (int r = 4 * g; r < 4 * g + 4; ++r) {
-          const int q0 = 8 * (r >> 2) + (r & 3);
-          if ((moved >> q0) & 0x11ull) {
-            const float ar = __shfl(alpha, q0 + 4 * hh);
-#pragma unroll
-            for (int mt = 0; mt < 4; ++mt) of[mt][r] = __fmul_rn(of[mt][r], ar);
-          }
-        }
-      }
+      // ab: lane 32 hh + i holds alpha of query i + 4 hh (a row rotation by 4
+      // lanes in the upper half; the lanes read below never leave their row
+      // of 16), so register r's factor is lane q0 of its own 32-lane half
+      const float ab = __int_as_float(
+          __builtin_amdgcn_update_dpp(__float_as_int(alpha), __float_as_int(alpha), 0x12C, 0xC, 0xF, false));
+      rescale_group<0>(of, ab, moved);
+      rescale_group<1>(of, ab, moved);
+      rescale_group<2>(of, ab, moved);
+      rescale_group<3>(of, ab, moved);
     }
     __builtin_amdgcn_sched_barrier(0);
 

@@ -40,6 +40,14 @@
 // queries, so the per-channel V scale ratio is one register per tile, and
 // alpha reaches the query rows by a lane permute when some row's max moved.
 //
+// Software pipeline over blocks: once a 64-key group's probabilities are
+// packed, its two score registers take the next block's scores of the same
+// chunks, and those score products run on the matrix core while the vector
+// unit computes the following group's probabilities (the PV products of the
+// packed group likewise), so a block starts with its scores in registers.
+// Three LDS tile buffers hold blocks j, j + 1 (read by the early score
+// products) and j + 2 (written during block j); one barrier per block.
+//
 // The plain kernels are built from this file; ra_attn_e2m3_debug.hip builds
 // the debug-dump kernels from the same source (two translation units compile
 // in parallel).
@@ -100,8 +108,6 @@ __device__ __forceinline__ v6i pack_fp6(v16f lo, v16f hi) {
   return r;
 }
 
-// Emits nothing; it makes the output tile's registers look read and written
-// here, so the multiplies before it are not sunk past the code after it.
 // Maximum of a chunk's 16 exact scores as eight three-input maxima, seeded
 // with the lowest finite binary32: the seed is below every score, so the
 // chain needs no quieting of its first two inputs, and a chunk whose keys
@@ -135,14 +141,6 @@ __device__ __forceinline__ void rescale_group(v16f (&o)[4], float ab, unsigned l
   rescale_row<4 * G + 3>(o, ab, moved);
 }
 
-__device__ __forceinline__ void pin(v16f (&o)[4]) {
-#if defined(__HIP_DEVICE_COMPILE__)
-  asm volatile("" : "+v"(o[0]), "+v"(o[1]), "+v"(o[2]), "+v"(o[3]));
-#else
-  (void)o;
-#endif
-}
-
 // 24-byte record -> operand registers (6 used dwords)
 __device__ __forceinline__ v8i load_rec(const uint8_t* p) {
   const uint2 a = *reinterpret_cast<const uint2*>(p);
@@ -154,10 +152,10 @@ __device__ __forceinline__ v8i load_rec(const uint8_t* p) {
 
 // K and V code tiles of one block go global -> registers -> LDS: every thread
 // moves three 16-byte (KV = 128) or 8-byte (KV = 64) pieces of each, adjacent
-// threads adjacent pieces.  The global loads of block j + 2 are issued at the
-// end of block j and written to LDS in the middle of block j + 1 (after its
-// row maxima), so their latency overlaps the barrier and the score products
-// (and the pieces are dead again while the probabilities take the registers).
+// threads adjacent pieces.  The global loads of block j + 3 are issued at the
+// end of block j and written to LDS in block j + 1, once its first 64-key
+// group is packed, so their latency overlaps the barrier, the row maxima and
+// the first probabilities.
 template <int KV>
 struct TilePiece {
   // 16-byte (KV = 128) or 8-byte (KV = 64) pieces as 32-bit vectors, six per thread
@@ -193,8 +191,8 @@ __global__ __launch_bounds__(kThreads, 8 / kWaves) void k_attn_e2m3(AttnArgs a) 
   constexpr int NCH = KV / 32;   // 32-key chunks
   constexpr int NG = KV / 64;    // 64-key groups (one PV instruction each)
   constexpr int KB = KV * 96;    // bytes of K (and of V) codes per block
-  __shared__ __align__(16) uint8_t sK[2][KB];
-  __shared__ __align__(16) uint8_t sV[2][KB];
+  __shared__ __align__(16) uint8_t sK[3][KB];
+  __shared__ __align__(16) uint8_t sV[3][KB];
   __shared__ __align__(16) float sR[2][kD];   // V scale ratio w_old / w_new, channel 32 mt + j at 4 j + mt
   __shared__ __align__(16) float sW[kD];      // final V scale per channel
   __shared__ __align__(16) float sKs[2][KTOK ? KV : 1];
@@ -295,77 +293,74 @@ __global__ __launch_bounds__(kThreads, 8 / kWaves) void k_attn_e2m3(AttnArgs a) 
   int vr = 0;
 
   static_assert(KB == 3 * kThreads * static_cast<int>(sizeof(typename TilePiece<KV>::T)), "three pieces per thread");
+  // Three tile buffers: block j's tiles sit in buffer j % 3; block j + 1's are
+  // already in LDS while block j is processed (its score products run during
+  // block j's probabilities), and block j + 2's are written during block j.
+  const int t1 = nblocks > 1 ? 1 : 0, t2 = nblocks > 2 ? 2 : nblocks - 1;
   TilePiece<KV> tp;
   tp.load(kbase, vbase, tid);
   tp.store(sK[0], sV[0], tid);
-  tp.load(kbase + (nblocks > 1 ? KB : 0), vbase + (nblocks > 1 ? KB : 0), tid);
+  tp.load(kbase + t1 * KB, vbase + t1 * KB, tid);
+  tp.store(sK[1], sV[1], tid);
+  tp.load(kbase + t2 * KB, vbase + t2 * KB, tid);
   store_aux(0, 0, fetch_aux(0));
   Aux pf{0.f, 0.f, 0.f};
   if (nblocks > 1) pf = fetch_aux(1);
   __syncthreads();
 
+  // ---- S^T = K Q^T (exact integer scores in binary32), chunks c0 and c0 + 1
+  //      of the tile at kt.  s carries the scores of the next block from one
+  //      block to the next. ----
+  v16f s[NCH];
+  auto krec = [&](const uint8_t* kt, int ch, int kc) {
+    return load_rec(&kt[(((ch * 2 + kc) * 2 + hh) * 32 + j) * 24]);
+  };
+  auto score_pair = [&](const v8i (&kr)[4], int c0) {
+    v16f z;
+#pragma unroll
+    for (int r = 0; r < 16; ++r) z[r] = 0.f;
+    s[c0] = mfma6(kr[0], qop[0], z);
+    s[c0 + 1] = mfma6(kr[1], qop[0], z);
+    s[c0] = mfma6(kr[2], qop[1], s[c0]);
+    s[c0 + 1] = mfma6(kr[3], qop[1], s[c0 + 1]);
+  };
+  // the four K records of chunks c0, c0 + 1 (channel half kc = t / 2), one
+  // record per scheduling region so reads of two records are not merged
+  auto read_kpair = [&](v8i (&kr)[4], const uint8_t* kt, int c0) {
+#pragma unroll
+    for (int t = 0; t < 4; ++t) {
+      kr[t] = krec(kt, c0 + (t & 1), t >> 1);
+      __builtin_amdgcn_sched_barrier(0);
+    }
+  };
+  {
+    v8i kr[4];
+#pragma unroll
+    for (int c0 = 0; c0 < NCH; c0 += 2) {
+      read_kpair(kr, sK[0], c0);
+      score_pair(kr, c0);
+    }
+  }
+  int tb = 0;   // buffer of the current block's tiles (block index mod 3)
+
   // One block of KV keys.  MASKED (keys past N) only for the partial last
   // block, which runs outside the main loop so the full blocks carry no masking.
-  auto step = [&](int jb, auto masked_tag) {
+  // MORE: a next block exists (every block but the last); as a template
+  // argument it keeps the step one basic block from the probabilities on, so
+  // the products stay where they are placed between them.
+  auto step = [&](int jb, auto masked_tag, auto more_tag) {
     constexpr bool MASKED = decltype(masked_tag)::value;
-    const int buf = jb & 1;
+    constexpr bool more = decltype(more_tag)::value;
+    const int buf = jb & 1;   // side-data buffers
     const int key0 = jb * KV;
-    if (jb + 1 < nblocks) {
+    const int tbn = tb == 2 ? 0 : tb + 1;   // next block's tiles
+    const int tbw = tbn == 2 ? 0 : tbn + 1; // tiles written in this block (block j + 2)
+    if (more) {
       store_aux(jb + 1, buf ^ 1, pf);
       if (jb + 2 < nblocks) pf = fetch_aux(jb + 2);
     }
     __builtin_amdgcn_sched_barrier(0);
 
-    // ---- S^T = K Q^T: exact integer scores in binary32.  The first channel
-    //      half of every chunk goes first, so the two products into one
-    //      accumulator are NCH instructions apart; operands are read from LDS
-    //      two instructions ahead. ----
-    v16f s[NCH];
-    constexpr int NQ = 2 * NCH;
-    auto krec = [&](int t) {
-      const int ch = t % NCH, kc = t / NCH;
-      return load_rec(&sK[buf][(((ch * 2 + kc) * 2 + hh) * 32 + j) * 24]);
-    };
-    // The V scale ratio of a new group rescales O' (register r of tile mt is
-    // channel 32 mt + j) while the score products run: it does not depend on
-    // S, so its multiplies fill the matrix-core latency.  They are issued
-    // unconditionally (by 1 within a V group: exact) so that they stay in the
-    // straight-line code between the products; O' is rescaled by the V ratio
-    // before alpha, as before.
-    const bool vchange = vr == 0 && jb > 0;   // first block of a new V group
-    if (++vr == a.v_bpg) vr = 0;
-    float4 rr = make_float4(1.f, 1.f, 1.f, 1.f);
-    if (vchange) rr = *reinterpret_cast<const float4*>(&sR[buf][4 * j]);
-    constexpr int RPS = 16 / NQ;   // O' registers rescaled per score product
-    // (one record per scheduling region: reads of two records are not merged)
-    v8i ka = krec(0);
-    __builtin_amdgcn_sched_barrier(0);
-    v8i kb = krec(1);
-    __builtin_amdgcn_sched_barrier(0);
-#pragma unroll
-    for (int t = 0; t < NQ; ++t) {
-      const v8i kn = (t + 2 < NQ) ? krec(t + 2) : ka;
-      const int ch = t % NCH;
-      if (t < NCH) {
-        v16f z;
-#pragma unroll
-        for (int r = 0; r < 16; ++r) z[r] = 0.f;
-        s[ch] = mfma6(ka, qop[0], z);
-      } else {
-        s[ch] = mfma6(ka, qop[1], s[ch]);
-      }
-#pragma unroll
-      for (int r = RPS * t; r < RPS * (t + 1); ++r) {
-        of[0][r] = __fmul_rn(of[0][r], rr.x);
-        of[1][r] = __fmul_rn(of[1][r], rr.y);
-        of[2][r] = __fmul_rn(of[2][r], rr.z);
-        of[3][r] = __fmul_rn(of[3][r], rr.w);
-      }
-      pin(of);
-      ka = kb;
-      kb = kn;
-      __builtin_amdgcn_sched_barrier(0);
-    }
     // key of accumulator register r in chunk ch: key0 + 32*ch + 8*(r/4) + 4*hh + r%4
     if (DEBUG) {
       if (bh == a.dbg_bh && qrow >= a.dbg_row0 && qrow < a.dbg_row0 + a.dbg_rows && a.dbg_s) {
@@ -387,8 +382,25 @@ __global__ __launch_bounds__(kThreads, 8 / kWaves) void k_attn_e2m3(AttnArgs a) 
           if (key0 + ch * 32 + 8 * (r >> 2) + 4 * hh + (r & 3) >= N) s[ch][r] = -INFINITY;
     }
 
+    // The V scale ratio of a new group rescales O' (register r of tile mt is
+    // channel 32 mt + j); the multiplies do not depend on S and fill the
+    // latency of the maximum's dependent chain.  They are issued
+    // unconditionally (by 1 within a V group: exact); O' is rescaled by the V
+    // ratio before alpha.
+    const bool vchange = vr == 0 && jb > 0;   // first block of a new V group
+    if (++vr == a.v_bpg) vr = 0;
+    float4 rr = make_float4(1.f, 1.f, 1.f, 1.f);
+    if (vchange) rr = *reinterpret_cast<const float4*>(&sR[buf][4 * j]);
+#pragma unroll
+    for (int r = 0; r < 16; ++r) {
+      of[0][r] = __fmul_rn(of[0][r], rr.x);
+      of[1][r] = __fmul_rn(of[1][r], rr.y);
+      of[2][r] = __fmul_rn(of[2][r], rr.z);
+      of[3][r] = __fmul_rn(of[3][r], rr.w);
+    }
+
     // ---- block row maximum of fl(S * c) (c >= 0, so it is fl(max S * c);
-    //      a fully masked chunk gives -inf, or NaN when c == 0, which fmax ignores) ----
+    //      a fully masked chunk gives the seed of chunk_max, far below) ----
     float cch[NCH];
     float tmax = -INFINITY;
     if (QB) {
@@ -414,14 +426,9 @@ __global__ __launch_bounds__(kThreads, 8 / kWaves) void k_attn_e2m3(AttnArgs a) 
       }
     } else if (!KTOK && a.k_group >= KV) {
       // one K scale for the whole block: a single product after the maximum
-      float cm[NCH];
+      float mx = chunk_max(s[0]);
 #pragma unroll
-      for (int ch = 0; ch < NCH; ++ch) {
-        cm[ch] = chunk_max(s[ch]);
-      }
-      float mx = cm[0];
-#pragma unroll
-      for (int ch = 1; ch < NCH; ++ch) mx = fmaxf(mx, cm[ch]);
+      for (int ch = 1; ch < NCH; ++ch) mx = fmaxf(mx, chunk_max(s[ch]));
       const float c0 = __fmul_rn(cq, sKc[buf][0]);
 #pragma unroll
       for (int ch = 0; ch < NCH; ++ch) cch[ch] = c0;
@@ -468,50 +475,49 @@ __global__ __launch_bounds__(kThreads, 8 / kWaves) void k_attn_e2m3(AttnArgs a) 
     __builtin_amdgcn_sched_barrier(0);
 
     // ---- P, codes u = rint(15 P) packed as E2M3 u/8, row sums, PV.  15 P
-    //      overwrites the score's register, so the 32 converter
-    //      inputs of a 64-key group are the two chunks' accumulators in place:
-    //      element 2i + c2 of the packed operand is register i of chunk 2gg + c2. ----
-    // the next block's tiles go to LDS here, once this block's maximum is known
-    if (jb + 1 < nblocks) tp.store(sK[buf ^ 1], sV[buf ^ 1], tid);
-    __builtin_amdgcn_sched_barrier(0);
+    //      overwrites the score's register, so the 32 converter inputs of a
+    //      64-key group are the two chunks' accumulators in place: element
+    //      2i + c2 of the packed operand is register i of chunk 2gg + c2.
+    //      Once a group is packed, its two score registers take the next
+    //      block's scores of the same chunks; the products of group gg (PV,
+    //      and the next block's scores) are interleaved with the
+    //      probabilities of group gg + 1. ----
     float ls[4];   // independent partial sums, started by the first four values
+    // probabilities of registers 4 q .. 4 q + 3 of chunk ch
+    auto probs4 = [&](int ch, int q) {
 #pragma unroll
-    for (int gg = 0; gg < NG; ++gg) {
-      // the group's four V records (B operands of O = P V~) are read before
-      // its probabilities, so the LDS latency is hidden behind them; one
-      // record per scheduling region, so reads of two records are not merged
-      // into one instruction (which costs register moves)
-      v8i vrec[4];
+      for (int r = 4 * q; r < 4 * q + 4; ++r) {
+        float P;   // pscale * P
+        if (QB) {
+          P = __builtin_amdgcn_exp2f(__fsub_rn(s[ch][r], mq));
+        } else {
+          float c;
+          if (KTOK) c = __fmul_rn(cq, sKs[buf][ch * 32 + 8 * (r >> 2) + 4 * hh + (r & 3)]);
+          else c = cch[ch];
+          P = __builtin_amdgcn_exp2f(__fmaf_rn(s[ch][r], c, -mq));
+        }
+        if (MASKED && s[ch][r] == -INFINITY) P = 0.f;
+        const float lv = LQ ? __builtin_rintf(P) : P;
+        if (ch == 0 && r < 4) ls[r] = lv;
+        else ls[r & 3] += lv;
+        s[ch][r] = P;
+      }
+    };
+    v8i vrec[4];   // V records of the group in flight (B operands of O = P V~)
+    v8i kr[4];     // K records of the next block's chunk pair
+    v8i B;         // packed codes of the group in flight (A operand of O = P V~)
+    auto read_vrecs = [&](int gg) {
 #pragma unroll
       for (int t = 0; t < 4; ++t) {
-        vrec[t] = load_rec(&sV[buf][(((gg * 4 + t) * 2 + hh) * 32 + j) * 24]);
+        vrec[t] = load_rec(&sV[tb][(((gg * 4 + t) * 2 + hh) * 32 + j) * 24]);
         __builtin_amdgcn_sched_barrier(0);
       }
-#pragma unroll
-      for (int c2 = 0; c2 < 2; ++c2) {
-        const int ch = 2 * gg + c2;
-#pragma unroll
-        for (int r = 0; r < 16; ++r) {
-          float P;   // pscale * P
-          if (QB) {
-            P = __builtin_amdgcn_exp2f(__fsub_rn(s[ch][r], mq));
-          } else {
-            float c;
-            if (KTOK) c = __fmul_rn(cq, sKs[buf][ch * 32 + 8 * (r >> 2) + 4 * hh + (r & 3)]);
-            else c = cch[ch];
-            P = __builtin_amdgcn_exp2f(__fmaf_rn(s[ch][r], c, -mq));
-          }
-          if (MASKED && s[ch][r] == -INFINITY) P = 0.f;
-          const float lv = LQ ? __builtin_rintf(P) : P;
-          if (gg == 0 && c2 == 0 && r < 4) ls[r] = lv;
-          else ls[r & 3] += lv;
-          s[ch][r] = P;
-        }
-      }
+    };
+    auto pack_group = [&](int gg) {
       // E2M3(rint(15 P) / 8): the conversion divides by the power-of-two
       // scale exactly and rounds to nearest even on the uniform 1/8 grid
       const v6i pk6 = pack_fp6(s[2 * gg], s[2 * gg + 1]);
-      const v8i B = v8i{pk6[0], pk6[1], pk6[2], pk6[3], pk6[4], pk6[5], 0, 0};   // A operand of O = P V~
+      B = v8i{pk6[0], pk6[1], pk6[2], pk6[3], pk6[4], pk6[5], 0, 0};
       if (DEBUG) {
         if (bh == a.dbg_bh && qrow >= a.dbg_row0 && qrow < a.dbg_row0 + a.dbg_rows && a.dbg_u) {
           const size_t rowo = static_cast<size_t>(qrow - a.dbg_row0);
@@ -527,25 +533,77 @@ __global__ __launch_bounds__(kThreads, 8 / kWaves) void k_attn_e2m3(AttnArgs a) 
             }
         }
       }
+    };
+
+    read_vrecs(0);
 #pragma unroll
-      for (int t = 0; t < 4; ++t) of[t] = mfma6(B, vrec[t], of[t]);
+    for (int q = 0; q < 8; ++q) probs4(q >> 2, q & 3);
+    pack_group(0);
+    __builtin_amdgcn_sched_barrier(0);
+    // block j + 2's tiles into the buffer block j - 1 used
+    tp.store(sK[tbw], sV[tbw], tid);
+    __builtin_amdgcn_sched_barrier(0);
+    if (more) read_kpair(kr, sK[tbn], 0);
+#pragma unroll
+    for (int gg = 1; gg < NG; ++gg) {
+      // products of group gg - 1, one per region with four probabilities of group gg
+#pragma unroll
+      for (int t = 0; t < 4; ++t) {
+        of[t] = mfma6(B, vrec[t], of[t]);
+        probs4(2 * gg, t);
+        __builtin_amdgcn_sched_barrier(0);
+      }
+      read_vrecs(gg);
+      if (more) {
+        v16f z;
+#pragma unroll
+        for (int r = 0; r < 16; ++r) z[r] = 0.f;
+        const int c0 = 2 * gg - 2;
+        s[c0] = mfma6(kr[0], qop[0], z);
+        probs4(2 * gg + 1, 0);
+        __builtin_amdgcn_sched_barrier(0);
+        s[c0 + 1] = mfma6(kr[1], qop[0], z);
+        probs4(2 * gg + 1, 1);
+        __builtin_amdgcn_sched_barrier(0);
+        s[c0] = mfma6(kr[2], qop[1], s[c0]);
+        probs4(2 * gg + 1, 2);
+        __builtin_amdgcn_sched_barrier(0);
+        s[c0 + 1] = mfma6(kr[3], qop[1], s[c0 + 1]);
+        probs4(2 * gg + 1, 3);
+        __builtin_amdgcn_sched_barrier(0);
+      } else {
+#pragma unroll
+        for (int q = 0; q < 4; ++q) probs4(2 * gg + 1, q);
+        __builtin_amdgcn_sched_barrier(0);
+      }
+      if (more) read_kpair(kr, sK[tbn], 2 * gg);
+      pack_group(gg);
       __builtin_amdgcn_sched_barrier(0);
     }
+    // products of the last group
+#pragma unroll
+    for (int t = 0; t < 4; ++t) of[t] = mfma6(B, vrec[t], of[t]);
+    if (more) score_pair(kr, NCH - 2);
+    __builtin_amdgcn_sched_barrier(0);
     l = __fmaf_rn(l, alpha, (ls[0] + ls[1]) + (ls[2] + ls[3]));
     if (DEBUG && a.dbg_m && hh == 0 && bh == a.dbg_bh && qrow >= a.dbg_row0 && qrow < a.dbg_row0 + a.dbg_rows)
       a.dbg_m[static_cast<size_t>(qrow - a.dbg_row0) * nblocks + jb] = mnew;
     {
       // unconditional (the last blocks reload the final tile), so the pieces
       // are not live through the block body
-      const size_t nb2 = static_cast<size_t>(jb + 2 < nblocks ? jb + 2 : nblocks - 1) * KB;
-      tp.load(kbase + nb2, vbase + nb2, tid);
+      const size_t nb3 = static_cast<size_t>(jb + 3 < nblocks ? jb + 3 : nblocks - 1) * KB;
+      tp.load(kbase + nb3, vbase + nb3, tid);
     }
+    tb = tbn;
     __syncthreads();
   };
 
-  const int nfull = N / KV;
-  for (int jb = 0; jb < nfull; ++jb) step(jb, std::integral_constant<bool, false>());
-  if (nfull < nblocks) step(nfull, std::integral_constant<bool, true>());
+  // every block but the last is full; the last runs with the key checks
+  // (which mask nothing when it is full)
+  using kNo = std::integral_constant<bool, false>;
+  using kYes = std::integral_constant<bool, true>;
+  for (int jb = 0; jb + 1 < nblocks; ++jb) step(jb, kNo(), kYes());
+  step(nblocks - 1, kYes(), kNo());
 
   if (tid < kD) sW[tid] = wcur;
   __syncthreads();

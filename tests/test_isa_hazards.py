@@ -128,9 +128,7 @@ def test_no_kernel_uses_scratch():
     memory: a small array indexed with a run-time value (or a by-value argument
     indexed that way) lands there and costs a round trip to memory per access.
     Exempt: the debug instantiations of the attention kernel (they dump S, P
-    codes and maxima for the parity tests and spill freely) and, up to 16 bytes,
-    the key-bias (Q smoothing) attention instantiations, which spill two
-    registers at the 256-register limit."""
+    codes and maxima for the parity tests and spill freely)."""
     asm = _asm()
     names = re.findall(r"\.amdhsa_kernel\s+(\S+)", asm)
     sizes = [int(z) for z in re.findall(r"\.amdhsa_private_segment_fixed_size\s+(\d+)", asm)]
@@ -140,8 +138,7 @@ def test_no_kernel_uses_scratch():
         m = re.search(r"k_attn_e2m3ILi\d+ELb([01])ELb([01])ELb([01])ELb([01])ELb([01])E", n)
         if m and m.group(3) == "1":
             continue                      # debug dump instantiation
-        limit = 16 if (m and m.group(4) == "1") else 0   # key-bias variant
-        if z > limit:
+        if z > 0:
             bad.append((n, z))
     assert any("k_pass" in n for n in names) and any("k_attn_e2m3" in n for n in names)
     assert not bad, f"kernels with a private segment: {bad}"

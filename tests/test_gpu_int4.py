@@ -116,9 +116,33 @@ def _workloads():
 @pytest.mark.parametrize("case", CASES)
 def test_int4_codes_scores_and_output(ora, wname, case, fmt):
     """Producer codes/scales/means bit-exact; S, m bit-exact; P codes up to ties; O <= 2e-3."""
-    torch, ra = _torch(), _ra()
     from paper_2607_02584_amd import datagen as dg
     w = dg.WORKLOADS["c1"] if wname == "c1" else _small_ragged(wname)
+    _check_case(ora, w, wname, case, fmt)
+
+
+# sequence lengths around whole numbers of 64- and 128-key blocks: one, two,
+# three and four blocks, each full and with a partial last block (the kernels
+# compute a block's scores during the previous block, so the first and last
+# blocks take their own paths)
+BOUNDARY_GRIDS = {64: (1, 8, 8), 128: (2, 8, 8), 129: (3, 43, 1), 192: (3, 8, 8), 256: (4, 8, 8),
+                  257: (1, 1, 257), 384: (6, 8, 8), 385: (5, 7, 11), 512: (8, 8, 8)}
+
+
+@pytest.mark.parametrize("fmt", ["e2m3", "int4"])
+@pytest.mark.parametrize("n", list(BOUNDARY_GRIDS))
+@pytest.mark.parametrize("kv", [64, 128])
+def test_block_count_boundaries(ora, n, kv, fmt):
+    """The same bars at every block count from one to four, full and partial last blocks."""
+    from paper_2607_02584_amd import datagen as dg
+    T, Hg, W = BOUNDARY_GRIDS[n]
+    w = dg.small_workload(f"n{n}", T, Hg, W, H=1, seed=40 + n)
+    assert w.N == n
+    _check_case(ora, w, f"n{n}", (1, 128, 128, 128, kv, 0, 3), fmt)
+
+
+def _check_case(ora, w, wname, case, fmt):
+    torch, ra = _torch(), _ra()
     rot, qg, kg, vg, kv, pq, sm, *rest = case
     vrot = rest[0] if rest else 0
     lq = rest[1] if len(rest) > 1 else 0

@@ -22,11 +22,14 @@
 //    (group of tokens, channel) (V): s = amax/7, code = clamp(rint(z*7/amax)).
 //
 // Work decomposition: one workgroup of 256 threads per tile of 128 tokens of
-// one head.  Q/K: thread t handles channels 16*(t%8) .. +15 of the rows
-// t/8 + 32p (p = 0..3), each row read as eight 32-byte pieces, with the RoPE
+// one head.  Q/K: thread t handles channels 32*(t%4) .. +31 of the rows
+// t/4 + 64p (p = 0, 1), each row read as four 64-byte pieces, with the RoPE
 // table rows the tile needs staged in LDS.  V: thread t handles channels
 // 4*(t%32) .. +3 of the rows t/32 + 8p (16 rows), each row read as 32 8-byte
-// pieces.  These kernels are HBM-bound.
+// pieces.  A pass is bound by its HBM traffic and by the per-element vector
+// work (RoPE, rotation, quantization, packing) together: the jobs of one
+// pass share the grid so that the vector-heavy Q/K tiles and the lighter V
+// tiles run side by side.
 #include "ra_internal.h"
 #include "rotate_attn.h"
 

@@ -30,6 +30,8 @@
 // work (RoPE, rotation, quantization, packing) together: the jobs of one
 // pass share the grid so that the vector-heavy Q/K tiles and the lighter V
 // tiles run side by side.
+#include <type_traits>
+
 #include "ra_internal.h"
 #include "rotate_attn.h"
 
@@ -247,6 +249,9 @@ __device__ __forceinline__ void rope_item(const RopeTables& t, int N, int n0, co
   const int W = t.grid[2], Hg = t.grid[1], HW = Hg * W;
   StagePlan sp{};
   if (STAGED) sp = stage_plan(t, n0, N);
+  // only the last tile has rows past N: the zeroing below is skipped (a
+  // uniform branch) everywhere else
+  const bool tail = n0 + kTile > N;
 #pragma unroll
   for (int p = 0; p < kQkPasses; ++p) {
     const int nl = 64 * p + r64, n = n0 + nl;
@@ -280,9 +285,11 @@ __device__ __forceinline__ void rope_item(const RopeTables& t, int N, int n0, co
       y[2 * k] = __fmaf_rn(x1, g.z, __fmul_rn(x0, g.x));
       y[2 * k + 1] = __fmaf_rn(x1, g.w, __fmul_rn(x0, g.y));
     }
-    if (n >= N) {
+    if (tail) {
+      if (n >= N) {
 #pragma unroll
-      for (int c = 0; c < 32; ++c) y[c] = 0.f;
+        for (int c = 0; c < 32; ++c) y[c] = 0.f;
+      }
     }
     if constexpr (ROT == RA_ROT_HALF) {
       // output pair P of axis a (first channel o_a) mixes RoPE channels
@@ -304,9 +311,11 @@ __device__ __forceinline__ void rope_item(const RopeTables& t, int N, int n0, co
         y[2 * k] = __fmaf_rn(bv, r.z, __fmul_rn(av, r.x));
         y[2 * k + 1] = __fmaf_rn(bv, r.w, __fmul_rn(av, r.y));
       }
-      if (n >= N) {
+      if (tail) {
+        if (n >= N) {
 #pragma unroll
-        for (int c = 0; c < 32; ++c) y[c] = 0.f;
+          for (int c = 0; c < 32; ++c) y[c] = 0.f;
+        }
       }
     } else if constexpr (ROT == RA_ROT_HADAMARD) {
       // y <- y H_128, widest stride first: strides 64 and 32 pair the lanes
@@ -560,26 +569,34 @@ __device__ __forceinline__ void load_v_tile(const VArgs& a, int bh, int tile, fl
     const int n = tile * kTile + p * 8 + rr;
     raw[p] = *reinterpret_cast<const uint2*>(xb + static_cast<size_t>(n < a.N ? n : a.N - 1) * kD + 4 * cl);
   }
-  for (int p = 0; p < 16; ++p) {
-    const int n = tile * kTile + p * 8 + rr;
-    float x[4] = {0.f, 0.f, 0.f, 0.f};
-    if (n < a.N) {
-      x[0] = h2f<F16>(static_cast<uint16_t>(raw[p].x & 0xffff));
-      x[1] = h2f<F16>(static_cast<uint16_t>(raw[p].x >> 16));
-      x[2] = h2f<F16>(static_cast<uint16_t>(raw[p].y & 0xffff));
-      x[3] = h2f<F16>(static_cast<uint16_t>(raw[p].y >> 16));
-    }
-    // online V rotation (Sec. 4.3): the row times H, before smoothing
-    if constexpr (VHAD) hadamard_row(x, cl);
-    if (n < a.N && a.center) {
-      x[0] = __fsub_rn(x[0], m.x);
-      x[1] = __fsub_rn(x[1], m.y);
-      x[2] = __fsub_rn(x[2], m.z);
-      x[3] = __fsub_rn(x[3], m.w);
-    }
+  // rows past N (only in the last tile: a uniform choice between two copies
+  // of the loop) are zero and not centred
+  auto rows = [&](auto tail_tag) {
+    constexpr bool TAIL = decltype(tail_tag)::value;
+    for (int p = 0; p < 16; ++p) {
+      const int n = tile * kTile + p * 8 + rr;
+      const bool in = !TAIL || n < a.N;
+      float x[4] = {0.f, 0.f, 0.f, 0.f};
+      if (in) {
+        x[0] = h2f<F16>(static_cast<uint16_t>(raw[p].x & 0xffff));
+        x[1] = h2f<F16>(static_cast<uint16_t>(raw[p].x >> 16));
+        x[2] = h2f<F16>(static_cast<uint16_t>(raw[p].y & 0xffff));
+        x[3] = h2f<F16>(static_cast<uint16_t>(raw[p].y >> 16));
+      }
+      // online V rotation (Sec. 4.3): the row times H, before smoothing
+      if constexpr (VHAD) hadamard_row(x, cl);
+      if (in && a.center) {
+        x[0] = __fsub_rn(x[0], m.x);
+        x[1] = __fsub_rn(x[1], m.y);
+        x[2] = __fsub_rn(x[2], m.z);
+        x[3] = __fsub_rn(x[3], m.w);
+      }
 #pragma unroll
-    for (int c = 0; c < 4; ++c) z[p][c] = x[c];
-  }
+      for (int c = 0; c < 4; ++c) z[p][c] = x[c];
+    }
+  };
+  if ((tile + 1) * kTile > a.N) rows(std::integral_constant<bool, true>());
+  else rows(std::integral_constant<bool, false>());
 }
 
 // LDS: 8 x 128 binary64.

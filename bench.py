@@ -190,9 +190,28 @@ def main():
         torch.cuda.synchronize()
         log(f"profile run done (copy kernel moved {COPY_BYTES} bytes each way)")
         return
-    for _ in range(args.warmup):
-        step()
+    wev = [tuple(torch.cuda.Event(enable_timing=True) for _ in range(3)) for _ in range(max(args.warmup, 1))]
+    for i in range(args.warmup):
+        step(wev[i])
     torch.cuda.synchronize()
+    est_ms = wev[args.warmup - 1][0].elapsed_time(wev[args.warmup - 1][1]) if args.warmup > 0 else 5.0
+    # The shader clock while the attention kernel runs back to back for about
+    # one second, sampled in the second half.  This runs before the timed
+    # steps: the first launches of a cold GPU ramp the clock up (the first ten
+    # or so run up to 15 % slower), and the fallback below is timed after it,
+    # so both paths are timed at the settled clock.
+    read_sclk = sclk_reader(torch, dev)
+    clk = []
+    n_launch = max(40, int(1000.0 / max(est_ms, 0.1)))
+    for _ in range(n_launch):
+        ra.attn_int4(p, bufs["q_codes"], bufs["q_scale"], bufs["k_codes"], bufs["k_scale"], bufs["v_codes"],
+                     bufs["v_scale"], bufs["mu_v"], o)
+    time.sleep(0.4 * n_launch * est_ms * 1e-3)
+    for _ in range(12):
+        time.sleep(0.02)
+        clk.append(read_sclk())
+    torch.cuda.synchronize()
+    clk = [c for c in clk if c is not None]
     log(f"warmup done; timing {args.steps} steps")
     evs = [tuple(torch.cuda.Event(enable_timing=True) for _ in range(3)) for _ in range(args.steps)]
     t0 = torch.cuda.Event(enable_timing=True)
@@ -215,20 +234,6 @@ def main():
                     "the launch stream, mean over the timed steps)"}
     log(f"producers {prod_ms * 1e3:.1f} us: {prod['gbps']} GB/s algorithmic ({prod['frac']:.3f} of HBM peak), "
         f"{prod['gbps_two_pass']} GB/s of bytes moved")
-    # the shader clock while the attention kernel runs back to back for about
-    # one second, sampled in the second half (the first launches ramp it up)
-    read_sclk = sclk_reader(torch, dev)
-    clk = []
-    n_launch = max(40, int(1000.0 / attn_ms))
-    for _ in range(n_launch):
-        ra.attn_int4(p, bufs["q_codes"], bufs["q_scale"], bufs["k_codes"], bufs["k_scale"], bufs["v_codes"],
-                     bufs["v_scale"], bufs["mu_v"], o)
-    time.sleep(0.4 * n_launch * attn_ms * 1e-3)
-    for _ in range(12):
-        time.sleep(0.02)
-        clk.append(read_sclk())
-    torch.cuda.synchronize()
-    clk = [c for c in clk if c is not None]
     gpu = {"name": torch.cuda.get_device_properties(dev).name, "arch": torch.cuda.get_device_properties(dev).gcnArchName,
            "compute_units": torch.cuda.get_device_properties(dev).multi_processor_count,
            "sclk_mhz_under_load": {"median": float(np.median(clk)), "min": min(clk), "max": max(clk),

@@ -272,13 +272,29 @@ def main():
         f_step = a0.elapsed_time(a1) / nrep
         f_attn = float(np.mean([x.elapsed_time(y) for x, y in e]))
         fb_kernel_ms = f_attn
+        # the shader clock under the fallback kernel (untimed, about 0.6 s of
+        # back-to-back launches, sampled in the second half): the matrix-core
+        # heavy kernel may run at another clock than the INT4 kernel
+        nfb = max(20, int(600.0 / f_attn))
+        for _ in range(nfb):
+            ra.attn_fp16(pf, wsf, of)
+        time.sleep(0.4 * nfb * f_attn * 1e-3)
+        fclk = []
+        for _ in range(8):
+            time.sleep(0.02)
+            fclk.append(read_sclk())
+        torch.cuda.synchronize()
+        fclk = [c for c in fclk if c is not None]
         extra = {
             "bf16_fallback": {"op_ms": round(f_step, 4), "kernel_ms": round(f_attn, 4),
                               "kernel_tflops": round(ops / (f_attn * 1e-3) / 1e12, 1),
-                              "kernel_frac_of_bf16_peak": round(ops / (f_attn * 1e-3) / 1e12 / BF16_PEAK_TFLOPS, 4)},
+                              "kernel_frac_of_bf16_peak": round(ops / (f_attn * 1e-3) / 1e12 / BF16_PEAK_TFLOPS, 4),
+                              "sclk_mhz_under_load": {"median": float(np.median(fclk)), "min": min(fclk),
+                                                      "max": max(fclk), "samples": len(fclk)} if fclk else None},
             "speedup_vs_bf16": {"kernel": round(f_attn / attn_ms, 3), "op": round(f_step / ms_step, 3)},
         }
-        log(f"bf16 fallback op {f_step:.3f} ms, kernel {f_attn:.3f} ms; speedup kernel {f_attn / attn_ms:.2f}x")
+        log(f"bf16 fallback op {f_step:.3f} ms, kernel {f_attn:.3f} ms; speedup kernel {f_attn / attn_ms:.2f}x; "
+            f"shader clock under the fallback {extra['bf16_fallback']['sclk_mhz_under_load']}")
 
     # context only: PyTorch's own scaled_dot_product_attention on the same shape,
     # bf16, restricted to its flash / memory-efficient backends (never the math path)

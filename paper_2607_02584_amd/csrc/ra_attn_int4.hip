@@ -30,11 +30,12 @@
 //                 lane's own (applied only when some row of the wave moved its
 //                 maximum); each block's int32 product is converted and scaled
 //                 by its V group's per-channel factor into the binary32 O.
-// K and V codes arrive packed (two per byte); a workgroup stages one KV block
-// in LDS, expanding each nibble c to the int8 value 16c with two bit
-// operations per four codes (the factor 16 is folded into the scales, which is
-// exact).  Q is expanded once per wave to plain int8 codes.  Two workgroups of
-// four waves share a compute unit.
+// K and V codes arrive packed (two per byte); a workgroup stages them in LDS,
+// expanding each nibble c to the int8 value 16c with two bit operations per
+// four codes (the factor 16 is folded into the scales, which is exact).  Q is
+// expanded once per wave to plain int8 codes.  Two workgroups of four waves
+// share a compute unit.  The next block's score products run beside this
+// block's PV conversion (software pipeline), so K is staged two blocks ahead.
 #include <type_traits>
 
 #include "ra_internal.h"
@@ -74,11 +75,12 @@ struct Stage {
   uint2 v[KV / 32];
 };
 
+// the packed K codes of block jk and the packed V codes of block jv
 template <int KV>
-__device__ __forceinline__ void stage_load(const AttnArgs& a, int bh, int jb, Stage<KV>& st) {
+__device__ __forceinline__ void stage_load(const AttnArgs& a, int bh, int jk, int jv, Stage<KV>& st) {
   const int tid = threadIdx.x;
-  const uint8_t* kb = a.kc + static_cast<size_t>(bh) * a.Npad * 64 + static_cast<size_t>(jb) * KV * 64;
-  const uint8_t* vb = a.vc + static_cast<size_t>(bh) * a.Npad * 64 + static_cast<size_t>(jb) * KV * 64;
+  const uint8_t* kb = a.kc + static_cast<size_t>(bh) * a.Npad * 64 + static_cast<size_t>(jk) * KV * 64;
+  const uint8_t* vb = a.vc + static_cast<size_t>(bh) * a.Npad * 64 + static_cast<size_t>(jv) * KV * 64;
 #pragma unroll
   for (int i = 0; i < KV / 32; ++i) {
     st.k[i] = *reinterpret_cast<const uint2*>(kb + (i * 256 + tid) * 8);
@@ -174,36 +176,53 @@ __global__ __launch_bounds__(256, 2) void k_attn_int4(AttnArgs a) {
   // running maximum m and row sum l of pscale P (LQ: of the codes u)
   float m = -INFINITY, l = 0.f;
 
+  // Software pipeline over blocks: a block's score products run while the
+  // previous block's PV products are converted (matrix core and vector unit
+  // side by side), so a block starts with its scores in registers.  K tiles
+  // are therefore staged two blocks ahead and V tiles one block ahead: block
+  // j + 2's K goes where block j's K was (its scores were taken during block
+  // j - 1), block j + 1's V where block j - 1's V was; two LDS buffers each.
+  auto blk = [&](int b) { return b < nblocks ? b : nblocks - 1; };
   Stage<KV> st;
-  stage_load<KV>(a, bh, 0, st);
+  stage_load<KV>(a, bh, 0, 0, st);
   stage_store<KV>(st, sK[0], sV[0]);
+  stage_load<KV>(a, bh, blk(1), blk(1), st);
+  stage_store<KV>(st, sK[1], sV[1]);
   stage_aux(0, 0);
   __syncthreads();
 
-  // One block of KV keys; MASKED (keys past N) only for the partial last block.
-  auto step = [&](int jb, auto masked_tag) {
+  // S^T = K Q^T of one 32-key chunk of the K tile kt (int32, 16 x the exact S)
+  v16i si[NCH];
+  auto score_chunk = [&](const uint8_t* kt, int ch) {
+    si[ch] = v16i{0, 0, 0, 0, 0, 0, 0, 0, 0, 0, 0, 0, 0, 0, 0, 0};
+#pragma unroll
+    for (int kc = 0; kc < 4; ++kc) {
+      const v4i A = *reinterpret_cast<const v4i*>(&kt[(((ch * 8) + 2 * kc + hh) * 32 + j) * 16]);
+      si[ch] = __builtin_amdgcn_mfma_i32_32x32x32_i8(A, qop[kc], si[ch], 0, 0, 0);
+    }
+  };
+#pragma unroll
+  for (int ch = 0; ch < NCH; ++ch) score_chunk(sK[0], ch);
+  stage_load<KV>(a, bh, blk(2), blk(1), st);
+  __syncthreads();   // every wave has read block 0's K before it is overwritten
+
+  // One block of KV keys; MASKED (keys past N) only for the last block (a full
+  // last block masks nothing).  MORE: a next block exists; as a template
+  // argument it keeps the product phase one basic block.
+  auto step = [&](int jb, auto masked_tag, auto more_tag) {
     constexpr bool MASKED = decltype(masked_tag)::value;
+    constexpr bool more = decltype(more_tag)::value;
     const int buf = jb & 1;
-    const bool more = jb + 1 < nblocks;
-    if (more) stage_load<KV>(a, bh, jb + 1, st);
     const int key0 = jb * KV;
     // key of accumulator register r in chunk ch: key0 + ch*32 + 8*(r/4) + 4*hh + r%4
     auto is_out = [&](int ch, int r) { return MASKED && key0 + ch * 32 + 8 * (r >> 2) + 4 * hh + (r & 3) >= N; };
 
-    // ---- S^T = K Q^T (int32, 16 x the exact S), kept as binary32 (exact:
-    //      |16 S| <= 16 * 6272 < 2^24) ----
+    // ---- the block's int32 scores, kept as binary32 (exact: |16 S| <= 16 * 6272 < 2^24) ----
     float s[NCH][16];
 #pragma unroll
-    for (int ch = 0; ch < NCH; ++ch) {
-      v16i si = v16i{0, 0, 0, 0, 0, 0, 0, 0, 0, 0, 0, 0, 0, 0, 0, 0};
+    for (int ch = 0; ch < NCH; ++ch)
 #pragma unroll
-      for (int kc = 0; kc < 4; ++kc) {
-        const v4i A = *reinterpret_cast<const v4i*>(&sK[buf][(((ch * 8) + 2 * kc + hh) * 32 + j) * 16]);
-        si = __builtin_amdgcn_mfma_i32_32x32x32_i8(A, qop[kc], si, 0, 0, 0);
-      }
-#pragma unroll
-      for (int r = 0; r < 16; ++r) s[ch][r] = static_cast<float>(si[r]);
-    }
+      for (int r = 0; r < 16; ++r) s[ch][r] = static_cast<float>(si[ch][r]);
     if (DEBUG) {
       if (bh == a.dbg_bh && qrow >= a.dbg_row0 && qrow < a.dbg_row0 + a.dbg_rows && a.dbg_s) {
         const size_t rowo = static_cast<size_t>(qrow - a.dbg_row0);
@@ -302,12 +321,10 @@ __global__ __launch_bounds__(256, 2) void k_attn_int4(AttnArgs a) {
       }
     }
 
-    // the next block's tiles go to LDS here (its buffer was last read before
-    // the previous barrier), so the staging registers die early
-    if (more) {
-      stage_store<KV>(st, sK[buf ^ 1], sV[buf ^ 1]);
-      stage_aux(jb + 1, buf ^ 1);
-    }
+    // block j + 2's K and block j + 1's V go to LDS here, so the staging
+    // registers die early
+    stage_store<KV>(st, sK[buf], sV[buf ^ 1]);
+    if (more) stage_aux(jb + 1, buf ^ 1);
     // ---- O^T += V^T P^T (int32 per block), then O = alpha O + acc * dq; the
     //      alpha rescale only when some row of the wave moved its maximum ----
     if (__ballot(alpha != 1.0f) != 0) {
@@ -316,34 +333,70 @@ __global__ __launch_bounds__(256, 2) void k_attn_int4(AttnArgs a) {
 #pragma unroll
         for (int r = 0; r < 16; ++r) of[mt][r] = __fmul_rn(of[mt][r], alpha);
     }
+    __builtin_amdgcn_sched_barrier(0);
+    // the products of output tile mt (and the next block's scores of chunk mt)
+    // run beside the conversion of tile mt - 1: one scheduling region per
+    // tile, a quarter of the conversion after every second product
+    v16i acc[2];
+    auto convert_q = [&](int mt, int rq) {   // registers 4 rq .. 4 rq + 3 of tile mt
+      const float4 dq = *reinterpret_cast<const float4*>(&sDq[buf][mt * 32 + 8 * rq + 4 * hh]);
+      const float d4[4] = {dq.x, dq.y, dq.z, dq.w};
 #pragma unroll
-    for (int mt = 0; mt < 4; ++mt) {
-      v16i acc = v16i{0, 0, 0, 0, 0, 0, 0, 0, 0, 0, 0, 0, 0, 0, 0, 0};
-#pragma unroll
-      for (int ch = 0; ch < NCH; ++ch) {
-        const v4i B = v4i{static_cast<int>(pk[ch][0]), static_cast<int>(pk[ch][1]), static_cast<int>(pk[ch][2]),
-                          static_cast<int>(pk[ch][3])};
-        const v4i A = *reinterpret_cast<const v4i*>(&sV[buf][((ch * 2 + hh) * 128 + mt * 32 + j) * 16]);
-        acc = __builtin_amdgcn_mfma_i32_32x32x32_i8(A, B, acc, 0, 0, 0);
+      for (int t = 0; t < 4; ++t) {
+        const int r = 4 * rq + t;
+        of[mt][r] = __fmaf_rn(static_cast<float>(acc[mt & 1][r]), d4[t], of[mt][r]);
       }
+    };
+    // region g = 8 mt + i: i < NCH the PV product of tile mt with chunk i;
+    // 4 <= i < 8 (more, mt < NCH) the next block's score product of chunk mt,
+    // channel quarter i - 4; its A operand is read from LDS two regions ahead
+    const uint8_t* kn = sK[buf ^ 1];
+    auto has = [&](int g) {
+      const int mt = g >> 3, i = g & 7;
+      return i < NCH || (more && i >= 4 && mt < NCH);
+    };
+    auto opA = [&](int g) {
+      const int mt = g >> 3, i = g & 7;
+      if (i < NCH) return *reinterpret_cast<const v4i*>(&sV[buf][((i * 2 + hh) * 128 + mt * 32 + j) * 16]);
+      return *reinterpret_cast<const v4i*>(&kn[(((mt * 8) + 2 * (i - 4) + hh) * 32 + j) * 16]);
+    };
+    const v16i zero16 = v16i{0, 0, 0, 0, 0, 0, 0, 0, 0, 0, 0, 0, 0, 0, 0, 0};
+    v4i a0 = opA(0), a1 = opA(1);
+    __builtin_amdgcn_sched_barrier(0);
 #pragma unroll
-      for (int rq = 0; rq < 4; ++rq) {
-        const float4 dq = *reinterpret_cast<const float4*>(&sDq[buf][mt * 32 + 8 * rq + 4 * hh]);
-        const float d4[4] = {dq.x, dq.y, dq.z, dq.w};
-#pragma unroll
-        for (int t = 0; t < 4; ++t) {
-          const int r = 4 * rq + t;
-          of[mt][r] = __fmaf_rn(static_cast<float>(acc[r]), d4[t], of[mt][r]);
+    for (int g = 0; g < 32; ++g) {
+      const int mt = g >> 3, i = g & 7;
+      // the operand two products ahead
+      int g2 = g + 1;
+      while (g2 < 32 && !has(g2)) ++g2;
+      int g3 = g2 + 1;
+      while (g3 < 32 && !has(g3)) ++g3;
+      if (has(g)) {
+        const v4i an = g3 < 32 ? opA(g3) : a0;
+        if (i < NCH) {
+          const v4i B = v4i{static_cast<int>(pk[i][0]), static_cast<int>(pk[i][1]), static_cast<int>(pk[i][2]),
+                            static_cast<int>(pk[i][3])};
+          acc[mt & 1] = __builtin_amdgcn_mfma_i32_32x32x32_i8(a0, B, i == 0 ? zero16 : acc[mt & 1], 0, 0, 0);
+        } else {
+          const int kc = i - 4;
+          si[mt] = __builtin_amdgcn_mfma_i32_32x32x32_i8(a0, qop[kc], kc == 0 ? zero16 : si[mt], 0, 0, 0);
         }
+        a0 = a1;
+        a1 = an;
       }
+      if (mt > 0 && (i & 1)) convert_q(mt - 1, i >> 1);
+      if ((i & 7) == 7) __builtin_amdgcn_sched_barrier(0);
     }
-
+#pragma unroll
+    for (int rq = 0; rq < 4; ++rq) convert_q(3, rq);
+    if (more) stage_load<KV>(a, bh, blk(jb + 3), blk(jb + 2), st);
     __syncthreads();
   };
 
-  const int nfull = N / KV;
-  for (int jb = 0; jb < nfull; ++jb) step(jb, std::integral_constant<bool, false>());
-  if (nfull < nblocks) step(nfull, std::integral_constant<bool, true>());
+  using kNo = std::integral_constant<bool, false>;
+  using kYes = std::integral_constant<bool, true>;
+  for (int jb = 0; jb + 1 < nblocks; ++jb) step(jb, kNo(), kYes());
+  step(nblocks - 1, kYes(), kNo());
 
   // ---- epilogue: O = O' pscale / l + mu_v (rotated back by H when V was
   //      rotated online); l is pscale * sum P, or the sum of the codes ----

@@ -156,14 +156,13 @@ __device__ __forceinline__ V as_vec(uint4 u) {
   return __builtin_bit_cast(V, u);
 }
 
-// K and V tiles of one block of KV keys (KV * 256 bytes each) move global ->
-// registers -> LDS; each thread carries KV / 16 16-byte pieces of each.  The
-// loads of block j + 2 are issued at the end of block j and stored in the
-// middle of block j + 1.
+// K and V tiles move global -> registers -> LDS; each thread carries KV / 16
+// 16-byte pieces of each (the K and V pieces may belong to different blocks).
 template <int KV>
 struct Tile16 {
   typedef unsigned T __attribute__((ext_vector_type(4)));
   static constexpr int NP = KV / 16;
+  static_assert(NP * 16 * 256 == KV * kD * 2, "pieces cover the tile");
   T k[NP], v[NP];
   __device__ __forceinline__ void load(const uint16_t* kg, const uint16_t* vg, int tid) {
     const T* K = reinterpret_cast<const T*>(kg) + tid;
@@ -191,8 +190,17 @@ struct Tile16 {
 // operands share one lane layout), with V read as the B operand in the key
 // order of its relayout, so a lane of the output tile holds one channel of 16
 // queries (query 8 (r / 4) + 4 hh + r % 4 in register r).
+//
+// Software pipeline over blocks: once a 32-key chunk's probabilities are
+// rounded to 16 bits, its score registers take the next block's scores of
+// the same chunk; those products and the chunk's PV products run on the
+// matrix core beside the next chunk's probabilities, with their LDS operands
+// read two products ahead, and a block starts with its scores in registers.
+// K tiles are staged two blocks ahead and V tiles one block ahead, so two LDS
+// buffers of each suffice (block j + 2's K goes where block j's K was, whose
+// scores were taken during block j - 1).
 template <bool F16, int kKV>
-__global__ __launch_bounds__(256, 2) void k_attn16(Fp16Args a) {
+__global__ __launch_bounds__(256, kKV == 64 ? 2 : 1) void k_attn16(Fp16Args a) {
   typedef typename MF<F16>::vec vec;
   constexpr int NCH = kKV / 32;
   constexpr int TILE = kKV * kD;  // elements of K (and of V) per block
@@ -210,6 +218,7 @@ __global__ __launch_bounds__(256, 2) void k_attn16(Fp16Args a) {
   const uint16_t* kbase = a.k + hoff;
   const uint16_t* vbase = a.v + hoff;
   const float Kc = a.Kc;
+  auto blk = [&](int b) { return static_cast<size_t>(b < nblocks ? b : nblocks - 1) * TILE; };
 
   vec qop[8];
   {
@@ -225,31 +234,35 @@ __global__ __launch_bounds__(256, 2) void k_attn16(Fp16Args a) {
     for (int r = 0; r < 16; ++r) of[mt][r] = 0.f;
   float m = -INFINITY, l = 0.f;
 
+  auto kop = [&](const uint16_t* kt, int ch, int kc) {
+    return as_vec<vec>(*reinterpret_cast<const uint4*>(&kt[(((ch * 8 + kc) * 2 + hh) * 32 + j) * 8]));
+  };
+  v16f s[NCH];
+
+  // prologue: K and V of block 0 and K of block 1 in LDS, block 0's scores;
+  // then V of block 1 and K of block 2 staged for the first step
   Tile16<kKV> tp;
   tp.load(kbase, vbase, tid);
   tp.store(sK[0], sV[0], tid);
-  tp.load(kbase + (nblocks > 1 ? TILE : 0), vbase + (nblocks > 1 ? TILE : 0), tid);
+  tp.load(kbase + blk(1), vbase + blk(1), tid);
+  tp.store(sK[1], sV[1], tid);
   __syncthreads();
+#pragma unroll
+  for (int ch = 0; ch < NCH; ++ch)
+#pragma unroll
+    for (int r = 0; r < 16; ++r) s[ch][r] = 0.f;
+#pragma unroll
+  for (int kc = 0; kc < 8; ++kc)
+#pragma unroll
+    for (int ch = 0; ch < NCH; ++ch) s[ch] = MF<F16>::mfma(kop(sK[0], ch, kc), qop[kc], s[ch]);
+  tp.load(kbase + blk(2), vbase + blk(1), tid);
+  __syncthreads();   // every wave has read block 0's K before it is overwritten
 
-  auto step = [&](int jb, auto masked_tag) {
+  auto step = [&](int jb, auto masked_tag, auto more_tag) {
     constexpr bool MASKED = decltype(masked_tag)::value;
+    constexpr bool more = decltype(more_tag)::value;
     const int buf = jb & 1;
     const int key0 = jb * kKV;
-
-    // ---- S^T = K Q^T; the chunks' products alternate so that consecutive
-    //      instructions accumulate into different registers ----
-    v16f s[NCH];
-#pragma unroll
-    for (int ch = 0; ch < NCH; ++ch)
-#pragma unroll
-      for (int r = 0; r < 16; ++r) s[ch][r] = 0.f;
-#pragma unroll
-    for (int kc = 0; kc < 8; ++kc)
-#pragma unroll
-      for (int ch = 0; ch < NCH; ++ch) {
-        const vec A = as_vec<vec>(*reinterpret_cast<const uint4*>(&sK[buf][(((ch * 8 + kc) * 2 + hh) * 32 + j) * 8]));
-        s[ch] = MF<F16>::mfma(A, qop[kc], s[ch]);
-      }
     if (MASKED) {
 #pragma unroll
       for (int ch = 0; ch < NCH; ++ch)
@@ -281,52 +294,82 @@ __global__ __launch_bounds__(256, 2) void k_attn16(Fp16Args a) {
       }
     }
     __builtin_amdgcn_sched_barrier(0);
-    if (jb + 1 < nblocks) tp.store(sK[buf ^ 1], sV[buf ^ 1], tid);
+    // block j + 2's K where block j's was, block j + 1's V where block j - 1's was
+    tp.store(sK[buf], sV[buf ^ 1], tid);
     __builtin_amdgcn_sched_barrier(0);
 
     // ---- P = 2^(S Kc - m) in 16 bits, row sums of the unrounded P, O += P V ----
     float ls[4];
+    uint32_t pw[NCH][8];
+    auto probs = [&](int ch, int r2) {   // registers 2 r2, 2 r2 + 1 of chunk ch
+      float P[2];
 #pragma unroll
-    for (int ch = 0; ch < NCH; ++ch) {
-      uint32_t pw[8];
-#pragma unroll
-      for (int r2 = 0; r2 < 8; ++r2) {
-        float P[2];
-#pragma unroll
-        for (int u = 0; u < 2; ++u) {
-          const int r = 2 * r2 + u;
-          float p = __builtin_amdgcn_exp2f(__fmaf_rn(s[ch][r], Kc, -mnew));
-          if (MASKED && s[ch][r] == -INFINITY) p = 0.f;
-          if (ch == 0 && r < 4) ls[r] = p;
-          else ls[r & 3] += p;
-          P[u] = p;
-        }
-        pw[r2] = pack2<F16>(P[0], P[1]);
+      for (int u = 0; u < 2; ++u) {
+        const int r = 2 * r2 + u;
+        float p = __builtin_amdgcn_exp2f(__fmaf_rn(s[ch][r], Kc, -mnew));
+        if (MASKED && s[ch][r] == -INFINITY) p = 0.f;
+        if (ch == 0 && r < 4) ls[r] = p;
+        else ls[r & 3] += p;
+        P[u] = p;
       }
-      // k-step stp covers registers 8 stp .. 8 stp + 7 of the chunk
+      pw[ch][r2] = pack2<F16>(P[0], P[1]);
+    };
+    // the products of chunk c (group c): 8 PV products (k-step stp = i / 4,
+    // tile mt = i % 4), then, with a next block, its 8 score products of chunk
+    // c (channel step kc = i - 8); operand of product i of group c
+    const uint16_t* kn = sK[buf ^ 1];
+    auto opB = [&](int c, int i) {
+      if (i < 8)
+        return as_vec<vec>(
+            *reinterpret_cast<const uint4*>(&sV[buf][(((c * 2 + (i >> 2)) * 2 + hh) * 128 + (i & 3) * 32 + j) * 8]));
+      return kop(kn, c, i - 8);
+    };
+    constexpr int NPR = more ? 16 : 8;   // products per chunk
+    auto product = [&](int c, int i, vec op) {
+      if (i < 8) {
+        const int stp = i >> 2, mt = i & 3;
+        const vec A = as_vec<vec>(
+            make_uint4(pw[c][4 * stp], pw[c][4 * stp + 1], pw[c][4 * stp + 2], pw[c][4 * stp + 3]));
+        of[mt] = MF<F16>::mfma(A, op, of[mt]);
+      } else {
+        const int kc = i - 8;
+        if (kc == 0) {
 #pragma unroll
-      for (int stp = 0; stp < 2; ++stp) {
-        const vec A = as_vec<vec>(make_uint4(pw[4 * stp], pw[4 * stp + 1], pw[4 * stp + 2], pw[4 * stp + 3]));
-#pragma unroll
-        for (int mt = 0; mt < 4; ++mt) {
-          const vec B =
-              as_vec<vec>(*reinterpret_cast<const uint4*>(&sV[buf][(((ch * 2 + stp) * 2 + hh) * 128 + mt * 32 + j) * 8]));
-          of[mt] = MF<F16>::mfma(A, B, of[mt]);
+          for (int r = 0; r < 16; ++r) s[c][r] = 0.f;
         }
+        s[c] = MF<F16>::mfma(op, qop[kc], s[c]);
+      }
+    };
+#pragma unroll
+    for (int r2 = 0; r2 < 8; ++r2) probs(0, r2);
+    vec o0 = opB(0, 0), o1 = opB(0, 1);
+    __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+    for (int c = 0; c < NCH; ++c) {
+      // chunk c's products, beside chunk c + 1's probabilities
+#pragma unroll
+      for (int i = 0; i < NPR; ++i) {
+        // the operand two products ahead (into the next chunk's products)
+        const int n2 = i + 2;
+        const int c2 = n2 < NPR ? c : c + 1, i2 = n2 < NPR ? n2 : n2 - NPR;
+        const vec on = c2 < NCH ? opB(c2, i2) : o0;
+        product(c, i, o0);
+        o0 = o1;
+        o1 = on;
+        constexpr int PER = NPR / 8;   // products per pair of probabilities
+        if (c + 1 < NCH && i % PER == PER - 1) probs(c + 1, i / PER);
       }
       __builtin_amdgcn_sched_barrier(0);
     }
     l = __fmaf_rn(l, alpha, (ls[0] + ls[1]) + (ls[2] + ls[3]));
-    {
-      const size_t nb2 = static_cast<size_t>(jb + 2 < nblocks ? jb + 2 : nblocks - 1) * TILE;
-      tp.load(kbase + nb2, vbase + nb2, tid);
-    }
+    tp.load(kbase + blk(jb + 3), vbase + blk(jb + 2), tid);
     __syncthreads();
   };
 
-  const int nfull = N / kKV;
-  for (int jb = 0; jb < nfull; ++jb) step(jb, std::integral_constant<bool, false>());
-  if (nfull < nblocks) step(nfull, std::integral_constant<bool, true>());
+  using kNo = std::integral_constant<bool, false>;
+  using kYes = std::integral_constant<bool, true>;
+  for (int jb = 0; jb + 1 < nblocks; ++jb) step(jb, kNo(), kYes());
+  step(nblocks - 1, kYes(), kNo());
 
   // ---- epilogue: O / l ----
   const float ltot = l + __shfl_xor(l, 32);

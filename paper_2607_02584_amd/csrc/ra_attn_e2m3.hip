@@ -539,20 +539,20 @@ __global__ __launch_bounds__(kThreads, 8 / kWaves) void k_attn_e2m3(AttnArgs a) 
 #pragma unroll
     for (int q = 0; q < 8; ++q) probs4(q >> 2, q & 3);
     pack_group(0);
-    __builtin_amdgcn_sched_barrier(0);
     // block j + 2's tiles into the buffer block j - 1 used
     tp.store(sK[tbw], sV[tbw], tid);
     __builtin_amdgcn_sched_barrier(0);
     if (more) read_kpair(kr, sK[tbn], 0);
 #pragma unroll
     for (int gg = 1; gg < NG; ++gg) {
-      // products of group gg - 1, one per region with four probabilities of group gg
+      // products of group gg - 1 beside the probabilities of group gg (the
+      // compiler interleaves them within the region)
 #pragma unroll
       for (int t = 0; t < 4; ++t) {
         of[t] = mfma6(B, vrec[t], of[t]);
         probs4(2 * gg, t);
-        __builtin_amdgcn_sched_barrier(0);
       }
+      __builtin_amdgcn_sched_barrier(0);
       read_vrecs(gg);
       if (more) {
         v16f z;
@@ -561,13 +561,10 @@ __global__ __launch_bounds__(kThreads, 8 / kWaves) void k_attn_e2m3(AttnArgs a) 
         const int c0 = 2 * gg - 2;
         s[c0] = mfma6(kr[0], qop[0], z);
         probs4(2 * gg + 1, 0);
-        __builtin_amdgcn_sched_barrier(0);
         s[c0 + 1] = mfma6(kr[1], qop[0], z);
         probs4(2 * gg + 1, 1);
-        __builtin_amdgcn_sched_barrier(0);
         s[c0] = mfma6(kr[2], qop[1], s[c0]);
         probs4(2 * gg + 1, 2);
-        __builtin_amdgcn_sched_barrier(0);
         s[c0 + 1] = mfma6(kr[3], qop[1], s[c0 + 1]);
         probs4(2 * gg + 1, 3);
         __builtin_amdgcn_sched_barrier(0);
@@ -578,7 +575,6 @@ __global__ __launch_bounds__(kThreads, 8 / kWaves) void k_attn_e2m3(AttnArgs a) 
       }
       if (more) read_kpair(kr, sK[tbn], 2 * gg);
       pack_group(gg);
-      __builtin_amdgcn_sched_barrier(0);
     }
     // products of the last group
 #pragma unroll

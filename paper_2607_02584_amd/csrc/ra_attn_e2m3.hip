@@ -580,7 +580,6 @@ __global__ __launch_bounds__(kThreads, 8 / kWaves) void k_attn_e2m3(AttnArgs a) 
 #pragma unroll
     for (int t = 0; t < 4; ++t) of[t] = mfma6(B, vrec[t], of[t]);
     if (more) score_pair(kr, NCH - 2);
-    __builtin_amdgcn_sched_barrier(0);
     l = __fmaf_rn(l, alpha, (ls[0] + ls[1]) + (ls[2] + ls[3]));
     if (DEBUG && a.dbg_m && hh == 0 && bh == a.dbg_bh && qrow >= a.dbg_row0 && qrow < a.dbg_row0 + a.dbg_rows)
       a.dbg_m[static_cast<size_t>(qrow - a.dbg_row0) * nblocks + jb] = mnew;

@@ -67,9 +67,10 @@ typedef int v8i __attribute__((ext_vector_type(8)));
 typedef int v6i __attribute__((ext_vector_type(6)));
 typedef float v16f __attribute__((ext_vector_type(16)));
 
-// A workgroup of 4 waves (one per SIMD) covers 128 queries; two workgroups
-// share a compute unit.
-constexpr int kWaves = 4;
+// A workgroup of 8 waves (two per SIMD) covers 256 queries and owns a compute
+// unit: the K/V tiles of a block are fetched once per unit, not once per
+// 128 queries.
+constexpr int kWaves = 8;
 constexpr int kThreads = 64 * kWaves;
 constexpr int kBlockM = 32 * kWaves;  // queries per workgroup
 constexpr int kScaleOne = 127;  // E8M0 block scale 2^0
@@ -151,15 +152,15 @@ __device__ __forceinline__ v8i load_rec(const uint8_t* p) {
 }
 
 // K and V code tiles of one block go global -> registers -> LDS: every thread
-// moves three 16-byte (KV = 128) or 8-byte (KV = 64) pieces of each, adjacent
+// moves three 8-byte (KV = 128) or 4-byte (KV = 64) pieces of each, adjacent
 // threads adjacent pieces.  The global loads of block j + 3 are issued at the
 // end of block j and written to LDS in block j + 1, once its first 64-key
 // group is packed, so their latency overlaps the barrier, the row maxima and
 // the first probabilities.
 template <int KV>
 struct TilePiece {
-  // 16-byte (KV = 128) or 8-byte (KV = 64) pieces as 32-bit vectors, six per thread
-  typedef unsigned T __attribute__((ext_vector_type(KV == 128 ? 4 : 2)));
+  // 8-byte (KV = 128) or 4-byte (KV = 64) pieces as 32-bit vectors, six per thread
+  typedef unsigned T __attribute__((ext_vector_type(KV == 128 ? 2 : 1)));
   T k0, k1, k2, v0, v1, v2;
   __device__ __forceinline__ void load(const uint8_t* kg, const uint8_t* vg, int tid) {
     const T* K = reinterpret_cast<const T*>(kg) + tid;
@@ -245,7 +246,7 @@ __global__ __launch_bounds__(kThreads, 8 / kWaves) void k_attn_e2m3(AttnArgs a) 
   // handles key t of the block (waves 2 and 3, or wave 2 alone for 64-key
   // blocks), or the K scale of chunk t (t < NCH, grouped K: k_group is 32, 64
   // or 128, so the group index is a shift).
-  const bool kwave = KV == 128 ? wave >= 2 : wave == 2;
+  const bool kwave = KV == 128 ? (wave == 2 || wave == 3) : wave == 2;
   const int kgs = __builtin_ctz(static_cast<unsigned>(a.k_group));
   auto fetch_aux = [&](int jb) {
     Aux f{0.f, 0.f, 0.f};

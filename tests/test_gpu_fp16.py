@@ -75,6 +75,36 @@ def test_fp16_fallback_parity(ora, wname, dtype, kv):
         assert err <= O_TOL
 
 
+# sequence lengths around whole numbers of 64- and 128-key blocks (the kernel
+# takes a block's scores during the previous block, so the first and the last
+# blocks take their own paths)
+BOUNDARY_GRIDS = {64: (1, 8, 8), 128: (2, 8, 8), 129: (3, 43, 1), 192: (3, 8, 8), 256: (4, 8, 8),
+                  257: (1, 1, 257), 384: (6, 8, 8), 385: (5, 7, 11)}
+
+
+@pytest.mark.parametrize("n", list(BOUNDARY_GRIDS))
+@pytest.mark.parametrize("kv", [64, 128])
+def test_fallback_block_count_boundaries(ora, n, kv):
+    """The fallback at every block count from one to six, full and partial last blocks."""
+    torch, ra = _torch(), _ra()
+    from paper_2607_02584_amd import datagen as dg
+    T, Hg, W = BOUNDARY_GRIDS[n]
+    w = dg.small_workload(f"n{n}", T, Hg, W, H=1, seed=60 + n)
+    assert w.N == n
+    q, k, v = dg.make_inputs(w)
+    p = ra.make_params(w.B, w.H, (w.T, w.Hg, w.W), w.split, w.theta, rotation=0, out_dtype=ra.FP32, kv_block=kv)
+    ws = ra.workspace(p, ra.PATH_FP16)
+    qd, kd, vd = (ra.to_device_bits(x) for x in (q, k, v))
+    o = torch.empty((1, n, 128), dtype=torch.float32, device="cuda")
+    ra.fwd_fp16(p, qd, kd, vd, o, ws)
+    torch.cuda.synchronize()
+    geo = ora.Geometry(w.T, w.Hg, w.W, w.split, w.theta)
+    O_ref = ora.fwd_fp16_head(geo, q[0, 0], k[0, 0], v[0, 0], kv_block=kv)
+    err = np.abs(o[0].cpu().numpy() - O_ref).max() / np.abs(O_ref).max()
+    print(f"[fallback boundary] N={n} kv_block={kv}: O rel err {err:.3e}", flush=True)
+    assert err <= O_TOL
+
+
 def test_fallback_c2_full_size_sampled_rows(ora):
     """The 32760-token layer in the launch configuration the benchmark times
     (12 heads, bf16 inputs, 64-key blocks), fp32 output: sampled query rows of two

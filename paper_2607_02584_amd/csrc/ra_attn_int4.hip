@@ -335,8 +335,8 @@ __global__ __launch_bounds__(256, 2) void k_attn_int4(AttnArgs a) {
     }
     __builtin_amdgcn_sched_barrier(0);
     // the products of output tile mt (and the next block's scores of chunk mt)
-    // run beside the conversion of tile mt - 1: one scheduling region per
-    // tile, a quarter of the conversion after every second product
+    // run beside the conversion of tile mt - 1 (a quarter of it after every
+    // second product), all in one scheduling region
     v16i acc[2];
     auto convert_q = [&](int mt, int rq) {   // registers 4 rq .. 4 rq + 3 of tile mt
       const float4 dq = *reinterpret_cast<const float4*>(&sDq[buf][mt * 32 + 8 * rq + 4 * hh]);
@@ -385,7 +385,7 @@ __global__ __launch_bounds__(256, 2) void k_attn_int4(AttnArgs a) {
         a1 = an;
       }
       if (mt > 0 && (i & 1)) convert_q(mt - 1, i >> 1);
-      if ((i & 7) == 7) __builtin_amdgcn_sched_barrier(0);
+
     }
 #pragma unroll
     for (int rq = 0; rq < 4; ++rq) convert_q(3, rq);

@@ -333,7 +333,6 @@ __global__ __launch_bounds__(256, 2) void k_attn_int4(AttnArgs a) {
 #pragma unroll
         for (int r = 0; r < 16; ++r) of[mt][r] = __fmul_rn(of[mt][r], alpha);
     }
-    __builtin_amdgcn_sched_barrier(0);
     // the products of output tile mt (and the next block's scores of chunk mt)
     // run beside the conversion of tile mt - 1 (a quarter of it after every
     // second product), all in one scheduling region
@@ -362,7 +361,6 @@ __global__ __launch_bounds__(256, 2) void k_attn_int4(AttnArgs a) {
     };
     const v16i zero16 = v16i{0, 0, 0, 0, 0, 0, 0, 0, 0, 0, 0, 0, 0, 0, 0, 0};
     v4i a0 = opA(0), a1 = opA(1);
-    __builtin_amdgcn_sched_barrier(0);
 #pragma unroll
     for (int g = 0; g < 32; ++g) {
       const int mt = g >> 3, i = g & 7;

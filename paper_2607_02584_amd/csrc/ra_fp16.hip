@@ -293,10 +293,8 @@ __global__ __launch_bounds__(256, kKV == 64 ? 2 : 1) void k_attn16(Fp16Args a) {
         for (int mt = 0; mt < 4; ++mt) of[mt][r] = __fmul_rn(of[mt][r], ar);
       }
     }
-    __builtin_amdgcn_sched_barrier(0);
     // block j + 2's K where block j's was, block j + 1's V where block j - 1's was
     tp.store(sK[buf], sV[buf ^ 1], tid);
-    __builtin_amdgcn_sched_barrier(0);
 
     // ---- P = 2^(S Kc - m) in 16 bits, row sums of the unrounded P, O += P V ----
     float ls[4];
@@ -343,7 +341,6 @@ __global__ __launch_bounds__(256, kKV == 64 ? 2 : 1) void k_attn16(Fp16Args a) {
 #pragma unroll
     for (int r2 = 0; r2 < 8; ++r2) probs(0, r2);
     vec o0 = opB(0, 0), o1 = opB(0, 1);
-    __builtin_amdgcn_sched_barrier(0);
 #pragma unroll
     for (int c = 0; c < NCH; ++c) {
       // chunk c's products, beside chunk c + 1's probabilities
@@ -359,7 +356,6 @@ __global__ __launch_bounds__(256, kKV == 64 ? 2 : 1) void k_attn16(Fp16Args a) {
         constexpr int PER = NPR / 8;   // products per pair of probabilities
         if (c + 1 < NCH && i % PER == PER - 1) probs(c + 1, i / PER);
       }
-      __builtin_amdgcn_sched_barrier(0);
     }
     l = __fmaf_rn(l, alpha, (ls[0] + ls[1]) + (ls[2] + ls[3]));
     tp.load(kbase + blk(jb + 3), vbase + blk(jb + 2), tid);

@@ -236,6 +236,13 @@ __device__ __forceinline__ float quad_xor(float v) {
   return __int_as_float(__builtin_amdgcn_mov_dpp(__float_as_int(v), M == 1 ? 0xB1 : 0x4E, 0xF, 0xF, false));
 }
 
+// Wave-wide lane mask of the lanes with (lane mod 4) < n, n >= 0.
+__device__ __forceinline__ uint64_t lanes_c4_below(int n) {
+  const uint32_t nib = (1u << (n < 4 ? n : 4)) - 1u;
+  const uint32_t half = nib * 0x11111111u;
+  return (static_cast<uint64_t>(half) << 32) | half;
+}
+
 // The thread's two rows of the tile at n0 after RoPE and the rotation:
 // z[p][c] is channel 32 c4 + c of tile row 64 p + r64 (zero for rows past N).
 // STAGED: table rows from LDS (st, stage_plan's layout), else straight from the
@@ -252,6 +259,19 @@ __device__ __forceinline__ void rope_item(const RopeTables& t, int N, int n0, co
   // only the last tile has rows past N: the zeroing below is skipped (a
   // uniform branch) everywhere else
   const bool tail = n0 + kTile > N;
+  // lanes (c4 = lane mod 4) whose pair 16 c4 + k lies before the axis
+  // boundary b = 16 q + r: exactly those with c4 < q + (k < r), so per
+  // boundary two wave-wide masks, chosen per k, decide the axis of every pair
+  const int bnd[2] = {np0, np0 + np1};
+  uint64_t below[2][2];
+  int bnd_r[2];
+#pragma unroll
+  for (int i = 0; i < 2; ++i) {
+    const int q = bnd[i] >> 4;
+    bnd_r[i] = bnd[i] & 15;
+    below[i][0] = lanes_c4_below(q + 1);
+    below[i][1] = lanes_c4_below(q);
+  }
 #pragma unroll
   for (int p = 0; p < kQkPasses; ++p) {
     const int nl = 64 * p + r64, n = n0 + nl;
@@ -268,18 +288,35 @@ __device__ __forceinline__ void rope_item(const RopeTables& t, int N, int n0, co
       const int row = STAGED ? (sp.bypos[ax] ? pos[ax] : lin[ax] - sp.lin0[ax]) : pos[ax];
       so[ax] = (STAGED ? sp.base[ax] : 0) + row * (t.split[ax] / 2);
     }
-    // pair P of axis a sits at so[a] + P - (first pair of a)
-    const int o1 = so[1] - np0, o2 = so[2] - np0 - np1;
+    // pair P of axis a sits at so[a] + P - (first pair of a).  Per axis, the
+    // entry the thread's first pair (16 c4) would have on it; pair 16 c4 + k
+    // is entry k from the base of its axis, so the per-pair offset is a
+    // constant and only the base is chosen per pair
+    const int P0 = 16 * c4;
+    const float4* base[3];
+    if constexpr (STAGED) {
+      // byte offsets into the staged rows, kept opaque so that the compiler
+      // selects the scaled offsets instead of scaling the selected index
+      int bo[3] = {16 * (so[0] + P0), 16 * (so[1] + P0 - np0), 16 * (so[2] + P0 - np0 - np1)};
+#pragma unroll
+      for (int ax = 0; ax < 3; ++ax) {
+        asm volatile("" : "+v"(bo[ax]));
+        base[ax] = reinterpret_cast<const float4*>(reinterpret_cast<const uint8_t*>(st) + bo[ax]);
+      }
+    } else {
+      base[0] = t.axis[0] + (so[0] + P0);
+      base[1] = t.axis[1] + (so[1] + P0 - np0);
+      base[2] = t.axis[2] + (so[2] + P0 - np0 - np1);
+    }
     const uint32_t w[16] = {raw[p][0].x, raw[p][0].y, raw[p][0].z, raw[p][0].w, raw[p][1].x, raw[p][1].y,
                             raw[p][1].z, raw[p][1].w, raw[p][2].x, raw[p][2].y, raw[p][2].z, raw[p][2].w,
                             raw[p][3].x, raw[p][3].y, raw[p][3].z, raw[p][3].w};
     float y[32];
 #pragma unroll
     for (int k = 0; k < 16; ++k) {
-      const int P = 16 * c4 + k;
-      const int ax = (P >= np0) + (P >= np0 + np1);
-      const int off = (ax == 0 ? so[0] : (ax == 1 ? o1 : o2)) + P;
-      const float4 g = STAGED ? st[off] : (ax == 0 ? t.axis[0] : (ax == 1 ? t.axis[1] : t.axis[2]))[off];
+      const bool ax0 = __builtin_amdgcn_inverse_ballot_w64(below[0][k < bnd_r[0] ? 0 : 1]);
+      const bool ax01 = __builtin_amdgcn_inverse_ballot_w64(below[1][k < bnd_r[1] ? 0 : 1]);
+      const float4 g = (ax0 ? base[0] : (ax01 ? base[1] : base[2]))[k];
       const float x0 = h2f<F16>(static_cast<uint16_t>(w[k] & 0xffff));
       const float x1 = h2f<F16>(static_cast<uint16_t>(w[k] >> 16));
       y[2 * k] = __fmaf_rn(x1, g.z, __fmul_rn(x0, g.x));
@@ -561,6 +598,8 @@ template <bool F16, bool VHAD>
 __device__ __forceinline__ void load_v_tile(const VArgs& a, int bh, int tile, float z[16][4]) {
   const int tid = threadIdx.x, rr = tid >> 5, cl = tid & 31;
   const uint16_t* xb = a.x + static_cast<size_t>(bh) * a.N * kD;
+  // without centring the subtracted mean is 0 (x - 0 == x exactly, also for
+  // -0), so the subtraction needs no per-element select
   float4 m = make_float4(0.f, 0.f, 0.f, 0.f);
   if (a.center) m = mean4(a.sums + static_cast<size_t>(bh) * kD, a.N, cl);
   uint2 raw[16];
@@ -585,7 +624,7 @@ __device__ __forceinline__ void load_v_tile(const VArgs& a, int bh, int tile, fl
       }
       // online V rotation (Sec. 4.3): the row times H, before smoothing
       if constexpr (VHAD) hadamard_row(x, cl);
-      if (in && a.center) {
+      if (in) {
         x[0] = __fsub_rn(x[0], m.x);
         x[1] = __fsub_rn(x[1], m.y);
         x[2] = __fsub_rn(x[2], m.z);

@@ -142,10 +142,15 @@ __device__ __forceinline__ void rescale_group(v16f (&o)[4], float ab, unsigned l
   rescale_row<4 * G + 3>(o, ab, moved);
 }
 
-// 24-byte record -> operand registers (6 used dwords)
+// 24-byte record -> operand registers (6 used dwords).  The fences keep the
+// three reads apart: merged into paired reads, whose offset field stops at
+// 2 KiB, the records of a tile would each need an address add, while single
+// reads reach every record of the tile from one base.
 __device__ __forceinline__ v8i load_rec(const uint8_t* p) {
   const uint2 a = *reinterpret_cast<const uint2*>(p);
+  __builtin_amdgcn_sched_barrier(0);
   const uint2 b = *reinterpret_cast<const uint2*>(p + 8);
+  __builtin_amdgcn_sched_barrier(0);
   const uint2 c = *reinterpret_cast<const uint2*>(p + 16);
   return v8i{static_cast<int>(a.x), static_cast<int>(a.y), static_cast<int>(b.x), static_cast<int>(b.y),
              static_cast<int>(c.x), static_cast<int>(c.y), 0, 0};

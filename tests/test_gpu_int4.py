@@ -141,6 +141,35 @@ def test_block_count_boundaries(ora, n, kv, fmt):
     _check_case(ora, w, f"n{n}", (1, 128, 128, 128, kv, 0, 3), fmt)
 
 
+# RoPE splits whose axis boundaries (in pairs: D_t/2 and (D_t + D_h)/2) fall
+# at a multiple of 16 pairs (the first pair of a thread's 16), at the first
+# and last pairs, and in the middle of a thread's range; the geometries keep
+# the tile's table rows in LDS, except the two 130- and 160-wide ones, whose
+# 128 W rows of 21 or 24 pairs (more than 40 KB) the producer reads from the
+# tables in place
+SPLIT_CASES = {
+    "t16": ((32, 48, 48), (3, 7, 11)),       # boundaries 16, 40
+    "t32h16": ((64, 32, 32), (3, 7, 11)),    # boundaries 32, 48
+    "t1h1": ((2, 2, 124), (2, 3, 40)),       # boundaries 1, 2
+    "t62h1": ((124, 2, 2), (3, 7, 11)),      # boundaries 62, 63
+    "inplace": ((44, 42, 42), (1, 2, 160)),  # boundaries 22, 43, tables read in place
+    "inplace_t16": ((32, 48, 48), (1, 3, 130)),
+}
+
+
+@pytest.mark.parametrize("fmt", ["e2m3", "int4"])
+@pytest.mark.parametrize("rot", [1, 2])
+@pytest.mark.parametrize("sname", list(SPLIT_CASES))
+def test_rope_split_axis_boundaries(ora, sname, rot, fmt):
+    """Producer codes and the whole forward at RoPE splits that put the axis
+    boundaries at every kind of place within a thread's 16 pairs, with the
+    table rows staged in LDS and read in place."""
+    from paper_2607_02584_amd import datagen as dg
+    split, (T, Hg, W) = SPLIT_CASES[sname]
+    w = dg.small_workload(f"split_{sname}", T, Hg, W, H=1, split=split, seed=60)
+    _check_case(ora, w, f"split_{sname}", (rot, 128, 128, 128, 128, 0, 3), fmt)
+
+
 def _check_case(ora, w, wname, case, fmt):
     torch, ra = _torch(), _ra()
     rot, qg, kg, vg, kv, pq, sm, *rest = case

@@ -261,6 +261,12 @@ __global__ __launch_bounds__(256, kKV == 64 ? 2 : 1) void k_attn16(Fp16Args a) {
   auto step = [&](int jb, auto masked_tag, auto more_tag) {
     constexpr bool MASKED = decltype(masked_tag)::value;
     constexpr bool more = decltype(more_tag)::value;
+    // Issue priority: the block's dependent chain of vector work (maximum,
+    // alpha, the first chunk's probabilities) and the first chunk's products
+    // run at the higher priority, the remaining products at the lower one,
+    // so the waves of a SIMD alternate halves (about 2 % faster than one
+    // priority throughout).
+    __builtin_amdgcn_s_setprio(1);
     const int buf = jb & 1;
     const int key0 = jb * kKV;
     if (MASKED) {
@@ -356,6 +362,7 @@ __global__ __launch_bounds__(256, kKV == 64 ? 2 : 1) void k_attn16(Fp16Args a) {
         constexpr int PER = NPR / 8;   // products per pair of probabilities
         if (c + 1 < NCH && i % PER == PER - 1) probs(c + 1, i / PER);
       }
+      if (c == 0) __builtin_amdgcn_s_setprio(0);
     }
     l = __fmaf_rn(l, alpha, (ls[0] + ls[1]) + (ls[2] + ls[3]));
     tp.load(kbase + blk(jb + 3), vbase + blk(jb + 2), tid);

@@ -28,8 +28,9 @@
 // 4*(t%32) .. +3 of the rows t/32 + 8p (16 rows), each row read as 32 8-byte
 // pieces.  A pass is bound by its HBM traffic and by the per-element vector
 // work (RoPE, rotation, quantization, packing) together: the jobs of one
-// pass share the grid so that the vector-heavy Q/K tiles and the lighter V
-// tiles run side by side.
+// pass share one grid, one job after another in the grid's order (one launch,
+// and the end of one job overlaps the start of the next; taking the jobs in
+// turn block by block was slower).
 #include <type_traits>
 
 #include "ra_internal.h"

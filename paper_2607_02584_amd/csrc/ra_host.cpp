@@ -364,7 +364,7 @@ struct ProdOut {
 // caller's stream: one prologue kernel (the table copy, the zero fills), then
 // the passes.  Each pass is one launch holding every job whose inputs are
 // ready, so independent work (the channel sums of K and V, the codes of an
-// unsmoothed Q) runs side by side: pass 0 the sums and every code pass that
+// unsmoothed Q) shares one launch: pass 0 the sums and every code pass that
 // needs none; pass 1 the codes that need sums (and the V group maxima when V
 // groups straddle tiles); pass 2 the V codes after those maxima.
 int produce(const ra_params* p, const ra::RopeTables& t, const TableCopy& tc, const void* q, const void* k,

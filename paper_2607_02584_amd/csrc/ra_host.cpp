@@ -420,6 +420,19 @@ int produce(const ra_params* p, const ra::RopeTables& t, const TableCopy& tc, co
     a.Npad = static_cast<int>(z.Npad);
     a.is_fp16 = p->in_dtype == RA_FP16;
     a.e2m3 = p->code_format == RA_CODES_E2M3;
+    ra::QkArgs qq = a;
+    qq.x = static_cast<const uint16_t*>(q);
+    qq.codes = out.qc;
+    qq.scales = out.qs;
+    qq.sums = w.qsum;
+    qq.center = center_q;
+    qq.mu_out = center_q ? (out.mu_q ? out.mu_q : w.mu_q) : nullptr;
+    qq.group = p->q_group;
+    // an unsmoothed Q's codes come first in the first pass, so that K and V,
+    // read again by the code pass, are the most recently read inputs when it
+    // starts (the memory-side cache still holds much of them; 0.168 -> 0.164
+    // ms for the 32760-token layer's producers inside the INT4 step)
+    if (!center_q) add(0, ra::kQkQuant, &qq, nullptr);
     if (center_k) {
       ra::QkArgs ak = a;
       ak.x = static_cast<const uint16_t*>(k);
@@ -431,16 +444,8 @@ int produce(const ra_params* p, const ra::RopeTables& t, const TableCopy& tc, co
       aq.x = static_cast<const uint16_t*>(q);
       aq.sums = w.qsum;
       add(0, ra::kQkSums, &aq, nullptr);
+      add(1, ra::kQkQuant, &qq, nullptr);
     }
-    ra::QkArgs qq = a;
-    qq.x = static_cast<const uint16_t*>(q);
-    qq.codes = out.qc;
-    qq.scales = out.qs;
-    qq.sums = w.qsum;
-    qq.center = center_q;
-    qq.mu_out = center_q ? (out.mu_q ? out.mu_q : w.mu_q) : nullptr;
-    qq.group = p->q_group;
-    add(center_q ? 1 : 0, ra::kQkQuant, &qq, nullptr);
     ra::QkArgs kq = a;
     kq.x = static_cast<const uint16_t*>(k);
     kq.codes = out.kc;
